@@ -1,0 +1,223 @@
+"""CPU oracle, part 2: greedy autoregressive decoding and the paper's three
+parallel decoding algorithms.
+
+TEST INFRASTRUCTURE ONLY (see oracle/model.py): never called by the HIP path.
+
+Notation follows Section 3: the target y = (y_1 .. y_m) solves the triangular
+system of Eq. (2), f(y_i, y_{1:i-1}, x) = y_i - argmax p_theta(y_i | y_{1:i-1}, x) = 0.
+Here y is a 0-based numpy array, so y[t] is y_{t+1}.  The decoder input at
+position p is [BOS] for p = 0 and y[p-1] otherwise, and its prediction is the
+new value of y[p]; this is the "shift left" of predictions that Appendix A
+mentions.  One iteration is one decoder forward over the active block.
+
+Readings where the paper leaves a detail open (each is listed in the design
+notes of the repository as well):
+
+* Algorithms 2 and 3 leave the block loop with a ``break`` when a block stops;
+  the text of Section 3.2 says decoding then continues with the next block, so
+  ``break`` ends only the current block's Jacobi loop.
+* Blocks are half-open, [i, i+L) with L = min(b, m - i); the last one is cut at m.
+* Each block runs at most L iterations: after L Jacobi iterations the block is
+  exact by the triangular structure (its j-th token is exact after j
+  iterations), so it counts as converged.  PJ's cap is the m of its for-loop.
+  This keeps Proposition 1's bound of at most m iterations.
+* StopC (Eq. (3)) compares the whole block with its previous value.
+* CheckEOS returns the absolute index of the first [EOS] of a converged block;
+  the output keeps that [EOS].  HGJ's horizon h defaults to m (Section 4.1);
+  its autoregressive tail tests the token it just produced and never runs past m.
+* PJ and PGJ solve all m equations; their output is cut after the first [EOS].
+* Greedy AR stops after producing [EOS] (Eq. (1) with the usual end-of-sentence rule).
+* The argmax takes the lowest index on exact ties; non-finite logits raise.
+"""
+from __future__ import annotations
+
+import dataclasses
+from typing import List, Optional
+
+import numpy as np
+
+from .model import ArgmaxRecord, Encoded, Model, argmax_rows
+
+PAD, BOS, EOS = 0, 1, 2
+
+
+@dataclasses.dataclass
+class Result:
+    y: np.ndarray                 # final iterate (length m; AR/HGJ: up to the stop)
+    out: np.ndarray               # output ids, cut after the first EOS (inclusive)
+    k: int                        # decoder forwards (iterations) used
+    hit_max_iters: bool = False
+    records: List[ArgmaxRecord] = dataclasses.field(default_factory=list)
+    iterates: List[tuple] = dataclasses.field(default_factory=list)   # (k, i, block tokens)
+
+    def min_rel_margin(self) -> float:
+        """Smallest (top1 - top2) / max|logit| over every argmax evaluated."""
+        if not self.records:
+            return float("inf")
+        return min((r.top1 - r.top2) / max(r.linf, 1e-30) for r in self.records)
+
+
+def cut_at_eos(y: np.ndarray) -> np.ndarray:
+    hit = np.nonzero(y == EOS)[0]
+    return y[: hit[0] + 1].copy() if len(hit) else y.copy()
+
+
+class Solver:
+    """Evaluates the map F over a block of the draft, with a KV cache.
+
+    F(y)[p] = argmax p_theta(. | BOS, y[0..p-1], x).  ``block(y, i, L)``
+    returns the new y[i..i+L-1] given the committed prefix y[0..i-1], whose
+    K/V are in the cache, and writes the K/V of positions i..i+L-1.
+    With recompute=True it ignores the cache and recomputes positions
+    0..i+L-1 from scratch (brute force).
+    """
+
+    def __init__(self, model: Model, enc: Encoded, m: int, recompute: bool = False):
+        self.model, self.enc, self.m, self.recompute = model, enc, m, recompute
+        self.cache = model.new_cache(m)
+        self.records: List[ArgmaxRecord] = []
+
+    def inputs(self, y: np.ndarray, i: int, L: int) -> np.ndarray:
+        return np.array([BOS if p == 0 else int(y[p - 1]) for p in range(i, i + L)], np.int64)
+
+    def block(self, y: np.ndarray, i: int, L: int) -> np.ndarray:
+        if self.recompute:
+            cache = self.model.new_cache(self.m)
+            h = self.model.decode_rows(self.enc, cache, self.inputs(y, 0, i + L), 0)[i:]
+        else:
+            h = self.model.decode_rows(self.enc, self.cache, self.inputs(y, i, L), i)
+        recs = argmax_rows(self.model.logits(h), i)
+        self.records.extend(recs)
+        return np.array([r.token for r in recs], np.int32)
+
+
+def _init(m: int, init: Optional[np.ndarray]) -> np.ndarray:
+    """InitT (Section 3.3): all [PAD] unless an explicit draft is given."""
+    return np.full(m, PAD, np.int32) if init is None else np.array(init, np.int32).copy()
+
+
+def greedy(model: Model, enc: Encoded, m: int, stop_at_eos: bool = True,
+           max_iters: Optional[int] = None, recompute: bool = False) -> Result:
+    """Greedy autoregressive decoding, Eq. (1): y[t] = argmax p(. | y[0..t-1], x), t = 0..m-1."""
+    s = Solver(model, enc, m, recompute)
+    cap = m if max_iters is None or max_iters <= 0 else max_iters
+    y = np.full(m, PAD, np.int32)
+    k, t = 0, 0
+    while t < m:
+        if k >= cap:
+            return Result(y[:t], cut_at_eos(y[:t]), k, True, s.records)
+        y[t] = s.block(y, t, 1)[0]
+        k += 1
+        t += 1
+        if stop_at_eos and y[t - 1] == EOS:
+            break
+    return Result(y[:t].copy(), cut_at_eos(y[:t]), k, False, s.records)
+
+
+def jacobi(model: Model, enc: Encoded, m: int, init=None, max_iters: Optional[int] = None,
+           recompute: bool = False) -> Result:
+    """Parallel Jacobi decoding, Algorithm 1: update all m positions from the previous iterate."""
+    s = Solver(model, enc, m, recompute)
+    cap = m if max_iters is None or max_iters <= 0 else min(m, max_iters)
+    y = _init(m, init)
+    res = Result(y, y, 0)
+    for j in range(1, m + 1):
+        if j > cap:
+            res.hit_max_iters = True
+            break
+        o = y.copy()
+        y = s.block(y, 0, m)
+        res.k = j
+        res.iterates.append((j, 0, y.copy()))
+        if np.array_equal(y, o):          # StopC, Eq. (3)
+            break
+    res.y, res.out, res.records = y, cut_at_eos(y), s.records
+    return res
+
+
+def gs_jacobi(model: Model, enc: Encoded, m: int, b: int, init=None,
+              max_iters: Optional[int] = None, recompute: bool = False) -> Result:
+    """Parallel GS-Jacobi decoding, Algorithm 2: Jacobi inside b-blocks, Gauss-Seidel across them."""
+    s = Solver(model, enc, m, recompute)
+    cap = m if max_iters is None or max_iters <= 0 else max_iters
+    y = _init(m, init)
+    res = Result(y, y, 0)
+    i = 0
+    while i < m:
+        L = min(b, m - i)
+        for j in range(1, L + 1):
+            if res.k >= cap:
+                res.hit_max_iters = True
+                break
+            o = y[i:i + L].copy()
+            y[i:i + L] = s.block(y, i, L)
+            res.k += 1
+            res.iterates.append((res.k, i, y[i:i + L].copy()))
+            if np.array_equal(y[i:i + L], o):
+                break
+        if res.hit_max_iters:
+            break
+        i += L
+    res.y, res.out, res.records = y, cut_at_eos(y), s.records
+    return res
+
+
+def hybrid(model: Model, enc: Encoded, m: int, b: int, h: Optional[int] = None, init=None,
+           max_iters: Optional[int] = None, recompute: bool = False) -> Result:
+    """Hybrid GS-Jacobi decoding, Algorithm 3.
+
+    GS-Jacobi blocks up to the horizon h; a converged block that holds [EOS]
+    ends decoding at its first [EOS].  Without [EOS] before h, decoding goes on
+    autoregressively from position h until [EOS] or m.
+    """
+    s = Solver(model, enc, m, recompute)
+    cap = m if max_iters is None or max_iters <= 0 else max_iters
+    h = m if h is None else min(h, m)
+    y = _init(m, init)
+    res = Result(y, y, 0)
+    i = 0
+    eos_cond = False
+    while i < h and not eos_cond and not res.hit_max_iters:
+        L = min(b, h - i)
+        for j in range(1, L + 1):
+            if res.k >= cap:
+                res.hit_max_iters = True
+                break
+            o = y[i:i + L].copy()
+            y[i:i + L] = s.block(y, i, L)
+            res.k += 1
+            res.iterates.append((res.k, i, y[i:i + L].copy()))
+            stop = np.array_equal(y[i:i + L], o) or j == L
+            hit = np.nonzero(y[i:i + L] == EOS)[0]
+            if stop and len(hit):
+                y = y[: i + int(hit[0]) + 1].copy()
+                eos_cond = True
+                break
+            if stop:
+                break
+        if not eos_cond and not res.hit_max_iters:
+            i += L
+    while not eos_cond and not res.hit_max_iters and i < m:
+        if res.k >= cap:
+            res.hit_max_iters = True
+            break
+        y[i] = s.block(y, i, 1)[0]
+        res.k += 1
+        res.iterates.append((res.k, i, y[i:i + 1].copy()))
+        i += 1
+        eos_cond = bool(y[i - 1] == EOS)
+    res.y, res.out, res.records = y, cut_at_eos(y), s.records
+    return res
+
+
+def decode(model: Model, enc: Encoded, m: int, mode: str, block: int = 1, **kw) -> Result:
+    """Dispatch by mode name: ar, jacobi, gs_jacobi, hybrid."""
+    if mode == "ar":
+        return greedy(model, enc, m, **kw)
+    if mode == "jacobi":
+        return jacobi(model, enc, m, **kw)
+    if mode == "gs_jacobi":
+        return gs_jacobi(model, enc, m, block, **kw)
+    if mode == "hybrid":
+        return hybrid(model, enc, m, block, **kw)
+    raise ValueError(mode)
