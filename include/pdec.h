@@ -1,0 +1,205 @@
+/*
+ * pdec -- parallel (Jacobi / GS-Jacobi / hybrid) decoding of an
+ * encoder-decoder Transformer on AMD Instinct MI355X (gfx950).
+ *
+ * The library solves the triangular system of greedy decoding
+ *   y_i = argmax p_theta(y_i | y_1..y_{i-1}, x),  i = 1..m        (Section 3.1, Eq. (1)-(2))
+ * with the fixed-point iterations of Section 3.2 / Appendix A:
+ *   PD_AR         greedy autoregressive decoding, one token per decoder forward;
+ *   PD_JACOBI     Algorithm 1 (PJ): all m positions updated from the previous iterate;
+ *   PD_GS_JACOBI  Algorithm 2 (PGJ): Jacobi inside blocks of b positions,
+ *                 Gauss-Seidel from block to block;
+ *   PD_HYBRID     Algorithm 3 (HGJ): PGJ up to a horizon h, then greedy steps;
+ *                 stops at the first [EOS] of a converged block.
+ * Every decoder forward ("iteration") runs hand-written HIP kernels: a decoder
+ * pass over the active block (causal self-attention over a KV cache,
+ * cross-attention to the encoder memory, FFN, LayerNorm), a fused vocabulary
+ * projection + argmax that never stores logits, and an on-device stopping
+ * test (Eq. (3): the block is unchanged) that commits converged blocks and
+ * lays out the next iteration, so the loop needs no host round trip.
+ *
+ * Memory ownership.  Every device buffer (weights, workspace, inputs, outputs)
+ * is allocated and freed by the caller; the library never allocates device
+ * memory.  pd_model / pd_ctx own host-side state only (plus one pinned host
+ * word per context for completion polling).  Weight and workspace buffers
+ * must stay valid and unchanged while a model / context uses them.
+ *
+ * Threads and streams.  A pd_ctx is used by one host thread at a time; calls
+ * on it are enqueued on the stream given to each call and are asynchronous
+ * unless stated otherwise.  A context's workspace holds the encoder state
+ * between pd_encode and pd_decode, so those two calls must be ordered (same
+ * stream, or synchronised).
+ *
+ * Errors.  Every call returns pd_status.  Argument / shape / state errors are
+ * detected on the host before anything is enqueued.  PD_E_DEVICE reports a
+ * HIP launch or runtime failure; pd_last_error() holds a message for the
+ * calling thread.  Numerical anomalies found on the device (a non-finite
+ * logit) are reported per sentence in out_flags only.
+ */
+#ifndef PDEC_H_
+#define PDEC_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t pd_status;
+enum {
+  PD_OK = 0,
+  PD_E_ARG = 1,          /* invalid argument value (mode, block, pointer, ...) */
+  PD_E_SHAPE = 2,        /* a size exceeds what the model / context was built for */
+  PD_E_WORKSPACE = 3,    /* workspace missing, misaligned or too small */
+  PD_E_DEVICE = 4,       /* HIP error */
+  PD_E_UNSUPPORTED = 5,  /* configuration the kernels do not handle */
+  PD_E_STATE = 6         /* call out of order (e.g. decode before encode) */
+};
+
+/* Decoding modes (Section 3.2). */
+enum { PD_AR = 0, PD_JACOBI = 1, PD_GS_JACOBI = 2, PD_HYBRID = 3 };
+
+/* Storage types of weights and activations. */
+enum { PD_F32 = 0, PD_BF16 = 1 };
+
+/* Per-sentence result flags (out_flags bits). */
+enum {
+  PD_FLAG_CONVERGED = 1,    /* every position solved (or [EOS] reached in a converged block) */
+  PD_FLAG_EOS = 2,          /* stopped at [EOS] (PD_AR, PD_HYBRID) */
+  PD_FLAG_MAX_ITERS = 4,    /* stopped by max_iters before convergence */
+  PD_FLAG_NONFINITE = 8     /* a logit was NaN/Inf at some iteration */
+};
+
+/*
+ * Model shape.  The model is p_theta of Section 3.1 with the two shapes of
+ * Section 4.1 ("Model Configuration"): post-LN (x <- LN(x + Sub(x))) or pre-LN
+ * (x <- x + Sub(LN(x)), plus a final LayerNorm after encoder and decoder),
+ * ReLU or exact-erf GELU FFN, sinusoidal positions, one token embedding E[V][d]
+ * shared by encoder input, decoder input and the output projection
+ * logits = logit_scale * h . E^T + out_bias.
+ *   d_model must be a multiple of 8 and of n_heads; d_model / n_heads must be
+ *   16, 32, 64 or 128; d_ff a multiple of 8.
+ *   enc_emb_scale / dec_emb_scale multiply E[token] at the encoder / decoder
+ *   input (a negative value selects sqrt(d_model)).
+ *   bf16 models store weights, K/V, attention outputs, FFN hidden values, the
+ *   residual stream and LayerNorm outputs feeding a product in bfloat16
+ *   (round to nearest even) and accumulate in float.
+ */
+typedef struct {
+  int32_t n_enc, n_dec, d_model, n_heads, d_ff, vocab;
+  int32_t pre_ln;        /* 0: post-LN, 1: pre-LN with final LayerNorms */
+  int32_t act_gelu;      /* 0: ReLU, 1: GELU (erf) */
+  int32_t dtype;         /* PD_F32 or PD_BF16 */
+  int32_t pad_id, bos_id, eos_id;
+  float ln_eps;
+  float logit_scale;
+  float enc_emb_scale;
+  float dec_emb_scale;
+} pd_config;
+
+typedef struct pd_model pd_model;
+typedef struct pd_ctx pd_ctx;
+
+/*
+ * Number of weight tensors of a configuration, and the shape of tensor idx
+ * (rows x cols; cols = 1 for vectors).  Canonical order:
+ *   0 emb [V][d]          1 out_bias [V]
+ *   encoder layer l (12 tensors each):
+ *     w_qkv [3d][d], b_qkv [3d], w_o [d][d], b_o [d], ln1_g [d], ln1_b [d],
+ *     w1 [d_ff][d], b1 [d_ff], w2 [d][d_ff], b2 [d], ln2_g [d], ln2_b [d]
+ *   pre-LN only: enc_ln_g [d], enc_ln_b [d]
+ *   decoder layer l (20 tensors each):
+ *     w_qkv [3d][d], b_qkv [3d], w_o [d][d], b_o [d], ln1_g [d], ln1_b [d],
+ *     ca_w_q [d][d], ca_b_q [d], ca_w_kv [2d][d], ca_b_kv [2d], ca_w_o [d][d], ca_b_o [d],
+ *     ln2_g [d], ln2_b [d],
+ *     w1 [d_ff][d], b1 [d_ff], w2 [d][d_ff], b2 [d], ln3_g [d], ln3_b [d]
+ *   pre-LN only: dec_ln_g [d], dec_ln_b [d]
+ * Matrices are row-major [out][in]; w_qkv stacks the Q, K and V projections.
+ * Returns -1 for an invalid configuration.
+ */
+int32_t pd_weight_count(const pd_config* cfg);
+pd_status pd_weight_shape(const pd_config* cfg, int32_t idx, int64_t* rows, int64_t* cols);
+
+/*
+ * Bind a configuration to caller-owned device weights.  dev_weights holds
+ * n_weights device pointers in canonical order, each 16-byte aligned, of
+ * element type float (PD_F32) or bfloat16 bit patterns (PD_BF16).  The
+ * pointers are stored, not copied.  Returns PD_E_ARG for a null / misaligned
+ * pointer or a wrong count, PD_E_UNSUPPORTED for shapes the kernels reject.
+ */
+pd_status pd_model_create(const pd_config* cfg, const void* const* dev_weights, int32_t n_weights,
+                          pd_model** out);
+void pd_model_destroy(pd_model* model);
+
+/*
+ * Device workspace needed by a context that decodes up to max_batch sentences
+ * with sources of at most max_src tokens and targets of at most max_tgt
+ * positions (max_tgt <= 1024).  Covers every mode, including PD_JACOBI with
+ * blocks of max_tgt positions.
+ */
+pd_status pd_ctx_workspace_bytes(const pd_model* model, int32_t max_batch, int32_t max_src,
+                                 int32_t max_tgt, size_t* bytes);
+
+/*
+ * Create a context on caller-owned device workspace (256-byte aligned, at
+ * least pd_ctx_workspace_bytes).  The workspace holds activations, the
+ * cross-attention and self-attention K/V caches, drafts and control state.
+ */
+pd_status pd_ctx_create(const pd_model* model, int32_t max_batch, int32_t max_src, int32_t max_tgt,
+                        void* dev_workspace, size_t workspace_bytes, pd_ctx** out);
+void pd_ctx_destroy(pd_ctx* ctx);
+
+/*
+ * Encode a batch of B sources (the conditioning x of p_theta(y | x)).
+ *   src_ids  device int32 [B][n_max], token ids, rows padded after src_len[b]
+ *            (ids outside [0, vocab) are clamped into it)
+ *   src_len  HOST int32 [B], 1 <= src_len[b] <= n_max
+ * Runs the encoder and writes the cross-attention K/V of every decoder layer
+ * into the context.  Padded positions are masked out of every attention.
+ * PD_E_SHAPE if B > max_batch or n_max > max_src.
+ */
+pd_status pd_encode(pd_ctx* ctx, const int32_t* src_ids, const int32_t* src_len, int32_t B,
+                    int32_t n_max, void* stream);
+
+/*
+ * Decode the batch of the last pd_encode on this context.
+ *   mode      PD_AR, PD_JACOBI, PD_GS_JACOBI or PD_HYBRID
+ *   block     block size b >= 1 (PD_GS_JACOBI, PD_HYBRID); ignored otherwise
+ *             (PD_JACOBI uses one block of m positions, PD_AR blocks of 1)
+ *   horizon   PD_HYBRID parallel horizon h (<= 0: h = m); ignored otherwise
+ *   max_iters per-sentence cap on decoder forwards (<= 0: m, which every mode
+ *             needs at most, Proposition 1)
+ *   tgt_m     HOST int32 [B] (B of the last pd_encode), number of target
+ *             positions m of each sentence, 1 <= tgt_m[b] <= max_tgt
+ *   out_ids   device int32 [B][out_ld], out_ld >= max(tgt_m): the solution
+ *             cut after its first [EOS] (inclusive) and [PAD]-filled
+ *   out_len   device int32 [B]: output length (first [EOS] + 1, else m)
+ *   out_k     device int32 [B]: iterations (decoder forwards) used
+ *   out_flags device int32 [B]: PD_FLAG_* bits
+ * The initial draft is all [PAD] (Section 3.3, "Initialization").  Sentences
+ * of a batch iterate independently; a sentence's result does not depend on
+ * the other sentences.  The call blocks the host until the iteration has
+ * converged (it polls a completion word once per iteration), then enqueues
+ * the output writes on the stream.
+ */
+pd_status pd_decode(pd_ctx* ctx, int32_t mode, int32_t block, int32_t horizon, int32_t max_iters,
+                    const int32_t* tgt_m, int32_t* out_ids, int32_t out_ld, int32_t* out_len,
+                    int32_t* out_k, int32_t* out_flags, void* stream);
+
+/*
+ * Verification only: teacher-forced logits of the encoded batch.
+ *   tgt_in  device int32 [B][T] decoder inputs (BOS first), T <= max_tgt
+ *   logits  device float [B][T][V]
+ * Uses the same kernels as pd_decode, with the argmax replaced by a store.
+ */
+pd_status pd_debug_logits(pd_ctx* ctx, const int32_t* tgt_in, int32_t T, float* logits, void* stream);
+
+/* Message of the last failing call on this thread ("" if none). */
+const char* pd_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PDEC_H_ */

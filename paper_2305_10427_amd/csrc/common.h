@@ -1,0 +1,157 @@
+// Device-side helpers shared by the decoding kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace pdec {
+
+constexpr int kWave = 64;
+
+// bfloat16 storage is a raw 16-bit pattern: the upper half of an IEEE float.
+typedef uint16_t bf16_t;
+
+__device__ __forceinline__ float bf16_to_f32(bf16_t h) {
+  return __uint_as_float(static_cast<uint32_t>(h) << 16);
+}
+
+// Round-to-nearest-even float -> bfloat16 (NaN kept quiet).
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) return static_cast<bf16_t>((u >> 16) | 0x40);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return static_cast<bf16_t>(u >> 16);
+}
+
+// Storage-type traits: load/store one element as float.
+template <typename T> struct Elt;
+template <> struct Elt<float> {
+  static __device__ __forceinline__ float load(const float* p, size_t i) { return p[i]; }
+  static __device__ __forceinline__ void store(float* p, size_t i, float v) { p[i] = v; }
+  // value as it would be after a store + load (identity for float)
+  static __device__ __forceinline__ float round(float v) { return v; }
+};
+template <> struct Elt<bf16_t> {
+  static __device__ __forceinline__ float load(const bf16_t* p, size_t i) { return bf16_to_f32(p[i]); }
+  static __device__ __forceinline__ void store(bf16_t* p, size_t i, float v) { p[i] = f32_to_bf16(v); }
+  static __device__ __forceinline__ float round(float v) { return bf16_to_f32(f32_to_bf16(v)); }
+};
+
+// Load 16 bytes of T starting at element i (i aligned to 16/sizeof(T)) as floats.
+template <typename T> struct Vec16;
+template <> struct Vec16<float> {
+  static constexpr int N = 4;
+  static __device__ __forceinline__ void load(const float* p, size_t i, float* out) {
+    float4 v = *reinterpret_cast<const float4*>(p + i);
+    out[0] = v.x; out[1] = v.y; out[2] = v.z; out[3] = v.w;
+  }
+};
+template <> struct Vec16<bf16_t> {
+  static constexpr int N = 8;
+  static __device__ __forceinline__ void load(const bf16_t* p, size_t i, float* out) {
+    uint4 v = *reinterpret_cast<const uint4*>(p + i);
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      out[2 * j] = __uint_as_float(w[j] << 16);
+      out[2 * j + 1] = __uint_as_float(w[j] & 0xffff0000u);
+    }
+  }
+};
+
+// Load N consecutive elements of T (N = 4 or 8, aligned) as floats.
+template <typename T, int N>
+__device__ __forceinline__ void load_n(const T* p, size_t i, float* out) {
+  constexpr int V = Vec16<T>::N;
+  static_assert(N % V == 0 || V % N == 0, "vector width");
+  if constexpr (N >= V) {
+#pragma unroll
+    for (int j = 0; j < N; j += V) Vec16<T>::load(p, i + j, out + j);
+  } else {
+#pragma unroll
+    for (int j = 0; j < N; ++j) out[j] = Elt<T>::load(p, i + j);
+  }
+}
+
+// Butterfly sum over the 64 lanes of a wave; every lane gets the total.
+// The pairing order is fixed, so the result is bitwise reproducible.
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
+  return v;
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v = fmaxf(v, __shfl_xor(v, off));
+  return v;
+}
+
+// Sum of M values per lane across the 64 lanes of a wave (M a power of two,
+// M <= 64).  Halving exchange: after log2(M) steps each lane holds one partial
+// of value index j = lane >> (6 - log2 M); the remaining steps finish the sum
+// inside groups of 64 / M lanes.  Returns the total of value j in every lane of
+// group j.  Fixed pairing order: bitwise reproducible.
+template <int M>
+__device__ __forceinline__ float wave_reduce_scatter(float (&v)[M], int lane) {
+  static_assert(M >= 1 && M <= 64 && (M & (M - 1)) == 0, "M must be a power of two <= 64");
+  int off = 32;
+#pragma unroll
+  for (int half = M / 2; half >= 1; half >>= 1, off >>= 1) {
+    const bool upper = (lane & off) != 0;
+#pragma unroll
+    for (int j = 0; j < half; ++j) {
+      const float send = upper ? v[j] : v[j + half];
+      const float keep = upper ? v[j + half] : v[j];
+      v[j] = keep + __shfl_xor(send, off);
+    }
+  }
+  float r = v[0];
+  for (; off >= 1; off >>= 1) r += __shfl_xor(r, off);
+  return r;
+}
+
+template <int M> struct Log2 { static constexpr int v = 1 + Log2<M / 2>::v; };
+template <> struct Log2<1> { static constexpr int v = 0; };
+
+// Order-preserving map of a float to uint32 (larger float -> larger key).
+__device__ __forceinline__ uint32_t float_key(float f) {
+  uint32_t u = __float_as_uint(f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// Mean and 1/sqrt(var + eps) of one row of K elements, lane split as in the
+// products: lane handles k = c*64*EPL + lane*EPL + e.
+template <typename WT, typename XT>
+__device__ __forceinline__ void ln_stats(const XT* x, int K, int lane, float eps,
+                                         float& mean, float& rstd) {
+  constexpr int EPL = Vec16<WT>::N;
+  float s = 0.f;
+  for (int k0 = lane * EPL; k0 < K; k0 += kWave * EPL) {
+    float v[EPL];
+    load_n<XT, EPL>(x, k0, v);
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) s += v[e];
+  }
+  mean = wave_sum(s) / static_cast<float>(K);
+  float q = 0.f;
+  for (int k0 = lane * EPL; k0 < K; k0 += kWave * EPL) {
+    float v[EPL];
+    load_n<XT, EPL>(x, k0, v);
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) {
+      const float t = v[e] - mean;
+      q = fmaf(t, t, q);
+    }
+  }
+  const float var = wave_sum(q) / static_cast<float>(K);
+  rstd = 1.0f / sqrtf(var + eps);
+}
+
+// LayerNorm of one element given its row statistics (same expression
+// everywhere it is evaluated, so the result is bitwise identical).
+__device__ __forceinline__ float ln_apply(float x, float mean, float rstd, float g, float b) {
+  return fmaf((x - mean) * rstd, g, b);
+}
+
+}  // namespace pdec

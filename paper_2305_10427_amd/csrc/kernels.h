@@ -1,0 +1,161 @@
+// Internal launch interface between the host runtime and the HIP kernels.
+// Nothing here crosses the public C ABI (include/pdec.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace pdec {
+
+enum DType { DT_F32 = 0, DT_BF16 = 1 };
+
+// Where row r of an activation matrix lives: sentence s and input position p.
+// With sent == nullptr the rows are laid out densely, s = r / per_sent, p = r % per_sent.
+struct RowMap {
+  const int* sent;
+  const int* pos;
+  int per_sent;
+};
+
+enum Prologue { PRO_NONE = 0, PRO_LN = 1 };
+enum Epilogue {
+  EPI_F32 = 0,     // out_f32 = acc + bias
+  EPI_ACT = 1,     // out (storage type) = act(acc + bias)
+  EPI_RESID = 2,   // out_f32 or out = acc + bias + resid
+  EPI_QKV = 3,     // cols [0,q_cols) -> out_f32; next d -> K cache; next d -> V cache
+  EPI_ARGMAX = 4,  // logits = scale * acc + bias, reduced to a per-(row, workgroup) best
+  EPI_LOGITS = 5,  // out_f32 = scale * acc + bias (verification only)
+};
+
+struct GemmArgs {
+  const int* n_rows_dev;   // row count read on device (nullptr: use n_rows)
+  int n_rows;
+  // input rows [R][ldx]; element type float if x_f32 else the storage type
+  const void* x;
+  int ldx;
+  int x_f32;
+  // LayerNorm prologue (PRO_LN): x <- LN(x) * g + b, rounded to the storage type
+  const void* ln_g;
+  const void* ln_b;
+  float ln_eps;
+  void* ln_out;            // optional: workgroup 0 writes the normalised rows here
+  int ldlo;
+  // weights W[N][K] row-major (storage type), bias[N]
+  const void* w;
+  const void* bias;
+  int N, K;
+  // epilogues
+  float* out_f32;
+  void* out;
+  int ldo;
+  const void* resid;
+  int ldr;
+  int resid_f32;
+  int act;                 // 1 relu, 2 gelu (EPI_ACT)
+  int q_cols;              // EPI_QKV
+  void* kc;                // EPI_QKV: K / V caches [S][H][T][dh] of one layer
+  void* vc;
+  int H, dh, T, d;
+  RowMap rows;
+  float logit_scale;       // EPI_ARGMAX
+  uint2* partials;         // [row][part_ld] = (order key of best logit, index | nonfinite << 31)
+  int part_ld;
+};
+
+struct AttnArgs {
+  const int* n_rows_dev;
+  int n_rows;
+  const float* q;          // [R][ldq] float, unscaled
+  int ldq;
+  const void* kc;          // [S][H][T][dh] storage type
+  const void* vc;
+  int H, dh, T;
+  RowMap rows;
+  int causal;              // 1: row at position p sees keys 0..p; 0: keys 0..klen[s]-1
+  const int* klen;
+  void* out;               // [R][ldo] storage type
+  int ldo;
+  float scale;             // 1/sqrt(dh)
+};
+
+struct EmbedArgs {
+  const int* n_rows_dev;
+  int n_rows;
+  const int* tok;          // [R] token of each row
+  RowMap rows;             // position of each row
+  const void* emb;         // E[V][d]
+  float scale;
+  int d;
+  int vocab;               // ids outside [0, vocab) are clamped into it
+  void* out;               // [R][d] storage type
+};
+
+struct LnArgs {
+  const int* n_rows_dev;
+  int n_rows;
+  const void* x;
+  int x_f32;
+  const void* g;
+  const void* b;
+  float eps;
+  int d;
+  void* out;               // storage type
+};
+
+// Per-sentence decoding state kept on the device.
+struct SentState {
+  int m;          // target length (number of equations)
+  int i;          // first position of the current block
+  int L;          // current block length (0 when done)
+  int j;          // iterations spent on the current block
+  int k;          // total iterations
+  int done;
+  int flags;
+  int row0;       // first row of this sentence in the current iteration
+};
+
+struct CtrlArgs {
+  SentState* st;
+  int B;
+  int mode, block, horizon, max_iters;
+  const int* tgt_m;        // [B]
+  int* y;                  // [B][ldy] draft
+  int ldy;
+  const int* new_tok;      // [R] argmax of each row of the last iteration
+  const int* row_flags;    // [R] nonzero: a non-finite logit was seen
+  int* row_sent;           // [R_max] rows of the next iteration
+  int* row_pos;
+  int* row_tok;
+  int* n_rows;             // device scalar
+  int* host_done;          // mapped pinned host flag (may be null)
+  int pad_id, bos_id, eos_id;
+  int R_max;
+  // finalize
+  int* out_ids; int out_ld; int* out_len; int* out_k; int* out_flags;
+};
+
+struct ReduceArgs {
+  const int* n_rows_dev;
+  const uint2* partials;
+  int part_ld;
+  int n_parts;
+  int* new_tok;
+  int* row_flags;
+};
+
+// launchers (return hipError_t of the launch)
+hipError_t launch_gemm(int dtype, int pro, int epi, int row_tile, const GemmArgs& a, int grid, hipStream_t s);
+hipError_t launch_attn(int dtype, const AttnArgs& a, int R_max, hipStream_t s);
+hipError_t launch_embed(int dtype, const EmbedArgs& a, int R_max, hipStream_t s);
+hipError_t launch_ln(int dtype, const LnArgs& a, int R_max, hipStream_t s);
+hipError_t launch_argmax_reduce(const ReduceArgs& a, int R_max, hipStream_t s);
+hipError_t launch_ctrl_init(const CtrlArgs& a, hipStream_t s);
+hipError_t launch_ctrl_step(const CtrlArgs& a, hipStream_t s);
+hipError_t launch_finalize(const CtrlArgs& a, hipStream_t s);
+
+// Number of 16-byte weight vectors a lane loads per K-chunk is one; the
+// elements per lane are 16 / sizeof(weight).  Kernels that must reproduce the
+// same LayerNorm statistics use this same split.
+inline int elems_per_lane(int dtype) { return dtype == DT_BF16 ? 8 : 4; }
+
+}  // namespace pdec

@@ -1,0 +1,648 @@
+// Host runtime behind the C ABI of include/pdec.h: configuration checks,
+// workspace planning, the encoder pass, the decoder pass of one iteration and
+// the iteration loop of the four decoding modes.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "kernels.h"
+#include "../../include/pdec.h"
+
+using namespace pdec;
+
+namespace {
+
+thread_local std::string g_err;
+
+pd_status fail(pd_status st, const std::string& msg) {
+  g_err = msg;
+  return st;
+}
+
+#define PD_HIP(call)                                                                        \
+  do {                                                                                      \
+    hipError_t e_ = (call);                                                                 \
+    if (e_ != hipSuccess)                                                                   \
+      return fail(PD_E_DEVICE, std::string(#call " failed: ") + hipGetErrorString(e_));     \
+  } while (0)
+
+constexpr int kVocabWGs = 1024;     // workgroups of the fused vocabulary kernel (partials per row)
+constexpr int kMaxGemmWGs = 2048;
+constexpr int kFuseLnMaxRows = 64;  // above this the LayerNorm runs as its own kernel
+constexpr size_t kAlign = 256;
+
+int weight_count(const pd_config& c) {
+  return 2 + 12 * c.n_enc + (c.pre_ln ? 2 : 0) + 20 * c.n_dec + (c.pre_ln ? 2 : 0);
+}
+
+bool check_config(const pd_config* c, std::string* why) {
+  if (c == nullptr) { *why = "null config"; return false; }
+  if (c->n_enc < 1 || c->n_dec < 1 || c->d_model < 8 || c->n_heads < 1 || c->d_ff < 8 || c->vocab < 4) {
+    *why = "non-positive model size";
+    return false;
+  }
+  if (c->dtype != PD_F32 && c->dtype != PD_BF16) { *why = "dtype must be PD_F32 or PD_BF16"; return false; }
+  if (c->d_model % c->n_heads != 0) { *why = "d_model must be a multiple of n_heads"; return false; }
+  const int dh = c->d_model / c->n_heads;
+  if (dh != 16 && dh != 32 && dh != 64 && dh != 128) { *why = "head dim must be 16, 32, 64 or 128"; return false; }
+  if (c->d_model % 8 != 0 || c->d_ff % 8 != 0) { *why = "d_model and d_ff must be multiples of 8"; return false; }
+  for (int id : {c->pad_id, c->bos_id, c->eos_id})
+    if (id < 0 || id >= c->vocab) { *why = "special token id out of vocabulary"; return false; }
+  if (!(c->ln_eps > 0.f)) { *why = "ln_eps must be positive"; return false; }
+  return true;
+}
+
+void shape_of(const pd_config& c, int idx, int64_t* rows, int64_t* cols) {
+  const int64_t d = c.d_model, f = c.d_ff, V = c.vocab;
+  *cols = 1;
+  if (idx == 0) { *rows = V; *cols = d; return; }
+  if (idx == 1) { *rows = V; return; }
+  int t = idx - 2;
+  if (t < 12 * c.n_enc) {
+    static const int64_t r_[12] = {3, 3, 1, 1, 1, 1, -1, -1, 1, 1, 1, 1};
+    static const int c_[12] = {1, 0, 1, 0, 0, 0, 1, 0, 2, 0, 0, 0};   // 1: d, 2: d_ff, 0: vector
+    const int j = t % 12;
+    *rows = r_[j] > 0 ? r_[j] * d : f;
+    *cols = c_[j] == 1 ? d : (c_[j] == 2 ? f : 1);
+    return;
+  }
+  t -= 12 * c.n_enc;
+  if (c.pre_ln) {
+    if (t < 2) { *rows = d; return; }
+    t -= 2;
+  }
+  if (t < 20 * c.n_dec) {
+    static const int64_t r_[20] = {3, 3, 1, 1, 1, 1, 1, 1, 2, 2, 1, 1, 1, 1, -1, -1, 1, 1, 1, 1};
+    static const int c_[20] = {1, 0, 1, 0, 0, 0, 1, 0, 1, 0, 1, 0, 0, 0, 1, 0, 2, 0, 0, 0};
+    const int j = t % 20;
+    *rows = r_[j] > 0 ? r_[j] * d : f;
+    *cols = c_[j] == 1 ? d : (c_[j] == 2 ? f : 1);
+    return;
+  }
+  *rows = d;   // final decoder LayerNorm
+}
+
+}  // namespace
+
+struct pd_model {
+  pd_config cfg;
+  std::vector<const void*> w;
+  int dt;          // DT_F32 / DT_BF16
+  int d, H, dh, dff, V;
+  float enc_scale, dec_scale;
+
+  const void* enc(int l, int j) const { return w[2 + 12 * l + j]; }
+  const void* enc_ln(int j) const { return w[2 + 12 * cfg.n_enc + j]; }
+  int dec_base() const { return 2 + 12 * cfg.n_enc + (cfg.pre_ln ? 2 : 0); }
+  const void* dec(int l, int j) const { return w[dec_base() + 20 * l + j]; }
+  const void* dec_ln(int j) const { return w[dec_base() + 20 * cfg.n_dec + j]; }
+};
+
+namespace {
+
+enum { E_WQKV = 0, E_BQKV, E_WO, E_BO, E_LN1G, E_LN1B, E_W1, E_B1, E_W2, E_B2, E_LN2G, E_LN2B };
+enum {
+  D_WQKV = 0, D_BQKV, D_WO, D_BO, D_LN1G, D_LN1B, D_CWQ, D_CBQ, D_CWKV, D_CBKV, D_CWO, D_CBO,
+  D_LN2G, D_LN2B, D_W1, D_B1, D_W2, D_B2, D_LN3G, D_LN3B
+};
+
+struct Layout {
+  size_t x_res, s_buf, q_buf, a_buf, h_buf;
+  size_t enc_k, enc_v, cross_k, cross_v, self_k, self_v;
+  size_t partials, new_tok, row_flags, row_sent, row_pos, row_tok;
+  size_t st, y, tgt_m, src_len, n_rows;
+  size_t total;
+};
+
+Layout plan(const pd_model& M, int max_batch, int max_src, int max_tgt) {
+  Layout L{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off += (bytes + kAlign - 1) / kAlign * kAlign;
+    return at;
+  };
+  const size_t es = M.dt == DT_BF16 ? 2 : 4;
+  const size_t rows_dec = static_cast<size_t>(max_batch) * max_tgt;
+  const size_t rows = std::max(static_cast<size_t>(max_batch) * max_src, rows_dec);
+  const size_t d = M.d;
+  L.x_res = take(rows * d * es);
+  L.s_buf = take(rows * d * 4);
+  L.q_buf = take(rows * d * 4);
+  L.a_buf = take(rows * d * es);
+  L.h_buf = take(rows * M.dff * es);
+  const size_t enc_kv = static_cast<size_t>(max_batch) * max_src * d * es;
+  L.enc_k = take(enc_kv);
+  L.enc_v = take(enc_kv);
+  L.cross_k = take(enc_kv * M.cfg.n_dec);
+  L.cross_v = take(enc_kv * M.cfg.n_dec);
+  const size_t self_kv = rows_dec * d * es * M.cfg.n_dec;
+  L.self_k = take(self_kv);
+  L.self_v = take(self_kv);
+  L.partials = take(rows_dec * kVocabWGs * sizeof(uint2));
+  L.new_tok = take(rows_dec * 4);
+  L.row_flags = take(rows_dec * 4);
+  L.row_sent = take(rows_dec * 4);
+  L.row_pos = take(rows_dec * 4);
+  L.row_tok = take(rows_dec * 4);
+  L.st = take(static_cast<size_t>(max_batch) * sizeof(SentState));
+  L.y = take(rows_dec * 4);
+  L.tgt_m = take(static_cast<size_t>(max_batch) * 4);
+  L.src_len = take(static_cast<size_t>(max_batch) * 4);
+  L.n_rows = take(4);
+  L.total = off;
+  return L;
+}
+
+}  // namespace
+
+struct pd_ctx {
+  const pd_model* M;
+  int max_batch, max_src, max_tgt;
+  char* ws;
+  Layout L;
+  int* host_pinned;       // [0]: done word (device-written); [1 .. ]: staging for lengths
+  int* host_done_dev;     // device view of host_pinned[0]
+  int* stage_src;         // pinned staging copies of host length arrays
+  int* stage_tgt;
+  hipEvent_t stage_ev;
+  std::vector<hipEvent_t> it_ev;
+  int enc_B = 0, enc_nmax = 0;
+  bool encoded = false;
+
+  template <typename T> T* at(size_t off) const { return reinterpret_cast<T*>(ws + off); }
+};
+
+namespace {
+
+int row_tile_for(int R_max) {
+  if (R_max <= 1) return 1;
+  if (R_max <= 2) return 2;
+  if (R_max <= 4) return 4;
+  return 8;
+}
+
+int gemm_grid(int N) {
+  const int groups = (N + 3) / 4;
+  return std::max(1, std::min((groups + 3) / 4, kMaxGemmWGs));
+}
+
+// Rows processed by one pass: count (device or host), layout and tokens.
+struct Rows {
+  const int* n_dev;
+  int n_host;
+  RowMap map;
+  const int* tok;
+  int R_max;
+};
+
+GemmArgs gemm_base(const Rows& r) {
+  GemmArgs g;
+  std::memset(&g, 0, sizeof(g));
+  g.n_rows_dev = r.n_dev;
+  g.n_rows = r.n_host;
+  g.rows = r.map;
+  return g;
+}
+
+// One matrix product.  pro_ln: normalise x (float if x_f32) with (lg, lb)
+// first; for many rows the LayerNorm runs as its own kernel into ln_tmp.
+hipError_t run_gemm(const pd_ctx& C, const Rows& r, GemmArgs g, int epi, bool pro_ln, void* ln_tmp,
+                    int grid, hipStream_t s) {
+  const pd_model& M = *C.M;
+  int pro = PRO_NONE;
+  if (pro_ln) {
+    if (r.R_max <= kFuseLnMaxRows) {
+      pro = PRO_LN;
+    } else {
+      LnArgs la{r.n_dev, r.n_host, g.x, g.x_f32, g.ln_g, g.ln_b, M.cfg.ln_eps, g.K, ln_tmp};
+      hipError_t e = launch_ln(M.dt, la, r.R_max, s);
+      if (e != hipSuccess) return e;
+      g.x = ln_tmp;
+      g.x_f32 = 0;
+      g.ldx = g.K;
+      g.ln_out = nullptr;
+    }
+  }
+  return launch_gemm(M.dt, pro, epi, row_tile_for(r.R_max), g, grid, s);
+}
+
+// Decoder pass over the rows of one iteration (or the teacher-forced rows of
+// pd_debug_logits), ending in the fused vocabulary argmax or a logits store.
+hipError_t decoder_pass(pd_ctx& C, const Rows& r, float* logits, hipStream_t s) {
+  const pd_model& M = *C.M;
+  const pd_config& cfg = M.cfg;
+  const int d = M.d;
+  const bool pre = cfg.pre_ln != 0;
+  void* x_res = C.at<char>(C.L.x_res);
+  float* s_buf = C.at<float>(C.L.s_buf);
+  float* q_buf = C.at<float>(C.L.q_buf);
+  void* a_buf = C.at<char>(C.L.a_buf);
+  void* h_buf = C.at<char>(C.L.h_buf);
+  const size_t es = M.dt == DT_BF16 ? 2 : 4;
+  const size_t self_layer = static_cast<size_t>(C.max_batch) * C.max_tgt * d * es;
+  const size_t cross_layer = static_cast<size_t>(C.max_batch) * C.max_src * d * es;
+  hipError_t e;
+
+  EmbedArgs ea{r.n_dev, r.n_host, r.tok, r.map, M.w[0], M.dec_scale, d, M.V, x_res};
+  if ((e = launch_embed(M.dt, ea, r.R_max, s)) != hipSuccess) return e;
+
+  for (int l = 0; l < cfg.n_dec; ++l) {
+    // self-attention: Q -> q_buf, K/V of the block -> cache (layer l)
+    GemmArgs g = gemm_base(r);
+    if (pre) {
+      g.x = x_res; g.x_f32 = 0; g.ln_g = M.dec(l, D_LN1G); g.ln_b = M.dec(l, D_LN1B);
+    } else if (l > 0) {
+      g.x = s_buf; g.x_f32 = 1; g.ln_g = M.dec(l - 1, D_LN3G); g.ln_b = M.dec(l - 1, D_LN3B);
+      g.ln_out = x_res; g.ldlo = d;
+    } else {
+      g.x = x_res; g.x_f32 = 0;
+    }
+    const bool ln_qkv = pre || l > 0;
+    g.ldx = d; g.ln_eps = cfg.ln_eps;
+    g.w = M.dec(l, D_WQKV); g.bias = M.dec(l, D_BQKV); g.N = 3 * d; g.K = d;
+    g.out_f32 = q_buf; g.ldo = d; g.q_cols = d;
+    g.kc = C.at<char>(C.L.self_k) + l * self_layer; g.vc = C.at<char>(C.L.self_v) + l * self_layer;
+    g.H = M.H; g.dh = M.dh; g.T = C.max_tgt; g.d = d;
+    // post-LN with a separate LayerNorm kernel writes the residual stream itself
+    if ((e = run_gemm(C, r, g, EPI_QKV, ln_qkv, pre ? a_buf : x_res, gemm_grid(3 * d), s)) != hipSuccess) return e;
+
+    AttnArgs aa{r.n_dev, r.n_host, q_buf, d, g.kc, g.vc, M.H, M.dh, C.max_tgt, r.map, 1, nullptr,
+                a_buf, d, 1.0f / std::sqrt(static_cast<float>(M.dh))};
+    if ((e = launch_attn(M.dt, aa, r.R_max, s)) != hipSuccess) return e;
+
+    g = gemm_base(r);
+    g.x = a_buf; g.ldx = d; g.w = M.dec(l, D_WO); g.bias = M.dec(l, D_BO); g.N = d; g.K = d;
+    g.resid = x_res; g.ldr = d; g.ldo = d;
+    if (pre) g.out = x_res; else g.out_f32 = s_buf;
+    if ((e = run_gemm(C, r, g, EPI_RESID, false, nullptr, gemm_grid(d), s)) != hipSuccess) return e;
+
+    // cross-attention to the encoder memory
+    g = gemm_base(r);
+    if (pre) { g.x = x_res; g.x_f32 = 0; g.ln_g = M.dec(l, D_LN2G); g.ln_b = M.dec(l, D_LN2B); }
+    else { g.x = s_buf; g.x_f32 = 1; g.ln_g = M.dec(l, D_LN1G); g.ln_b = M.dec(l, D_LN1B); g.ln_out = x_res; g.ldlo = d; }
+    g.ldx = d; g.ln_eps = cfg.ln_eps;
+    g.w = M.dec(l, D_CWQ); g.bias = M.dec(l, D_CBQ); g.N = d; g.K = d; g.out_f32 = q_buf; g.ldo = d;
+    if ((e = run_gemm(C, r, g, EPI_F32, true, pre ? a_buf : x_res, gemm_grid(d), s)) != hipSuccess) return e;
+
+    aa = AttnArgs{r.n_dev, r.n_host, q_buf, d, C.at<char>(C.L.cross_k) + l * cross_layer,
+                  C.at<char>(C.L.cross_v) + l * cross_layer, M.H, M.dh, C.max_src, r.map, 0,
+                  C.at<int>(C.L.src_len), a_buf, d, 1.0f / std::sqrt(static_cast<float>(M.dh))};
+    if ((e = launch_attn(M.dt, aa, r.R_max, s)) != hipSuccess) return e;
+
+    g = gemm_base(r);
+    g.x = a_buf; g.ldx = d; g.w = M.dec(l, D_CWO); g.bias = M.dec(l, D_CBO); g.N = d; g.K = d;
+    g.resid = x_res; g.ldr = d; g.ldo = d;
+    if (pre) g.out = x_res; else g.out_f32 = s_buf;
+    if ((e = run_gemm(C, r, g, EPI_RESID, false, nullptr, gemm_grid(d), s)) != hipSuccess) return e;
+
+    // feed-forward
+    g = gemm_base(r);
+    if (pre) { g.x = x_res; g.x_f32 = 0; g.ln_g = M.dec(l, D_LN3G); g.ln_b = M.dec(l, D_LN3B); }
+    else { g.x = s_buf; g.x_f32 = 1; g.ln_g = M.dec(l, D_LN2G); g.ln_b = M.dec(l, D_LN2B); g.ln_out = x_res; g.ldlo = d; }
+    g.ldx = d; g.ln_eps = cfg.ln_eps;
+    g.w = M.dec(l, D_W1); g.bias = M.dec(l, D_B1); g.N = M.dff; g.K = d;
+    g.out = h_buf; g.ldo = M.dff; g.act = cfg.act_gelu ? 2 : 1;
+    if ((e = run_gemm(C, r, g, EPI_ACT, true, pre ? a_buf : x_res, gemm_grid(M.dff), s)) != hipSuccess) return e;
+
+    g = gemm_base(r);
+    g.x = h_buf; g.ldx = M.dff; g.w = M.dec(l, D_W2); g.bias = M.dec(l, D_B2); g.N = d; g.K = M.dff;
+    g.resid = x_res; g.ldr = d; g.ldo = d;
+    if (pre) g.out = x_res; else g.out_f32 = s_buf;
+    if ((e = run_gemm(C, r, g, EPI_RESID, false, nullptr, gemm_grid(d), s)) != hipSuccess) return e;
+  }
+
+  // vocabulary projection (tied embedding) fused with the argmax
+  GemmArgs g = gemm_base(r);
+  if (pre) { g.x = x_res; g.x_f32 = 0; g.ln_g = M.dec_ln(0); g.ln_b = M.dec_ln(1); }
+  else { g.x = s_buf; g.x_f32 = 1; g.ln_g = M.dec(cfg.n_dec - 1, D_LN3G); g.ln_b = M.dec(cfg.n_dec - 1, D_LN3B); }
+  g.ldx = d; g.ln_eps = cfg.ln_eps;
+  g.w = M.w[0]; g.bias = M.w[1]; g.N = M.V; g.K = d; g.logit_scale = cfg.logit_scale;
+  if (logits != nullptr) {
+    g.out_f32 = logits; g.ldo = M.V;
+    return run_gemm(C, r, g, EPI_LOGITS, true, a_buf, gemm_grid(M.V), s);
+  }
+  g.partials = C.at<uint2>(C.L.partials);
+  g.part_ld = kVocabWGs;
+  if ((e = run_gemm(C, r, g, EPI_ARGMAX, true, a_buf, kVocabWGs, s)) != hipSuccess) return e;
+  ReduceArgs ra{r.n_dev, C.at<uint2>(C.L.partials), kVocabWGs, kVocabWGs, C.at<int>(C.L.new_tok),
+                C.at<int>(C.L.row_flags)};
+  return launch_argmax_reduce(ra, r.R_max, s);
+}
+
+hipError_t encoder_pass(pd_ctx& C, const int32_t* src, int B, int n_max, hipStream_t s) {
+  const pd_model& M = *C.M;
+  const pd_config& cfg = M.cfg;
+  const int d = M.d;
+  const bool pre = cfg.pre_ln != 0;
+  void* x_res = C.at<char>(C.L.x_res);
+  float* s_buf = C.at<float>(C.L.s_buf);
+  float* q_buf = C.at<float>(C.L.q_buf);
+  void* a_buf = C.at<char>(C.L.a_buf);
+  void* h_buf = C.at<char>(C.L.h_buf);
+  const size_t es = M.dt == DT_BF16 ? 2 : 4;
+  const size_t cross_layer = static_cast<size_t>(C.max_batch) * C.max_src * d * es;
+  const int R = B * n_max;
+  Rows r{nullptr, R, RowMap{nullptr, nullptr, n_max}, src, R};
+  const int* klen = C.at<int>(C.L.src_len);
+  const float scale = 1.0f / std::sqrt(static_cast<float>(M.dh));
+  hipError_t e;
+
+  EmbedArgs ea{nullptr, R, src, r.map, M.w[0], M.enc_scale, d, M.V, x_res};
+  if ((e = launch_embed(M.dt, ea, R, s)) != hipSuccess) return e;
+  for (int l = 0; l < cfg.n_enc; ++l) {
+    const void* in = x_res;
+    if (pre) {
+      LnArgs la{nullptr, R, x_res, 0, M.enc(l, E_LN1G), M.enc(l, E_LN1B), cfg.ln_eps, d, a_buf};
+      if ((e = launch_ln(M.dt, la, R, s)) != hipSuccess) return e;
+      in = a_buf;
+    }
+    GemmArgs g = gemm_base(r);
+    g.x = in; g.ldx = d; g.w = M.enc(l, E_WQKV); g.bias = M.enc(l, E_BQKV); g.N = 3 * d; g.K = d;
+    g.out_f32 = q_buf; g.ldo = d; g.q_cols = d;
+    g.kc = C.at<char>(C.L.enc_k); g.vc = C.at<char>(C.L.enc_v);
+    g.H = M.H; g.dh = M.dh; g.T = C.max_src; g.d = d;
+    if ((e = launch_gemm(M.dt, PRO_NONE, EPI_QKV, 8, g, gemm_grid(3 * d), s)) != hipSuccess) return e;
+    AttnArgs aa{nullptr, R, q_buf, d, g.kc, g.vc, M.H, M.dh, C.max_src, r.map, 0, klen, a_buf, d, scale};
+    if ((e = launch_attn(M.dt, aa, R, s)) != hipSuccess) return e;
+    g = gemm_base(r);
+    g.x = a_buf; g.ldx = d; g.w = M.enc(l, E_WO); g.bias = M.enc(l, E_BO); g.N = d; g.K = d;
+    g.resid = x_res; g.ldr = d; g.ldo = d;
+    if (pre) g.out = x_res; else g.out_f32 = s_buf;
+    if ((e = launch_gemm(M.dt, PRO_NONE, EPI_RESID, 8, g, gemm_grid(d), s)) != hipSuccess) return e;
+    if (!pre) {
+      LnArgs la{nullptr, R, s_buf, 1, M.enc(l, E_LN1G), M.enc(l, E_LN1B), cfg.ln_eps, d, x_res};
+      if ((e = launch_ln(M.dt, la, R, s)) != hipSuccess) return e;
+    }
+    in = x_res;
+    if (pre) {
+      LnArgs la{nullptr, R, x_res, 0, M.enc(l, E_LN2G), M.enc(l, E_LN2B), cfg.ln_eps, d, a_buf};
+      if ((e = launch_ln(M.dt, la, R, s)) != hipSuccess) return e;
+      in = a_buf;
+    }
+    g = gemm_base(r);
+    g.x = in; g.ldx = d; g.w = M.enc(l, E_W1); g.bias = M.enc(l, E_B1); g.N = M.dff; g.K = d;
+    g.out = h_buf; g.ldo = M.dff; g.act = cfg.act_gelu ? 2 : 1;
+    if ((e = launch_gemm(M.dt, PRO_NONE, EPI_ACT, 8, g, gemm_grid(M.dff), s)) != hipSuccess) return e;
+    g = gemm_base(r);
+    g.x = h_buf; g.ldx = M.dff; g.w = M.enc(l, E_W2); g.bias = M.enc(l, E_B2); g.N = d; g.K = M.dff;
+    g.resid = x_res; g.ldr = d; g.ldo = d;
+    if (pre) g.out = x_res; else g.out_f32 = s_buf;
+    if ((e = launch_gemm(M.dt, PRO_NONE, EPI_RESID, 8, g, gemm_grid(d), s)) != hipSuccess) return e;
+    if (!pre) {
+      LnArgs la{nullptr, R, s_buf, 1, M.enc(l, E_LN2G), M.enc(l, E_LN2B), cfg.ln_eps, d, x_res};
+      if ((e = launch_ln(M.dt, la, R, s)) != hipSuccess) return e;
+    }
+  }
+  const void* mem = x_res;
+  if (pre) {
+    LnArgs la{nullptr, R, x_res, 0, M.enc_ln(0), M.enc_ln(1), cfg.ln_eps, d, a_buf};
+    if ((e = launch_ln(M.dt, la, R, s)) != hipSuccess) return e;
+    mem = a_buf;
+  }
+  for (int l = 0; l < cfg.n_dec; ++l) {
+    GemmArgs g = gemm_base(r);
+    g.x = mem; g.ldx = d; g.w = M.dec(l, D_CWKV); g.bias = M.dec(l, D_CBKV); g.N = 2 * d; g.K = d;
+    g.q_cols = 0;
+    g.kc = C.at<char>(C.L.cross_k) + l * cross_layer; g.vc = C.at<char>(C.L.cross_v) + l * cross_layer;
+    g.H = M.H; g.dh = M.dh; g.T = C.max_src; g.d = d;
+    if ((e = launch_gemm(M.dt, PRO_NONE, EPI_QKV, 8, g, gemm_grid(2 * d), s)) != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+pd_status stage_lengths(pd_ctx* C, int* stage, const int32_t* host, int B, int* dev, hipStream_t s) {
+  PD_HIP(hipEventSynchronize(C->stage_ev));      // previous copy out of the staging area is done
+  std::memcpy(stage, host, sizeof(int32_t) * B);
+  PD_HIP(hipMemcpyAsync(dev, stage, sizeof(int32_t) * B, hipMemcpyHostToDevice, s));
+  PD_HIP(hipEventRecord(C->stage_ev, s));
+  return PD_OK;
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+}  // namespace
+
+extern "C" {
+
+const char* pd_last_error(void) { return g_err.c_str(); }
+
+int32_t pd_weight_count(const pd_config* cfg) {
+  std::string why;
+  if (!check_config(cfg, &why)) return -1;
+  return weight_count(*cfg);
+}
+
+pd_status pd_weight_shape(const pd_config* cfg, int32_t idx, int64_t* rows, int64_t* cols) {
+  std::string why;
+  if (!check_config(cfg, &why)) return fail(PD_E_ARG, why);
+  if (rows == nullptr || cols == nullptr) return fail(PD_E_ARG, "null output pointer");
+  if (idx < 0 || idx >= weight_count(*cfg)) return fail(PD_E_ARG, "weight index out of range");
+  shape_of(*cfg, idx, rows, cols);
+  return PD_OK;
+}
+
+pd_status pd_model_create(const pd_config* cfg, const void* const* dev_weights, int32_t n_weights,
+                          pd_model** out) {
+  std::string why;
+  if (out == nullptr) return fail(PD_E_ARG, "null output pointer");
+  *out = nullptr;
+  if (!check_config(cfg, &why)) return fail(PD_E_UNSUPPORTED, why);
+  if (dev_weights == nullptr) return fail(PD_E_ARG, "null weight array");
+  const int n = weight_count(*cfg);
+  if (n_weights != n) return fail(PD_E_ARG, "expected " + std::to_string(n) + " weights, got " + std::to_string(n_weights));
+  for (int i = 0; i < n; ++i)
+    if (dev_weights[i] == nullptr || !aligned(dev_weights[i], 16))
+      return fail(PD_E_ARG, "weight " + std::to_string(i) + " is null or not 16-byte aligned");
+  pd_model* m = new pd_model();
+  m->cfg = *cfg;
+  m->w.assign(dev_weights, dev_weights + n);
+  m->dt = cfg->dtype == PD_BF16 ? DT_BF16 : DT_F32;
+  m->d = cfg->d_model;
+  m->H = cfg->n_heads;
+  m->dh = cfg->d_model / cfg->n_heads;
+  m->dff = cfg->d_ff;
+  m->V = cfg->vocab;
+  const float sq = std::sqrt(static_cast<float>(cfg->d_model));
+  m->enc_scale = cfg->enc_emb_scale < 0.f ? sq : cfg->enc_emb_scale;
+  m->dec_scale = cfg->dec_emb_scale < 0.f ? sq : cfg->dec_emb_scale;
+  *out = m;
+  return PD_OK;
+}
+
+void pd_model_destroy(pd_model* model) { delete model; }
+
+pd_status pd_ctx_workspace_bytes(const pd_model* model, int32_t max_batch, int32_t max_src, int32_t max_tgt,
+                                 size_t* bytes) {
+  if (model == nullptr || bytes == nullptr) return fail(PD_E_ARG, "null argument");
+  if (max_batch < 1 || max_src < 1 || max_tgt < 1) return fail(PD_E_SHAPE, "limits must be positive");
+  if (max_tgt > 1024 || max_src > 1024) return fail(PD_E_SHAPE, "max_src and max_tgt must be <= 1024");
+  *bytes = plan(*model, max_batch, max_src, max_tgt).total;
+  return PD_OK;
+}
+
+pd_status pd_ctx_create(const pd_model* model, int32_t max_batch, int32_t max_src, int32_t max_tgt,
+                        void* dev_workspace, size_t workspace_bytes, pd_ctx** out) {
+  if (out == nullptr || model == nullptr) return fail(PD_E_ARG, "null argument");
+  *out = nullptr;
+  size_t need = 0;
+  pd_status st = pd_ctx_workspace_bytes(model, max_batch, max_src, max_tgt, &need);
+  if (st != PD_OK) return st;
+  if (dev_workspace == nullptr || !aligned(dev_workspace, kAlign))
+    return fail(PD_E_WORKSPACE, "workspace is null or not 256-byte aligned");
+  if (workspace_bytes < need)
+    return fail(PD_E_WORKSPACE, "workspace too small: need " + std::to_string(need) + " bytes");
+  pd_ctx* c = new pd_ctx();
+  c->M = model;
+  c->max_batch = max_batch;
+  c->max_src = max_src;
+  c->max_tgt = max_tgt;
+  c->ws = static_cast<char*>(dev_workspace);
+  c->L = plan(*model, max_batch, max_src, max_tgt);
+  hipError_t e = hipHostMalloc(reinterpret_cast<void**>(&c->host_pinned), sizeof(int) * (1 + 2 * max_batch),
+                               hipHostMallocMapped);
+  if (e != hipSuccess) { delete c; return fail(PD_E_DEVICE, std::string("hipHostMalloc: ") + hipGetErrorString(e)); }
+  c->host_pinned[0] = 0;
+  e = hipHostGetDevicePointer(reinterpret_cast<void**>(&c->host_done_dev), c->host_pinned, 0);
+  if (e != hipSuccess) {
+    hipHostFree(c->host_pinned);
+    delete c;
+    return fail(PD_E_DEVICE, std::string("hipHostGetDevicePointer: ") + hipGetErrorString(e));
+  }
+  c->stage_src = c->host_pinned + 1;
+  c->stage_tgt = c->host_pinned + 1 + max_batch;
+  hipEventCreateWithFlags(&c->stage_ev, hipEventDisableTiming);
+  c->it_ev.resize(2);
+  for (auto& ev : c->it_ev) hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+  *out = c;
+  return PD_OK;
+}
+
+void pd_ctx_destroy(pd_ctx* ctx) {
+  if (ctx == nullptr) return;
+  hipEventSynchronize(ctx->stage_ev);
+  for (auto ev : ctx->it_ev) { hipEventSynchronize(ev); hipEventDestroy(ev); }
+  hipEventDestroy(ctx->stage_ev);
+  hipHostFree(ctx->host_pinned);
+  delete ctx;
+}
+
+pd_status pd_encode(pd_ctx* ctx, const int32_t* src_ids, const int32_t* src_len, int32_t B, int32_t n_max,
+                    void* stream) {
+  if (ctx == nullptr || src_ids == nullptr || src_len == nullptr) return fail(PD_E_ARG, "null argument");
+  if (B < 1 || n_max < 1) return fail(PD_E_ARG, "B and n_max must be >= 1");
+  if (B > ctx->max_batch || n_max > ctx->max_src) return fail(PD_E_SHAPE, "batch or source length exceeds the context limits");
+  for (int b = 0; b < B; ++b)
+    if (src_len[b] < 1 || src_len[b] > n_max) return fail(PD_E_ARG, "src_len[" + std::to_string(b) + "] out of [1, n_max]");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  ctx->encoded = false;
+  pd_status st = stage_lengths(ctx, ctx->stage_src, src_len, B, ctx->at<int>(ctx->L.src_len), s);
+  if (st != PD_OK) return st;
+  hipError_t e = encoder_pass(*ctx, src_ids, B, n_max, s);
+  if (e != hipSuccess) return fail(PD_E_DEVICE, std::string("encoder launch: ") + hipGetErrorString(e));
+  ctx->enc_B = B;
+  ctx->enc_nmax = n_max;
+  ctx->encoded = true;
+  return PD_OK;
+}
+
+pd_status pd_decode(pd_ctx* ctx, int32_t mode, int32_t block, int32_t horizon, int32_t max_iters,
+                    const int32_t* tgt_m, int32_t* out_ids, int32_t out_ld, int32_t* out_len,
+                    int32_t* out_k, int32_t* out_flags, void* stream) {
+  if (ctx == nullptr || tgt_m == nullptr || out_ids == nullptr || out_len == nullptr || out_k == nullptr ||
+      out_flags == nullptr)
+    return fail(PD_E_ARG, "null argument");
+  if (!ctx->encoded) return fail(PD_E_STATE, "pd_decode called before pd_encode");
+  if (mode < PD_AR || mode > PD_HYBRID) return fail(PD_E_ARG, "unknown mode");
+  if ((mode == PD_GS_JACOBI || mode == PD_HYBRID) && block < 1) return fail(PD_E_ARG, "block must be >= 1");
+  const int B = ctx->enc_B;
+  int m_max = 0;
+  for (int b = 0; b < B; ++b) {
+    if (tgt_m[b] < 1 || tgt_m[b] > ctx->max_tgt)
+      return fail(PD_E_SHAPE, "tgt_m[" + std::to_string(b) + "] out of [1, max_tgt]");
+    m_max = std::max(m_max, tgt_m[b]);
+  }
+  if (out_ld < m_max) return fail(PD_E_ARG, "out_ld must be >= max(tgt_m)");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  pd_ctx& C = *ctx;
+  const pd_model& M = *C.M;
+  pd_status st = stage_lengths(ctx, C.stage_tgt, tgt_m, B, C.at<int>(C.L.tgt_m), s);
+  if (st != PD_OK) return st;
+
+  int Lmax = 1;
+  if (mode == PD_JACOBI) Lmax = m_max;
+  else if (mode == PD_GS_JACOBI || mode == PD_HYBRID) Lmax = std::min(block, m_max);
+  const int R_max = B * Lmax;
+  int iters = m_max;
+  if (max_iters > 0) iters = std::min(iters, max_iters);
+
+  CtrlArgs ca;
+  std::memset(&ca, 0, sizeof(ca));
+  ca.st = C.at<SentState>(C.L.st);
+  ca.B = B;
+  ca.mode = mode;
+  ca.block = std::max(block, 1);
+  ca.horizon = horizon;
+  ca.max_iters = max_iters;
+  ca.tgt_m = C.at<int>(C.L.tgt_m);
+  ca.y = C.at<int>(C.L.y);
+  ca.ldy = C.max_tgt;
+  ca.new_tok = C.at<int>(C.L.new_tok);
+  ca.row_flags = C.at<int>(C.L.row_flags);
+  ca.row_sent = C.at<int>(C.L.row_sent);
+  ca.row_pos = C.at<int>(C.L.row_pos);
+  ca.row_tok = C.at<int>(C.L.row_tok);
+  ca.n_rows = C.at<int>(C.L.n_rows);
+  ca.host_done = C.host_done_dev;
+  ca.pad_id = M.cfg.pad_id;
+  ca.bos_id = M.cfg.bos_id;
+  ca.eos_id = M.cfg.eos_id;
+  ca.R_max = R_max;
+  ca.out_ids = out_ids;
+  ca.out_ld = out_ld;
+  ca.out_len = out_len;
+  ca.out_k = out_k;
+  ca.out_flags = out_flags;
+
+  Rows r{ca.n_rows, 0, RowMap{ca.row_sent, ca.row_pos, 0}, ca.row_tok, R_max};
+  hipError_t e = launch_ctrl_init(ca, s);
+  if (e != hipSuccess) return fail(PD_E_DEVICE, std::string("init launch: ") + hipGetErrorString(e));
+  volatile int* done = C.host_pinned;
+  for (int it = 0; it < iters; ++it) {
+    e = decoder_pass(C, r, nullptr, s);
+    if (e == hipSuccess) e = launch_ctrl_step(ca, s);
+    if (e == hipSuccess) e = hipEventRecord(C.it_ev[it & 1], s);
+    if (e != hipSuccess) return fail(PD_E_DEVICE, std::string("iteration launch: ") + hipGetErrorString(e));
+    if (it >= 1) {
+      // the previous iteration has finished when its event completes; its
+      // control step has published whether every sentence is done
+      hipEvent_t ev = C.it_ev[(it - 1) & 1];
+      while ((e = hipEventQuery(ev)) == hipErrorNotReady) {
+      }
+      if (e != hipSuccess) return fail(PD_E_DEVICE, std::string("iteration: ") + hipGetErrorString(e));
+      if (*done) break;
+    }
+  }
+  e = launch_finalize(ca, s);
+  if (e != hipSuccess) return fail(PD_E_DEVICE, std::string("finalize launch: ") + hipGetErrorString(e));
+  return PD_OK;
+}
+
+pd_status pd_debug_logits(pd_ctx* ctx, const int32_t* tgt_in, int32_t T, float* logits, void* stream) {
+  if (ctx == nullptr || tgt_in == nullptr || logits == nullptr) return fail(PD_E_ARG, "null argument");
+  if (!ctx->encoded) return fail(PD_E_STATE, "pd_debug_logits called before pd_encode");
+  if (T < 1 || T > ctx->max_tgt) return fail(PD_E_SHAPE, "T out of [1, max_tgt]");
+  const int B = ctx->enc_B;
+  const int R = B * T;
+  Rows r{nullptr, R, RowMap{nullptr, nullptr, T}, tgt_in, R};
+  hipError_t e = decoder_pass(*ctx, r, logits, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(PD_E_DEVICE, std::string("decoder launch: ") + hipGetErrorString(e));
+  return PD_OK;
+}
+
+}  // extern "C"

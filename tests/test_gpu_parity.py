@@ -1,0 +1,245 @@
+"""Parity of the HIP decoding path (through the C ABI) with the CPU oracle.
+
+Every test is marked gpu: it needs an MI355X and the built libpdec.so.  The
+oracle (oracle/) provides every expected value; nothing expected comes from
+the GPU path itself."""
+import dataclasses
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2305_10427_amd import configs as C, pdec, synth
+from tests.parity import TOL, classify, gpu_decode_batch, summarize
+
+pytestmark = pytest.mark.gpu
+
+TINY = C.TINY
+CHAIN = dataclasses.replace(C.TINY, name="chain", logit_scale=-3.0)
+SMALL_PRE_BF16 = dataclasses.replace(C.TINY, name="small_pre", pre_ln=True, act_gelu=True, dtype=C.BF16)
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+def build(cfg, seed=0, max_batch=4, max_src=32, max_tgt=32, **wkw):
+    w = synth.make_weights(cfg, seed=seed, **wkw)
+    gm = pdec.Model(cfg, w)
+    ctx = pdec.Context(gm, max_batch, max_src, max_tgt)
+    return w, gm, ctx, oracle.Model(cfg, w.values)
+
+
+def sources(vocab, count, n=16, seed=1):
+    g = np.random.default_rng(seed)
+    return [g.integers(4, vocab, n).astype(np.int32) for _ in range(count)]
+
+
+def run_modes(cfg, ctx, M, srcs, m, modes, tol):
+    labels = []
+    for src in srcs:
+        enc = M.encode(src)
+        greedy = oracle.greedy(M, enc, m)
+        for mode, b in modes:
+            say(f"case cfg={cfg.name} mode={mode} b={b} m={m} n={len(src)}")
+            want = oracle.decode(M, enc, m, mode, b)
+            g = gpu_decode_batch(ctx, [src], [m], mode, b)[0]
+            lab = classify(g, want, greedy, tol)
+            assert not lab.startswith("FAIL"), f"{mode} b={b}: {lab}"
+            assert g.k <= m
+            labels.append(lab)
+    return labels
+
+
+@pytest.mark.parametrize("cfg,wkw", [(TINY, {}), (TINY, dict(bias_std=0.5, ln_std=0.3)),
+                                     (CHAIN, dict(bias_std=0.5, ln_std=0.3)),
+                                     (SMALL_PRE_BF16, dict(bias_std=0.3, ln_std=0.2))],
+                         ids=["tiny", "tiny_bias", "chain", "small_pre_bf16"])
+def test_all_modes_match_oracle_small(cfg, wkw):
+    _, _, ctx, M = build(cfg, seed=3, **wkw)
+    modes = [("ar", 1), ("jacobi", 0), ("gs_jacobi", 4), ("hybrid", 4), ("gs_jacobi", 3), ("hybrid", 1)]
+    labels = []
+    for m in (1, 5, 16):
+        labels += run_modes(cfg, ctx, M, sources(cfg.vocab, 4, seed=11), m, modes, TOL[cfg.dtype])
+    s = summarize(labels)
+    say("summary", cfg.name, s)
+    assert s["exact"] >= 0.9 * len(labels)
+
+
+def test_parallel_modes_equal_gpu_greedy_bitwise():
+    """All modes evaluate the same map on the GPU, so they agree with GPU greedy exactly."""
+    _, _, ctx, _ = build(CHAIN, seed=1, bias_std=0.5, ln_std=0.3)
+    for src in sources(CHAIN.vocab, 6, seed=5):
+        ar = gpu_decode_batch(ctx, [src], [16], "ar")[0]
+        for mode, b in [("jacobi", 0), ("gs_jacobi", 2), ("gs_jacobi", 5), ("hybrid", 3)]:
+            say(f"case chain mode={mode} b={b}")
+            g = gpu_decode_batch(ctx, [src], [16], mode, b)[0]
+            np.testing.assert_array_equal(g.ids, ar.ids)
+
+
+def test_context_free_decoder_closed_form_k():
+    cfg = dataclasses.replace(TINY, dec_emb_scale=0.0)
+    _, _, ctx, M = build(cfg, seed=4, bias_std=0.3)
+    for src in sources(cfg.vocab, 3, seed=5):
+        for m in (2, 5, 16):
+            ref = oracle.greedy(M, M.encode(src), m, stop_at_eos=False).y
+            if np.any(ref == C.PAD_ID) or np.any(ref == C.EOS_ID):
+                continue
+            say(f"case context-free m={m}")
+            assert gpu_decode_batch(ctx, [src], [m], "jacobi")[0].k == min(2, m)
+            for b in (1, 2, 3, 4):
+                want = sum(min(2, min(b, m - i)) for i in range(0, m, b))
+                assert gpu_decode_batch(ctx, [src], [m], "gs_jacobi", b)[0].k == want
+
+
+def test_hybrid_eos_fixtures():
+    from tests.test_oracle_decode import eos_cases
+    for cfg, seed in [(TINY, 8), (CHAIN, 9)]:
+        wkw = dict(bias_std=0.5, ln_std=0.3)
+        for b in (3, 4):
+            found = eos_cases(cfg, seed, wkw, b)
+            for kind, (B, src, q) in found.items():
+                say(f"case eos cfg={cfg.name} b={b} kind={kind} q={q}")
+                _, _, ctx, M = build(cfg, seed=seed, eos_bias=B, **wkw)
+                enc = M.encode(src)
+                greedy = oracle.greedy(M, enc, 16)
+                for mode, bb in [("ar", 1), ("hybrid", b), ("gs_jacobi", b)]:
+                    want = oracle.decode(M, enc, 16, mode, bb)
+                    g = gpu_decode_batch(ctx, [src], [16], mode, bb)[0]
+                    lab = classify(g, want, greedy, TOL[cfg.dtype])
+                    assert not lab.startswith("FAIL"), f"{kind} {mode}: {lab}"
+                    if mode != "gs_jacobi" and kind != "absent" and lab == "exact":
+                        assert g.flags & pdec.FLAG_EOS
+
+
+@pytest.mark.parametrize("cfg", [TINY, SMALL_PRE_BF16], ids=["tiny_f32", "small_pre_bf16"])
+def test_teacher_forced_logits_within_tolerance(cfg):
+    import torch
+    _, _, ctx, M = build(cfg, seed=6, max_tgt=96, bias_std=0.3, ln_std=0.2)
+    srcs = sources(cfg.vocab, 2, n=13, seed=2)
+    tgt = np.concatenate([np.ones((2, 1), np.int32),
+                          np.random.default_rng(3).integers(0, cfg.vocab, (2, 11)).astype(np.int32)], 1)
+    src = np.stack(srcs)
+    ctx.encode(torch.from_numpy(src).cuda(), [13, 13])
+    got = ctx.debug_logits(torch.from_numpy(tgt)).cpu().numpy()
+    for r in range(2):
+        ref = M.teacher_forced_logits(M.encode(srcs[r]), tgt[r])
+        rel = np.abs(got[r] - ref).max(-1) / np.abs(ref).max(-1)
+        say(f"case logits cfg={cfg.name} max rel err {rel.max():.3g}")
+        assert rel.max() < TOL[cfg.dtype]
+
+
+@pytest.mark.parametrize("cfg", [TINY, SMALL_PRE_BF16], ids=["tiny_f32", "small_pre_bf16"])
+def test_rows_are_invariant_to_block_and_batch(cfg):
+    """A row's logits are bitwise the same whatever else is in the call: fewer
+    or more positions (row tiles, fused or separate LayerNorm) and batch mates."""
+    import torch
+    _, _, ctx, _ = build(cfg, seed=7, max_batch=3, max_tgt=96, bias_std=0.3, ln_std=0.2)
+    srcs = sources(cfg.vocab, 3, n=10, seed=4)
+    g = np.random.default_rng(9)
+    tgt = np.concatenate([np.ones((3, 1), np.int32), g.integers(0, cfg.vocab, (3, 89)).astype(np.int32)], 1)
+    ctx.encode(torch.from_numpy(np.stack(srcs)).cuda(), [10, 10, 10])
+    full = ctx.debug_logits(torch.from_numpy(tgt)).cpu().numpy()           # 3 x 90 rows (> 64: separate LN)
+    for T in (1, 3, 8):
+        say(f"case row-invariance T={T}")
+        part = ctx.debug_logits(torch.from_numpy(np.ascontiguousarray(tgt[:, :T]))).cpu().numpy()
+        np.testing.assert_array_equal(part, full[:, :T])
+    ctx.encode(torch.from_numpy(np.stack(srcs[1:2])).cuda(), [10])
+    alone = ctx.debug_logits(torch.from_numpy(np.ascontiguousarray(tgt[1:2, :8]))).cpu().numpy()
+    np.testing.assert_array_equal(alone[0], full[1, :8])
+
+
+def test_batched_sentences_equal_single_decodes():
+    _, _, ctx, M = build(TINY, seed=2, max_batch=4, bias_std=0.5, ln_std=0.3)
+    g = np.random.default_rng(21)
+    srcs = [g.integers(4, TINY.vocab, n).astype(np.int32) for n in (5, 16, 9, 12)]
+    ms = [3, 16, 7, 11]
+    for mode, b in [("ar", 1), ("jacobi", 0), ("gs_jacobi", 3), ("hybrid", 4)]:
+        say(f"case batch mode={mode} b={b}")
+        batch = gpu_decode_batch(ctx, srcs, ms, mode, b)
+        for r in range(4):
+            one = gpu_decode_batch(ctx, [srcs[r]], [ms[r]], mode, b)[0]
+            np.testing.assert_array_equal(batch[r].ids, one.ids)
+            assert batch[r].k == one.k
+            want = oracle.decode(M, M.encode(srcs[r]), ms[r], mode, b)
+            lab = classify(batch[r], want, oracle.greedy(M, M.encode(srcs[r]), ms[r]), TOL[C.F32])
+            assert not lab.startswith("FAIL"), lab
+
+
+def test_max_iters_and_horizon():
+    _, _, ctx, M = build(CHAIN, seed=1, bias_std=0.5, ln_std=0.3)
+    src = sources(CHAIN.vocab, 1, seed=3)[0]
+    enc = M.encode(src)
+    greedy = oracle.greedy(M, enc, 12)
+    for mode, b in [("ar", 1), ("jacobi", 0), ("gs_jacobi", 4), ("hybrid", 4)]:
+        say(f"case max_iters mode={mode}")
+        want = oracle.decode(M, enc, 12, mode, b, max_iters=3)
+        g = gpu_decode_batch(ctx, [src], [12], mode, b, max_iters=3)[0]
+        assert g.k == 3 and (g.flags & pdec.FLAG_MAX_ITERS)
+        n = len(want.out)
+        if mode == "ar":      # greedy stops early: compare the produced prefix
+            np.testing.assert_array_equal(g.ids[:n], want.out)
+        else:
+            np.testing.assert_array_equal(g.ids, want.out)
+    for h in (1, 4, 7, 12):
+        say(f"case horizon h={h}")
+        want = oracle.hybrid(M, enc, 12, 3, h=h)
+        g = gpu_decode_batch(ctx, [src], [12], "hybrid", 3, horizon=h)[0]
+        assert classify(g, want, greedy, TOL[C.F32]) == "exact"
+
+
+def test_error_paths_on_device():
+    import torch
+    w = synth.make_weights(TINY, 0)
+    gm = pdec.Model(TINY, w)
+    ctx = pdec.Context(gm, 2, 16, 16)
+    with pytest.raises(pdec.PdError) as e:
+        ctx.B = 1
+        ctx.decode("ar", [4])
+    assert e.value.status == 6                          # decode before encode
+    ctx.encode(torch.ones((1, 8), dtype=torch.int32).cuda() * 7, [8])
+    for kw, status in [(dict(mode=9, tgt_m=[4]), 1), (dict(mode="ar", tgt_m=[17]), 2),
+                       (dict(mode="gs_jacobi", tgt_m=[4], block=0), 1)]:
+        with pytest.raises(pdec.PdError) as e:
+            ctx.decode(**kw)
+        assert e.value.status == status
+    with pytest.raises(pdec.PdError) as e:
+        ctx.encode(torch.ones((3, 8), dtype=torch.int32).cuda(), [8, 8, 8])   # batch > max_batch
+    assert e.value.status == 2
+    with pytest.raises(pdec.PdError) as e:
+        ctx.encode(torch.ones((1, 8), dtype=torch.int32).cuda(), [9])         # length > n_max
+    assert e.value.status == 1
+
+
+def _full_size(wl_name, n_sent, m_cap, modes):
+    wl = C.WORKLOADS[wl_name]
+    cfg = wl.model
+    w = synth.make_weights(cfg, seed=0)
+    gm = pdec.Model(cfg, w)
+    ctx = pdec.Context(gm, 1, 128, wl.tgt_cap)
+    M = oracle.Model(cfg, w.values)
+    labels = []
+    for src, m in synth.make_sentences(wl, seed=1, count=n_sent):
+        m = min(m, m_cap)
+        enc = M.encode(src)
+        greedy = oracle.greedy(M, enc, m)
+        for mode, b in modes:
+            say(f"case {wl_name} mode={mode} b={b} n={len(src)} m={m}")
+            want = oracle.decode(M, enc, m, mode, b)
+            g = gpu_decode_batch(ctx, [src], [m], mode, b)[0]
+            lab = classify(g, want, greedy, TOL[cfg.dtype])
+            say("  ->", lab, "k", g.k, "oracle k", want.k)
+            assert not lab.startswith("FAIL"), lab
+            labels.append(lab)
+    return labels
+
+
+@pytest.mark.parametrize("wl", ["mt_base_f32", "mt_base_bf16"])
+def test_mt_base_sampled_sentences(wl):
+    labels = _full_size(wl, 2, 128, [("ar", 1), ("gs_jacobi", 5), ("hybrid", 5)])
+    say(wl, summarize(labels))
+
+
+def test_large_sampled_sentence():
+    labels = _full_size("large", 1, 24, [("ar", 1), ("jacobi", 0), ("gs_jacobi", 16)])
+    say("large", summarize(labels))
