@@ -1,0 +1,197 @@
+#!/usr/bin/env python3
+"""Decode throughput of parallel decoding vs greedy decoding on one MI355X.
+
+Workload (default): the Transformer-base-shaped model (6+6 layers, d=512, 8
+heads, FFN 2048, vocabulary 58,101, shared embeddings) with seeded random
+weights, 200 synthetic sources with lengths uniform in [10, 60] and
+m = min(n + 10, 128) target positions, batch 1 (the paper's online setting).
+A step is the decode of one sentence (pd_decode, batch 1) with its source
+already encoded and resident in HBM; the timed region covers K steps.
+
+One JSON line on stdout: value = target tokens/s of the headline mode
+(hybrid GS-Jacobi, b = 5) in bf16, plus greedy and GS-Jacobi numbers, k/m,
+the float32 model, the roofline of the fused vocabulary kernel and the CPU
+oracle baseline.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def run_mode(ctxs, sents, outs, mode, block, steps, warmup, timing=False):
+    import torch
+    n = len(sents)
+    order = [i % n for i in range(warmup + steps)]
+    for i in order[:warmup]:
+        ctxs[i].decode(mode, [sents[i][1]], block=block, out=outs[i])
+    torch.cuda.synchronize()
+    if timing:
+        for c in ctxs:
+            c.set_timing(True)
+    t0 = time.perf_counter()
+    for i in order[warmup:]:
+        ctxs[i].decode(mode, [sents[i][1]], block=block, out=outs[i])
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    toks = ks = ms = 0
+    for i in order[warmup:]:
+        toks += int(outs[i][1][0])
+        ks += int(outs[i][2][0])
+        ms += sents[i][1]
+    res = {"tokens": toks, "seconds": dt, "tokens_per_s": toks / dt, "k": ks, "m": ms, "k_over_m": ks / ms,
+           "ms_per_step": 1e3 * dt / steps}
+    if timing:
+        launches = total_ms = 0
+        for c in ctxs:
+            n_l, t_ms = c.vocab_timing()
+            launches += n_l
+            total_ms += t_ms
+            c.set_timing(False)
+        res["vocab_launches"] = launches
+        res["vocab_ms"] = total_ms
+    return res
+
+
+def gpu_workload(wl_name, steps, warmup, modes, headline):
+    import torch
+    from paper_2305_10427_amd import configs as C, pdec, synth
+    wl = C.WORKLOADS[wl_name]
+    cfg = wl.model
+    t0 = time.perf_counter()
+    w = synth.make_weights(cfg, seed=0)
+    model = pdec.Model(cfg, w)
+    sents = synth.make_sentences(wl, seed=1)
+    max_src = max(len(s) for s, _ in sents)
+    ctxs, outs = [], []
+    for src, m in sents:
+        c = pdec.Context(model, 1, max_src, wl.tgt_cap)
+        c.encode(torch.from_numpy(src[None]).cuda(), [len(src)])
+        ctxs.append(c)
+        outs.append((torch.empty((1, wl.tgt_cap), dtype=torch.int32, device="cuda"),
+                     torch.empty(1, dtype=torch.int32, device="cuda"),
+                     torch.empty(1, dtype=torch.int32, device="cuda"),
+                     torch.empty(1, dtype=torch.int32, device="cuda")))
+    torch.cuda.synchronize()
+    log(f"[{wl_name}] weights {model.weight_bytes() / 1e6:.1f} MB, {len(sents)} sentences encoded "
+        f"in {time.perf_counter() - t0:.1f}s")
+    res = {}
+    for mode, b in modes:
+        r = run_mode(ctxs, sents, outs, mode, b, steps, warmup, timing=(mode, b) == headline)
+        res[f"{mode}_b{b}"] = r
+        log(f"[{wl_name}] {mode:9s} b={b}: {r['tokens_per_s']:9.1f} tok/s  {r['ms_per_step']:7.3f} ms/sentence  "
+            f"k/m={r['k_over_m']:.3f}")
+    return cfg, w, sents, model, res
+
+
+def cpu_baseline(cfg, weights, sents, mode, block, budget_s):
+    """The oracle as it stands, on the host cores, on a bounded sample."""
+    import numpy as np
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:                       # noqa: BLE001
+        threads = len(os.sched_getaffinity(0))
+    M = oracle.Model(cfg, weights.values)
+    toks = n = 0
+    t0 = time.perf_counter()
+    dec_s = 0.0
+    for src, m in sents:
+        enc = M.encode(src)
+        t1 = time.perf_counter()
+        r = oracle.decode(M, enc, m, mode, block)
+        dec_s += time.perf_counter() - t1
+        toks += len(r.out)
+        n += 1
+        if time.perf_counter() - t0 > budget_s:
+            break
+    return {"value": toks / dec_s, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"first {n} sentences of the same workload, {mode} b={block}, decode only "
+                      f"(numpy float64 oracle, {dec_s:.1f}s)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-f32", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); sentence-level data "
+              "parallelism across GPUs is not built.", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    torch.cuda.set_device(0)
+
+    headline = ("hybrid", 5)
+    modes = [("ar", 1), ("gs_jacobi", 5), ("hybrid", 5)]
+    cfg, w, sents, model, res = gpu_workload("mt_base_bf16", args.steps, args.warmup, modes, headline)
+    f32 = None
+    if not args.no_f32:
+        _, _, _, _, f32 = gpu_workload("mt_base_f32", args.steps, args.warmup, modes, headline)
+
+    h = res[f"{headline[0]}_b{headline[1]}"]
+    # roofline of the fused vocabulary projection + argmax (bytes: E [V][d] and the output bias, bf16)
+    bytes_per_launch = cfg.vocab * (cfg.d_model + 1) * 2
+    avg_ms = h["vocab_ms"] / max(h["vocab_launches"], 1)
+    achieved = bytes_per_launch / (avg_ms * 1e-3) / 1e9
+    roof = {"kernel": "k_gemm<bf16,PRO_LN,EPI_ARGMAX> (fused vocab projection + argmax)", "bound": "hbm",
+            "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+            "avg_launch_us": round(avg_ms * 1e3, 2), "launches": h["vocab_launches"],
+            "bytes_per_launch": bytes_per_launch}
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(cfg, w, sents, headline[0], headline[1], args.cpu_seconds)
+        log(f"[cpu] oracle {cpu['value']:.1f} tok/s on {cpu['cores']} threads ({cpu['sample']})")
+
+    line = {
+        "metric": "target tokens/s (parallel vs greedy AR decode) + iterations/sentence k/m",
+        "value": round(h["tokens_per_s"], 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(h["ms_per_step"], 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded random weights and sources)",
+        "config": {"workload": "mt_base_bf16: 6+6 layers, d=512, 8 heads, FFN 2048, V=58101, batch 1, "
+                               "200 sources n~U[10,60], m=min(n+10,128)",
+                   "mode": headline[0], "block": headline[1], "global_batch": 1, "parallelism": "none"},
+        "modes": {k: {"tokens_per_s": round(v["tokens_per_s"], 1), "k_over_m": round(v["k_over_m"], 4),
+                      "ms_per_sentence": round(v["ms_per_step"], 4)} for k, v in res.items()},
+        "speedup_vs_ar": round(h["tokens_per_s"] / res["ar_b1"]["tokens_per_s"], 3),
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    if f32 is not None:
+        line["f32"] = {k: {"tokens_per_s": round(v["tokens_per_s"], 1), "k_over_m": round(v["k_over_m"], 4)}
+                       for k, v in f32.items()}
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -78,8 +78,9 @@ enum {
  * ReLU or exact-erf GELU FFN, sinusoidal positions, one token embedding E[V][d]
  * shared by encoder input, decoder input and the output projection
  * logits = logit_scale * h . E^T + out_bias.
- *   d_model must be a multiple of 8 and of n_heads; d_model / n_heads must be
- *   16, 32, 64 or 128; d_ff a multiple of 8.
+ *   d_model must be a multiple of 32 and of n_heads, at most 1024 (bf16) or
+ *   512 (f32); d_model / n_heads must be 16, 32, 64 or 128; d_ff a multiple
+ *   of 32.
  *   enc_emb_scale / dec_emb_scale multiply E[token] at the encoder / decoder
  *   input (a negative value selects sqrt(d_model)).
  *   bf16 models store weights, K/V, attention outputs, FFN hidden values, the
@@ -194,6 +195,17 @@ pd_status pd_decode(pd_ctx* ctx, int32_t mode, int32_t block, int32_t horizon, i
  * Uses the same kernels as pd_decode, with the argmax replaced by a store.
  */
 pd_status pd_debug_logits(pd_ctx* ctx, const int32_t* tgt_in, int32_t T, float* logits, void* stream);
+
+/*
+ * Timing of the fused vocabulary projection + argmax kernel, the kernel that
+ * moves most bytes per iteration.  With timing enabled, pd_decode records a
+ * pair of HIP events on its stream around every launch of that kernel and
+ * accumulates their elapsed times; pd_ctx_vocab_timing returns the number of
+ * launches and their total milliseconds since the last pd_ctx_set_timing.
+ * Timing adds two event records per iteration.
+ */
+pd_status pd_ctx_set_timing(pd_ctx* ctx, int32_t enable);
+pd_status pd_ctx_vocab_timing(const pd_ctx* ctx, int64_t* launches, double* total_ms);
 
 /* Message of the last failing call on this thread ("" if none). */
 const char* pd_last_error(void);

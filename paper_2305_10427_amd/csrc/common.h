@@ -120,32 +120,49 @@ __device__ __forceinline__ uint32_t float_key(float f) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-// Mean and 1/sqrt(var + eps) of one row of K elements, lane split as in the
-// products: lane handles k = c*64*EPL + lane*EPL + e.
-template <typename WT, typename XT>
-__device__ __forceinline__ void ln_stats(const XT* x, int K, int lane, float eps,
-                                         float& mean, float& rstd) {
-  constexpr int EPL = Vec16<WT>::N;
-  float s = 0.f;
-  for (int k0 = lane * EPL; k0 < K; k0 += kWave * EPL) {
-    float v[EPL];
-    load_n<XT, EPL>(x, k0, v);
+// LayerNorm statistics of one row of K elements (K a multiple of 8, K <= 1024)
+// computed by a group of 16 consecutive lanes.  Lane j of the group holds
+// elements k = 8*j + 128*t + e (t < 8, e < 8, k < K) in v[t][e] and sums them
+// in that order; the 16 lane sums are combined by xor-1, 2, 4, 8 pairings.
+// Mean first, then the mean of squared deviations (two passes over the values
+// held in registers).  All 64 lanes of the wave must call this (invalid rows
+// pass valid = false and contribute zeros).  The matrix-product prologue and
+// the row LayerNorm kernel both use it, so a row's statistics are bitwise the
+// same wherever they are computed.
+template <typename XT>
+__device__ __forceinline__ void ln_stats_g16(const XT* x, int K, int j, float eps, bool valid,
+                                             float (&v)[8][8], float& mean, float& rstd) {
 #pragma unroll
-    for (int e = 0; e < EPL; ++e) s += v[e];
-  }
-  mean = wave_sum(s) / static_cast<float>(K);
-  float q = 0.f;
-  for (int k0 = lane * EPL; k0 < K; k0 += kWave * EPL) {
-    float v[EPL];
-    load_n<XT, EPL>(x, k0, v);
+  for (int t = 0; t < 8; ++t) {
+    const int k0 = 8 * j + 128 * t;
+    if (valid && k0 < K) load_n<XT, 8>(x, k0, v[t]);
+    else {
 #pragma unroll
-    for (int e = 0; e < EPL; ++e) {
-      const float t = v[e] - mean;
-      q = fmaf(t, t, q);
+      for (int e = 0; e < 8; ++e) v[t][e] = 0.f;
     }
   }
-  const float var = wave_sum(q) / static_cast<float>(K);
-  rstd = 1.0f / sqrtf(var + eps);
+  float s = 0.f;
+#pragma unroll
+  for (int t = 0; t < 8; ++t)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) s += v[t][e];
+#pragma unroll
+  for (int off = 1; off < 16; off <<= 1) s += __shfl_xor(s, off);
+  mean = s / static_cast<float>(K);
+  float q = 0.f;
+#pragma unroll
+  for (int t = 0; t < 8; ++t) {
+    if (8 * j + 128 * t < K) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float d = v[t][e] - mean;
+        q = fmaf(d, d, q);
+      }
+    }
+  }
+#pragma unroll
+  for (int off = 1; off < 16; off <<= 1) q += __shfl_xor(q, off);
+  rstd = 1.0f / sqrtf(q / static_cast<float>(K) + eps);
 }
 
 // LayerNorm of one element given its row statistics (same expression

@@ -105,27 +105,33 @@ __global__ __launch_bounds__(256) void k_embed(EmbedArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Row LayerNorm, one wave per row, same lane split and expression as the
-// LayerNorm prologue of the matrix products.
-template <typename WT, typename AT, typename XT>
+// Row LayerNorm, 4 rows per wave with 16 lanes per row, statistics by
+// ln_stats_g16 (the same lane split and pairing as the LayerNorm prologue of
+// the matrix products).
+template <typename WT, typename XT>
 __global__ __launch_bounds__(256) void k_ln(LnArgs a) {
-  constexpr int EPL = Vec16<WT>::N;
   const int lane = threadIdx.x & (kWave - 1);
-  const int row = blockIdx.x * 4 + threadIdx.x / kWave;
+  const int wave = threadIdx.x / kWave;
+  const int j = lane & 15;
+  const int row = (blockIdx.x * 4 + wave) * 4 + (lane >> 4);
   const int R = a.n_rows_dev ? *a.n_rows_dev : a.n_rows;
-  if (row >= R) return;
-  const XT* x = static_cast<const XT*>(a.x) + static_cast<size_t>(row) * a.d;
-  float mean, rstd;
-  ln_stats<WT, XT>(x, a.d, lane, a.eps, mean, rstd);
-  for (int k0 = lane * EPL; k0 < a.d; k0 += kWave * EPL) {
-    float v[EPL], g[EPL], b[EPL];
-    load_n<XT, EPL>(x, k0, v);
-    load_n<WT, EPL>(static_cast<const WT*>(a.g), k0, g);
-    load_n<WT, EPL>(static_cast<const WT*>(a.b), k0, b);
+  const bool ok = row < R;
+  const XT* x = static_cast<const XT*>(a.x) + static_cast<size_t>(ok ? row : 0) * a.d;
+  float v[8][8], mean, rstd;
+  ln_stats_g16<XT>(x, a.d, j, a.eps, ok, v, mean, rstd);
+  if (!ok) return;
 #pragma unroll
-    for (int e = 0; e < EPL; ++e)
-      Elt<AT>::store(static_cast<AT*>(a.out), static_cast<size_t>(row) * a.d + k0 + e,
-                     ln_apply(v[e], mean, rstd, g[e], b[e]));
+  for (int t = 0; t < 8; ++t) {
+    const int k0 = 8 * j + 128 * t;
+    if (k0 < a.d) {
+      float g[8], b[8];
+      load_n<WT, 8>(static_cast<const WT*>(a.g), k0, g);
+      load_n<WT, 8>(static_cast<const WT*>(a.b), k0, b);
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        Elt<WT>::store(static_cast<WT*>(a.out), static_cast<size_t>(row) * a.d + k0 + e,
+                       ln_apply(v[t][e], mean, rstd, g[e], b[e]));
+    }
   }
 }
 
@@ -328,13 +334,14 @@ hipError_t launch_embed(int dtype, const EmbedArgs& a, int R_max, hipStream_t s)
 }
 
 hipError_t launch_ln(int dtype, const LnArgs& a, int R_max, hipStream_t s) {
-  const int grid = (R_max + 3) / 4;
+  const int grid = (R_max + 15) / 16;
   if (grid == 0) return hipSuccess;
+  if (a.d % 8 != 0 || a.d > 1024) return hipErrorInvalidValue;
   if (dtype == DT_BF16) {
-    if (a.x_f32) hipLaunchKernelGGL((k_ln<bf16_t, bf16_t, float>), dim3(grid), dim3(256), 0, s, a);
-    else hipLaunchKernelGGL((k_ln<bf16_t, bf16_t, bf16_t>), dim3(grid), dim3(256), 0, s, a);
+    if (a.x_f32) hipLaunchKernelGGL((k_ln<bf16_t, float>), dim3(grid), dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((k_ln<bf16_t, bf16_t>), dim3(grid), dim3(256), 0, s, a);
   } else {
-    hipLaunchKernelGGL((k_ln<float, float, float>), dim3(grid), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((k_ln<float, float>), dim3(grid), dim3(256), 0, s, a);
   }
   return hipGetLastError();
 }

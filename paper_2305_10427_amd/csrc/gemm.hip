@@ -1,151 +1,216 @@
-// Weight-streaming matrix products for the decoder/encoder of p_theta.
+// Matrix products of the decoder/encoder of p_theta on the MFMA units.
 //
 // Y[r][n] = sum_k X[r][k] * W[n][k] (+ epilogue), W stored [N][K] row-major.
-// The decoder rows of one iteration are few (batch x block), so the product
-// is bound by reading W once: every wave streams whole 16-byte vectors of NC
-// weight rows across its 64 lanes (coalesced along K), multiplies them with
-// RT input rows held in registers and reduces across lanes at the end.
+// A workgroup of 4 waves computes 16 rows x 16 columns (KSPLIT = 4: the waves
+// split K and their partial tiles are summed in wave order) or 16 rows x 64
+// columns (KSPLIT = 1: each wave owns 16 columns and the whole K).  One MFMA
+// step multiplies a 16 x KS slice of X with a KS x 16 slice of W^T:
+//   bf16: v_mfma_f32_16x16x32_bf16, KS = 32, a lane feeds 8 consecutive k;
+//   f32 : 4 x v_mfma_f32_16x16x4_f32, KS = 16, a lane feeds 4 consecutive k,
+//         one per instruction.
+// Lane l feeds row / column (l & 15) at k = k0 + EPL * (l >> 4) + e, the same
+// assignment for X and W, and reads 16 contiguous bytes of each.  The result
+// tile holds C[4 * (l >> 4) + i][l & 15] in element i of lane l.
 //
-// Reduction order per output element is fixed: each lane accumulates its K
-// slice in increasing k with FMAs, then a fixed lane-pairing tree sums the 64
-// lane partials.  It does not depend on how many rows the call has or on which
-// slot of a row tile a row lands in, so a row's result is bitwise the same in
-// a block of L rows and alone (greedy decoding and the Jacobi iterations then
-// evaluate exactly the same map).
+// Decoding at batch 1 has 1..16 rows per iteration: one 16-row tile, so a
+// block of L rows costs what one row costs and the bound is streaming W.
+// Each output element is accumulated over k in a fixed order (MFMA steps in
+// increasing k, then the KSPLIT partials in wave order), independent of how
+// many rows the call has and of the tile slot a row occupies: a row's result
+// is bitwise the same in a block of L rows and alone, so greedy decoding and
+// the Jacobi iterations evaluate exactly the same map.
 //
-// Prologue PRO_LN normalises each input row (LayerNorm with the lane split of
-// ln_stats below) before use and rounds it to the storage type; workgroup 0
+// All loads a wave needs (weights, inputs, bias) are issued before any
+// result is needed; the device row count only gates the stores, so its load
+// overlaps the rest.  Rows between the device count and the launch bound are
+// computed from stale activations and discarded.
+//
+// Prologue PRO_LN normalises the input rows (LayerNorm, statistics from
+// ln_stats16) and rounds them to the storage type before use; workgroup 0
 // can write the normalised rows out as the new residual stream.
 //
-// Epilogue EPI_ARGMAX turns the product into the fused vocabulary projection
-// + argmax: logits = s * acc + bias are never stored, each workgroup keeps the
-// best (value, lowest index) per row and writes one partial per row.
+// Epilogue EPI_ARGMAX is the fused vocabulary projection + argmax: logits =
+// s * acc + bias are never stored; each workgroup keeps the best (largest
+// value, then lowest index) per row and writes one partial per row.
 #include "common.h"
 #include "kernels.h"
 
 namespace pdec {
 
-constexpr int kNC = 4;        // weight rows (output columns) per wave per pass
-constexpr int kWavesPerWG = 4;
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float floatx4_t __attribute__((ext_vector_type(4)));
+
+template <typename T> struct Mma;
+template <> struct Mma<bf16_t> {
+  static constexpr int KS = 32;
+  static constexpr int EPL = 8;
+  typedef uint4 frag;
+  static __device__ __forceinline__ floatx4_t step(frag a, frag b, floatx4_t c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b),
+                                                   c, 0, 0, 0);
+  }
+  static __device__ __forceinline__ frag load(const bf16_t* p) { return *reinterpret_cast<const uint4*>(p); }
+  static __device__ __forceinline__ frag zero() { return make_uint4(0, 0, 0, 0); }
+  static __device__ __forceinline__ frag pack(const float* v) {
+    uint32_t w[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      w[j] = static_cast<uint32_t>(f32_to_bf16(v[2 * j])) | (static_cast<uint32_t>(f32_to_bf16(v[2 * j + 1])) << 16);
+    return make_uint4(w[0], w[1], w[2], w[3]);
+  }
+};
+template <> struct Mma<float> {
+  static constexpr int KS = 16;
+  static constexpr int EPL = 4;
+  typedef float4 frag;
+  static __device__ __forceinline__ floatx4_t step(frag a, frag b, floatx4_t c) {
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, b.x, c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, b.y, c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, b.z, c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, b.w, c, 0, 0, 0);
+    return c;
+  }
+  static __device__ __forceinline__ frag load(const float* p) { return *reinterpret_cast<const float4*>(p); }
+  static __device__ __forceinline__ frag zero() { return make_float4(0.f, 0.f, 0.f, 0.f); }
+  static __device__ __forceinline__ frag pack(const float* v) { return make_float4(v[0], v[1], v[2], v[3]); }
+};
 
 __device__ __forceinline__ float gelu_erf(float v) {
   return 0.5f * v * (1.0f + erff(v * 0.70710678118654752f));
 }
 
-template <typename WT, typename AT, int RT, int PRO, int EPI, int XF32>
+constexpr int kUnroll = 8;   // MFMA steps whose loads are issued together
+
+template <typename WT, int PRO, int EPI, int XF32, int KSPLIT>
 __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
+  using AT = WT;
   using XT = typename std::conditional<XF32 != 0, float, AT>::type;
-  constexpr int EPL = Vec16<WT>::N;
-  constexpr int M = kNC * RT;
-  constexpr int LGM = Log2<M>::v;
+  using MM = Mma<WT>;
+  using frag = typename MM::frag;
+  constexpr int KS = MM::KS;
+  constexpr int EPL = MM::EPL;
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = threadIdx.x / kWave;
-  const int R = a.n_rows_dev ? *a.n_rows_dev : a.n_rows;
-  if (R <= 0) return;
+  const int lr = lane & 15;          // row (X) / column (W) fed by this lane
+  const int lg = lane >> 4;          // k group of this lane
   const int K = a.K, N = a.N;
-  const int n_groups = (N + kNC - 1) / kNC;
-  const int wave_gid = blockIdx.x * kWavesPerWG + wave;
-  const int wave_stride = gridDim.x * kWavesPerWG;
+  const int n0 = (KSPLIT == 4 ? blockIdx.x * 16 : (blockIdx.x * 4 + wave) * 16);
+  const int col = n0 + lr;           // weight row loaded by this lane, and output column it finishes
+  const int n_steps = K / KS;
+  const int s_begin = KSPLIT == 4 ? (n_steps * wave) / 4 : 0;
+  const int s_end = KSPLIT == 4 ? (n_steps * (wave + 1)) / 4 : n_steps;
   const WT* __restrict__ W = static_cast<const WT*>(a.w);
-  const WT* __restrict__ bias = static_cast<const WT*>(a.bias);
   const XT* __restrict__ X = static_cast<const XT*>(a.x);
+  const int R_max = a.n_rows;        // rows that may be read (launch bound)
+  const int R = a.n_rows_dev ? *a.n_rows_dev : a.n_rows;
+  const float bias_v = (col < N) ? Elt<WT>::load(static_cast<const WT*>(a.bias), col) : 0.f;
 
-  __shared__ uint32_t s_key[kWavesPerWG][M];
-  __shared__ int s_idx[kWavesPerWG][M];
+  __shared__ float s_part[4][4][64];
+  __shared__ uint32_t s_key[4][16];
+  __shared__ int s_idx[4][16];
+  // PRO_LN: the normalised 16-row input tile, rows padded by 16 bytes
+  extern __shared__ __align__(16) unsigned char s_dyn[];
+  AT* sA = reinterpret_cast<AT*>(s_dyn);
+  const int lda = K + 16 / static_cast<int>(sizeof(AT));
 
-  const int j_own = lane >> (6 - LGM);
-  const bool owner = (lane & ((1 << (6 - LGM)) - 1)) == 0;
-  const int n_own = j_own / RT;
-  const int r_own = j_own % RT;
-
-  for (int r0 = 0; r0 < R; r0 += RT) {
-    const int nr = min(RT, R - r0);
-    float mean[RT], rstd[RT];
+  const int m_first = blockIdx.y * 16 * a.mt_per_wg;
+  const int m_last = min(R_max, m_first + 16 * a.mt_per_wg);
+  for (int m0 = m_first; m0 < m_last; m0 += 16) {
+    if (m0 > m_first && m0 >= R) break;
+    const int arow = m0 + lr;                 // X row fed by this lane
+    const bool arow_ok = arow < R_max;
     if constexpr (PRO == PRO_LN) {
+      // wave w normalises rows 4w .. 4w+3 of the tile, 16 lanes per row
+      const int tr = 4 * wave + lg;
+      const int row = m0 + tr;
+      const bool ok = row < R_max;
+      float v[8][8], mean, rstd;
+      ln_stats_g16<XT>(X + static_cast<size_t>(ok ? row : 0) * a.ldx, K, lr, a.ln_eps, ok, v, mean, rstd);
+      const bool write_out = a.ln_out != nullptr && blockIdx.x == 0 && row < R;
 #pragma unroll
-      for (int r = 0; r < RT; ++r) {
-        mean[r] = 0.f;
-        rstd[r] = 0.f;
-        if (r < nr) ln_stats<WT, XT>(X + static_cast<size_t>(r0 + r) * a.ldx, K, lane, a.ln_eps, mean[r], rstd[r]);
+      for (int t = 0; t < 8; ++t) {
+        const int k0 = 8 * lr + 128 * t;
+        if (k0 < K) {
+          float gv[8], bv[8], y[8];
+          load_n<WT, 8>(static_cast<const WT*>(a.ln_g), k0, gv);
+          load_n<WT, 8>(static_cast<const WT*>(a.ln_b), k0, bv);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) y[e] = Elt<AT>::round(ln_apply(v[t][e], mean, rstd, gv[e], bv[e]));
+#pragma unroll
+          for (int e = 0; e < 8; ++e) Elt<AT>::store(sA, static_cast<size_t>(tr) * lda + k0 + e, y[e]);
+          if (write_out) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+              Elt<AT>::store(static_cast<AT*>(a.ln_out), static_cast<size_t>(row) * a.ldlo + k0 + e, y[e]);
+          }
+        }
       }
+      __syncthreads();
     }
-    uint32_t best_key = 0;
-    int best_idx = 0x7fffffff;
-    int nonfinite = 0;
-    bool first_pass = true;
-    for (int g = wave_gid; g < n_groups; g += wave_stride) {
-      float acc[kNC][RT];
+    floatx4_t acc = {0.f, 0.f, 0.f, 0.f};
+    for (int s0 = s_begin; s0 < s_end; s0 += kUnroll) {
+      frag af[kUnroll], bf[kUnroll];
 #pragma unroll
-      for (int n = 0; n < kNC; ++n)
-#pragma unroll
-        for (int r = 0; r < RT; ++r) acc[n][r] = 0.f;
-      for (int k0 = lane * EPL; k0 < K; k0 += kWave * EPL) {
-        float xv[RT][EPL];
-#pragma unroll
-        for (int r = 0; r < RT; ++r) {
-          if (r < nr) {
-            load_n<XT, EPL>(X, static_cast<size_t>(r0 + r) * a.ldx + k0, xv[r]);
-            if constexpr (PRO == PRO_LN) {
-              float gv[EPL], bv[EPL];
-              load_n<WT, EPL>(static_cast<const WT*>(a.ln_g), k0, gv);
-              load_n<WT, EPL>(static_cast<const WT*>(a.ln_b), k0, bv);
-#pragma unroll
-              for (int e = 0; e < EPL; ++e)
-                xv[r][e] = Elt<AT>::round(ln_apply(xv[r][e], mean[r], rstd[r], gv[e], bv[e]));
-              if (a.ln_out != nullptr && blockIdx.x == 0 && wave == 0 && first_pass) {
-#pragma unroll
-                for (int e = 0; e < EPL; ++e)
-                  Elt<AT>::store(static_cast<AT*>(a.ln_out), static_cast<size_t>(r0 + r) * a.ldlo + k0 + e, xv[r][e]);
-              }
-            }
+      for (int u = 0; u < kUnroll; ++u) {
+        const int k = (s0 + u) * KS + EPL * lg;
+        const bool ok = s0 + u < s_end;
+        bf[u] = (ok && col < N) ? MM::load(W + static_cast<size_t>(col) * K + k) : MM::zero();
+        if constexpr (PRO == PRO_LN) {
+          af[u] = ok ? MM::load(sA + static_cast<size_t>(lr) * lda + k) : MM::zero();
+        } else {
+          if (ok && arow_ok) {
+            float xv[EPL];
+            load_n<XT, EPL>(X, static_cast<size_t>(arow) * a.ldx + k, xv);
+            af[u] = MM::pack(xv);
           } else {
-#pragma unroll
-            for (int e = 0; e < EPL; ++e) xv[r][e] = 0.f;
+            af[u] = MM::zero();
           }
-        }
-#pragma unroll
-        for (int n = 0; n < kNC; ++n) {
-          const int col = g * kNC + n;
-          float wv[EPL];
-          if (col < N) {
-            load_n<WT, EPL>(W, static_cast<size_t>(col) * K + k0, wv);
-          } else {
-#pragma unroll
-            for (int e = 0; e < EPL; ++e) wv[e] = 0.f;
-          }
-#pragma unroll
-          for (int r = 0; r < RT; ++r)
-#pragma unroll
-            for (int e = 0; e < EPL; ++e) acc[n][r] = fmaf(wv[e], xv[r][e], acc[n][r]);
         }
       }
-      first_pass = false;
-      float vals[M];
 #pragma unroll
-      for (int n = 0; n < kNC; ++n)
+      for (int u = 0; u < kUnroll; ++u) acc = MM::step(af[u], bf[u], acc);
+    }
+    if constexpr (PRO == PRO_LN) __syncthreads();   // sA is rewritten by the next tile
+    // combine the K-split partials: wave w finishes element i = w of every lane
+    float cv[4];
+    int n_elems;
+    if constexpr (KSPLIT == 4) {
 #pragma unroll
-        for (int r = 0; r < RT; ++r) vals[n * RT + r] = acc[n][r];
-      float v = wave_reduce_scatter<M>(vals, lane);
-      const int col = g * kNC + n_own;
-      const int row = r0 + r_own;
-      if (!owner || col >= N || r_own >= nr) continue;
-      const float bv = Elt<WT>::load(bias, col);
+      for (int i = 0; i < 4; ++i) s_part[wave][i][lane] = acc[i];
+      __syncthreads();
+      cv[0] = ((s_part[0][wave][lane] + s_part[1][wave][lane]) + s_part[2][wave][lane]) + s_part[3][wave][lane];
+      n_elems = 1;
+      __syncthreads();
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) cv[i] = acc[i];
+      n_elems = 4;
+    }
+    uint32_t bk[4] = {0, 0, 0, 0};
+    int bi[4] = {0x7fffffff, 0x7fffffff, 0x7fffffff, 0x7fffffff};
+    int nf = 0;
+    for (int e = 0; e < n_elems; ++e) {
+      const int i = KSPLIT == 4 ? wave : e;
+      const int row = m0 + 4 * lg + i;
+      const float v = cv[e];
+      if (row >= R || col >= N) continue;
       if constexpr (EPI == EPI_F32) {
-        a.out_f32[static_cast<size_t>(row) * a.ldo + col] = v + bv;
+        a.out_f32[static_cast<size_t>(row) * a.ldo + col] = v + bias_v;
       } else if constexpr (EPI == EPI_ACT) {
-        v += bv;
-        v = (a.act == 2) ? gelu_erf(v) : fmaxf(v, 0.f);
-        Elt<AT>::store(static_cast<AT*>(a.out), static_cast<size_t>(row) * a.ldo + col, v);
+        float t = v + bias_v;
+        t = (a.act == 2) ? gelu_erf(t) : fmaxf(t, 0.f);
+        Elt<AT>::store(static_cast<AT*>(a.out), static_cast<size_t>(row) * a.ldo + col, t);
       } else if constexpr (EPI == EPI_RESID) {
-        v += bv;
         const size_t ri = static_cast<size_t>(row) * a.ldr + col;
-        v += a.resid_f32 ? static_cast<const float*>(a.resid)[ri] : Elt<AT>::load(static_cast<const AT*>(a.resid), ri);
-        if (a.out_f32 != nullptr) a.out_f32[static_cast<size_t>(row) * a.ldo + col] = v;
-        else Elt<AT>::store(static_cast<AT*>(a.out), static_cast<size_t>(row) * a.ldo + col, v);
+        const float rv = a.resid_f32 ? static_cast<const float*>(a.resid)[ri]
+                                     : Elt<AT>::load(static_cast<const AT*>(a.resid), ri);
+        const float t = (v + bias_v) + rv;
+        if (a.out_f32 != nullptr) a.out_f32[static_cast<size_t>(row) * a.ldo + col] = t;
+        else Elt<AT>::store(static_cast<AT*>(a.out), static_cast<size_t>(row) * a.ldo + col, t);
       } else if constexpr (EPI == EPI_QKV) {
-        v += bv;
+        const float t = v + bias_v;
         if (col < a.q_cols) {
-          a.out_f32[static_cast<size_t>(row) * a.ldo + col] = v;
+          a.out_f32[static_cast<size_t>(row) * a.ldo + col] = t;
         } else {
           const int c = col - a.q_cols;
           const int which = c / a.d;
@@ -156,41 +221,54 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
           if (a.rows.sent != nullptr) { s = a.rows.sent[row]; p = a.rows.pos[row]; }
           else { s = row / a.rows.per_sent; p = row - s * a.rows.per_sent; }
           const size_t idx = ((static_cast<size_t>(s) * a.H + hh) * a.T + p) * a.dh + dd;
-          Elt<AT>::store(static_cast<AT*>(which == 0 ? a.kc : a.vc), idx, v);
+          Elt<AT>::store(static_cast<AT*>(which == 0 ? a.kc : a.vc), idx, t);
         }
       } else if constexpr (EPI == EPI_LOGITS) {
-        a.out_f32[static_cast<size_t>(row) * a.ldo + col] = fmaf(a.logit_scale, v, bv);
+        a.out_f32[static_cast<size_t>(row) * a.ldo + col] = fmaf(a.logit_scale, v, bias_v);
       } else if constexpr (EPI == EPI_ARGMAX) {
-        const float logit = fmaf(a.logit_scale, v, bv);   // s * (h . E[col]) + bias[col]
-        if (!isfinite(logit)) {
-          nonfinite = 1;
-        } else {
-          const uint32_t key = float_key(logit);
-          if (key > best_key) { best_key = key; best_idx = col; }   // columns rise: first max kept
-        }
+        const float logit = fmaf(a.logit_scale, v, bias_v);   // s * (h . E[col]) + bias[col]
+        if (!isfinite(logit)) nf = 1;
+        else { bk[e] = float_key(logit); bi[e] = col; }
       }
     }
     if constexpr (EPI == EPI_ARGMAX) {
-      // workgroup-level best per row: (largest key, then lowest index)
-      if (owner) {
-        s_key[wave][j_own] = best_key;
-        s_idx[wave][j_own] = best_idx | (nonfinite << 31);
+      static_assert(KSPLIT == 1, "the fused argmax runs with whole-K waves");
+      // best of each row over the 16 columns held by one 16-lane group
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+#pragma unroll
+        for (int off = 1; off < 16; off <<= 1) {
+          const uint32_t ok = __shfl_xor(bk[e], off);
+          const int oi = __shfl_xor(bi[e], off);
+          if (ok > bk[e] || (ok == bk[e] && oi < bi[e])) { bk[e] = ok; bi[e] = oi; }
+        }
+      }
+      nf |= __shfl_xor(nf, 1);
+      nf |= __shfl_xor(nf, 2);
+      nf |= __shfl_xor(nf, 4);
+      nf |= __shfl_xor(nf, 8);
+      if (lr == 0) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          s_key[wave][4 * lg + e] = bk[e];
+          s_idx[wave][4 * lg + e] = bi[e] | (nf << 31);
+        }
       }
       __syncthreads();
-      if (threadIdx.x < RT && static_cast<int>(threadIdx.x) < nr) {
+      if (threadIdx.x < 16) {
         const int r = threadIdx.x;
-        uint32_t bk = 0;
-        int bi = 0x7fffffff, nf = 0;
-        for (int w = 0; w < kWavesPerWG; ++w)
-          for (int n = 0; n < kNC; ++n) {
-            const uint32_t k = s_key[w][n * RT + r];
-            const int raw = s_idx[w][n * RT + r];
-            const int i = raw & 0x7fffffff;
-            nf |= (raw >> 31) & 1;
-            if (k > bk || (k == bk && i < bi)) { bk = k; bi = i; }
-          }
-        a.partials[static_cast<size_t>(r0 + r) * a.part_ld + blockIdx.x] =
-            make_uint2(bk, static_cast<uint32_t>(bi) | (static_cast<uint32_t>(nf) << 31));
+        uint32_t kk = 0;
+        int ii = 0x7fffffff, ff = 0;
+        for (int w = 0; w < 4; ++w) {
+          const uint32_t k2 = s_key[w][r];
+          const int raw = s_idx[w][r];
+          const int i2 = raw & 0x7fffffff;
+          ff |= (raw >> 31) & 1;
+          if (k2 > kk || (k2 == kk && i2 < ii)) { kk = k2; ii = i2; }
+        }
+        if (m0 + r < R)
+          a.partials[static_cast<size_t>(m0 + r) * a.part_ld + blockIdx.x] =
+              make_uint2(kk, static_cast<uint32_t>(ii) | (static_cast<uint32_t>(ff) << 31));
       }
       __syncthreads();
     }
@@ -199,62 +277,58 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
 
 namespace {
 
-template <typename WT, typename AT, int RT, int PRO, int EPI, int XF32>
-hipError_t launch_t(const GemmArgs& a, int grid, hipStream_t s) {
-  hipLaunchKernelGGL((k_gemm<WT, AT, RT, PRO, EPI, XF32>), dim3(grid), dim3(256), 0, s, a);
+template <typename WT, int PRO, int EPI, int XF32>
+hipError_t launch_t(GemmArgs a, int ksplit, hipStream_t s) {
+  const int tiles = (a.n_rows + 15) / 16;
+  const int gy = tiles < 64 ? tiles : 64;
+  a.mt_per_wg = (tiles + gy - 1) / gy;
+  const size_t lds = PRO == PRO_LN ? gemm_ln_lds_bytes(a.K, sizeof(WT)) : 0;
+  if (EPI == EPI_ARGMAX || ksplit != 4) {
+    hipLaunchKernelGGL((k_gemm<WT, PRO, EPI, XF32, 1>), dim3(gemm_grid(EPI, a.N, 1), gy), dim3(256), lds, s, a);
+  } else if constexpr (EPI != EPI_ARGMAX) {
+    hipLaunchKernelGGL((k_gemm<WT, PRO, EPI, XF32, 4>), dim3(gemm_grid(EPI, a.N, 4), gy), dim3(256), lds, s, a);
+  }
   return hipGetLastError();
 }
 
-template <typename WT, typename AT, int PRO, int EPI, int XF32>
-hipError_t launch_rt(int row_tile, const GemmArgs& a, int grid, hipStream_t s) {
-  switch (row_tile) {
-    case 1: return launch_t<WT, AT, 1, PRO, EPI, XF32>(a, grid, s);
-    case 2: return launch_t<WT, AT, 2, PRO, EPI, XF32>(a, grid, s);
-    case 4: return launch_t<WT, AT, 4, PRO, EPI, XF32>(a, grid, s);
-    case 8: return launch_t<WT, AT, 8, PRO, EPI, XF32>(a, grid, s);
+template <typename WT, int PRO, int XF32>
+hipError_t launch_epi(int epi, const GemmArgs& a, int ksplit, hipStream_t s) {
+  switch (epi) {
+    case EPI_F32: return launch_t<WT, PRO, EPI_F32, XF32>(a, ksplit, s);
+    case EPI_ACT: return launch_t<WT, PRO, EPI_ACT, XF32>(a, ksplit, s);
+    case EPI_RESID: return launch_t<WT, PRO, EPI_RESID, XF32>(a, ksplit, s);
+    case EPI_QKV: return launch_t<WT, PRO, EPI_QKV, XF32>(a, ksplit, s);
+    case EPI_ARGMAX: return launch_t<WT, PRO, EPI_ARGMAX, XF32>(a, ksplit, s);
+    case EPI_LOGITS: return launch_t<WT, PRO, EPI_LOGITS, XF32>(a, ksplit, s);
     default: return hipErrorInvalidValue;
   }
 }
 
-template <typename WT, typename AT>
-hipError_t launch_dt(int pro, int epi, int row_tile, const GemmArgs& a, int grid, hipStream_t s) {
-  if (pro == PRO_LN) {
-    if (a.x_f32) {
-      switch (epi) {
-        case EPI_F32: return launch_rt<WT, AT, PRO_LN, EPI_F32, 1>(row_tile, a, grid, s);
-        case EPI_ACT: return launch_rt<WT, AT, PRO_LN, EPI_ACT, 1>(row_tile, a, grid, s);
-        case EPI_QKV: return launch_rt<WT, AT, PRO_LN, EPI_QKV, 1>(row_tile, a, grid, s);
-        case EPI_ARGMAX: return launch_rt<WT, AT, PRO_LN, EPI_ARGMAX, 1>(row_tile, a, grid, s);
-        case EPI_LOGITS: return launch_rt<WT, AT, PRO_LN, EPI_LOGITS, 1>(row_tile, a, grid, s);
-        default: return hipErrorInvalidValue;
-      }
-    }
-    switch (epi) {
-      case EPI_F32: return launch_rt<WT, AT, PRO_LN, EPI_F32, 0>(row_tile, a, grid, s);
-      case EPI_ACT: return launch_rt<WT, AT, PRO_LN, EPI_ACT, 0>(row_tile, a, grid, s);
-      case EPI_QKV: return launch_rt<WT, AT, PRO_LN, EPI_QKV, 0>(row_tile, a, grid, s);
-      case EPI_ARGMAX: return launch_rt<WT, AT, PRO_LN, EPI_ARGMAX, 0>(row_tile, a, grid, s);
-      case EPI_LOGITS: return launch_rt<WT, AT, PRO_LN, EPI_LOGITS, 0>(row_tile, a, grid, s);
-      default: return hipErrorInvalidValue;
-    }
-  }
+template <typename WT>
+hipError_t launch_dt(int pro, int epi, const GemmArgs& a, int ksplit, hipStream_t s) {
+  if (pro == PRO_LN)
+    return a.x_f32 ? launch_epi<WT, PRO_LN, 1>(epi, a, ksplit, s) : launch_epi<WT, PRO_LN, 0>(epi, a, ksplit, s);
   if (a.x_f32) return hipErrorInvalidValue;
-  switch (epi) {
-    case EPI_F32: return launch_rt<WT, AT, PRO_NONE, EPI_F32, 0>(row_tile, a, grid, s);
-    case EPI_ACT: return launch_rt<WT, AT, PRO_NONE, EPI_ACT, 0>(row_tile, a, grid, s);
-    case EPI_RESID: return launch_rt<WT, AT, PRO_NONE, EPI_RESID, 0>(row_tile, a, grid, s);
-    case EPI_QKV: return launch_rt<WT, AT, PRO_NONE, EPI_QKV, 0>(row_tile, a, grid, s);
-    case EPI_ARGMAX: return launch_rt<WT, AT, PRO_NONE, EPI_ARGMAX, 0>(row_tile, a, grid, s);
-    case EPI_LOGITS: return launch_rt<WT, AT, PRO_NONE, EPI_LOGITS, 0>(row_tile, a, grid, s);
-    default: return hipErrorInvalidValue;
-  }
+  return launch_epi<WT, PRO_NONE, 0>(epi, a, ksplit, s);
 }
 
 }  // namespace
 
-hipError_t launch_gemm(int dtype, int pro, int epi, int row_tile, const GemmArgs& a, int grid, hipStream_t s) {
-  if (dtype == DT_BF16) return launch_dt<bf16_t, bf16_t>(pro, epi, row_tile, a, grid, s);
-  return launch_dt<float, float>(pro, epi, row_tile, a, grid, s);
+size_t gemm_ln_lds_bytes(int K, size_t elt) { return 16 * (static_cast<size_t>(K) * elt + 16); }
+
+int gemm_grid(int epi, int N, int ksplit) {
+  if (epi == EPI_ARGMAX || ksplit != 4) return (N + 63) / 64;
+  return (N + 15) / 16;
+}
+
+hipError_t launch_gemm(int dtype, int pro, int epi, int ksplit, const GemmArgs& a, hipStream_t s) {
+  if (a.n_rows <= 0) return hipSuccess;
+  const int ks = dtype == DT_BF16 ? Mma<bf16_t>::KS : Mma<float>::KS;
+  if (a.K % ks != 0 || a.K % 32 != 0) return hipErrorInvalidValue;
+  if (pro == PRO_LN && (a.K > 1024 || gemm_ln_lds_bytes(a.K, dtype == DT_BF16 ? 2 : 4) > 65536))
+    return hipErrorInvalidValue;
+  if (dtype == DT_BF16) return launch_dt<bf16_t>(pro, epi, a, ksplit, s);
+  return launch_dt<float>(pro, epi, a, ksplit, s);
 }
 
 }  // namespace pdec

@@ -28,8 +28,9 @@ enum Epilogue {
 };
 
 struct GemmArgs {
-  const int* n_rows_dev;   // row count read on device (nullptr: use n_rows)
-  int n_rows;
+  const int* n_rows_dev;   // row count read on device (nullptr: n_rows is exact)
+  int n_rows;              // launch bound on the rows (rows >= the device count are discarded)
+  int mt_per_wg;           // 16-row tiles per workgroup row (grid.y = ceil(tiles / mt_per_wg))
   // input rows [R][ldx]; element type float if x_f32 else the storage type
   const void* x;
   int ldx;
@@ -144,7 +145,9 @@ struct ReduceArgs {
 };
 
 // launchers (return hipError_t of the launch)
-hipError_t launch_gemm(int dtype, int pro, int epi, int row_tile, const GemmArgs& a, int grid, hipStream_t s);
+hipError_t launch_gemm(int dtype, int pro, int epi, int ksplit, const GemmArgs& a, hipStream_t s);
+int gemm_grid(int epi, int N, int ksplit);
+size_t gemm_ln_lds_bytes(int K, size_t elt);
 hipError_t launch_attn(int dtype, const AttnArgs& a, int R_max, hipStream_t s);
 hipError_t launch_embed(int dtype, const EmbedArgs& a, int R_max, hipStream_t s);
 hipError_t launch_ln(int dtype, const LnArgs& a, int R_max, hipStream_t s);
@@ -153,9 +156,5 @@ hipError_t launch_ctrl_init(const CtrlArgs& a, hipStream_t s);
 hipError_t launch_ctrl_step(const CtrlArgs& a, hipStream_t s);
 hipError_t launch_finalize(const CtrlArgs& a, hipStream_t s);
 
-// Number of 16-byte weight vectors a lane loads per K-chunk is one; the
-// elements per lane are 16 / sizeof(weight).  Kernels that must reproduce the
-// same LayerNorm statistics use this same split.
-inline int elems_per_lane(int dtype) { return dtype == DT_BF16 ? 8 : 4; }
 
 }  // namespace pdec

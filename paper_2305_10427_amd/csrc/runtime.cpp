@@ -31,8 +31,6 @@ pd_status fail(pd_status st, const std::string& msg) {
       return fail(PD_E_DEVICE, std::string(#call " failed: ") + hipGetErrorString(e_));     \
   } while (0)
 
-constexpr int kVocabWGs = 1024;     // workgroups of the fused vocabulary kernel (partials per row)
-constexpr int kMaxGemmWGs = 2048;
 constexpr int kFuseLnMaxRows = 64;  // above this the LayerNorm runs as its own kernel
 constexpr size_t kAlign = 256;
 
@@ -50,7 +48,11 @@ bool check_config(const pd_config* c, std::string* why) {
   if (c->d_model % c->n_heads != 0) { *why = "d_model must be a multiple of n_heads"; return false; }
   const int dh = c->d_model / c->n_heads;
   if (dh != 16 && dh != 32 && dh != 64 && dh != 128) { *why = "head dim must be 16, 32, 64 or 128"; return false; }
-  if (c->d_model % 8 != 0 || c->d_ff % 8 != 0) { *why = "d_model and d_ff must be multiples of 8"; return false; }
+  if (c->d_model % 32 != 0 || c->d_ff % 32 != 0) { *why = "d_model and d_ff must be multiples of 32"; return false; }
+  if (c->d_model > (c->dtype == PD_BF16 ? 1024 : 512)) {
+    *why = "d_model must be <= 1024 (bf16) or <= 512 (f32)";
+    return false;
+  }
   for (int id : {c->pad_id, c->bos_id, c->eos_id})
     if (id < 0 || id >= c->vocab) { *why = "special token id out of vocabulary"; return false; }
   if (!(c->ln_eps > 0.f)) { *why = "ln_eps must be positive"; return false; }
@@ -129,6 +131,7 @@ Layout plan(const pd_model& M, int max_batch, int max_src, int max_tgt) {
   };
   const size_t es = M.dt == DT_BF16 ? 2 : 4;
   const size_t rows_dec = static_cast<size_t>(max_batch) * max_tgt;
+  const size_t vocab_wgs = static_cast<size_t>(gemm_grid(EPI_ARGMAX, M.V, 1));
   const size_t rows = std::max(static_cast<size_t>(max_batch) * max_src, rows_dec);
   const size_t d = M.d;
   L.x_res = take(rows * d * es);
@@ -144,7 +147,7 @@ Layout plan(const pd_model& M, int max_batch, int max_src, int max_tgt) {
   const size_t self_kv = rows_dec * d * es * M.cfg.n_dec;
   L.self_k = take(self_kv);
   L.self_v = take(self_kv);
-  L.partials = take(rows_dec * kVocabWGs * sizeof(uint2));
+  L.partials = take(rows_dec * vocab_wgs * sizeof(uint2));
   L.new_tok = take(rows_dec * 4);
   L.row_flags = take(rows_dec * 4);
   L.row_sent = take(rows_dec * 4);
@@ -172,6 +175,12 @@ struct pd_ctx {
   int* stage_tgt;
   hipEvent_t stage_ev;
   std::vector<hipEvent_t> it_ev;
+  // vocabulary-kernel timing: event pairs per in-flight iteration slot
+  bool timing = false;
+  hipEvent_t tv0[2], tv1[2];
+  bool tv_pending[2] = {false, false};
+  int64_t tv_launches = 0;
+  double tv_ms = 0.0;
   int enc_B = 0, enc_nmax = 0;
   bool encoded = false;
 
@@ -179,18 +188,6 @@ struct pd_ctx {
 };
 
 namespace {
-
-int row_tile_for(int R_max) {
-  if (R_max <= 1) return 1;
-  if (R_max <= 2) return 2;
-  if (R_max <= 4) return 4;
-  return 8;
-}
-
-int gemm_grid(int N) {
-  const int groups = (N + 3) / 4;
-  return std::max(1, std::min((groups + 3) / 4, kMaxGemmWGs));
-}
 
 // Rows processed by one pass: count (device or host), layout and tokens.
 struct Rows {
@@ -205,7 +202,7 @@ GemmArgs gemm_base(const Rows& r) {
   GemmArgs g;
   std::memset(&g, 0, sizeof(g));
   g.n_rows_dev = r.n_dev;
-  g.n_rows = r.n_host;
+  g.n_rows = r.R_max;
   g.rows = r.map;
   return g;
 }
@@ -213,7 +210,7 @@ GemmArgs gemm_base(const Rows& r) {
 // One matrix product.  pro_ln: normalise x (float if x_f32) with (lg, lb)
 // first; for many rows the LayerNorm runs as its own kernel into ln_tmp.
 hipError_t run_gemm(const pd_ctx& C, const Rows& r, GemmArgs g, int epi, bool pro_ln, void* ln_tmp,
-                    int grid, hipStream_t s) {
+                    hipStream_t s) {
   const pd_model& M = *C.M;
   int pro = PRO_NONE;
   if (pro_ln) {
@@ -229,12 +226,13 @@ hipError_t run_gemm(const pd_ctx& C, const Rows& r, GemmArgs g, int epi, bool pr
       g.ln_out = nullptr;
     }
   }
-  return launch_gemm(M.dt, pro, epi, row_tile_for(r.R_max), g, grid, s);
+  const int ksplit = (epi == EPI_ARGMAX || epi == EPI_LOGITS) ? 1 : 4;
+  return launch_gemm(M.dt, pro, epi, ksplit, g, s);
 }
 
 // Decoder pass over the rows of one iteration (or the teacher-forced rows of
 // pd_debug_logits), ending in the fused vocabulary argmax or a logits store.
-hipError_t decoder_pass(pd_ctx& C, const Rows& r, float* logits, hipStream_t s) {
+hipError_t decoder_pass(pd_ctx& C, const Rows& r, float* logits, hipStream_t s, int slot = -1) {
   const pd_model& M = *C.M;
   const pd_config& cfg = M.cfg;
   const int d = M.d;
@@ -270,7 +268,7 @@ hipError_t decoder_pass(pd_ctx& C, const Rows& r, float* logits, hipStream_t s) 
     g.kc = C.at<char>(C.L.self_k) + l * self_layer; g.vc = C.at<char>(C.L.self_v) + l * self_layer;
     g.H = M.H; g.dh = M.dh; g.T = C.max_tgt; g.d = d;
     // post-LN with a separate LayerNorm kernel writes the residual stream itself
-    if ((e = run_gemm(C, r, g, EPI_QKV, ln_qkv, pre ? a_buf : x_res, gemm_grid(3 * d), s)) != hipSuccess) return e;
+    if ((e = run_gemm(C, r, g, EPI_QKV, ln_qkv, pre ? a_buf : x_res, s)) != hipSuccess) return e;
 
     AttnArgs aa{r.n_dev, r.n_host, q_buf, d, g.kc, g.vc, M.H, M.dh, C.max_tgt, r.map, 1, nullptr,
                 a_buf, d, 1.0f / std::sqrt(static_cast<float>(M.dh))};
@@ -280,7 +278,7 @@ hipError_t decoder_pass(pd_ctx& C, const Rows& r, float* logits, hipStream_t s) 
     g.x = a_buf; g.ldx = d; g.w = M.dec(l, D_WO); g.bias = M.dec(l, D_BO); g.N = d; g.K = d;
     g.resid = x_res; g.ldr = d; g.ldo = d;
     if (pre) g.out = x_res; else g.out_f32 = s_buf;
-    if ((e = run_gemm(C, r, g, EPI_RESID, false, nullptr, gemm_grid(d), s)) != hipSuccess) return e;
+    if ((e = run_gemm(C, r, g, EPI_RESID, false, nullptr, s)) != hipSuccess) return e;
 
     // cross-attention to the encoder memory
     g = gemm_base(r);
@@ -288,7 +286,7 @@ hipError_t decoder_pass(pd_ctx& C, const Rows& r, float* logits, hipStream_t s) 
     else { g.x = s_buf; g.x_f32 = 1; g.ln_g = M.dec(l, D_LN1G); g.ln_b = M.dec(l, D_LN1B); g.ln_out = x_res; g.ldlo = d; }
     g.ldx = d; g.ln_eps = cfg.ln_eps;
     g.w = M.dec(l, D_CWQ); g.bias = M.dec(l, D_CBQ); g.N = d; g.K = d; g.out_f32 = q_buf; g.ldo = d;
-    if ((e = run_gemm(C, r, g, EPI_F32, true, pre ? a_buf : x_res, gemm_grid(d), s)) != hipSuccess) return e;
+    if ((e = run_gemm(C, r, g, EPI_F32, true, pre ? a_buf : x_res, s)) != hipSuccess) return e;
 
     aa = AttnArgs{r.n_dev, r.n_host, q_buf, d, C.at<char>(C.L.cross_k) + l * cross_layer,
                   C.at<char>(C.L.cross_v) + l * cross_layer, M.H, M.dh, C.max_src, r.map, 0,
@@ -299,7 +297,7 @@ hipError_t decoder_pass(pd_ctx& C, const Rows& r, float* logits, hipStream_t s) 
     g.x = a_buf; g.ldx = d; g.w = M.dec(l, D_CWO); g.bias = M.dec(l, D_CBO); g.N = d; g.K = d;
     g.resid = x_res; g.ldr = d; g.ldo = d;
     if (pre) g.out = x_res; else g.out_f32 = s_buf;
-    if ((e = run_gemm(C, r, g, EPI_RESID, false, nullptr, gemm_grid(d), s)) != hipSuccess) return e;
+    if ((e = run_gemm(C, r, g, EPI_RESID, false, nullptr, s)) != hipSuccess) return e;
 
     // feed-forward
     g = gemm_base(r);
@@ -308,13 +306,13 @@ hipError_t decoder_pass(pd_ctx& C, const Rows& r, float* logits, hipStream_t s) 
     g.ldx = d; g.ln_eps = cfg.ln_eps;
     g.w = M.dec(l, D_W1); g.bias = M.dec(l, D_B1); g.N = M.dff; g.K = d;
     g.out = h_buf; g.ldo = M.dff; g.act = cfg.act_gelu ? 2 : 1;
-    if ((e = run_gemm(C, r, g, EPI_ACT, true, pre ? a_buf : x_res, gemm_grid(M.dff), s)) != hipSuccess) return e;
+    if ((e = run_gemm(C, r, g, EPI_ACT, true, pre ? a_buf : x_res, s)) != hipSuccess) return e;
 
     g = gemm_base(r);
     g.x = h_buf; g.ldx = M.dff; g.w = M.dec(l, D_W2); g.bias = M.dec(l, D_B2); g.N = d; g.K = M.dff;
     g.resid = x_res; g.ldr = d; g.ldo = d;
     if (pre) g.out = x_res; else g.out_f32 = s_buf;
-    if ((e = run_gemm(C, r, g, EPI_RESID, false, nullptr, gemm_grid(d), s)) != hipSuccess) return e;
+    if ((e = run_gemm(C, r, g, EPI_RESID, false, nullptr, s)) != hipSuccess) return e;
   }
 
   // vocabulary projection (tied embedding) fused with the argmax
@@ -325,12 +323,18 @@ hipError_t decoder_pass(pd_ctx& C, const Rows& r, float* logits, hipStream_t s) 
   g.w = M.w[0]; g.bias = M.w[1]; g.N = M.V; g.K = d; g.logit_scale = cfg.logit_scale;
   if (logits != nullptr) {
     g.out_f32 = logits; g.ldo = M.V;
-    return run_gemm(C, r, g, EPI_LOGITS, true, a_buf, gemm_grid(M.V), s);
+    return run_gemm(C, r, g, EPI_LOGITS, true, a_buf, s);
   }
+  const int vocab_wgs = gemm_grid(EPI_ARGMAX, M.V, 1);
   g.partials = C.at<uint2>(C.L.partials);
-  g.part_ld = kVocabWGs;
-  if ((e = run_gemm(C, r, g, EPI_ARGMAX, true, a_buf, kVocabWGs, s)) != hipSuccess) return e;
-  ReduceArgs ra{r.n_dev, C.at<uint2>(C.L.partials), kVocabWGs, kVocabWGs, C.at<int>(C.L.new_tok),
+  g.part_ld = vocab_wgs;
+  if (slot >= 0 && (e = hipEventRecord(C.tv0[slot], s)) != hipSuccess) return e;
+  if ((e = run_gemm(C, r, g, EPI_ARGMAX, true, a_buf, s)) != hipSuccess) return e;
+  if (slot >= 0) {
+    if ((e = hipEventRecord(C.tv1[slot], s)) != hipSuccess) return e;
+    C.tv_pending[slot] = true;
+  }
+  ReduceArgs ra{r.n_dev, C.at<uint2>(C.L.partials), vocab_wgs, vocab_wgs, C.at<int>(C.L.new_tok),
                 C.at<int>(C.L.row_flags)};
   return launch_argmax_reduce(ra, r.R_max, s);
 }
@@ -367,14 +371,14 @@ hipError_t encoder_pass(pd_ctx& C, const int32_t* src, int B, int n_max, hipStre
     g.out_f32 = q_buf; g.ldo = d; g.q_cols = d;
     g.kc = C.at<char>(C.L.enc_k); g.vc = C.at<char>(C.L.enc_v);
     g.H = M.H; g.dh = M.dh; g.T = C.max_src; g.d = d;
-    if ((e = launch_gemm(M.dt, PRO_NONE, EPI_QKV, 8, g, gemm_grid(3 * d), s)) != hipSuccess) return e;
+    if ((e = launch_gemm(M.dt, PRO_NONE, EPI_QKV, 4, g, s)) != hipSuccess) return e;
     AttnArgs aa{nullptr, R, q_buf, d, g.kc, g.vc, M.H, M.dh, C.max_src, r.map, 0, klen, a_buf, d, scale};
     if ((e = launch_attn(M.dt, aa, R, s)) != hipSuccess) return e;
     g = gemm_base(r);
     g.x = a_buf; g.ldx = d; g.w = M.enc(l, E_WO); g.bias = M.enc(l, E_BO); g.N = d; g.K = d;
     g.resid = x_res; g.ldr = d; g.ldo = d;
     if (pre) g.out = x_res; else g.out_f32 = s_buf;
-    if ((e = launch_gemm(M.dt, PRO_NONE, EPI_RESID, 8, g, gemm_grid(d), s)) != hipSuccess) return e;
+    if ((e = launch_gemm(M.dt, PRO_NONE, EPI_RESID, 4, g, s)) != hipSuccess) return e;
     if (!pre) {
       LnArgs la{nullptr, R, s_buf, 1, M.enc(l, E_LN1G), M.enc(l, E_LN1B), cfg.ln_eps, d, x_res};
       if ((e = launch_ln(M.dt, la, R, s)) != hipSuccess) return e;
@@ -388,12 +392,12 @@ hipError_t encoder_pass(pd_ctx& C, const int32_t* src, int B, int n_max, hipStre
     g = gemm_base(r);
     g.x = in; g.ldx = d; g.w = M.enc(l, E_W1); g.bias = M.enc(l, E_B1); g.N = M.dff; g.K = d;
     g.out = h_buf; g.ldo = M.dff; g.act = cfg.act_gelu ? 2 : 1;
-    if ((e = launch_gemm(M.dt, PRO_NONE, EPI_ACT, 8, g, gemm_grid(M.dff), s)) != hipSuccess) return e;
+    if ((e = launch_gemm(M.dt, PRO_NONE, EPI_ACT, 4, g, s)) != hipSuccess) return e;
     g = gemm_base(r);
     g.x = h_buf; g.ldx = M.dff; g.w = M.enc(l, E_W2); g.bias = M.enc(l, E_B2); g.N = d; g.K = M.dff;
     g.resid = x_res; g.ldr = d; g.ldo = d;
     if (pre) g.out = x_res; else g.out_f32 = s_buf;
-    if ((e = launch_gemm(M.dt, PRO_NONE, EPI_RESID, 8, g, gemm_grid(d), s)) != hipSuccess) return e;
+    if ((e = launch_gemm(M.dt, PRO_NONE, EPI_RESID, 4, g, s)) != hipSuccess) return e;
     if (!pre) {
       LnArgs la{nullptr, R, s_buf, 1, M.enc(l, E_LN2G), M.enc(l, E_LN2B), cfg.ln_eps, d, x_res};
       if ((e = launch_ln(M.dt, la, R, s)) != hipSuccess) return e;
@@ -411,7 +415,7 @@ hipError_t encoder_pass(pd_ctx& C, const int32_t* src, int B, int n_max, hipStre
     g.q_cols = 0;
     g.kc = C.at<char>(C.L.cross_k) + l * cross_layer; g.vc = C.at<char>(C.L.cross_v) + l * cross_layer;
     g.H = M.H; g.dh = M.dh; g.T = C.max_src; g.d = d;
-    if ((e = launch_gemm(M.dt, PRO_NONE, EPI_QKV, 8, g, gemm_grid(2 * d), s)) != hipSuccess) return e;
+    if ((e = launch_gemm(M.dt, PRO_NONE, EPI_QKV, 4, g, s)) != hipSuccess) return e;
   }
   return hipSuccess;
 }
@@ -425,6 +429,20 @@ pd_status stage_lengths(pd_ctx* C, int* stage, const int32_t* host, int B, int* 
 }
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+// Fold a completed event pair of the vocabulary kernel into the totals.
+hipError_t take_timing(pd_ctx& C, int slot) {
+  if (!C.tv_pending[slot]) return hipSuccess;
+  hipError_t e = hipEventSynchronize(C.tv1[slot]);
+  if (e != hipSuccess) return e;
+  float ms = 0.f;
+  e = hipEventElapsedTime(&ms, C.tv0[slot], C.tv1[slot]);
+  if (e != hipSuccess) return e;
+  C.tv_ms += ms;
+  C.tv_launches += 1;
+  C.tv_pending[slot] = false;
+  return hipSuccess;
+}
 
 }  // namespace
 
@@ -519,6 +537,10 @@ pd_status pd_ctx_create(const pd_model* model, int32_t max_batch, int32_t max_sr
   hipEventCreateWithFlags(&c->stage_ev, hipEventDisableTiming);
   c->it_ev.resize(2);
   for (auto& ev : c->it_ev) hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+  for (int i = 0; i < 2; ++i) {
+    hipEventCreate(&c->tv0[i]);
+    hipEventCreate(&c->tv1[i]);
+  }
   *out = c;
   return PD_OK;
 }
@@ -527,6 +549,11 @@ void pd_ctx_destroy(pd_ctx* ctx) {
   if (ctx == nullptr) return;
   hipEventSynchronize(ctx->stage_ev);
   for (auto ev : ctx->it_ev) { hipEventSynchronize(ev); hipEventDestroy(ev); }
+  for (int i = 0; i < 2; ++i) {
+    hipEventSynchronize(ctx->tv1[i]);
+    hipEventDestroy(ctx->tv0[i]);
+    hipEventDestroy(ctx->tv1[i]);
+  }
   hipEventDestroy(ctx->stage_ev);
   hipHostFree(ctx->host_pinned);
   delete ctx;
@@ -614,7 +641,10 @@ pd_status pd_decode(pd_ctx* ctx, int32_t mode, int32_t block, int32_t horizon, i
   if (e != hipSuccess) return fail(PD_E_DEVICE, std::string("init launch: ") + hipGetErrorString(e));
   volatile int* done = C.host_pinned;
   for (int it = 0; it < iters; ++it) {
-    e = decoder_pass(C, r, nullptr, s);
+    const int slot = C.timing ? (it & 1) : -1;
+    if (slot >= 0 && (e = take_timing(C, slot)) != hipSuccess)
+      return fail(PD_E_DEVICE, std::string("timing: ") + hipGetErrorString(e));
+    e = decoder_pass(C, r, nullptr, s, slot);
     if (e == hipSuccess) e = launch_ctrl_step(ca, s);
     if (e == hipSuccess) e = hipEventRecord(C.it_ev[it & 1], s);
     if (e != hipSuccess) return fail(PD_E_DEVICE, std::string("iteration launch: ") + hipGetErrorString(e));
@@ -630,6 +660,26 @@ pd_status pd_decode(pd_ctx* ctx, int32_t mode, int32_t block, int32_t horizon, i
   }
   e = launch_finalize(ca, s);
   if (e != hipSuccess) return fail(PD_E_DEVICE, std::string("finalize launch: ") + hipGetErrorString(e));
+  if (C.timing) {
+    for (int slot = 0; slot < 2; ++slot)
+      if ((e = take_timing(C, slot)) != hipSuccess) return fail(PD_E_DEVICE, std::string("timing: ") + hipGetErrorString(e));
+  }
+  return PD_OK;
+}
+
+pd_status pd_ctx_set_timing(pd_ctx* ctx, int32_t enable) {
+  if (ctx == nullptr) return fail(PD_E_ARG, "null context");
+  ctx->timing = enable != 0;
+  ctx->tv_launches = 0;
+  ctx->tv_ms = 0.0;
+  ctx->tv_pending[0] = ctx->tv_pending[1] = false;
+  return PD_OK;
+}
+
+pd_status pd_ctx_vocab_timing(const pd_ctx* ctx, int64_t* launches, double* total_ms) {
+  if (ctx == nullptr || launches == nullptr || total_ms == nullptr) return fail(PD_E_ARG, "null argument");
+  *launches = ctx->tv_launches;
+  *total_ms = ctx->tv_ms;
   return PD_OK;
 }
 

@@ -41,7 +41,7 @@ class pd_config(ctypes.Structure):
 
 EXPORTS = ("pd_weight_count", "pd_weight_shape", "pd_model_create", "pd_model_destroy",
            "pd_ctx_workspace_bytes", "pd_ctx_create", "pd_ctx_destroy", "pd_encode", "pd_decode",
-           "pd_debug_logits", "pd_last_error")
+           "pd_debug_logits", "pd_ctx_set_timing", "pd_ctx_vocab_timing", "pd_last_error")
 
 _lib = None
 
@@ -75,6 +75,10 @@ def load_library(path: str = LIB_PATH):
     L.pd_decode.restype = I32
     L.pd_debug_logits.argtypes = [VP, VP, I32, VP, VP]
     L.pd_debug_logits.restype = I32
+    L.pd_ctx_set_timing.argtypes = [VP, I32]
+    L.pd_ctx_set_timing.restype = I32
+    L.pd_ctx_vocab_timing.argtypes = [VP, P(I64), P(ctypes.c_double)]
+    L.pd_ctx_vocab_timing.restype = I32
     L.pd_last_error.argtypes = []
     L.pd_last_error.restype = ctypes.c_char_p
     _lib = L
@@ -204,6 +208,15 @@ class Context:
                                               ctypes.c_void_p(logits.data_ptr()),
                                               ctypes.c_void_p(_stream_handle(stream))))
         return logits
+
+    def set_timing(self, enable: bool):
+        _check(load_library().pd_ctx_set_timing(self.handle, int(enable)))
+
+    def vocab_timing(self):
+        """(launches, total_ms) of the fused vocabulary kernel since set_timing(True)."""
+        n, ms = ctypes.c_int64(), ctypes.c_double()
+        _check(load_library().pd_ctx_vocab_timing(self.handle, ctypes.byref(n), ctypes.byref(ms)))
+        return n.value, ms.value
 
     def __del__(self):
         if getattr(self, "handle", None) and _lib is not None:
