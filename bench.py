@@ -36,6 +36,13 @@ def run_mode(ctxs, sents, outs, mode, block, steps, warmup, timing=False):
     import torch
     n = len(sents)
     order = [i % n for i in range(warmup + steps)]
+    # one-time setup: every context captures and instantiates its iteration
+    # graph for this mode (and timing setting) on its first decode
+    for i in range(n):
+        ctxs[i].set_timing(timing)
+        ctxs[i].decode(mode, [sents[i][1]], block=block, out=outs[i])
+        ctxs[i].set_timing(False)
+    torch.cuda.synchronize()
     for i in order[:warmup]:
         ctxs[i].decode(mode, [sents[i][1]], block=block, out=outs[i])
     torch.cuda.synchronize()

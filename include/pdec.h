@@ -202,7 +202,8 @@ pd_status pd_debug_logits(pd_ctx* ctx, const int32_t* tgt_in, int32_t T, float* 
  * pair of HIP events on its stream around every launch of that kernel and
  * accumulates their elapsed times; pd_ctx_vocab_timing returns the number of
  * launches and their total milliseconds since the last pd_ctx_set_timing.
- * Timing adds two event records per iteration.
+ * Timing adds two event records per iteration; timed iterations are launched
+ * kernel by kernel instead of replaying the captured iteration graph.
  */
 pd_status pd_ctx_set_timing(pd_ctx* ctx, int32_t enable);
 pd_status pd_ctx_vocab_timing(const pd_ctx* ctx, int64_t* launches, double* total_ms);

@@ -120,20 +120,22 @@ __device__ __forceinline__ uint32_t float_key(float f) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-// LayerNorm statistics of one row of K elements (K a multiple of 8, K <= 1024)
-// computed by a group of 16 consecutive lanes.  Lane j of the group holds
-// elements k = 8*j + 128*t + e (t < 8, e < 8, k < K) in v[t][e] and sums them
-// in that order; the 16 lane sums are combined by xor-1, 2, 4, 8 pairings.
+// LayerNorm statistics of one row of K elements (K a multiple of 8,
+// K <= 128 * NT) computed by a group of 16 consecutive lanes.  Lane j of the
+// group holds elements k = 8*j + 128*t + e (t < NT, e < 8, k < K) in v[t][e]
+// and sums them in that order (the result does not depend on NT once
+// 128 * NT >= K: absent chunks are never added); the 16 lane sums are combined by xor-1, 2, 4, 8 pairings.
 // Mean first, then the mean of squared deviations (two passes over the values
 // held in registers).  All 64 lanes of the wave must call this (invalid rows
 // pass valid = false and contribute zeros).  The matrix-product prologue and
 // the row LayerNorm kernel both use it, so a row's statistics are bitwise the
 // same wherever they are computed.
-template <typename XT>
+template <typename XT, int NT>
 __device__ __forceinline__ void ln_stats_g16(const XT* x, int K, int j, float eps, bool valid,
                                              float (&v)[8][8], float& mean, float& rstd) {
+  static_assert(NT >= 1 && NT <= 8, "at most 1024 elements");
 #pragma unroll
-  for (int t = 0; t < 8; ++t) {
+  for (int t = 0; t < NT; ++t) {
     const int k0 = 8 * j + 128 * t;
     if (valid && k0 < K) load_n<XT, 8>(x, k0, v[t]);
     else {
@@ -143,7 +145,7 @@ __device__ __forceinline__ void ln_stats_g16(const XT* x, int K, int j, float ep
   }
   float s = 0.f;
 #pragma unroll
-  for (int t = 0; t < 8; ++t)
+  for (int t = 0; t < NT; ++t)
 #pragma unroll
     for (int e = 0; e < 8; ++e) s += v[t][e];
 #pragma unroll
@@ -151,7 +153,7 @@ __device__ __forceinline__ void ln_stats_g16(const XT* x, int K, int j, float ep
   mean = s / static_cast<float>(K);
   float q = 0.f;
 #pragma unroll
-  for (int t = 0; t < 8; ++t) {
+  for (int t = 0; t < NT; ++t) {
     if (8 * j + 128 * t < K) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) {

@@ -86,7 +86,16 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
 // ---------------------------------------------------------------------------
 // Token embedding x = E[tok] * scale + PE(pos), PE the interleaved sinusoid
 // (columns 2i, 2i+1 = sin, cos of pos * 10000^(-2i/d)), evaluated in double.
-template <typename WT, typename AT>
+template <typename WT>
+__device__ __forceinline__ float embed_elem(const WT* emb, int tok, int p, int c, int d, float scale, int vocab) {
+  tok = min(max(tok, 0), vocab - 1);
+  const double freq = exp(-log(10000.0) * static_cast<double>(c & ~1) / d);
+  const double ang = static_cast<double>(p) * freq;
+  const float pe = static_cast<float>((c & 1) ? cos(ang) : sin(ang));
+  return Elt<WT>::load(emb, static_cast<size_t>(tok) * d + c) * scale + pe;
+}
+
+template <typename WT>
 __global__ __launch_bounds__(256) void k_embed(EmbedArgs a) {
   const int R = a.n_rows_dev ? *a.n_rows_dev : a.n_rows;
   const size_t total = static_cast<size_t>(R) * a.d;
@@ -95,12 +104,8 @@ __global__ __launch_bounds__(256) void k_embed(EmbedArgs a) {
     const int c = static_cast<int>(t - static_cast<size_t>(row) * a.d);
     int s, p;
     row_place(a.rows, row, s, p);
-    const int tok = min(max(a.tok[row], 0), a.vocab - 1);
-    const double freq = exp(-log(10000.0) * static_cast<double>(c & ~1) / a.d);
-    const double ang = static_cast<double>(p) * freq;
-    const float pe = static_cast<float>((c & 1) ? cos(ang) : sin(ang));
-    const float e = Elt<WT>::load(static_cast<const WT*>(a.emb), static_cast<size_t>(tok) * a.d + c);
-    Elt<AT>::store(static_cast<AT*>(a.out), t, e * a.scale + pe);
+    Elt<WT>::store(static_cast<WT*>(a.out), t,
+                   embed_elem<WT>(static_cast<const WT*>(a.emb), a.tok[row], p, c, a.d, a.scale, a.vocab));
   }
 }
 
@@ -108,7 +113,7 @@ __global__ __launch_bounds__(256) void k_embed(EmbedArgs a) {
 // Row LayerNorm, 4 rows per wave with 16 lanes per row, statistics by
 // ln_stats_g16 (the same lane split and pairing as the LayerNorm prologue of
 // the matrix products).
-template <typename WT, typename XT>
+template <typename WT, typename XT, int NT>
 __global__ __launch_bounds__(256) void k_ln(LnArgs a) {
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = threadIdx.x / kWave;
@@ -118,10 +123,10 @@ __global__ __launch_bounds__(256) void k_ln(LnArgs a) {
   const bool ok = row < R;
   const XT* x = static_cast<const XT*>(a.x) + static_cast<size_t>(ok ? row : 0) * a.d;
   float v[8][8], mean, rstd;
-  ln_stats_g16<XT>(x, a.d, j, a.eps, ok, v, mean, rstd);
+  ln_stats_g16<XT, NT>(x, a.d, j, a.eps, ok, v, mean, rstd);
   if (!ok) return;
 #pragma unroll
-  for (int t = 0; t < 8; ++t) {
+  for (int t = 0; t < NT; ++t) {
     const int k0 = 8 * j + 128 * t;
     if (k0 < a.d) {
       float g[8], b[8];
@@ -132,38 +137,6 @@ __global__ __launch_bounds__(256) void k_ln(LnArgs a) {
         Elt<WT>::store(static_cast<WT*>(a.out), static_cast<size_t>(row) * a.d + k0 + e,
                        ln_apply(v[t][e], mean, rstd, g[e], b[e]));
     }
-  }
-}
-
-// ---------------------------------------------------------------------------
-// Final argmax of each row over the per-workgroup partials of the fused
-// vocabulary kernel: largest logit, lowest index on exact ties.
-__global__ __launch_bounds__(256) void k_argmax_reduce(ReduceArgs a) {
-  const int lane = threadIdx.x & (kWave - 1);
-  const int row = blockIdx.x * 4 + threadIdx.x / kWave;
-  const int R = *a.n_rows_dev;
-  if (row >= R) return;
-  uint32_t bk = 0;
-  uint32_t bi = 0x7fffffffu;
-  uint32_t nf = 0;
-  const uint2* p = a.partials + static_cast<size_t>(row) * a.part_ld;
-  for (int t = lane; t < a.n_parts; t += kWave) {
-    const uint2 v = p[t];
-    const uint32_t i = v.y & 0x7fffffffu;
-    nf |= v.y >> 31;
-    if (v.x > bk || (v.x == bk && i < bi)) { bk = v.x; bi = i; }
-  }
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    const uint32_t ok = __shfl_xor(bk, off);
-    const uint32_t oi = __shfl_xor(bi, off);
-    nf |= __shfl_xor(nf, off);
-    if (ok > bk || (ok == bk && oi < bi)) { bk = ok; bi = oi; }
-  }
-  if (lane == 0) {
-    const bool none = bk == 0;           // no finite logit in the row
-    a.new_tok[row] = none ? 0 : static_cast<int>(bi);
-    a.row_flags[row] = (nf || none) ? 1 : 0;
   }
 }
 
@@ -196,8 +169,10 @@ __device__ __forceinline__ int block_len(const CtrlArgs& a, int i, int m) {
   }
 }
 
-// Lay out the rows of the next iteration (sentence order, block order) and
-// publish the row count.  Single workgroup.
+// Lay out the rows of the next iteration (sentence order, block order),
+// publish the row count and, when the control step owns the embedding,
+// write the embedded rows.  Single workgroup.
+template <typename WT>
 __device__ void emit_rows(const CtrlArgs& a) {
   __shared__ int s_total;
   if (threadIdx.x == 0) {
@@ -221,14 +196,27 @@ __device__ void emit_rows(const CtrlArgs& a) {
       a.row_tok[row] = p == 0 ? a.bos_id : y[p - 1];
     }
   }
+  const int total = s_total;
   if (threadIdx.x == 0) {
-    *a.n_rows = s_total;
+    *a.n_rows = total;
     if (a.host_done != nullptr)
-      __hip_atomic_store(a.host_done, s_total == 0 ? 1 : 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+      __hip_atomic_store(a.host_done, total == 0 ? 1 : 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  }
+  if (a.x_out != nullptr) {
+    __syncthreads();
+    const size_t n = static_cast<size_t>(total) * a.d;
+    for (size_t t = threadIdx.x; t < n; t += blockDim.x) {
+      const int row = static_cast<int>(t / a.d);
+      const int c = static_cast<int>(t - static_cast<size_t>(row) * a.d);
+      Elt<WT>::store(static_cast<WT*>(a.x_out), t,
+                     embed_elem<WT>(static_cast<const WT*>(a.emb), a.row_tok[row], a.row_pos[row], c, a.d,
+                                    a.emb_scale, a.vocab));
+    }
   }
 }
 
-__global__ __launch_bounds__(256) void k_ctrl_init(CtrlArgs a) {
+template <typename WT>
+__global__ __launch_bounds__(1024) void k_ctrl_init(CtrlArgs a) {
   for (int s = threadIdx.x; s < a.B; s += blockDim.x) {
     const int m = a.tgt_m[s];
     SentState st;
@@ -245,11 +233,46 @@ __global__ __launch_bounds__(256) void k_ctrl_init(CtrlArgs a) {
     for (int t = 0; t < a.ldy; ++t) y[t] = a.pad_id;      // InitT: all [PAD]
   }
   __syncthreads();
-  emit_rows(a);
+  emit_rows<WT>(a);
 }
 
-__global__ __launch_bounds__(256) void k_ctrl_step(CtrlArgs a) {
-  if (*a.n_rows == 0) return;
+// Argmax of each row over the per-workgroup partials of the fused vocabulary
+// kernel (largest logit, lowest index on exact ties), one wave per row.
+__device__ __forceinline__ void reduce_row(const uint2* p, int n_parts, int lane, int* tok, int* flag) {
+  uint32_t bk = 0;
+  uint32_t bi = 0x7fffffffu;
+  uint32_t nf = 0;
+  for (int t = lane; t < n_parts; t += kWave) {
+    const uint2 v = p[t];
+    const uint32_t i = v.y & 0x7fffffffu;
+    nf |= v.y >> 31;
+    if (v.x > bk || (v.x == bk && i < bi)) { bk = v.x; bi = i; }
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const uint32_t ok = __shfl_xor(bk, off);
+    const uint32_t oi = __shfl_xor(bi, off);
+    nf |= __shfl_xor(nf, off);
+    if (ok > bk || (ok == bk && oi < bi)) { bk = ok; bi = oi; }
+  }
+  if (lane == 0) {
+    const bool none = bk == 0;           // no finite logit in the row
+    *tok = none ? 0 : static_cast<int>(bi);
+    *flag = (nf || none) ? 1 : 0;
+  }
+}
+
+template <typename WT>
+__global__ __launch_bounds__(1024) void k_ctrl_step(CtrlArgs a) {
+  const int R = *a.n_rows;
+  if (R == 0) return;
+  if (a.partials != nullptr) {
+    const int lane = threadIdx.x & (kWave - 1);
+    for (int row = threadIdx.x / kWave; row < R; row += blockDim.x / kWave)
+      reduce_row(a.partials + static_cast<size_t>(row) * a.part_ld, a.n_parts, lane,
+                 const_cast<int*>(a.new_tok) + row, const_cast<int*>(a.row_flags) + row);
+    __syncthreads();
+  }
   for (int s = threadIdx.x; s < a.B; s += blockDim.x) {
     SentState st = a.st[s];
     if (st.done) continue;
@@ -284,7 +307,7 @@ __global__ __launch_bounds__(256) void k_ctrl_step(CtrlArgs a) {
     a.st[s] = st;
   }
   __syncthreads();
-  emit_rows(a);
+  emit_rows<WT>(a);
 }
 
 // Outputs: ids cut after the first [EOS] (inclusive) and [PAD]-filled, the
@@ -305,6 +328,13 @@ __global__ __launch_bounds__(256) void k_finalize(CtrlArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_argmax_reduce(ReduceArgs a) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int row = blockIdx.x * 4 + threadIdx.x / kWave;
+  if (row >= *a.n_rows_dev) return;
+  reduce_row(a.partials + static_cast<size_t>(row) * a.part_ld, a.n_parts, lane, a.new_tok + row, a.row_flags + row);
+}
+
 template <typename AT>
 static hipError_t launch_attn_t(const AttnArgs& a, int grid, hipStream_t s) {
   switch (a.dh) {
@@ -328,8 +358,8 @@ hipError_t launch_embed(int dtype, const EmbedArgs& a, int R_max, hipStream_t s)
   const size_t total = static_cast<size_t>(R_max) * a.d;
   const int grid = static_cast<int>(std::min<size_t>((total + 255) / 256, 4096));
   if (grid == 0) return hipSuccess;
-  if (dtype == DT_BF16) hipLaunchKernelGGL((k_embed<bf16_t, bf16_t>), dim3(grid), dim3(256), 0, s, a);
-  else hipLaunchKernelGGL((k_embed<float, float>), dim3(grid), dim3(256), 0, s, a);
+  if (dtype == DT_BF16) hipLaunchKernelGGL((k_embed<bf16_t>), dim3(grid), dim3(256), 0, s, a);
+  else hipLaunchKernelGGL((k_embed<float>), dim3(grid), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
@@ -338,27 +368,36 @@ hipError_t launch_ln(int dtype, const LnArgs& a, int R_max, hipStream_t s) {
   if (grid == 0) return hipSuccess;
   if (a.d % 8 != 0 || a.d > 1024) return hipErrorInvalidValue;
   if (dtype == DT_BF16) {
-    if (a.x_f32) hipLaunchKernelGGL((k_ln<bf16_t, float>), dim3(grid), dim3(256), 0, s, a);
-    else hipLaunchKernelGGL((k_ln<bf16_t, bf16_t>), dim3(grid), dim3(256), 0, s, a);
+    if (a.d > 512) {
+      if (a.x_f32) hipLaunchKernelGGL((k_ln<bf16_t, float, 8>), dim3(grid), dim3(256), 0, s, a);
+      else hipLaunchKernelGGL((k_ln<bf16_t, bf16_t, 8>), dim3(grid), dim3(256), 0, s, a);
+    } else {
+      if (a.x_f32) hipLaunchKernelGGL((k_ln<bf16_t, float, 4>), dim3(grid), dim3(256), 0, s, a);
+      else hipLaunchKernelGGL((k_ln<bf16_t, bf16_t, 4>), dim3(grid), dim3(256), 0, s, a);
+    }
   } else {
-    hipLaunchKernelGGL((k_ln<float, float>), dim3(grid), dim3(256), 0, s, a);
+    if (a.d > 512) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((k_ln<float, float, 4>), dim3(grid), dim3(256), 0, s, a);
   }
   return hipGetLastError();
 }
 
 hipError_t launch_argmax_reduce(const ReduceArgs& a, int R_max, hipStream_t s) {
+  if (R_max <= 0) return hipSuccess;
   const int grid = (R_max + 3) / 4;
   hipLaunchKernelGGL(k_argmax_reduce, dim3(grid), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
-hipError_t launch_ctrl_init(const CtrlArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(k_ctrl_init, dim3(1), dim3(256), 0, s, a);
+hipError_t launch_ctrl_init(int dtype, const CtrlArgs& a, hipStream_t s) {
+  if (dtype == DT_BF16) hipLaunchKernelGGL(k_ctrl_init<bf16_t>, dim3(1), dim3(1024), 0, s, a);
+  else hipLaunchKernelGGL(k_ctrl_init<float>, dim3(1), dim3(1024), 0, s, a);
   return hipGetLastError();
 }
 
-hipError_t launch_ctrl_step(const CtrlArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(k_ctrl_step, dim3(1), dim3(256), 0, s, a);
+hipError_t launch_ctrl_step(int dtype, const CtrlArgs& a, hipStream_t s) {
+  if (dtype == DT_BF16) hipLaunchKernelGGL(k_ctrl_step<bf16_t>, dim3(1), dim3(1024), 0, s, a);
+  else hipLaunchKernelGGL(k_ctrl_step<float>, dim3(1), dim3(1024), 0, s, a);
   return hipGetLastError();
 }
 

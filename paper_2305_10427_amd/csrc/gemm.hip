@@ -51,6 +51,14 @@ template <> struct Mma<bf16_t> {
   }
   static __device__ __forceinline__ frag load(const bf16_t* p) { return *reinterpret_cast<const uint4*>(p); }
   static __device__ __forceinline__ frag zero() { return make_uint4(0, 0, 0, 0); }
+  static __device__ __forceinline__ void unpack(frag f, float* v) {
+    const uint32_t w[4] = {f.x, f.y, f.z, f.w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      v[2 * j] = __uint_as_float(w[j] << 16);
+      v[2 * j + 1] = __uint_as_float(w[j] & 0xffff0000u);
+    }
+  }
   static __device__ __forceinline__ frag pack(const float* v) {
     uint32_t w[4];
 #pragma unroll
@@ -72,6 +80,7 @@ template <> struct Mma<float> {
   }
   static __device__ __forceinline__ frag load(const float* p) { return *reinterpret_cast<const float4*>(p); }
   static __device__ __forceinline__ frag zero() { return make_float4(0.f, 0.f, 0.f, 0.f); }
+  static __device__ __forceinline__ void unpack(frag f, float* v) { v[0] = f.x; v[1] = f.y; v[2] = f.z; v[3] = f.w; }
   static __device__ __forceinline__ frag pack(const float* v) { return make_float4(v[0], v[1], v[2], v[3]); }
 };
 
@@ -79,9 +88,9 @@ __device__ __forceinline__ float gelu_erf(float v) {
   return 0.5f * v * (1.0f + erff(v * 0.70710678118654752f));
 }
 
-constexpr int kUnroll = 8;   // MFMA steps whose loads are issued together
+constexpr int kDepth = 8;   // MFMA steps per weight batch; two batches are in flight
 
-template <typename WT, int PRO, int EPI, int XF32, int KSPLIT>
+template <typename WT, int PRO, int EPI, int XF32, int KSPLIT, int LNT>
 __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
   using AT = WT;
   using XT = typename std::conditional<XF32 != 0, float, AT>::type;
@@ -89,6 +98,7 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
   using frag = typename MM::frag;
   constexpr int KS = MM::KS;
   constexpr int EPL = MM::EPL;
+  constexpr int D = kDepth;
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = threadIdx.x / kWave;
   const int lr = lane & 15;          // row (X) / column (W) fed by this lane
@@ -101,9 +111,33 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
   const int s_end = KSPLIT == 4 ? (n_steps * (wave + 1)) / 4 : n_steps;
   const WT* __restrict__ W = static_cast<const WT*>(a.w);
   const XT* __restrict__ X = static_cast<const XT*>(a.x);
+  const WT* __restrict__ wrow = W + static_cast<size_t>(col < N ? col : 0) * K + EPL * lg;
   const int R_max = a.n_rows;        // rows that may be read (launch bound)
-  const int R = a.n_rows_dev ? *a.n_rows_dev : a.n_rows;
+  const int m_first = blockIdx.y * 16 * a.mt_per_wg;
+  const int m_last = min(R_max, m_first + 16 * a.mt_per_wg);
+
+  // Loads that do not depend on the previous kernel go out first: the first
+  // weight batch, the bias, the residual of the first tile's outputs.
+  frag bcur[D];
+#pragma unroll
+  for (int u = 0; u < D; ++u) {
+    const int step = s_begin + u;
+    bcur[u] = (step < s_end && col < N) ? MM::load(wrow + step * KS) : MM::zero();
+  }
   const float bias_v = (col < N) ? Elt<WT>::load(static_cast<const WT*>(a.bias), col) : 0.f;
+  constexpr int NE = KSPLIT == 4 ? 1 : 4;       // output elements finished per lane
+  float rpre[NE];
+  if constexpr (EPI == EPI_RESID) {
+#pragma unroll
+    for (int e = 0; e < NE; ++e) {
+      const int row = m_first + 4 * lg + (KSPLIT == 4 ? wave : e);
+      const size_t ri = static_cast<size_t>(row) * a.ldr + col;
+      rpre[e] = (row < R_max && col < N)
+                    ? (a.resid_f32 ? static_cast<const float*>(a.resid)[ri] : Elt<AT>::load(static_cast<const AT*>(a.resid), ri))
+                    : 0.f;
+    }
+  }
+  const int R = a.n_rows_dev ? *a.n_rows_dev : a.n_rows;
 
   __shared__ float s_part[4][4][64];
   __shared__ uint32_t s_key[4][16];
@@ -113,22 +147,27 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
   AT* sA = reinterpret_cast<AT*>(s_dyn);
   const int lda = K + 16 / static_cast<int>(sizeof(AT));
 
-  const int m_first = blockIdx.y * 16 * a.mt_per_wg;
-  const int m_last = min(R_max, m_first + 16 * a.mt_per_wg);
   for (int m0 = m_first; m0 < m_last; m0 += 16) {
     if (m0 > m_first && m0 >= R) break;
     const int arow = m0 + lr;                 // X row fed by this lane
     const bool arow_ok = arow < R_max;
+    if (m0 != m_first) {
+#pragma unroll
+      for (int u = 0; u < D; ++u) {
+        const int step = s_begin + u;
+        bcur[u] = (step < s_end && col < N) ? MM::load(wrow + step * KS) : MM::zero();
+      }
+    }
     if constexpr (PRO == PRO_LN) {
       // wave w normalises rows 4w .. 4w+3 of the tile, 16 lanes per row
       const int tr = 4 * wave + lg;
       const int row = m0 + tr;
       const bool ok = row < R_max;
       float v[8][8], mean, rstd;
-      ln_stats_g16<XT>(X + static_cast<size_t>(ok ? row : 0) * a.ldx, K, lr, a.ln_eps, ok, v, mean, rstd);
+      ln_stats_g16<XT, LNT>(X + static_cast<size_t>(ok ? row : 0) * a.ldx, K, lr, a.ln_eps, ok, v, mean, rstd);
       const bool write_out = a.ln_out != nullptr && blockIdx.x == 0 && row < R;
 #pragma unroll
-      for (int t = 0; t < 8; ++t) {
+      for (int t = 0; t < LNT; ++t) {
         const int k0 = 8 * lr + 128 * t;
         if (k0 < K) {
           float gv[8], bv[8], y[8];
@@ -148,13 +187,22 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
       __syncthreads();
     }
     floatx4_t acc = {0.f, 0.f, 0.f, 0.f};
-    for (int s0 = s_begin; s0 < s_end; s0 += kUnroll) {
-      frag af[kUnroll], bf[kUnroll];
+    for (int s0 = s_begin; s0 < s_end; s0 += D) {
+      // next weight batch goes out before this batch's products
+      frag bnext[D];
+      const bool more = s0 + D < s_end;
+      if (more) {
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
+        for (int u = 0; u < D; ++u) {
+          const int step = s0 + D + u;
+          bnext[u] = (step < s_end && col < N) ? MM::load(wrow + step * KS) : MM::zero();
+        }
+      }
+      frag af[D];
+#pragma unroll
+      for (int u = 0; u < D; ++u) {
         const int k = (s0 + u) * KS + EPL * lg;
         const bool ok = s0 + u < s_end;
-        bf[u] = (ok && col < N) ? MM::load(W + static_cast<size_t>(col) * K + k) : MM::zero();
         if constexpr (PRO == PRO_LN) {
           af[u] = ok ? MM::load(sA + static_cast<size_t>(lr) * lda + k) : MM::zero();
         } else {
@@ -168,28 +216,30 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
         }
       }
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) acc = MM::step(af[u], bf[u], acc);
+      for (int u = 0; u < D; ++u) acc = MM::step(af[u], bcur[u], acc);
+      if (more) {
+#pragma unroll
+        for (int u = 0; u < D; ++u) bcur[u] = bnext[u];
+      }
     }
     if constexpr (PRO == PRO_LN) __syncthreads();   // sA is rewritten by the next tile
     // combine the K-split partials: wave w finishes element i = w of every lane
     float cv[4];
-    int n_elems;
     if constexpr (KSPLIT == 4) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) s_part[wave][i][lane] = acc[i];
       __syncthreads();
       cv[0] = ((s_part[0][wave][lane] + s_part[1][wave][lane]) + s_part[2][wave][lane]) + s_part[3][wave][lane];
-      n_elems = 1;
       __syncthreads();
     } else {
 #pragma unroll
       for (int i = 0; i < 4; ++i) cv[i] = acc[i];
-      n_elems = 4;
     }
     uint32_t bk[4] = {0, 0, 0, 0};
     int bi[4] = {0x7fffffff, 0x7fffffff, 0x7fffffff, 0x7fffffff};
     int nf = 0;
-    for (int e = 0; e < n_elems; ++e) {
+#pragma unroll
+    for (int e = 0; e < NE; ++e) {
       const int i = KSPLIT == 4 ? wave : e;
       const int row = m0 + 4 * lg + i;
       const float v = cv[e];
@@ -202,8 +252,9 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
         Elt<AT>::store(static_cast<AT*>(a.out), static_cast<size_t>(row) * a.ldo + col, t);
       } else if constexpr (EPI == EPI_RESID) {
         const size_t ri = static_cast<size_t>(row) * a.ldr + col;
-        const float rv = a.resid_f32 ? static_cast<const float*>(a.resid)[ri]
-                                     : Elt<AT>::load(static_cast<const AT*>(a.resid), ri);
+        const float rv = m0 == m_first ? rpre[e]
+                         : (a.resid_f32 ? static_cast<const float*>(a.resid)[ri]
+                                        : Elt<AT>::load(static_cast<const AT*>(a.resid), ri));
         const float t = (v + bias_v) + rv;
         if (a.out_f32 != nullptr) a.out_f32[static_cast<size_t>(row) * a.ldo + col] = t;
         else Elt<AT>::store(static_cast<AT*>(a.out), static_cast<size_t>(row) * a.ldo + col, t);
@@ -277,18 +328,27 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
 
 namespace {
 
-template <typename WT, int PRO, int EPI, int XF32>
-hipError_t launch_t(GemmArgs a, int ksplit, hipStream_t s) {
+template <typename WT, int PRO, int EPI, int XF32, int LNT>
+hipError_t launch_k(GemmArgs a, int ksplit, hipStream_t s) {
   const int tiles = (a.n_rows + 15) / 16;
   const int gy = tiles < 64 ? tiles : 64;
   a.mt_per_wg = (tiles + gy - 1) / gy;
   const size_t lds = PRO == PRO_LN ? gemm_ln_lds_bytes(a.K, sizeof(WT)) : 0;
   if (EPI == EPI_ARGMAX || ksplit != 4) {
-    hipLaunchKernelGGL((k_gemm<WT, PRO, EPI, XF32, 1>), dim3(gemm_grid(EPI, a.N, 1), gy), dim3(256), lds, s, a);
+    hipLaunchKernelGGL((k_gemm<WT, PRO, EPI, XF32, 1, LNT>), dim3(gemm_grid(EPI, a.N, 1), gy), dim3(256), lds, s, a);
   } else if constexpr (EPI != EPI_ARGMAX) {
-    hipLaunchKernelGGL((k_gemm<WT, PRO, EPI, XF32, 4>), dim3(gemm_grid(EPI, a.N, 4), gy), dim3(256), lds, s, a);
+    hipLaunchKernelGGL((k_gemm<WT, PRO, EPI, XF32, 4, LNT>), dim3(gemm_grid(EPI, a.N, 4), gy), dim3(256), lds, s, a);
   }
   return hipGetLastError();
+}
+
+// LayerNorm chunks of 128 elements held per lane: 4 covers d <= 512, 8 covers d <= 1024
+template <typename WT, int PRO, int EPI, int XF32>
+hipError_t launch_t(const GemmArgs& a, int ksplit, hipStream_t s) {
+  if constexpr (PRO == PRO_LN && std::is_same<WT, bf16_t>::value) {
+    if (a.K > 512) return launch_k<WT, PRO, EPI, XF32, 8>(a, ksplit, s);
+  }
+  return launch_k<WT, PRO, EPI, XF32, 4>(a, ksplit, s);
 }
 
 template <typename WT, int PRO, int XF32>
@@ -325,7 +385,7 @@ hipError_t launch_gemm(int dtype, int pro, int epi, int ksplit, const GemmArgs& 
   if (a.n_rows <= 0) return hipSuccess;
   const int ks = dtype == DT_BF16 ? Mma<bf16_t>::KS : Mma<float>::KS;
   if (a.K % ks != 0 || a.K % 32 != 0) return hipErrorInvalidValue;
-  if (pro == PRO_LN && (a.K > 1024 || gemm_ln_lds_bytes(a.K, dtype == DT_BF16 ? 2 : 4) > 65536))
+  if (pro == PRO_LN && (a.K > (dtype == DT_BF16 ? 1024 : 512) || gemm_ln_lds_bytes(a.K, dtype == DT_BF16 ? 2 : 4) > 65536))
     return hipErrorInvalidValue;
   if (dtype == DT_BF16) return launch_dt<bf16_t>(pro, epi, a, ksplit, s);
   return launch_dt<float>(pro, epi, a, ksplit, s);

@@ -131,6 +131,14 @@ struct CtrlArgs {
   int* host_done;          // mapped pinned host flag (may be null)
   int pad_id, bos_id, eos_id;
   int R_max;
+  // fused into the control step when non-null: the argmax over the vocabulary
+  // partials of the rows just computed, and the embedding of the next rows
+  const uint2* partials;
+  int part_ld, n_parts;
+  void* x_out;
+  const void* emb;
+  float emb_scale;
+  int d, vocab;
   // finalize
   int* out_ids; int out_ld; int* out_len; int* out_k; int* out_flags;
 };
@@ -152,8 +160,8 @@ hipError_t launch_attn(int dtype, const AttnArgs& a, int R_max, hipStream_t s);
 hipError_t launch_embed(int dtype, const EmbedArgs& a, int R_max, hipStream_t s);
 hipError_t launch_ln(int dtype, const LnArgs& a, int R_max, hipStream_t s);
 hipError_t launch_argmax_reduce(const ReduceArgs& a, int R_max, hipStream_t s);
-hipError_t launch_ctrl_init(const CtrlArgs& a, hipStream_t s);
-hipError_t launch_ctrl_step(const CtrlArgs& a, hipStream_t s);
+hipError_t launch_ctrl_init(int dtype, const CtrlArgs& a, hipStream_t s);
+hipError_t launch_ctrl_step(int dtype, const CtrlArgs& a, hipStream_t s);
 hipError_t launch_finalize(const CtrlArgs& a, hipStream_t s);
 
 

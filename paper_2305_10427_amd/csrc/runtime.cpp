@@ -6,6 +6,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <string>
 #include <vector>
@@ -164,8 +165,19 @@ Layout plan(const pd_model& M, int max_batch, int max_src, int max_tgt) {
 
 }  // namespace
 
+struct GraphKey {
+  int mode, block, horizon, max_iters, B, R_max, slot, fused;
+  bool operator==(const GraphKey& o) const {
+    return mode == o.mode && block == o.block && horizon == o.horizon && max_iters == o.max_iters && B == o.B &&
+           R_max == o.R_max && slot == o.slot && fused == o.fused;
+  }
+};
+
 struct pd_ctx {
   const pd_model* M;
+  hipStream_t capture = nullptr;       // private stream used only to capture iteration graphs
+  bool use_graphs = true;
+  std::vector<std::pair<GraphKey, hipGraphExec_t>> graphs;
   int max_batch, max_src, max_tgt;
   char* ws;
   Layout L;
@@ -232,7 +244,7 @@ hipError_t run_gemm(const pd_ctx& C, const Rows& r, GemmArgs g, int epi, bool pr
 
 // Decoder pass over the rows of one iteration (or the teacher-forced rows of
 // pd_debug_logits), ending in the fused vocabulary argmax or a logits store.
-hipError_t decoder_pass(pd_ctx& C, const Rows& r, float* logits, hipStream_t s, int slot = -1) {
+hipError_t decoder_pass(pd_ctx& C, const Rows& r, float* logits, hipStream_t s, int slot = -1, bool fused = false) {
   const pd_model& M = *C.M;
   const pd_config& cfg = M.cfg;
   const int d = M.d;
@@ -247,8 +259,10 @@ hipError_t decoder_pass(pd_ctx& C, const Rows& r, float* logits, hipStream_t s, 
   const size_t cross_layer = static_cast<size_t>(C.max_batch) * C.max_src * d * es;
   hipError_t e;
 
-  EmbedArgs ea{r.n_dev, r.n_host, r.tok, r.map, M.w[0], M.dec_scale, d, M.V, x_res};
-  if ((e = launch_embed(M.dt, ea, r.R_max, s)) != hipSuccess) return e;
+  if (!fused) {   // otherwise the control step has embedded the rows already
+    EmbedArgs ea{r.n_dev, r.n_host, r.tok, r.map, M.w[0], M.dec_scale, d, M.V, x_res};
+    if ((e = launch_embed(M.dt, ea, r.R_max, s)) != hipSuccess) return e;
+  }
 
   for (int l = 0; l < cfg.n_dec; ++l) {
     // self-attention: Q -> q_buf, K/V of the block -> cache (layer l)
@@ -334,6 +348,7 @@ hipError_t decoder_pass(pd_ctx& C, const Rows& r, float* logits, hipStream_t s, 
     if ((e = hipEventRecord(C.tv1[slot], s)) != hipSuccess) return e;
     C.tv_pending[slot] = true;
   }
+  if (fused) return hipSuccess;   // the control step reduces the partials
   ReduceArgs ra{r.n_dev, C.at<uint2>(C.L.partials), vocab_wgs, vocab_wgs, C.at<int>(C.L.new_tok),
                 C.at<int>(C.L.row_flags)};
   return launch_argmax_reduce(ra, r.R_max, s);
@@ -417,6 +432,36 @@ hipError_t encoder_pass(pd_ctx& C, const int32_t* src, int B, int n_max, hipStre
     g.H = M.H; g.dh = M.dh; g.T = C.max_src; g.d = d;
     if ((e = launch_gemm(M.dt, PRO_NONE, EPI_QKV, 4, g, s)) != hipSuccess) return e;
   }
+  return hipSuccess;
+}
+
+constexpr int kFuseCtrlMaxRows = 64;   // above this the argmax reduction and embedding run as own kernels
+
+// One decoding iteration: decoder pass over the current rows, fused
+// vocabulary argmax, control step.
+hipError_t iteration(pd_ctx& C, const Rows& r, const CtrlArgs& ca, hipStream_t s, int slot, bool fused) {
+  hipError_t e = decoder_pass(C, r, nullptr, s, slot, fused);
+  if (e != hipSuccess) return e;
+  return launch_ctrl_step(C.M->dt, ca, s);
+}
+
+// The iteration as a HIP graph, captured once per context and launch shape.
+hipError_t iteration_graph(pd_ctx& C, const GraphKey& key, const Rows& r, const CtrlArgs& ca, hipGraphExec_t* out) {
+  for (auto& kv : C.graphs)
+    if (kv.first == key) { *out = kv.second; return hipSuccess; }
+  hipError_t e = hipStreamBeginCapture(C.capture, hipStreamCaptureModeThreadLocal);
+  if (e != hipSuccess) return e;
+  hipError_t e_body = iteration(C, r, ca, C.capture, key.slot, key.fused != 0);
+  hipGraph_t g = nullptr;
+  e = hipStreamEndCapture(C.capture, &g);
+  if (e_body != hipSuccess) { if (g) hipGraphDestroy(g); return e_body; }
+  if (e != hipSuccess) return e;
+  hipGraphExec_t ex = nullptr;
+  e = hipGraphInstantiate(&ex, g, nullptr, nullptr, 0);
+  hipGraphDestroy(g);
+  if (e != hipSuccess) return e;
+  C.graphs.emplace_back(key, ex);
+  *out = ex;
   return hipSuccess;
 }
 
@@ -541,6 +586,9 @@ pd_status pd_ctx_create(const pd_model* model, int32_t max_batch, int32_t max_sr
     hipEventCreate(&c->tv0[i]);
     hipEventCreate(&c->tv1[i]);
   }
+  hipStreamCreateWithFlags(&c->capture, hipStreamNonBlocking);
+  const char* g = std::getenv("PDEC_GRAPHS");
+  c->use_graphs = !(g != nullptr && g[0] == '0');
   *out = c;
   return PD_OK;
 }
@@ -555,6 +603,8 @@ void pd_ctx_destroy(pd_ctx* ctx) {
     hipEventDestroy(ctx->tv1[i]);
   }
   hipEventDestroy(ctx->stage_ev);
+  for (auto& kv : ctx->graphs) hipGraphExecDestroy(kv.second);
+  if (ctx->capture) hipStreamDestroy(ctx->capture);
   hipHostFree(ctx->host_pinned);
   delete ctx;
 }
@@ -636,16 +686,32 @@ pd_status pd_decode(pd_ctx* ctx, int32_t mode, int32_t block, int32_t horizon, i
   ca.out_k = out_k;
   ca.out_flags = out_flags;
 
+  const bool fused = R_max <= kFuseCtrlMaxRows;
+  if (fused) {
+    ca.partials = C.at<uint2>(C.L.partials);
+    ca.part_ld = ca.n_parts = gemm_grid(EPI_ARGMAX, M.V, 1);
+    ca.x_out = C.at<char>(C.L.x_res);
+    ca.emb = M.w[0];
+    ca.emb_scale = M.dec_scale;
+    ca.d = M.d;
+    ca.vocab = M.V;
+  }
   Rows r{ca.n_rows, 0, RowMap{ca.row_sent, ca.row_pos, 0}, ca.row_tok, R_max};
-  hipError_t e = launch_ctrl_init(ca, s);
+  hipError_t e = launch_ctrl_init(M.dt, ca, s);
   if (e != hipSuccess) return fail(PD_E_DEVICE, std::string("init launch: ") + hipGetErrorString(e));
   volatile int* done = C.host_pinned;
   for (int it = 0; it < iters; ++it) {
     const int slot = C.timing ? (it & 1) : -1;
     if (slot >= 0 && (e = take_timing(C, slot)) != hipSuccess)
       return fail(PD_E_DEVICE, std::string("timing: ") + hipGetErrorString(e));
-    e = decoder_pass(C, r, nullptr, s, slot);
-    if (e == hipSuccess) e = launch_ctrl_step(ca, s);
+    if (C.use_graphs && slot < 0) {   // event-timed iterations are launched directly
+      hipGraphExec_t ex = nullptr;
+      const GraphKey key{mode, block, horizon, max_iters, B, R_max, slot, fused ? 1 : 0};
+      e = iteration_graph(C, key, r, ca, &ex);
+      if (e == hipSuccess) e = hipGraphLaunch(ex, s);
+    } else {
+      e = iteration(C, r, ca, s, slot, fused);
+    }
     if (e == hipSuccess) e = hipEventRecord(C.it_ev[it & 1], s);
     if (e != hipSuccess) return fail(PD_E_DEVICE, std::string("iteration launch: ") + hipGetErrorString(e));
     if (it >= 1) {

@@ -77,6 +77,23 @@ def test_parallel_modes_equal_gpu_greedy_bitwise():
             np.testing.assert_array_equal(g.ids, ar.ids)
 
 
+def test_graph_and_direct_launches_agree(monkeypatch):
+    """Iterations replayed from a captured HIP graph give the same ids and k as
+    directly launched iterations, on the fused (few rows) and separate (many
+    rows) control paths."""
+    results = {}
+    for graphs in ("1", "0"):
+        monkeypatch.setenv("PDEC_GRAPHS", graphs)
+        _, _, ctx, _ = build(CHAIN, seed=1, max_batch=4, max_tgt=40, bias_std=0.5, ln_std=0.3)
+        srcs = sources(CHAIN.vocab, 4, seed=8)
+        out = []
+        for mode, b, ms in [("ar", 1, [16] * 4), ("gs_jacobi", 5, [16] * 4), ("jacobi", 0, [40, 33, 20, 5])]:
+            say(f"case graphs={graphs} mode={mode}")
+            out.append([(g.ids.tolist(), g.k) for g in gpu_decode_batch(ctx, srcs, ms, mode, b)])
+        results[graphs] = out
+    assert results["1"] == results["0"]
+
+
 def test_context_free_decoder_closed_form_k():
     cfg = dataclasses.replace(TINY, dec_emb_scale=0.0)
     _, _, ctx, M = build(cfg, seed=4, bias_std=0.3)
