@@ -91,7 +91,7 @@ __device__ __forceinline__ float gelu_erf(float v) {
 constexpr int kDepth = 8;   // MFMA steps per weight batch; two batches are in flight
 
 template <typename WT, int PRO, int EPI, int XF32, int KSPLIT, int LNT>
-__global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
+__global__ __launch_bounds__(KSPLIT == 8 ? 512 : 256) void k_gemm(GemmArgs a) {
   using AT = WT;
   using XT = typename std::conditional<XF32 != 0, float, AT>::type;
   using MM = Mma<WT>;
@@ -104,11 +104,12 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
   const int lr = lane & 15;          // row (X) / column (W) fed by this lane
   const int lg = lane >> 4;          // k group of this lane
   const int K = a.K, N = a.N;
-  const int n0 = (KSPLIT == 4 ? blockIdx.x * 16 : (blockIdx.x * 4 + wave) * 16);
+  constexpr bool SPLIT = KSPLIT > 1;   // waves split K over one 16-column tile
+  const int n0 = (SPLIT ? blockIdx.x * 16 : (blockIdx.x * 4 + wave) * 16);
   const int col = n0 + lr;           // weight row loaded by this lane, and output column it finishes
   const int n_steps = K / KS;
-  const int s_begin = KSPLIT == 4 ? (n_steps * wave) / 4 : 0;
-  const int s_end = KSPLIT == 4 ? (n_steps * (wave + 1)) / 4 : n_steps;
+  const int s_begin = SPLIT ? (n_steps * wave) / KSPLIT : 0;
+  const int s_end = SPLIT ? (n_steps * (wave + 1)) / KSPLIT : n_steps;
   const WT* __restrict__ W = static_cast<const WT*>(a.w);
   const XT* __restrict__ X = static_cast<const XT*>(a.x);
   const WT* __restrict__ wrow = W + static_cast<size_t>(col < N ? col : 0) * K + EPL * lg;
@@ -125,21 +126,22 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
     bcur[u] = (step < s_end && col < N) ? MM::load(wrow + step * KS) : MM::zero();
   }
   const float bias_v = (col < N) ? Elt<WT>::load(static_cast<const WT*>(a.bias), col) : 0.f;
-  constexpr int NE = KSPLIT == 4 ? 1 : 4;       // output elements finished per lane
+  constexpr int NE = SPLIT ? 1 : 4;       // output elements finished per lane
+  const bool epi_wave = !SPLIT || wave < 4;   // waves that finish outputs
   float rpre[NE];
   if constexpr (EPI == EPI_RESID) {
 #pragma unroll
     for (int e = 0; e < NE; ++e) {
-      const int row = m_first + 4 * lg + (KSPLIT == 4 ? wave : e);
+      const int row = m_first + 4 * lg + (SPLIT ? wave : e);
       const size_t ri = static_cast<size_t>(row) * a.ldr + col;
-      rpre[e] = (row < R_max && col < N)
+      rpre[e] = (epi_wave && row < R_max && col < N)
                     ? (a.resid_f32 ? static_cast<const float*>(a.resid)[ri] : Elt<AT>::load(static_cast<const AT*>(a.resid), ri))
                     : 0.f;
     }
   }
   const int R = a.n_rows_dev ? *a.n_rows_dev : a.n_rows;
 
-  __shared__ float s_part[4][4][64];
+  __shared__ float s_part[KSPLIT > 1 ? KSPLIT : 1][4][64];
   __shared__ uint32_t s_key[4][16];
   __shared__ int s_idx[4][16];
   // PRO_LN: the normalised 16-row input tile, rows padded by 16 bytes
@@ -160,12 +162,14 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
     }
     if constexpr (PRO == PRO_LN) {
       // wave w normalises rows 4w .. 4w+3 of the tile, 16 lanes per row
-      const int tr = 4 * wave + lg;
+      // (with 8 waves, waves 4..7 repeat the statistics of waves 0..3 and store nothing)
+      const int tr = 4 * (wave & 3) + lg;
       const int row = m0 + tr;
       const bool ok = row < R_max;
+      const bool lead = wave < 4;
       float v[8][8], mean, rstd;
       ln_stats_g16<XT, LNT>(X + static_cast<size_t>(ok ? row : 0) * a.ldx, K, lr, a.ln_eps, ok, v, mean, rstd);
-      const bool write_out = a.ln_out != nullptr && blockIdx.x == 0 && row < R;
+      const bool write_out = lead && a.ln_out != nullptr && blockIdx.x == 0 && row < R;
 #pragma unroll
       for (int t = 0; t < LNT; ++t) {
         const int k0 = 8 * lr + 128 * t;
@@ -175,8 +179,10 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
           load_n<WT, 8>(static_cast<const WT*>(a.ln_b), k0, bv);
 #pragma unroll
           for (int e = 0; e < 8; ++e) y[e] = Elt<AT>::round(ln_apply(v[t][e], mean, rstd, gv[e], bv[e]));
+          if (lead) {
 #pragma unroll
-          for (int e = 0; e < 8; ++e) Elt<AT>::store(sA, static_cast<size_t>(tr) * lda + k0 + e, y[e]);
+            for (int e = 0; e < 8; ++e) Elt<AT>::store(sA, static_cast<size_t>(tr) * lda + k0 + e, y[e]);
+          }
           if (write_out) {
 #pragma unroll
             for (int e = 0; e < 8; ++e)
@@ -225,11 +231,16 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
     if constexpr (PRO == PRO_LN) __syncthreads();   // sA is rewritten by the next tile
     // combine the K-split partials: wave w finishes element i = w of every lane
     float cv[4];
-    if constexpr (KSPLIT == 4) {
+    if constexpr (SPLIT) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) s_part[wave][i][lane] = acc[i];
       __syncthreads();
-      cv[0] = ((s_part[0][wave][lane] + s_part[1][wave][lane]) + s_part[2][wave][lane]) + s_part[3][wave][lane];
+      cv[0] = 0.f;
+      if (epi_wave) {
+        cv[0] = s_part[0][wave][lane];
+#pragma unroll
+        for (int w = 1; w < KSPLIT; ++w) cv[0] += s_part[w][wave][lane];   // wave order
+      }
       __syncthreads();
     } else {
 #pragma unroll
@@ -240,10 +251,10 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs a) {
     int nf = 0;
 #pragma unroll
     for (int e = 0; e < NE; ++e) {
-      const int i = KSPLIT == 4 ? wave : e;
+      const int i = SPLIT ? wave : e;
       const int row = m0 + 4 * lg + i;
       const float v = cv[e];
-      if (row >= R || col >= N) continue;
+      if (!epi_wave || row >= R || col >= N) continue;
       if constexpr (EPI == EPI_F32) {
         a.out_f32[static_cast<size_t>(row) * a.ldo + col] = v + bias_v;
       } else if constexpr (EPI == EPI_ACT) {
@@ -334,10 +345,13 @@ hipError_t launch_k(GemmArgs a, int ksplit, hipStream_t s) {
   const int gy = tiles < 64 ? tiles : 64;
   a.mt_per_wg = (tiles + gy - 1) / gy;
   const size_t lds = PRO == PRO_LN ? gemm_ln_lds_bytes(a.K, sizeof(WT)) : 0;
-  if (EPI == EPI_ARGMAX || ksplit != 4) {
+  if (EPI == EPI_ARGMAX || ksplit == 1) {
     hipLaunchKernelGGL((k_gemm<WT, PRO, EPI, XF32, 1, LNT>), dim3(gemm_grid(EPI, a.N, 1), gy), dim3(256), lds, s, a);
   } else if constexpr (EPI != EPI_ARGMAX) {
-    hipLaunchKernelGGL((k_gemm<WT, PRO, EPI, XF32, 4, LNT>), dim3(gemm_grid(EPI, a.N, 4), gy), dim3(256), lds, s, a);
+    if (ksplit == 8)
+      hipLaunchKernelGGL((k_gemm<WT, PRO, EPI, XF32, 8, LNT>), dim3(gemm_grid(EPI, a.N, 8), gy), dim3(512), lds, s, a);
+    else
+      hipLaunchKernelGGL((k_gemm<WT, PRO, EPI, XF32, 4, LNT>), dim3(gemm_grid(EPI, a.N, 4), gy), dim3(256), lds, s, a);
   }
   return hipGetLastError();
 }
@@ -377,7 +391,7 @@ hipError_t launch_dt(int pro, int epi, const GemmArgs& a, int ksplit, hipStream_
 size_t gemm_ln_lds_bytes(int K, size_t elt) { return 16 * (static_cast<size_t>(K) * elt + 16); }
 
 int gemm_grid(int epi, int N, int ksplit) {
-  if (epi == EPI_ARGMAX || ksplit != 4) return (N + 63) / 64;
+  if (epi == EPI_ARGMAX || ksplit == 1) return (N + 63) / 64;
   return (N + 15) / 16;
 }
 

@@ -238,7 +238,7 @@ hipError_t run_gemm(const pd_ctx& C, const Rows& r, GemmArgs g, int epi, bool pr
       g.ln_out = nullptr;
     }
   }
-  const int ksplit = (epi == EPI_ARGMAX || epi == EPI_LOGITS) ? 1 : 4;
+  const int ksplit = (epi == EPI_ARGMAX || epi == EPI_LOGITS) ? 1 : (g.K >= 2048 ? 8 : 4);
   return launch_gemm(M.dt, pro, epi, ksplit, g, s);
 }
 
@@ -412,7 +412,7 @@ hipError_t encoder_pass(pd_ctx& C, const int32_t* src, int B, int n_max, hipStre
     g.x = h_buf; g.ldx = M.dff; g.w = M.enc(l, E_W2); g.bias = M.enc(l, E_B2); g.N = d; g.K = M.dff;
     g.resid = x_res; g.ldr = d; g.ldo = d;
     if (pre) g.out = x_res; else g.out_f32 = s_buf;
-    if ((e = launch_gemm(M.dt, PRO_NONE, EPI_RESID, 4, g, s)) != hipSuccess) return e;
+    if ((e = launch_gemm(M.dt, PRO_NONE, EPI_RESID, g.K >= 2048 ? 8 : 4, g, s)) != hipSuccess) return e;
     if (!pre) {
       LnArgs la{nullptr, R, s_buf, 1, M.enc(l, E_LN2G), M.enc(l, E_LN2B), cfg.ln_eps, d, x_res};
       if ((e = launch_ln(M.dt, la, R, s)) != hipSuccess) return e;
