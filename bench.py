@@ -73,7 +73,7 @@ def run_mode(ctxs, sents, outs, mode, block, steps, warmup, timing=False):
     return res
 
 
-def gpu_workload(wl_name, steps, warmup, modes, headline):
+def gpu_workload(wl_name, steps, warmup, modes, headline, n_sent=0):
     import torch
     from paper_2305_10427_amd import configs as C, pdec, synth
     wl = C.WORKLOADS[wl_name]
@@ -82,6 +82,8 @@ def gpu_workload(wl_name, steps, warmup, modes, headline):
     w = synth.make_weights(cfg, seed=0)
     model = pdec.Model(cfg, w)
     sents = synth.make_sentences(wl, seed=1)
+    if n_sent:
+        sents = sents[:n_sent]
     max_src = max(len(s) for s, _ in sents)
     ctxs, outs = [], []
     for src, m in sents:
@@ -131,14 +133,45 @@ def cpu_baseline(cfg, weights, sents, mode, block, budget_s):
                       f"(numpy float64 oracle, {dec_s:.1f}s)"}
 
 
+def measured_traffic():
+    """HBM bytes per launch of the fused vocabulary kernel from the committed
+    rocprofv3 counter summary, or None once the kernel source has changed."""
+    import hashlib
+    try:
+        rec = json.load(open(os.path.join(ROOT, "profiles", "vocab_argmax_mt_base_bf16.json")))
+        src = b"".join(open(os.path.join(ROOT, "paper_2305_10427_amd", "csrc", f), "rb").read()
+                       for f in ("gemm.hip", "common.h"))
+        if hashlib.sha256(src).hexdigest() != rec["kernel_source_sha256"]:
+            return None
+        return int(rec["traffic_bytes_per_launch"])
+    except (OSError, KeyError, ValueError):
+        return None
+
+
+def copy_calibration():
+    """Three plain device copies of 256 MiB (read 256 MiB + write 256 MiB each):
+    the reference kernel for scaling the HBM byte counters of a profile."""
+    import torch
+    src = torch.ones(64 << 20, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    log("[calibration] 3 x copy of 256 MiB done")
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--sentences", type=int, default=0, help="use the first N sentences (0: all)")
+    ap.add_argument("--modes", default="ar:1,gs_jacobi:5,hybrid:5")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-f32", action="store_true")
+    ap.add_argument("--no-large", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); sentence-level data "
@@ -150,12 +183,21 @@ def main():
         sys.exit(2)
     torch.cuda.set_device(0)
 
+    if args.copy_calibration:
+        copy_calibration()
     headline = ("hybrid", 5)
-    modes = [("ar", 1), ("gs_jacobi", 5), ("hybrid", 5)]
-    cfg, w, sents, model, res = gpu_workload("mt_base_bf16", args.steps, args.warmup, modes, headline)
+    modes = [(m.split(":")[0], int(m.split(":")[1])) for m in args.modes.split(",")]
+    if headline not in modes:
+        modes.append(headline)
+    cfg, w, sents, model, res = gpu_workload("mt_base_bf16", args.steps, args.warmup, modes, headline,
+                                             args.sentences)
     f32 = None
     if not args.no_f32:
-        _, _, _, _, f32 = gpu_workload("mt_base_f32", args.steps, args.warmup, modes, headline)
+        _, _, _, _, f32 = gpu_workload("mt_base_f32", args.steps, args.warmup, modes, headline, args.sentences)
+    large = None
+    if not args.no_large:
+        _, _, _, _, large = gpu_workload("large", min(args.steps, 20), min(args.warmup, 2),
+                                         [("ar", 1), ("gs_jacobi", 16)], ("gs_jacobi", 16), 20)
 
     h = res[f"{headline[0]}_b{headline[1]}"]
     # roofline of the fused vocabulary projection + argmax (bytes: E [V][d] and the output bias, bf16)
@@ -164,7 +206,7 @@ def main():
     achieved = bytes_per_launch / (avg_ms * 1e-3) / 1e9
     roof = {"kernel": "k_gemm<bf16,PRO_LN,EPI_ARGMAX> (fused vocab projection + argmax)", "bound": "hbm",
             "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(),
             "avg_launch_us": round(avg_ms * 1e3, 2), "launches": h["vocab_launches"],
             "bytes_per_launch": bytes_per_launch}
     cpu = None
@@ -190,13 +232,24 @@ def main():
                    "mode": headline[0], "block": headline[1], "global_batch": 1, "parallelism": "none"},
         "modes": {k: {"tokens_per_s": round(v["tokens_per_s"], 1), "k_over_m": round(v["k_over_m"], 4),
                       "ms_per_sentence": round(v["ms_per_step"], 4)} for k, v in res.items()},
-        "speedup_vs_ar": round(h["tokens_per_s"] / res["ar_b1"]["tokens_per_s"], 3),
+        "speedup_vs_ar": (round(h["tokens_per_s"] / res["ar_b1"]["tokens_per_s"], 3) if "ar_b1" in res else None),
         "roofline": roof,
         "cpu_baseline": cpu,
     }
     if f32 is not None:
         line["f32"] = {k: {"tokens_per_s": round(v["tokens_per_s"], 1), "k_over_m": round(v["k_over_m"], 4)}
                        for k, v in f32.items()}
+    if large is not None:
+        line["large_bf16"] = {
+            "workload": "12+12 layers, d=1024, 16 heads, FFN 4096 GELU, pre-LN, V=250027, batch 1, first 20 "
+                        "sources n~U[20,120], m=min(n+10,256)",
+            **{k: {"tokens_per_s": round(v["tokens_per_s"], 1), "k_over_m": round(v["k_over_m"], 4),
+                   "ms_per_sentence": round(v["ms_per_step"], 3)} for k, v in large.items()}}
+        lv = large["gs_jacobi_b16"]
+        lb = 250027 * 1025 * 2
+        lavg = lv["vocab_ms"] / max(lv["vocab_launches"], 1)
+        line["large_bf16"]["vocab_roofline"] = {"achieved": round(lb / (lavg * 1e-3) / 1e9, 1), "peak": HBM_PEAK_GBS,
+                                                "unit": "GB/s", "avg_launch_us": round(lavg * 1e3, 2)}
     print(json.dumps(line), flush=True)
 
 
