@@ -101,8 +101,12 @@ __device__ __forceinline__ float wave_reduce_scatter(float (&v)[M], int lane) {
     const bool upper = (lane & off) != 0;
 #pragma unroll
     for (int j = 0; j < half; ++j) {
-      const float send = upper ? v[j] : v[j + half];
-      const float keep = upper ? v[j + half] : v[j];
+      float a = v[j], b = v[j + half];
+      // opaque copies: the per-lane choice must stay a select of two values,
+      // not become a lane-dependent index into v (a long compare/select chain)
+      __asm__("" : "+v"(a), "+v"(b));
+      const float send = upper ? a : b;
+      const float keep = upper ? b : a;
       v[j] = keep + __shfl_xor(send, off);
     }
   }
@@ -130,24 +134,49 @@ __device__ __forceinline__ uint32_t float_key(float f) {
 // pass valid = false and contribute zeros).  The matrix-product prologue and
 // the row LayerNorm kernel both use it, so a row's statistics are bitwise the
 // same wherever they are computed.
+// Row elements held by one lane of a 16-lane LayerNorm group: eight
+// consecutive elements per 128-element slab.  bf16 rows stay packed (four
+// words per slab) and are widened on use, which is exact.
+template <typename XT, int NT> struct LnHold {
+  float v[NT][8];
+  __device__ __forceinline__ void load(const XT* x, int t, int k0) { load_n<XT, 8>(x, k0, v[t]); }
+  __device__ __forceinline__ void clear(int t) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[t][e] = 0.f;
+  }
+  __device__ __forceinline__ float get(int t, int e) const { return v[t][e]; }
+};
+template <int NT> struct LnHold<bf16_t, NT> {
+  uint32_t w[NT][4];
+  __device__ __forceinline__ void load(const bf16_t* x, int t, int k0) {
+    const uint4 q = *reinterpret_cast<const uint4*>(x + k0);
+    w[t][0] = q.x; w[t][1] = q.y; w[t][2] = q.z; w[t][3] = q.w;
+  }
+  __device__ __forceinline__ void clear(int t) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) w[t][e] = 0u;
+  }
+  __device__ __forceinline__ float get(int t, int e) const {
+    const uint32_t u = w[t][e >> 1];
+    return __uint_as_float((e & 1) ? (u & 0xffff0000u) : (u << 16));
+  }
+};
+
 template <typename XT, int NT>
 __device__ __forceinline__ void ln_stats_g16(const XT* x, int K, int j, float eps, bool valid,
-                                             float (&v)[8][8], float& mean, float& rstd) {
+                                             LnHold<XT, NT>& h, float& mean, float& rstd) {
   static_assert(NT >= 1 && NT <= 8, "at most 1024 elements");
+  const XT* xj = x + 8 * j;   // slab t of this lane starts 128 * t elements further on
 #pragma unroll
   for (int t = 0; t < NT; ++t) {
-    const int k0 = 8 * j + 128 * t;
-    if (valid && k0 < K) load_n<XT, 8>(x, k0, v[t]);
-    else {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) v[t][e] = 0.f;
-    }
+    if (valid && 8 * j + 128 * t < K) h.load(xj, t, 128 * t);
+    else h.clear(t);
   }
   float s = 0.f;
 #pragma unroll
   for (int t = 0; t < NT; ++t)
 #pragma unroll
-    for (int e = 0; e < 8; ++e) s += v[t][e];
+    for (int e = 0; e < 8; ++e) s += h.get(t, e);
 #pragma unroll
   for (int off = 1; off < 16; off <<= 1) s += __shfl_xor(s, off);
   mean = s / static_cast<float>(K);
@@ -157,7 +186,51 @@ __device__ __forceinline__ void ln_stats_g16(const XT* x, int K, int j, float ep
     if (8 * j + 128 * t < K) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const float d = v[t][e] - mean;
+        const float d = h.get(t, e) - mean;
+        q = fmaf(d, d, q);
+      }
+    }
+  }
+#pragma unroll
+  for (int off = 1; off < 16; off <<= 1) q += __shfl_xor(q, off);
+  rstd = 1.0f / sqrtf(q / static_cast<float>(K) + eps);
+}
+
+// The same statistics without holding the row: the slabs are read twice
+// (sum, then squared deviations) in the order ln_stats_g16 uses, so mean and
+// rstd are bitwise those of ln_stats_g16.  For kernels whose registers hold a
+// weight stream; the second read hits the cache.
+template <typename XT, int NT>
+__device__ __forceinline__ void ln_stats_g16_reread(const XT* x, int K, int j, float eps, bool valid,
+                                                    float& mean, float& rstd) {
+  static_assert(NT >= 1 && NT <= 8, "at most 1024 elements");
+  const XT* xj = x + 8 * j;
+  float s = 0.f;
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    if (valid && 8 * j + 128 * t < K) {
+      float v[8];
+      load_n<XT, 8>(xj, 128 * t, v);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) s += v[e];
+    }
+  }
+#pragma unroll
+  for (int off = 1; off < 16; off <<= 1) s += __shfl_xor(s, off);
+  mean = s / static_cast<float>(K);
+  float q = 0.f;
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    if (8 * j + 128 * t < K) {
+      float v[8];
+      if (valid) load_n<XT, 8>(xj, 128 * t, v);
+      else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = 0.f;
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float d = v[e] - mean;
         q = fmaf(d, d, q);
       }
     }

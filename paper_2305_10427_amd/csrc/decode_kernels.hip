@@ -1,5 +1,6 @@
 // Attention, embedding, LayerNorm, argmax reduction and the on-device
 // fixed-point control of the parallel decoding iteration.
+#include "attn.h"
 #include "common.h"
 #include "kernels.h"
 
@@ -19,68 +20,46 @@ __device__ __forceinline__ void row_place(const RowMap& m, int row, int& s, int&
 // The row at position p attends to keys 0..p of its own sentence (causal,
 // decoder self-attention over the KV cache whose block entries were written by
 // the QKV product of this iteration) or to keys 0..n_s-1 (encoder memory /
-// encoder self-attention, padded keys excluded).  Keys are visited in a fixed
-// order that depends only on the row's own key count, never on how many rows
-// the iteration has: lane j scores keys j, j+64, ...; the softmax max/sum use
-// fixed lane trees; lane d accumulates output dimension d over keys 0..n-1.
+// encoder self-attention, padded keys excluded).  The wave walks the row's
+// 64-key chunks in order (chunk_partial, merge_chunk); chunk boundaries depend
+// only on the row's own key count.
 template <typename AT, int DH>
 __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
-  __shared__ float s_p[4][kMaxKeys];
+  __shared__ float s_q[4][DH];
+  __shared__ AttnSlot<DH> s_slot[4];
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = threadIdx.x / kWave;
   const int R = a.n_rows_dev ? *a.n_rows_dev : a.n_rows;
   const int idx = blockIdx.x * 4 + wave;
   const int row = idx / a.H;
   const int hh = idx - row * a.H;
-  const bool active = row < R;
-  constexpr int dh = DH;
-  const AT* __restrict__ Kc = static_cast<const AT*>(a.kc);
-  const AT* __restrict__ Vc = static_cast<const AT*>(a.vc);
-  int nk = 0;
-  size_t base = 0;
-  float denom = 1.f;
-  if (active) {
-    int s, p;
-    row_place(a.rows, row, s, p);
-    nk = a.causal ? p + 1 : a.klen[s];
-    base = (static_cast<size_t>(s) * a.H + hh) * a.T * dh;
-    const float* q = a.q + static_cast<size_t>(row) * a.ldq + hh * dh;
-    float qv[DH];
-#pragma unroll
-    for (int d = 0; d < DH; ++d) qv[d] = q[d];
-    float mx = -INFINITY;
-    for (int key = lane; key < nk; key += kWave) {
-      const AT* kr = Kc + base + static_cast<size_t>(key) * dh;
-      float acc = 0.f;
-#pragma unroll
-      for (int d = 0; d < DH; d += Vec16<AT>::N) {
-        float kv[Vec16<AT>::N];
-        Vec16<AT>::load(kr, d, kv);
-#pragma unroll
-        for (int e = 0; e < Vec16<AT>::N; ++e) acc = fmaf(qv[d + e], kv[e], acc);
-      }
-      const float sc = acc * a.scale;
-      s_p[wave][key] = sc;
-      mx = fmaxf(mx, sc);
-    }
-    mx = wave_max(mx);
-    float sum = 0.f;
-    for (int key = lane; key < nk; key += kWave) {
-      const float e = expf(s_p[wave][key] - mx);
-      s_p[wave][key] = e;
-      sum += e;
-    }
-    denom = wave_sum(sum);
+  if (row >= R) return;   // no workgroup barrier below
+  int s, p;
+  row_place(a.rows, row, s, p);
+  const int nk = a.causal ? p + 1 : a.klen[s];
+  const size_t base = (static_cast<size_t>(s) * a.H + hh) * a.T * DH;
+  const AT* Kb = static_cast<const AT*>(a.kc) + base;
+  const AT* Vb = static_cast<const AT*>(a.vc) + base;
+  // the first chunk's K/V rows go out before the query
+  KeyRows<AT, DH> kr;
+  kr.load(Kb, Vb, lane, lane < nk);
+  const float* q = a.q + static_cast<size_t>(row) * a.ldq + hh * DH;
+  for (int d = lane; d < DH; d += kWave) s_q[wave][d] = q[d];
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  RowState<DH> st;
+  st.init();
+  for (int key0 = 0; key0 < nk; key0 += kAttnChunk) {
+    if (key0 > 0) kr.load(Kb, Vb, key0 + lane, key0 + lane < nk);
+    chunk_partial<AT, DH>(s_q[wave], kr, Vb, key0, nk, a.scale, lane, &s_slot[wave]);
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    merge_chunk<DH>(st, &s_slot[wave], lane);
+    __builtin_amdgcn_wave_barrier();
   }
-  __syncthreads();
-  if (active) {
-    for (int d = lane; d < dh; d += kWave) {
-      float o = 0.f;
-      for (int key = 0; key < nk; ++key)
-        o = fmaf(s_p[wave][key], Elt<AT>::load(Vc, base + static_cast<size_t>(key) * dh + d), o);
-      Elt<AT>::store(static_cast<AT*>(a.out), static_cast<size_t>(row) * a.ldo + hh * dh + d, o / denom);
-    }
-  }
+  row_output<AT, DH>(st, static_cast<AT*>(a.out) + static_cast<size_t>(row) * a.ldo + hh * DH, lane);
 }
 
 // ---------------------------------------------------------------------------
@@ -122,8 +101,9 @@ __global__ __launch_bounds__(256) void k_ln(LnArgs a) {
   const int R = a.n_rows_dev ? *a.n_rows_dev : a.n_rows;
   const bool ok = row < R;
   const XT* x = static_cast<const XT*>(a.x) + static_cast<size_t>(ok ? row : 0) * a.d;
-  float v[8][8], mean, rstd;
-  ln_stats_g16<XT, NT>(x, a.d, j, a.eps, ok, v, mean, rstd);
+  LnHold<XT, NT> h;
+  float mean, rstd;
+  ln_stats_g16<XT, NT>(x, a.d, j, a.eps, ok, h, mean, rstd);
   if (!ok) return;
 #pragma unroll
   for (int t = 0; t < NT; ++t) {
@@ -135,7 +115,7 @@ __global__ __launch_bounds__(256) void k_ln(LnArgs a) {
 #pragma unroll
       for (int e = 0; e < 8; ++e)
         Elt<WT>::store(static_cast<WT*>(a.out), static_cast<size_t>(row) * a.d + k0 + e,
-                       ln_apply(v[t][e], mean, rstd, g[e], b[e]));
+                       ln_apply(h.get(t, e), mean, rstd, g[e], b[e]));
     }
   }
 }
@@ -236,17 +216,29 @@ __global__ __launch_bounds__(1024) void k_ctrl_init(CtrlArgs a) {
   emit_rows<WT>(a);
 }
 
-// Argmax of each row over the per-workgroup partials of the fused vocabulary
-// kernel (largest logit, lowest index on exact ties), one wave per row.
-__device__ __forceinline__ void reduce_row(const uint2* p, int n_parts, int lane, int* tok, int* flag) {
-  uint32_t bk = 0;
-  uint32_t bi = 0x7fffffffu;
-  uint32_t nf = 0;
-  for (int t = lane; t < n_parts; t += kWave) {
-    const uint2 v = p[t];
-    const uint32_t i = v.y & 0x7fffffffu;
-    nf |= v.y >> 31;
-    if (v.x > bk || (v.x == bk && i < bi)) { bk = v.x; bi = i; }
+// Best entry of a set of argmax partials.
+struct Best {
+  uint32_t key;   // float_key of the logit (0: none)
+  uint32_t idx;   // token index, bit 31 set if a non-finite logit was seen
+};
+
+// (larger key, then lower index) wins; the non-finite bits are or-ed.  The
+// order of combination does not change the result.
+__device__ __forceinline__ void best_merge(uint32_t& bk, uint32_t& bi, uint32_t& nf, uint32_t k2, uint32_t raw) {
+  const uint32_t i2 = raw & 0x7fffffffu;
+  nf |= raw >> 31;
+  if (k2 > bk || (k2 == bk && i2 < bi)) { bk = k2; bi = i2; }
+}
+
+// Best over partials p[t0 .. t1) by one wave, eight loads per lane in flight.
+__device__ __forceinline__ Best reduce_span(const uint2* p, int t0, int t1, int lane) {
+  uint32_t bk = 0, bi = 0x7fffffffu, nf = 0;
+  for (int t = t0 + lane; t < t1; t += 8 * kWave) {
+    uint2 v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = t + u * kWave < t1 ? p[t + u * kWave] : make_uint2(0u, 0x7fffffffu);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) best_merge(bk, bi, nf, v[u].x, v[u].y);
   }
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) {
@@ -255,10 +247,38 @@ __device__ __forceinline__ void reduce_row(const uint2* p, int n_parts, int lane
     nf |= __shfl_xor(nf, off);
     if (ok > bk || (ok == bk && oi < bi)) { bk = ok; bi = oi; }
   }
-  if (lane == 0) {
-    const bool none = bk == 0;           // no finite logit in the row
-    *tok = none ? 0 : static_cast<int>(bi);
-    *flag = (nf || none) ? 1 : 0;
+  return Best{bk, bi | (nf << 31)};
+}
+
+// Argmax of each of R rows over the per-workgroup partials of the fused
+// vocabulary kernel (largest logit, lowest index on exact ties).  All waves of
+// the workgroup take part: a row's partials are split into S spans (S waves
+// per row, S = waves / R when R < waves), combined through LDS.  Ends with
+// the workgroup synchronised.
+__device__ void reduce_rows(const uint2* partials, int part_ld, int n_parts, int R, int* new_tok, int* row_flags) {
+  __shared__ Best s_best[32];
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = threadIdx.x / kWave;
+  const int nw = blockDim.x / kWave;                 // <= 32
+  const int S = R < nw ? nw / R : 1;                 // spans per row
+  const int rows_per_round = nw / S;
+  for (int row0 = 0; row0 < R; row0 += rows_per_round) {
+    const int row = row0 + wave / S;
+    const int span = wave - (wave / S) * S;
+    if (wave < rows_per_round * S && row < R) {
+      const Best b = reduce_span(partials + static_cast<size_t>(row) * part_ld, (n_parts * span) / S,
+                                 (n_parts * (span + 1)) / S, lane);
+      if (lane == 0) s_best[wave] = b;
+    }
+    __syncthreads();
+    if (static_cast<int>(threadIdx.x) < rows_per_round && row0 + static_cast<int>(threadIdx.x) < R) {
+      uint32_t bk = 0, bi = 0x7fffffffu, nf = 0;
+      for (int j = 0; j < S; ++j) best_merge(bk, bi, nf, s_best[threadIdx.x * S + j].key, s_best[threadIdx.x * S + j].idx);
+      const bool none = bk == 0;                     // no finite logit in the row
+      new_tok[row0 + threadIdx.x] = none ? 0 : static_cast<int>(bi);
+      row_flags[row0 + threadIdx.x] = (nf || none) ? 1 : 0;
+    }
+    __syncthreads();
   }
 }
 
@@ -266,13 +286,8 @@ template <typename WT>
 __global__ __launch_bounds__(1024) void k_ctrl_step(CtrlArgs a) {
   const int R = *a.n_rows;
   if (R == 0) return;
-  if (a.partials != nullptr) {
-    const int lane = threadIdx.x & (kWave - 1);
-    for (int row = threadIdx.x / kWave; row < R; row += blockDim.x / kWave)
-      reduce_row(a.partials + static_cast<size_t>(row) * a.part_ld, a.n_parts, lane,
-                 const_cast<int*>(a.new_tok) + row, const_cast<int*>(a.row_flags) + row);
-    __syncthreads();
-  }
+  if (a.partials != nullptr)
+    reduce_rows(a.partials, a.part_ld, a.n_parts, R, const_cast<int*>(a.new_tok), const_cast<int*>(a.row_flags));
   for (int s = threadIdx.x; s < a.B; s += blockDim.x) {
     SentState st = a.st[s];
     if (st.done) continue;
@@ -332,7 +347,12 @@ __global__ __launch_bounds__(256) void k_argmax_reduce(ReduceArgs a) {
   const int lane = threadIdx.x & (kWave - 1);
   const int row = blockIdx.x * 4 + threadIdx.x / kWave;
   if (row >= *a.n_rows_dev) return;
-  reduce_row(a.partials + static_cast<size_t>(row) * a.part_ld, a.n_parts, lane, a.new_tok + row, a.row_flags + row);
+  const Best b = reduce_span(a.partials + static_cast<size_t>(row) * a.part_ld, 0, a.n_parts, lane);
+  if (lane == 0) {
+    const bool none = b.key == 0;
+    a.new_tok[row] = none ? 0 : static_cast<int>(b.idx & 0x7fffffffu);
+    a.row_flags[row] = ((b.idx >> 31) || none) ? 1 : 0;
+  }
 }
 
 template <typename AT>

@@ -34,59 +34,9 @@
 // value, then lowest index) per row and writes one partial per row.
 #include "common.h"
 #include "kernels.h"
+#include "mma.h"
 
 namespace pdec {
-
-typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef float floatx4_t __attribute__((ext_vector_type(4)));
-
-template <typename T> struct Mma;
-template <> struct Mma<bf16_t> {
-  static constexpr int KS = 32;
-  static constexpr int EPL = 8;
-  typedef uint4 frag;
-  static __device__ __forceinline__ floatx4_t step(frag a, frag b, floatx4_t c) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b),
-                                                   c, 0, 0, 0);
-  }
-  static __device__ __forceinline__ frag load(const bf16_t* p) { return *reinterpret_cast<const uint4*>(p); }
-  static __device__ __forceinline__ frag zero() { return make_uint4(0, 0, 0, 0); }
-  static __device__ __forceinline__ void unpack(frag f, float* v) {
-    const uint32_t w[4] = {f.x, f.y, f.z, f.w};
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      v[2 * j] = __uint_as_float(w[j] << 16);
-      v[2 * j + 1] = __uint_as_float(w[j] & 0xffff0000u);
-    }
-  }
-  static __device__ __forceinline__ frag pack(const float* v) {
-    uint32_t w[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      w[j] = static_cast<uint32_t>(f32_to_bf16(v[2 * j])) | (static_cast<uint32_t>(f32_to_bf16(v[2 * j + 1])) << 16);
-    return make_uint4(w[0], w[1], w[2], w[3]);
-  }
-};
-template <> struct Mma<float> {
-  static constexpr int KS = 16;
-  static constexpr int EPL = 4;
-  typedef float4 frag;
-  static __device__ __forceinline__ floatx4_t step(frag a, frag b, floatx4_t c) {
-    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, b.x, c, 0, 0, 0);
-    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, b.y, c, 0, 0, 0);
-    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, b.z, c, 0, 0, 0);
-    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, b.w, c, 0, 0, 0);
-    return c;
-  }
-  static __device__ __forceinline__ frag load(const float* p) { return *reinterpret_cast<const float4*>(p); }
-  static __device__ __forceinline__ frag zero() { return make_float4(0.f, 0.f, 0.f, 0.f); }
-  static __device__ __forceinline__ void unpack(frag f, float* v) { v[0] = f.x; v[1] = f.y; v[2] = f.z; v[3] = f.w; }
-  static __device__ __forceinline__ frag pack(const float* v) { return make_float4(v[0], v[1], v[2], v[3]); }
-};
-
-__device__ __forceinline__ float gelu_erf(float v) {
-  return 0.5f * v * (1.0f + erff(v * 0.70710678118654752f));
-}
 
 constexpr int kDepth = 8;   // MFMA steps per weight batch; two batches are in flight
 
@@ -161,35 +111,10 @@ __global__ __launch_bounds__(KSPLIT == 8 ? 512 : 256) void k_gemm(GemmArgs a) {
       }
     }
     if constexpr (PRO == PRO_LN) {
-      // wave w normalises rows 4w .. 4w+3 of the tile, 16 lanes per row
-      // (with 8 waves, waves 4..7 repeat the statistics of waves 0..3 and store nothing)
-      const int tr = 4 * (wave & 3) + lg;
-      const int row = m0 + tr;
-      const bool ok = row < R_max;
-      const bool lead = wave < 4;
-      float v[8][8], mean, rstd;
-      ln_stats_g16<XT, LNT>(X + static_cast<size_t>(ok ? row : 0) * a.ldx, K, lr, a.ln_eps, ok, v, mean, rstd);
-      const bool write_out = lead && a.ln_out != nullptr && blockIdx.x == 0 && row < R;
-#pragma unroll
-      for (int t = 0; t < LNT; ++t) {
-        const int k0 = 8 * lr + 128 * t;
-        if (k0 < K) {
-          float gv[8], bv[8], y[8];
-          load_n<WT, 8>(static_cast<const WT*>(a.ln_g), k0, gv);
-          load_n<WT, 8>(static_cast<const WT*>(a.ln_b), k0, bv);
-#pragma unroll
-          for (int e = 0; e < 8; ++e) y[e] = Elt<AT>::round(ln_apply(v[t][e], mean, rstd, gv[e], bv[e]));
-          if (lead) {
-#pragma unroll
-            for (int e = 0; e < 8; ++e) Elt<AT>::store(sA, static_cast<size_t>(tr) * lda + k0 + e, y[e]);
-          }
-          if (write_out) {
-#pragma unroll
-            for (int e = 0; e < 8; ++e)
-              Elt<AT>::store(static_cast<AT*>(a.ln_out), static_cast<size_t>(row) * a.ldlo + k0 + e, y[e]);
-          }
-        }
-      }
+      if (wave < 4)
+        ln_tile<WT, XT, LNT>(X, a.ldx, K, m0, R_max, static_cast<const WT*>(a.ln_g), static_cast<const WT*>(a.ln_b),
+                             a.ln_eps, sA, lda, blockIdx.x == 0 ? static_cast<AT*>(a.ln_out) : nullptr, a.ldlo, R,
+                             wave, lane);
       __syncthreads();
     }
     floatx4_t acc = {0.f, 0.f, 0.f, 0.f};
@@ -289,7 +214,7 @@ __global__ __launch_bounds__(KSPLIT == 8 ? 512 : 256) void k_gemm(GemmArgs a) {
         a.out_f32[static_cast<size_t>(row) * a.ldo + col] = fmaf(a.logit_scale, v, bias_v);
       } else if constexpr (EPI == EPI_ARGMAX) {
         const float logit = fmaf(a.logit_scale, v, bias_v);   // s * (h . E[col]) + bias[col]
-        if (!isfinite(logit)) nf = 1;
+        if (!isfinite(logit)) nf |= 1 << e;   // bit e: a non-finite logit in row 4 lg + e
         else { bk[e] = float_key(logit); bi[e] = col; }
       }
     }
@@ -313,7 +238,7 @@ __global__ __launch_bounds__(KSPLIT == 8 ? 512 : 256) void k_gemm(GemmArgs a) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           s_key[wave][4 * lg + e] = bk[e];
-          s_idx[wave][4 * lg + e] = bi[e] | (nf << 31);
+          s_idx[wave][4 * lg + e] = bi[e] | (((nf >> e) & 1) << 31);
         }
       }
       __syncthreads();

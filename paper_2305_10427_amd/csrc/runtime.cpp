@@ -242,6 +242,14 @@ hipError_t run_gemm(const pd_ctx& C, const Rows& r, GemmArgs g, int epi, bool pr
   return launch_gemm(M.dt, pro, epi, ksplit, g, s);
 }
 
+// Iterations of at most one 16-row tile use the streaming vocabulary kernel
+// (vocab_grid(V) partials per row); larger ones the product kernel's argmax
+// epilogue (one partial per 64-column workgroup).
+constexpr int kVocabStreamMaxRows = 16;
+int vocab_parts(const pd_model& M, int R_max) {
+  return R_max <= kVocabStreamMaxRows ? vocab_grid(M.V) : gemm_grid(EPI_ARGMAX, M.V, 1);
+}
+
 // Decoder pass over the rows of one iteration (or the teacher-forced rows of
 // pd_debug_logits), ending in the fused vocabulary argmax or a logits store.
 hipError_t decoder_pass(pd_ctx& C, const Rows& r, float* logits, hipStream_t s, int slot = -1, bool fused = false) {
@@ -339,17 +347,19 @@ hipError_t decoder_pass(pd_ctx& C, const Rows& r, float* logits, hipStream_t s, 
     g.out_f32 = logits; g.ldo = M.V;
     return run_gemm(C, r, g, EPI_LOGITS, true, a_buf, s);
   }
-  const int vocab_wgs = gemm_grid(EPI_ARGMAX, M.V, 1);
   g.partials = C.at<uint2>(C.L.partials);
-  g.part_ld = vocab_wgs;
+  g.part_ld = gemm_grid(EPI_ARGMAX, M.V, 1);
+  const int n_parts = vocab_parts(M, r.R_max);
   if (slot >= 0 && (e = hipEventRecord(C.tv0[slot], s)) != hipSuccess) return e;
-  if ((e = run_gemm(C, r, g, EPI_ARGMAX, true, a_buf, s)) != hipSuccess) return e;
+  if (r.R_max <= kVocabStreamMaxRows) e = launch_vocab_argmax(M.dt, g, s);   // one row tile: streaming kernel
+  else e = run_gemm(C, r, g, EPI_ARGMAX, true, a_buf, s);
+  if (e != hipSuccess) return e;
   if (slot >= 0) {
     if ((e = hipEventRecord(C.tv1[slot], s)) != hipSuccess) return e;
     C.tv_pending[slot] = true;
   }
   if (fused) return hipSuccess;   // the control step reduces the partials
-  ReduceArgs ra{r.n_dev, C.at<uint2>(C.L.partials), vocab_wgs, vocab_wgs, C.at<int>(C.L.new_tok),
+  ReduceArgs ra{r.n_dev, C.at<uint2>(C.L.partials), g.part_ld, n_parts, C.at<int>(C.L.new_tok),
                 C.at<int>(C.L.row_flags)};
   return launch_argmax_reduce(ra, r.R_max, s);
 }
@@ -689,7 +699,8 @@ pd_status pd_decode(pd_ctx* ctx, int32_t mode, int32_t block, int32_t horizon, i
   const bool fused = R_max <= kFuseCtrlMaxRows;
   if (fused) {
     ca.partials = C.at<uint2>(C.L.partials);
-    ca.part_ld = ca.n_parts = gemm_grid(EPI_ARGMAX, M.V, 1);
+    ca.part_ld = gemm_grid(EPI_ARGMAX, M.V, 1);
+    ca.n_parts = vocab_parts(M, R_max);
     ca.x_out = C.at<char>(C.L.x_res);
     ca.emb = M.w[0];
     ca.emb_scale = M.dec_scale;

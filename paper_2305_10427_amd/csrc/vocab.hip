@@ -1,0 +1,194 @@
+// Fused vocabulary projection + argmax for iterations of at most 16 rows (one
+// MFMA row tile), the batch-1 decoding regime.
+//
+//   logit[r][v] = s * (LN(h_r) . E[v]) + b[v]      (never stored)
+//
+// Each workgroup returns, per row, the best (largest logit, lowest index) over
+// the columns it streamed; the control step reduces those partials.
+//
+// The V x d weight stream is the whole cost, so the kernel keeps it in flight:
+// a fixed grid of at most kVocabMaxWgs workgroups (all resident at once) whose
+// waves walk 16-column tiles t = w, w + W, w + 2W, ... (w the wave's global
+// index, W the waves in the grid).  Every lane keeps D 16-byte weight loads
+// outstanding in a ring over the flattened (tile, k step) sequence, so the
+// next tile's loads leave while the current tile is finished.
+//
+// Every logit is accumulated exactly as in the general product kernel with
+// whole-K waves (MFMA steps in increasing k from zero, then s * acc + b), so
+// both kernels pick the same token for a row.
+#include "common.h"
+#include "kernels.h"
+#include "mma.h"
+
+namespace pdec {
+
+#ifndef PDEC_VOCAB_DEPTH
+#define PDEC_VOCAB_DEPTH 16
+#endif
+constexpr int kVocabDepth = PDEC_VOCAB_DEPTH;   // weight loads in flight per lane
+
+template <typename WT, int XF32, int LNT, int D>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k_vocab(GemmArgs a) {
+  using AT = WT;
+  using XT = typename std::conditional<XF32 != 0, float, AT>::type;
+  using MM = Mma<WT>;
+  using frag = typename MM::frag;
+  constexpr int KS = MM::KS;
+  constexpr int EPL = MM::EPL;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = threadIdx.x / kWave;
+  const int lr = lane & 15;          // weight row (column of the logits) fed by this lane
+  const int lg = lane >> 4;          // k group of this lane; rows 4 lg .. 4 lg + 3 of the result
+  const int K = a.K, N = a.N;
+  const int n_steps = K / KS;
+  const int n_tiles = (N + 15) / 16;
+  const int W = gridDim.x * 4;
+  const int w_id = blockIdx.x * 4 + wave;
+  const int my_tiles = w_id < n_tiles ? (n_tiles - 1 - w_id) / W + 1 : 0;
+  const int total = my_tiles * n_steps;
+  const WT* __restrict__ E = static_cast<const WT*>(a.w);
+  const WT* __restrict__ bias = static_cast<const WT*>(a.bias);
+
+  // weight row of tile j for this lane (the last tile's rows beyond N repeat
+  // row N - 1; their logits are never used)
+  auto wrow = [&](int j) -> const WT* {
+    const int col = min((w_id + j * W) * 16 + lr, N - 1);
+    return E + static_cast<size_t>(col) * K + EPL * lg;
+  };
+
+  // prime the ring: the first D (tile, step) loads, before anything else
+  frag ring[D];
+  int jn = 0, sn = 0;                // (tile, step) of the next load
+  const WT* pn = wrow(0);
+#pragma unroll
+  for (int u = 0; u < D; ++u) {
+    if (u < total) {
+      ring[u] = MM::load(pn + sn * KS);
+      if (++sn == n_steps) { sn = 0; ++jn; pn = wrow(jn); }
+    }
+  }
+  float bias_v = my_tiles > 0 ? Elt<WT>::load(bias, min(w_id * 16 + lr, N - 1)) : 0.f;
+
+  // LayerNorm of the (at most 16) rows into LDS (rows re-read rather than
+  // held: the registers belong to the weight ring)
+  extern __shared__ __align__(16) unsigned char s_dyn[];
+  AT* sA = reinterpret_cast<AT*>(s_dyn);
+  const int lda = K + 16 / static_cast<int>(sizeof(AT));
+  ln_tile<WT, XT, LNT, false>(static_cast<const XT*>(a.x), a.ldx, K, 0, a.n_rows, static_cast<const WT*>(a.ln_g),
+                       static_cast<const WT*>(a.ln_b), a.ln_eps, sA, lda, nullptr, 0, 0, wave, lane);
+  const int R = a.n_rows_dev ? *a.n_rows_dev : a.n_rows;
+  __syncthreads();
+
+  // stream: consume step g from ring[g % D], refill it with step g + D
+  uint32_t bk[4] = {0u, 0u, 0u, 0u};
+  int bi[4] = {0x7fffffff, 0x7fffffff, 0x7fffffff, 0x7fffffff};
+  int nf = 0;                        // bit i: a non-finite logit in row 4 lg + i
+  floatx4_t acc = {0.f, 0.f, 0.f, 0.f};
+  int j = 0, s = 0;                  // (tile, step) being consumed
+  const AT* arow = sA + static_cast<size_t>(lr) * lda + EPL * lg;
+  for (int g0 = 0; g0 < total; g0 += D) {
+#pragma unroll
+    for (int u = 0; u < D; ++u) {
+      if (g0 + u >= total) break;
+      const frag b = ring[u];
+      if (g0 + u + D < total) {
+        ring[u] = MM::load(pn + sn * KS);
+        if (++sn == n_steps) { sn = 0; ++jn; pn = wrow(jn); }
+      }
+      acc = MM::step(MM::load(arow + s * KS), b, acc);
+      if (++s == n_steps) {
+        const int col = (w_id + j * W) * 16 + lr;
+        if (col < N) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            if (4 * lg + i >= R) continue;
+            const float logit = fmaf(a.logit_scale, acc[i], bias_v);   // s * (h . E[col]) + bias[col]
+            if (!isfinite(logit)) {
+              nf |= 1 << i;
+            } else {
+              const uint32_t key = float_key(logit);
+              if (key > bk[i] || (key == bk[i] && col < bi[i])) { bk[i] = key; bi[i] = col; }
+            }
+          }
+        }
+        acc = floatx4_t{0.f, 0.f, 0.f, 0.f};
+        s = 0;
+        ++j;
+        if (j < my_tiles) bias_v = Elt<WT>::load(bias, min((w_id + j * W) * 16 + lr, N - 1));
+      }
+    }
+  }
+
+  // best of each row over the 16 columns of a lane group, then over the waves
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1) {
+      const uint32_t ok = __shfl_xor(bk[i], off);
+      const int oi = __shfl_xor(bi[i], off);
+      if (ok > bk[i] || (ok == bk[i] && oi < bi[i])) { bk[i] = ok; bi[i] = oi; }
+    }
+  }
+#pragma unroll
+  for (int off = 1; off < 16; off <<= 1) nf |= __shfl_xor(nf, off);
+  __shared__ uint32_t s_key[4][16];
+  __shared__ int s_idx[4][16];
+  if (lr == 0) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      s_key[wave][4 * lg + i] = bk[i];
+      s_idx[wave][4 * lg + i] = bi[i] | (((nf >> i) & 1) << 31);
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x < 16 && static_cast<int>(threadIdx.x) < R) {
+    const int r = threadIdx.x;
+    uint32_t kk = 0;
+    int ii = 0x7fffffff, ff = 0;
+    for (int w = 0; w < 4; ++w) {
+      const uint32_t k2 = s_key[w][r];
+      const int raw = s_idx[w][r];
+      const int i2 = raw & 0x7fffffff;
+      ff |= (raw >> 31) & 1;
+      if (k2 > kk || (k2 == kk && i2 < ii)) { kk = k2; ii = i2; }
+    }
+    a.partials[static_cast<size_t>(r) * a.part_ld + blockIdx.x] =
+        make_uint2(kk, static_cast<uint32_t>(ii) | (static_cast<uint32_t>(ff) << 31));
+  }
+}
+
+int vocab_grid(int V) {
+  const int tiles = (V + 15) / 16;
+  return std::max(1, std::min(kVocabMaxWgs, (tiles + 3) / 4));
+}
+
+namespace {
+
+template <typename WT, int XF32>
+hipError_t launch_x(const GemmArgs& a, hipStream_t s) {
+  const size_t lds = gemm_ln_lds_bytes(a.K, sizeof(WT));
+  const dim3 grid(vocab_grid(a.N));
+  if constexpr (std::is_same<WT, bf16_t>::value) {
+    if (a.K > 512) {
+      hipLaunchKernelGGL((k_vocab<WT, XF32, 8, kVocabDepth>), grid, dim3(256), lds, s, a);
+      return hipGetLastError();
+    }
+  }
+  hipLaunchKernelGGL((k_vocab<WT, XF32, 4, kVocabDepth>), grid, dim3(256), lds, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_vocab_argmax(int dtype, const GemmArgs& a, hipStream_t s) {
+  if (a.n_rows <= 0) return hipSuccess;
+  if (a.n_rows > 16 || a.N <= 0) return hipErrorInvalidValue;
+  const int ks = dtype == DT_BF16 ? Mma<bf16_t>::KS : Mma<float>::KS;
+  if (a.K % ks != 0 || a.K % 32 != 0 || a.K > (dtype == DT_BF16 ? 1024 : 512) ||
+      a.part_ld < vocab_grid(a.N))
+    return hipErrorInvalidValue;
+  if (dtype == DT_BF16) return a.x_f32 ? launch_x<bf16_t, 1>(a, s) : launch_x<bf16_t, 0>(a, s);
+  return a.x_f32 ? launch_x<float, 1>(a, s) : launch_x<float, 0>(a, s);
+}
+
+}  // namespace pdec

@@ -17,6 +17,12 @@ pytestmark = pytest.mark.gpu
 TINY = C.TINY
 CHAIN = dataclasses.replace(C.TINY, name="chain", logit_scale=-3.0)
 SMALL_PRE_BF16 = dataclasses.replace(C.TINY, name="small_pre", pre_ln=True, act_gelu=True, dtype=C.BF16)
+# head widths 64 and 32, and a bf16 width above 512 (LayerNorm rows of more
+# than 512 elements per 16-lane group)
+MID_F32 = dataclasses.replace(C.TINY, name="mid_f32", d_model=128, n_heads=2, d_ff=256, vocab=700)
+MID_BF16 = dataclasses.replace(C.TINY, name="mid_bf16", d_model=256, n_heads=8, d_ff=512, vocab=700, dtype=C.BF16)
+WIDE_PRE_BF16 = dataclasses.replace(C.TINY, name="wide_pre", n_dec=1, n_enc=1, d_model=640, n_heads=10, d_ff=640,
+                                    vocab=500, pre_ln=True, act_gelu=True, dtype=C.BF16)
 
 
 def say(*a):
@@ -129,7 +135,8 @@ def test_hybrid_eos_fixtures():
                         assert g.flags & pdec.FLAG_EOS
 
 
-@pytest.mark.parametrize("cfg", [TINY, SMALL_PRE_BF16], ids=["tiny_f32", "small_pre_bf16"])
+@pytest.mark.parametrize("cfg", [TINY, SMALL_PRE_BF16, MID_F32, MID_BF16, WIDE_PRE_BF16],
+                         ids=["tiny_f32", "small_pre_bf16", "mid_f32", "mid_bf16", "wide_pre_bf16"])
 def test_teacher_forced_logits_within_tolerance(cfg):
     import torch
     _, _, ctx, M = build(cfg, seed=6, max_tgt=96, bias_std=0.3, ln_std=0.2)
@@ -146,7 +153,8 @@ def test_teacher_forced_logits_within_tolerance(cfg):
         assert rel.max() < TOL[cfg.dtype]
 
 
-@pytest.mark.parametrize("cfg", [TINY, SMALL_PRE_BF16], ids=["tiny_f32", "small_pre_bf16"])
+@pytest.mark.parametrize("cfg", [TINY, SMALL_PRE_BF16, MID_F32, MID_BF16, WIDE_PRE_BF16],
+                         ids=["tiny_f32", "small_pre_bf16", "mid_f32", "mid_bf16", "wide_pre_bf16"])
 def test_rows_are_invariant_to_block_and_batch(cfg):
     """A row's logits are bitwise the same whatever else is in the call: fewer
     or more positions (row tiles, fused or separate LayerNorm) and batch mates."""
