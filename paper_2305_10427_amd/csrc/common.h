@@ -163,8 +163,7 @@ template <int NT> struct LnHold<bf16_t, NT> {
 };
 
 template <typename XT, int NT>
-__device__ __forceinline__ void ln_stats_g16(const XT* x, int K, int j, float eps, bool valid,
-                                             LnHold<XT, NT>& h, float& mean, float& rstd) {
+__device__ __forceinline__ void ln_load_g16(const XT* x, int K, int j, bool valid, LnHold<XT, NT>& h) {
   static_assert(NT >= 1 && NT <= 8, "at most 1024 elements");
   const XT* xj = x + 8 * j;   // slab t of this lane starts 128 * t elements further on
 #pragma unroll
@@ -172,6 +171,11 @@ __device__ __forceinline__ void ln_stats_g16(const XT* x, int K, int j, float ep
     if (valid && 8 * j + 128 * t < K) h.load(xj, t, 128 * t);
     else h.clear(t);
   }
+}
+
+template <typename XT, int NT>
+__device__ __forceinline__ void ln_stats_held(const LnHold<XT, NT>& h, int K, int j, float eps, float& mean,
+                                              float& rstd) {
   float s = 0.f;
 #pragma unroll
   for (int t = 0; t < NT; ++t)
@@ -196,48 +200,11 @@ __device__ __forceinline__ void ln_stats_g16(const XT* x, int K, int j, float ep
   rstd = 1.0f / sqrtf(q / static_cast<float>(K) + eps);
 }
 
-// The same statistics without holding the row: the slabs are read twice
-// (sum, then squared deviations) in the order ln_stats_g16 uses, so mean and
-// rstd are bitwise those of ln_stats_g16.  For kernels whose registers hold a
-// weight stream; the second read hits the cache.
 template <typename XT, int NT>
-__device__ __forceinline__ void ln_stats_g16_reread(const XT* x, int K, int j, float eps, bool valid,
-                                                    float& mean, float& rstd) {
-  static_assert(NT >= 1 && NT <= 8, "at most 1024 elements");
-  const XT* xj = x + 8 * j;
-  float s = 0.f;
-#pragma unroll
-  for (int t = 0; t < NT; ++t) {
-    if (valid && 8 * j + 128 * t < K) {
-      float v[8];
-      load_n<XT, 8>(xj, 128 * t, v);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) s += v[e];
-    }
-  }
-#pragma unroll
-  for (int off = 1; off < 16; off <<= 1) s += __shfl_xor(s, off);
-  mean = s / static_cast<float>(K);
-  float q = 0.f;
-#pragma unroll
-  for (int t = 0; t < NT; ++t) {
-    if (8 * j + 128 * t < K) {
-      float v[8];
-      if (valid) load_n<XT, 8>(xj, 128 * t, v);
-      else {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = 0.f;
-      }
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float d = v[e] - mean;
-        q = fmaf(d, d, q);
-      }
-    }
-  }
-#pragma unroll
-  for (int off = 1; off < 16; off <<= 1) q += __shfl_xor(q, off);
-  rstd = 1.0f / sqrtf(q / static_cast<float>(K) + eps);
+__device__ __forceinline__ void ln_stats_g16(const XT* x, int K, int j, float eps, bool valid,
+                                             LnHold<XT, NT>& h, float& mean, float& rstd) {
+  ln_load_g16<XT, NT>(x, K, j, valid, h);
+  ln_stats_held<XT, NT>(h, K, j, eps, mean, rstd);
 }
 
 // LayerNorm of one element given its row statistics (same expression

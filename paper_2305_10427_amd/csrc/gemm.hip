@@ -67,7 +67,21 @@ __global__ __launch_bounds__(KSPLIT == 8 ? 512 : 256) void k_gemm(GemmArgs a) {
   const int m_first = blockIdx.y * 16 * a.mt_per_wg;
   const int m_last = min(R_max, m_first + 16 * a.mt_per_wg);
 
-  // Loads that do not depend on the previous kernel go out first: the first
+  // PRO_LN: the first tile's input rows and gamma / beta go out before the
+  // weights -- loads complete in issue order, and the LayerNorm must not
+  // wait for the weight stream.  Gamma and beta are staged through LDS (one
+  // 16-byte word per thread of the first 256).
+  LnTileRows<WT, XT, LNT> ln;
+  __shared__ uint4 s_gb[PRO == PRO_LN ? 2 : 1][128];
+  uint4 gb = make_uint4(0u, 0u, 0u, 0u);
+  const int gw = threadIdx.x & 127;
+  const bool gb_lane = PRO == PRO_LN && threadIdx.x < 256 && gw < K * static_cast<int>(sizeof(WT)) / 16;
+  if constexpr (PRO == PRO_LN) {
+    if (wave < 4) ln.load(X, a.ldx, K, m_first, R_max, wave, lane);
+    if (gb_lane) gb = static_cast<const uint4*>(threadIdx.x < 128 ? a.ln_g : a.ln_b)[gw];
+  }
+
+  // Then the loads that do not depend on the previous kernel: the first
   // weight batch, the bias, the residual of the first tile's outputs.
   frag bcur[D];
 #pragma unroll
@@ -98,12 +112,19 @@ __global__ __launch_bounds__(KSPLIT == 8 ? 512 : 256) void k_gemm(GemmArgs a) {
   extern __shared__ __align__(16) unsigned char s_dyn[];
   AT* sA = reinterpret_cast<AT*>(s_dyn);
   const int lda = K + 16 / static_cast<int>(sizeof(AT));
+  if constexpr (PRO == PRO_LN) {
+    if (gb_lane) s_gb[threadIdx.x >> 7][gw] = gb;
+    __syncthreads();
+  }
 
   for (int m0 = m_first; m0 < m_last; m0 += 16) {
     if (m0 > m_first && m0 >= R) break;
     const int arow = m0 + lr;                 // X row fed by this lane
     const bool arow_ok = arow < R_max;
     if (m0 != m_first) {
+      if constexpr (PRO == PRO_LN) {
+        if (wave < 4) ln.load(X, a.ldx, K, m0, R_max, wave, lane);
+      }
 #pragma unroll
       for (int u = 0; u < D; ++u) {
         const int step = s_begin + u;
@@ -112,9 +133,8 @@ __global__ __launch_bounds__(KSPLIT == 8 ? 512 : 256) void k_gemm(GemmArgs a) {
     }
     if constexpr (PRO == PRO_LN) {
       if (wave < 4)
-        ln_tile<WT, XT, LNT>(X, a.ldx, K, m0, R_max, static_cast<const WT*>(a.ln_g), static_cast<const WT*>(a.ln_b),
-                             a.ln_eps, sA, lda, blockIdx.x == 0 ? static_cast<AT*>(a.ln_out) : nullptr, a.ldlo, R,
-                             wave, lane);
+        ln.finish(K, a.ln_eps, reinterpret_cast<const WT*>(s_gb[0]), reinterpret_cast<const WT*>(s_gb[1]), sA, lda,
+                  blockIdx.x == 0 ? static_cast<AT*>(a.ln_out) : nullptr, a.ldlo, R);
       __syncthreads();
     }
     floatx4_t acc = {0.f, 0.f, 0.f, 0.f};

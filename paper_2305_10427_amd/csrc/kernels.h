@@ -158,9 +158,8 @@ int gemm_grid(int epi, int N, int ksplit);
 size_t gemm_ln_lds_bytes(int K, size_t elt);
 hipError_t launch_attn(int dtype, const AttnArgs& a, int R_max, hipStream_t s);
 // Fused vocabulary projection + argmax for at most 16 rows (streaming kernel);
-// writes vocab_grid(V) partials per row.
-constexpr int kVocabMaxWgs = 1024;
-int vocab_grid(int V);
+// writes vocab_grid(dtype, V, d) partials per row (at most ceil(V / 64)).
+int vocab_grid(int dtype, int V, int d);
 hipError_t launch_vocab_argmax(int dtype, const GemmArgs& a, hipStream_t s);
 hipError_t launch_embed(int dtype, const EmbedArgs& a, int R_max, hipStream_t s);
 hipError_t launch_ln(int dtype, const LnArgs& a, int R_max, hipStream_t s);

@@ -57,58 +57,51 @@ __device__ __forceinline__ float gelu_erf(float v) {
 }
 
 // LayerNorm of the 16-row input tile rows m0 .. m0+15 (rows >= R_max read as
-// zeros) into the LDS tile sA[16][lda] in the storage type.  Called by waves
-// 0..3 only: wave w owns tile rows 4w .. 4w+3 with 16 lanes per row
-// (ln_stats_g16).  If ln_out is non-null the normalised rows below R_out are
-// also written there.  The caller synchronises the workgroup afterwards.
-template <typename WT, typename XT, int LNT, bool HOLD = true>
-__device__ __forceinline__ void ln_tile(const XT* X, int ldx, int K, int m0, int R_max, const WT* g, const WT* b,
-                                        float eps, WT* sA, int lda, WT* ln_out, int ldlo, int R_out, int wave,
-                                        int lane) {
-  const int lr = lane & 15;
-  const int tr = 4 * wave + (lane >> 4);
-  const int row = m0 + tr;
-  const bool ok = row < R_max;
-  const XT* xr = X + static_cast<size_t>(ok ? row : 0) * ldx;
-  // HOLD: the lane keeps its row slabs in registers between statistics and
-  // output; otherwise it reads them again (same values, same arithmetic)
-  LnHold<XT, HOLD ? LNT : 1> h;
-  float mean, rstd;
-  if constexpr (HOLD) ln_stats_g16<XT, LNT>(xr, K, lr, eps, ok, h, mean, rstd);
-  else ln_stats_g16_reread<XT, LNT>(xr, K, lr, eps, ok, mean, rstd);
-  const bool write_out = ln_out != nullptr && row < R_out;
-  // per-lane bases; slab t adds the constant 128 * t
-  const WT* gj = g + 8 * lr;
-  const WT* bj = b + 8 * lr;
-  const XT* xj = xr + 8 * lr;
-  WT* aj = sA + static_cast<size_t>(tr) * lda + 8 * lr;
-  WT* oj = write_out ? ln_out + static_cast<size_t>(row) * ldlo + 8 * lr : nullptr;
+// zeros) into the LDS tile sA[16][lda] in the storage type, by waves 0..3:
+// wave w owns tile rows 4w .. 4w+3 with 16 lanes per row (statistics as in
+// ln_stats_g16).  load() issues the row loads and finish() computes the
+// statistics and writes the normalised rows (also to ln_out, rows below
+// R_out, when it is non-null), so a caller can issue other loads in between.
+// The caller synchronises the workgroup after finish().
+template <typename WT, typename XT, int LNT> struct LnTileRows {
+  LnHold<XT, LNT> h;
+  int lr, tr, row;
+  bool ok;
+  __device__ __forceinline__ void load(const XT* X, int ldx, int K, int m0, int R_max, int wave, int lane) {
+    lr = lane & 15;
+    tr = 4 * wave + (lane >> 4);
+    row = m0 + tr;
+    ok = row < R_max;
+    ln_load_g16<XT, LNT>(X + static_cast<size_t>(ok ? row : 0) * ldx, K, lr, ok, h);
+  }
+  // g, b: gamma and beta, in global memory or LDS
+  __device__ __forceinline__ void finish(int K, float eps, const WT* g, const WT* b, WT* sA, int lda, WT* ln_out,
+                                         int ldlo, int R_out) {
+    float mean, rstd;
+    ln_stats_held<XT, LNT>(h, K, lr, eps, mean, rstd);
+    const bool write_out = ln_out != nullptr && row < R_out;
+    // per-lane bases; slab t adds the constant 128 * t
+    const WT* gj = g + 8 * lr;
+    const WT* bj = b + 8 * lr;
+    WT* aj = sA + static_cast<size_t>(tr) * lda + 8 * lr;
+    WT* oj = write_out ? ln_out + static_cast<size_t>(row) * ldlo + 8 * lr : nullptr;
 #pragma unroll
-  for (int t = 0; t < LNT; ++t) {
-    if (8 * lr + 128 * t < K) {
-      float gv[8], bv[8], xv[8], y[8];
-      load_n<WT, 8>(gj, 128 * t, gv);
-      load_n<WT, 8>(bj, 128 * t, bv);
-      if constexpr (HOLD) {
+    for (int t = 0; t < LNT; ++t) {
+      if (8 * lr + 128 * t < K) {
+        float gv[8], bv[8], y[8];
+        load_n<WT, 8>(gj, 128 * t, gv);
+        load_n<WT, 8>(bj, 128 * t, bv);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) xv[e] = h.get(t, e);
-      } else {
-        if (ok) load_n<XT, 8>(xj, 128 * t, xv);
-        else {
+        for (int e = 0; e < 8; ++e) y[e] = Elt<WT>::round(ln_apply(h.get(t, e), mean, rstd, gv[e], bv[e]));
 #pragma unroll
-          for (int e = 0; e < 8; ++e) xv[e] = 0.f;
+        for (int e = 0; e < 8; ++e) Elt<WT>::store(aj, 128 * t + e, y[e]);
+        if (write_out) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) Elt<WT>::store(oj, 128 * t + e, y[e]);
         }
-      }
-#pragma unroll
-      for (int e = 0; e < 8; ++e) y[e] = Elt<WT>::round(ln_apply(xv[e], mean, rstd, gv[e], bv[e]));
-#pragma unroll
-      for (int e = 0; e < 8; ++e) Elt<WT>::store(aj, 128 * t + e, y[e]);
-      if (write_out) {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) Elt<WT>::store(oj, 128 * t + e, y[e]);
       }
     }
   }
-}
+};
 
 }  // namespace pdec

@@ -243,11 +243,11 @@ hipError_t run_gemm(const pd_ctx& C, const Rows& r, GemmArgs g, int epi, bool pr
 }
 
 // Iterations of at most one 16-row tile use the streaming vocabulary kernel
-// (vocab_grid(V) partials per row); larger ones the product kernel's argmax
+// (vocab_grid partials per row); larger ones the product kernel's argmax
 // epilogue (one partial per 64-column workgroup).
 constexpr int kVocabStreamMaxRows = 16;
 int vocab_parts(const pd_model& M, int R_max) {
-  return R_max <= kVocabStreamMaxRows ? vocab_grid(M.V) : gemm_grid(EPI_ARGMAX, M.V, 1);
+  return R_max <= kVocabStreamMaxRows ? vocab_grid(M.dt, M.V, M.d) : gemm_grid(EPI_ARGMAX, M.V, 1);
 }
 
 // Decoder pass over the rows of one iteration (or the teacher-forced rows of

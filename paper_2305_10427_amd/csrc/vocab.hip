@@ -7,7 +7,7 @@
 // the columns it streamed; the control step reduces those partials.
 //
 // The V x d weight stream is the whole cost, so the kernel keeps it in flight:
-// a fixed grid of at most kVocabMaxWgs workgroups (all resident at once) whose
+// a fixed grid of workgroups (all resident at once, see VocabShape) whose
 // waves walk 16-column tiles t = w, w + W, w + 2W, ... (w the wave's global
 // index, W the waves in the grid).  Every lane keeps D 16-byte weight loads
 // outstanding in a ring over the flattened (tile, k step) sequence, so the
@@ -22,13 +22,19 @@
 
 namespace pdec {
 
-#ifndef PDEC_VOCAB_DEPTH
-#define PDEC_VOCAB_DEPTH 16
-#endif
-constexpr int kVocabDepth = PDEC_VOCAB_DEPTH;   // weight loads in flight per lane
+// Ring depth (weight loads in flight per lane) and waves per SIMD of a
+// variant: rows of up to 512 elements leave room for a 12-deep ring at 4
+// waves per SIMD (1024 resident workgroups); wider bf16 rows hold twice the
+// LayerNorm slabs, so they run at 3 waves per SIMD (768 workgroups) with a
+// 16-deep ring (8 when the held rows are float).
+template <int LNT, int XF32> struct VocabShape {
+  static constexpr int D = LNT > 4 ? (XF32 ? 8 : 16) : 12;
+  static constexpr int OCC = LNT > 4 ? 3 : 4;
+  static constexpr int MAX_WGS = 256 * OCC;
+};
 
-template <typename WT, int XF32, int LNT, int D>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k_vocab(GemmArgs a) {
+template <typename WT, int XF32, int LNT, int D = VocabShape<LNT, XF32>::D>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(VocabShape<LNT, XF32>::OCC))) void k_vocab(GemmArgs a) {
   using AT = WT;
   using XT = typename std::conditional<XF32 != 0, float, AT>::type;
   using MM = Mma<WT>;
@@ -56,7 +62,18 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k
     return E + static_cast<size_t>(col) * K + EPL * lg;
   };
 
-  // prime the ring: the first D (tile, step) loads, before anything else
+  // Loads complete in issue order, so everything the LayerNorm prologue reads
+  // goes out before the weight ring: the rows (held in registers), then
+  // gamma and beta (one 16-byte word per lane, staged through LDS).
+  LnTileRows<WT, XT, LNT> ln;
+  ln.load(static_cast<const XT*>(a.x), a.ldx, K, 0, a.n_rows, wave, lane);
+  __shared__ uint4 s_gb[2][128];                   // gamma, beta: up to 2 KB each
+  const int gb_words = K * static_cast<int>(sizeof(WT)) / 16;
+  const int gw = threadIdx.x & 127;
+  uint4 gb = make_uint4(0u, 0u, 0u, 0u);
+  if (gw < gb_words) gb = static_cast<const uint4*>(threadIdx.x < 128 ? a.ln_g : a.ln_b)[gw];
+
+  // prime the ring: the first D (tile, step) loads
   frag ring[D];
   int jn = 0, sn = 0;                // (tile, step) of the next load
   const WT* pn = wrow(0);
@@ -69,13 +86,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k
   }
   float bias_v = my_tiles > 0 ? Elt<WT>::load(bias, min(w_id * 16 + lr, N - 1)) : 0.f;
 
-  // LayerNorm of the (at most 16) rows into LDS (rows re-read rather than
-  // held: the registers belong to the weight ring)
+  // LayerNorm of the (at most 16) rows into LDS while the weights arrive
+  if (gw < gb_words) s_gb[threadIdx.x >> 7][gw] = gb;
+  __syncthreads();
   extern __shared__ __align__(16) unsigned char s_dyn[];
   AT* sA = reinterpret_cast<AT*>(s_dyn);
   const int lda = K + 16 / static_cast<int>(sizeof(AT));
-  ln_tile<WT, XT, LNT, false>(static_cast<const XT*>(a.x), a.ldx, K, 0, a.n_rows, static_cast<const WT*>(a.ln_g),
-                       static_cast<const WT*>(a.ln_b), a.ln_eps, sA, lda, nullptr, 0, 0, wave, lane);
+  ln.finish(K, a.ln_eps, reinterpret_cast<const WT*>(s_gb[0]), reinterpret_cast<const WT*>(s_gb[1]), sA, lda,
+            nullptr, 0, 0);
   const int R = a.n_rows_dev ? *a.n_rows_dev : a.n_rows;
   __syncthreads();
 
@@ -157,9 +175,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void k
   }
 }
 
-int vocab_grid(int V) {
+int vocab_grid(int dtype, int V, int d) {
+  const int max_wgs = dtype == DT_BF16 && d > 512 ? VocabShape<8, 0>::MAX_WGS : VocabShape<4, 0>::MAX_WGS;
   const int tiles = (V + 15) / 16;
-  return std::max(1, std::min(kVocabMaxWgs, (tiles + 3) / 4));
+  return std::max(1, std::min(max_wgs, (tiles + 3) / 4));
 }
 
 namespace {
@@ -167,14 +186,14 @@ namespace {
 template <typename WT, int XF32>
 hipError_t launch_x(const GemmArgs& a, hipStream_t s) {
   const size_t lds = gemm_ln_lds_bytes(a.K, sizeof(WT));
-  const dim3 grid(vocab_grid(a.N));
+  const dim3 grid(vocab_grid(std::is_same<WT, bf16_t>::value ? DT_BF16 : DT_F32, a.N, a.K));
   if constexpr (std::is_same<WT, bf16_t>::value) {
     if (a.K > 512) {
-      hipLaunchKernelGGL((k_vocab<WT, XF32, 8, kVocabDepth>), grid, dim3(256), lds, s, a);
+      hipLaunchKernelGGL((k_vocab<WT, XF32, 8>), grid, dim3(256), lds, s, a);
       return hipGetLastError();
     }
   }
-  hipLaunchKernelGGL((k_vocab<WT, XF32, 4, kVocabDepth>), grid, dim3(256), lds, s, a);
+  hipLaunchKernelGGL((k_vocab<WT, XF32, 4>), grid, dim3(256), lds, s, a);
   return hipGetLastError();
 }
 
@@ -185,7 +204,7 @@ hipError_t launch_vocab_argmax(int dtype, const GemmArgs& a, hipStream_t s) {
   if (a.n_rows > 16 || a.N <= 0) return hipErrorInvalidValue;
   const int ks = dtype == DT_BF16 ? Mma<bf16_t>::KS : Mma<float>::KS;
   if (a.K % ks != 0 || a.K % 32 != 0 || a.K > (dtype == DT_BF16 ? 1024 : 512) ||
-      a.part_ld < vocab_grid(a.N))
+      a.part_ld < vocab_grid(dtype, a.N, a.K))
     return hipErrorInvalidValue;
   if (dtype == DT_BF16) return a.x_f32 ? launch_x<bf16_t, 1>(a, s) : launch_x<bf16_t, 0>(a, s);
   return a.x_f32 ? launch_x<float, 1>(a, s) : launch_x<float, 0>(a, s);
