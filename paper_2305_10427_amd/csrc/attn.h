@@ -1,13 +1,15 @@
-// Scaled dot-product attention of one query row, evaluated in chunks of 64
-// keys (one key per lane).
+// Scaled dot-product attention of one query row by one wave, in chunks of 64
+// keys.
 //
 // For one chunk (keys key0 .. key0+63 that are < nk):
-//   s_k = (q . k_k) * scale,  m_c = max_k s_k,  p_k = exp(s_k - m_c),
-//   l_c = sum_k p_k,  o_c = sum_k p_k v_k            (fixed lane trees)
+//   s_k = (q . k_k) * scale          lane k scores key key0 + k
+//   m_c = max_k s_k,  p_k = exp(s_k - m_c),  l_c = sum_k p_k     (DPP trees)
+//   o_c[d] = sum_k p_k v_k[d]        lane d, keys in increasing order (p and
+//                                    the chunk's V rows staged through LDS)
 // and a row's chunks are folded in chunk order:
 //   m' = max(m, m_c),  o <- o exp(m - m') + o_c exp(m_c - m'),  l likewise,
 // the output being o / l.  Chunk boundaries depend only on the row's own key
-// count, never on how many rows a launch holds or on which wave does a chunk.
+// count, never on how many rows a launch holds.
 #pragma once
 
 #include "common.h"
@@ -16,13 +18,8 @@ namespace pdec {
 
 constexpr int kAttnChunk = kWave;   // keys per chunk
 
-template <int DH> struct AttnSlot {
-  float m, l;
-  float o[DH];
-};
-
-// Running state of one row, held by one wave: m, l wave-uniform, lane d owns
-// output dimensions d, d + 64, ...
+// Running state of one row: m, l wave-uniform; lane d owns output dimensions
+// d, d + 64, ...
 template <int DH> struct RowState {
   static constexpr int NO = (DH + kWave - 1) / kWave;
   float m, l;
@@ -36,17 +33,17 @@ template <int DH> struct RowState {
 };
 
 // The K and V rows of the key a lane scores, as raw 16-byte words, loaded
-// before anything else so that their latency overlaps the query load.  V is
-// held only when it fits comfortably in registers (<= 256 bytes per row);
-// otherwise it is loaded pass by pass.
+// ahead of the query.  V is held only when it fits comfortably in registers
+// (<= 256 bytes per row); otherwise it is read again when staged.
 template <typename AT, int DH> struct KeyRows {
   static constexpr int V16 = Vec16<AT>::N;        // elements per 16-byte word
   static constexpr int NW = DH / V16;             // words per row
   static constexpr bool HOLD_V = DH * sizeof(AT) <= 256;
   uint4 k[NW];
   uint4 v[HOLD_V ? NW : 1];
+  // always loads (key 0 for an invalid lane): no load under a branch
   __device__ __forceinline__ void load(const AT* Kb, const AT* Vb, int key, bool valid) {
-    if (!valid) return;
+    key = valid ? key : 0;
     const uint4* kr = reinterpret_cast<const uint4*>(Kb + static_cast<size_t>(key) * DH);
 #pragma unroll
     for (int i = 0; i < NW; ++i) k[i] = kr[i];
@@ -56,6 +53,16 @@ template <typename AT, int DH> struct KeyRows {
       for (int i = 0; i < NW; ++i) v[i] = vr[i];
     }
   }
+};
+
+// Per-wave LDS staging of one chunk: the weights p_k and DP dimensions of the
+// 64 V rows at a time (rows padded by 16 bytes).
+template <typename AT, int DH> struct AttnStage {
+  static constexpr int DP0 = 8192 / (kAttnChunk * static_cast<int>(sizeof(AT)));
+  static constexpr int DP = DH < DP0 ? DH : DP0;  // dimensions per pass: 64 (bf16), 32 (f32)
+  static constexpr int LDV = DP + 16 / static_cast<int>(sizeof(AT));
+  float p[kAttnChunk];
+  AT v[kAttnChunk * LDV];
 };
 
 template <typename AT> __device__ __forceinline__ void unpack_word(uint4 w, float* out);
@@ -72,75 +79,67 @@ template <> __device__ __forceinline__ void unpack_word<bf16_t>(uint4 w, float* 
   }
 }
 
-// Partial of one chunk into *slot.  q is the row's query (DH floats, any
-// address space); kr holds the lane's key (key0 + lane) when it is < nk;
-// Vb points at key 0 of the row's [T][DH] V slice (used when V is not held).
+// Orders the wave's LDS writes before its following reads.
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// One chunk folded into the row state.  q: the row's query (DH floats, LDS);
+// kr: the lane's key (key0 + lane) when it is < nk; Vb: key 0 of the row's
+// [T][DH] V slice.  All 64 lanes must be active.
 template <typename AT, int DH>
-__device__ __forceinline__ void chunk_partial(const float* q, const KeyRows<AT, DH>& kr, const AT* Vb, int key0,
-                                              int nk, float scale, int lane, AttnSlot<DH>* slot) {
+__device__ __forceinline__ void chunk_fold(const float* q, const KeyRows<AT, DH>& kr, const AT* Vb, int key0, int nk,
+                                           float scale, int lane, AttnStage<AT, DH>& sm, RowState<DH>& st) {
   using KR = KeyRows<AT, DH>;
+  using SM = AttnStage<AT, DH>;
   constexpr int V16 = KR::V16;
   const int key = key0 + lane;
   const bool valid = key < nk;
-  float sc = -INFINITY;
-  if (valid) {
-    float acc = 0.f;
+  float acc = 0.f;
 #pragma unroll
-    for (int i = 0; i < KR::NW; ++i) {
-      float kv[V16];
-      unpack_word<AT>(kr.k[i], kv);
+  for (int i = 0; i < KR::NW; ++i) {
+    float kv[V16];
+    unpack_word<AT>(kr.k[i], kv);
 #pragma unroll
-      for (int e = 0; e < V16; ++e) acc = fmaf(q[i * V16 + e], kv[e], acc);
-    }
-    sc = acc * scale;
+    for (int e = 0; e < V16; ++e) acc = fmaf(q[i * V16 + e], kv[e], acc);
   }
-  const float m = wave_max(sc);
-  const float p = valid ? expf(sc - m) : 0.f;
-  const float l = wave_sum(p);
-  constexpr int HB = DH < 16 ? DH : 16;          // output dimensions per reduction pass
-  constexpr int SPREAD = kWave / HB;             // lanes holding each reduced value
-#pragma unroll
-  for (int h0 = 0; h0 < DH; h0 += HB) {
-    float pv[HB];
-    if (valid) {
-#pragma unroll
-      for (int d = 0; d < HB; d += V16) {
-        float vv[V16];
-        if constexpr (KR::HOLD_V) {
-          unpack_word<AT>(kr.v[(h0 + d) / V16], vv);
-        } else {
-          Vec16<AT>::load(Vb + static_cast<size_t>(key) * DH + h0, d, vv);
-        }
-#pragma unroll
-        for (int e = 0; e < V16; ++e) pv[d + e] = p * vv[e];
-      }
-    } else {
-#pragma unroll
-      for (int d = 0; d < HB; ++d) pv[d] = 0.f;
-    }
-    const float r = wave_reduce_scatter<HB>(pv, lane);
-    if ((lane & (SPREAD - 1)) == 0) slot->o[h0 + lane / SPREAD] = r;
-  }
-  if (lane == 0) {
-    slot->m = m;
-    slot->l = l;
-  }
-}
-
-// Fold one chunk partial into a row's running state.
-template <int DH>
-__device__ __forceinline__ void merge_chunk(RowState<DH>& st, const AttnSlot<DH>* c, int lane) {
-  const float cm = c->m;
-  const float mn = fmaxf(st.m, cm);
+  const float sc = valid ? acc * scale : -INFINITY;
+  const float mc = wave_max(sc);
+  const float p = valid ? expf(sc - mc) : 0.f;
+  const float lc = wave_sum(p);
+  const float mn = fmaxf(st.m, mc);
   const float a1 = expf(st.m - mn);
-  const float a2 = expf(cm - mn);
+  const float a2 = expf(mc - mn);
+  const int kc = min(kAttnChunk, nk - key0);       // keys of this chunk
+  sm.p[lane] = p;
 #pragma unroll
-  for (int i = 0; i < RowState<DH>::NO; ++i) {
-    const int d = lane + kWave * i;
-    const float co = d < DH ? c->o[d] : 0.f;
-    st.o[i] = st.o[i] * a1 + co * a2;
+  for (int p0 = 0; p0 < DH; p0 += SM::DP) {
+    // stage dimensions p0 .. p0+DP of the lane's V row
+    uint4* dst = reinterpret_cast<uint4*>(sm.v + lane * SM::LDV);
+#pragma unroll
+    for (int i = 0; i < SM::DP / V16; ++i) {
+      if constexpr (KR::HOLD_V) {
+        dst[i] = kr.v[p0 / V16 + i];
+      } else {
+        dst[i] = reinterpret_cast<const uint4*>(Vb + static_cast<size_t>(valid ? key : 0) * DH + p0)[i];
+      }
+    }
+    wave_lds_sync();
+    // lane (p0 + j) % 64 sums dimension p0 + j over the chunk's keys
+    const int j = lane - (p0 % kWave);
+    if (j >= 0 && j < SM::DP) {
+      float o4[4] = {0.f, 0.f, 0.f, 0.f};
+      for (int k = 0; k < kc; ++k)
+        o4[k & 3] = fmaf(sm.p[k], Elt<AT>::load(sm.v, k * SM::LDV + j), o4[k & 3]);
+      const float oc = (o4[0] + o4[1]) + (o4[2] + o4[3]);
+      float& so = st.o[(p0 + j) / kWave];
+      so = so * a1 + oc * a2;
+    }
+    wave_lds_sync();
   }
-  st.l = st.l * a1 + c->l * a2;
+  st.l = st.l * a1 + lc * a2;
   st.m = mn;
 }
 

@@ -17,10 +17,11 @@ __device__ __forceinline__ float bf16_to_f32(bf16_t h) {
 
 // Round-to-nearest-even float -> bfloat16 (NaN kept quiet).
 __device__ __forceinline__ bf16_t f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu)) return static_cast<bf16_t>((u >> 16) | 0x40);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return static_cast<bf16_t>(u >> 16);
+  const uint32_t u = __float_as_uint(f);
+  const uint32_t rne = (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;   // round to nearest even
+  const uint32_t qnan = (u >> 16) | 0x40u;                       // NaN: keep sign, set quiet bit
+  const bool is_nan = (u & 0x7fffffffu) > 0x7f800000u;
+  return static_cast<bf16_t>(is_nan ? qnan : rne);              // a select, not a branch
 }
 
 // Storage-type traits: load/store one element as float.
@@ -73,46 +74,72 @@ __device__ __forceinline__ void load_n(const T* p, size_t i, float* out) {
   }
 }
 
-// Butterfly sum over the 64 lanes of a wave; every lane gets the total.
-// The pairing order is fixed, so the result is bitwise reproducible.
+// Cross-lane reductions on DPP moves (a few cycles each, against a few
+// hundred for an LDS permute).  Inside a row of 16 lanes: exchange with lane
+// i^1, then i^2 (quad permutes), then the mirror in each half row (i <-> 7-i)
+// and in the row (i <-> 15-i).  Each step adds a lane's value and its partner's,
+// which both lanes of a pair compute alike, so after the four steps all 16
+// lanes hold the bitwise same total, in a fixed order.
+constexpr int kDppXor1 = 0xB1;         // quad_perm [1, 0, 3, 2]
+constexpr int kDppXor2 = 0x4E;         // quad_perm [2, 3, 0, 1]
+constexpr int kDppHalfMirror = 0x141;  // row_half_mirror
+constexpr int kDppMirror = 0x140;      // row_mirror
+
+template <int CTRL> __device__ __forceinline__ uint32_t dpp_u(uint32_t v) {
+  return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(v), CTRL, 0xF, 0xF, false));
+}
+template <int CTRL> __device__ __forceinline__ float dpp_f(float v) {
+  return __uint_as_float(dpp_u<CTRL>(__float_as_uint(v)));
+}
+
+__device__ __forceinline__ float group16_sum(float v) {
+  v += dpp_f<kDppXor1>(v);
+  v += dpp_f<kDppXor2>(v);
+  v += dpp_f<kDppHalfMirror>(v);
+  v += dpp_f<kDppMirror>(v);
+  return v;
+}
+__device__ __forceinline__ float group16_max(float v) {
+  v = fmaxf(v, dpp_f<kDppXor1>(v));
+  v = fmaxf(v, dpp_f<kDppXor2>(v));
+  v = fmaxf(v, dpp_f<kDppHalfMirror>(v));
+  v = fmaxf(v, dpp_f<kDppMirror>(v));
+  return v;
+}
+__device__ __forceinline__ uint32_t group16_or(uint32_t v) {
+  v |= dpp_u<kDppXor1>(v);
+  v |= dpp_u<kDppXor2>(v);
+  v |= dpp_u<kDppHalfMirror>(v);
+  v |= dpp_u<kDppMirror>(v);
+  return v;
+}
+
+// Best (larger key, then lower index) over each row of 16 lanes.  The
+// combination is associative and commutative, so every lane ends with the
+// same pair.
+__device__ __forceinline__ void best_take(uint32_t& bk, uint32_t& bi, uint32_t ok, uint32_t oi) {
+  if (ok > bk || (ok == bk && oi < bi)) { bk = ok; bi = oi; }
+}
+__device__ __forceinline__ void group16_best(uint32_t& bk, uint32_t& bi) {
+  best_take(bk, bi, dpp_u<kDppXor1>(bk), dpp_u<kDppXor1>(bi));
+  best_take(bk, bi, dpp_u<kDppXor2>(bk), dpp_u<kDppXor2>(bi));
+  best_take(bk, bi, dpp_u<kDppHalfMirror>(bk), dpp_u<kDppHalfMirror>(bi));
+  best_take(bk, bi, dpp_u<kDppMirror>(bk), dpp_u<kDppMirror>(bi));
+}
+
+// Whole-wave sum / max: the four row results (lanes 0, 16, 32, 48) are read
+// into scalars and combined as (r0 + r1) + (r2 + r3), the same in every lane.
+// All 64 lanes must be active.
+__device__ __forceinline__ float lane_read(float v, int l) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
+}
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
-  return v;
+  v = group16_sum(v);
+  return (lane_read(v, 0) + lane_read(v, 16)) + (lane_read(v, 32) + lane_read(v, 48));
 }
-
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) v = fmaxf(v, __shfl_xor(v, off));
-  return v;
-}
-
-// Sum of M values per lane across the 64 lanes of a wave (M a power of two,
-// M <= 64).  Halving exchange: after log2(M) steps each lane holds one partial
-// of value index j = lane >> (6 - log2 M); the remaining steps finish the sum
-// inside groups of 64 / M lanes.  Returns the total of value j in every lane of
-// group j.  Fixed pairing order: bitwise reproducible.
-template <int M>
-__device__ __forceinline__ float wave_reduce_scatter(float (&v)[M], int lane) {
-  static_assert(M >= 1 && M <= 64 && (M & (M - 1)) == 0, "M must be a power of two <= 64");
-  int off = 32;
-#pragma unroll
-  for (int half = M / 2; half >= 1; half >>= 1, off >>= 1) {
-    const bool upper = (lane & off) != 0;
-#pragma unroll
-    for (int j = 0; j < half; ++j) {
-      float a = v[j], b = v[j + half];
-      // opaque copies: the per-lane choice must stay a select of two values,
-      // not become a lane-dependent index into v (a long compare/select chain)
-      __asm__("" : "+v"(a), "+v"(b));
-      const float send = upper ? a : b;
-      const float keep = upper ? b : a;
-      v[j] = keep + __shfl_xor(send, off);
-    }
-  }
-  float r = v[0];
-  for (; off >= 1; off >>= 1) r += __shfl_xor(r, off);
-  return r;
+  v = group16_max(v);
+  return fmaxf(fmaxf(lane_read(v, 0), lane_read(v, 16)), fmaxf(lane_read(v, 32), lane_read(v, 48)));
 }
 
 template <int M> struct Log2 { static constexpr int v = 1 + Log2<M / 2>::v; };
@@ -134,27 +161,39 @@ __device__ __forceinline__ uint32_t float_key(float f) {
 // pass valid = false and contribute zeros).  The matrix-product prologue and
 // the row LayerNorm kernel both use it, so a row's statistics are bitwise the
 // same wherever they are computed.
-// Row elements held by one lane of a 16-lane LayerNorm group: eight
-// consecutive elements per 128-element slab.  bf16 rows stay packed (four
-// words per slab) and are widened on use, which is exact.
-template <typename XT, int NT> struct LnHold {
+// LayerNorm of a row of K elements (K a multiple of 8, K <= 512 * NT) by one
+// wave: lane j holds elements k = 8j + 512t + e (slab t < NT, e < 8).  Every
+// LayerNorm of the decoder (product and vocabulary prologues, the stand-alone
+// kernel) uses this split and order, so a row's normalised values are bitwise
+// the same wherever they are computed.
+//
+// The slabs are always loaded (from a valid address, so no load sits under a
+// branch); those outside the row are zeroed by mask() once the data is there.
+// bf16 rows stay packed and are widened on use, which is exact.
+template <typename XT, int NT> struct LnRow {
   float v[NT][8];
-  __device__ __forceinline__ void load(const XT* x, int t, int k0) { load_n<XT, 8>(x, k0, v[t]); }
-  __device__ __forceinline__ void clear(int t) {
+  uint32_t live;
+  __device__ __forceinline__ void load_slab(const XT* x, int t, int k0) { load_n<XT, 8>(x, k0, v[t]); }
+  __device__ __forceinline__ void mask() {
 #pragma unroll
-    for (int e = 0; e < 8; ++e) v[t][e] = 0.f;
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[t][e] = ((live >> t) & 1u) ? v[t][e] : 0.f;
   }
   __device__ __forceinline__ float get(int t, int e) const { return v[t][e]; }
 };
-template <int NT> struct LnHold<bf16_t, NT> {
+template <int NT> struct LnRow<bf16_t, NT> {
   uint32_t w[NT][4];
-  __device__ __forceinline__ void load(const bf16_t* x, int t, int k0) {
+  uint32_t live;
+  __device__ __forceinline__ void load_slab(const bf16_t* x, int t, int k0) {
     const uint4 q = *reinterpret_cast<const uint4*>(x + k0);
     w[t][0] = q.x; w[t][1] = q.y; w[t][2] = q.z; w[t][3] = q.w;
   }
-  __device__ __forceinline__ void clear(int t) {
+  __device__ __forceinline__ void mask() {
 #pragma unroll
-    for (int e = 0; e < 4; ++e) w[t][e] = 0u;
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) w[t][i] = ((live >> t) & 1u) ? w[t][i] : 0u;
   }
   __device__ __forceinline__ float get(int t, int e) const {
     const uint32_t u = w[t][e >> 1];
@@ -162,32 +201,34 @@ template <int NT> struct LnHold<bf16_t, NT> {
   }
 };
 
+// Issue the loads of row x (valid: the row exists; otherwise zeros).
 template <typename XT, int NT>
-__device__ __forceinline__ void ln_load_g16(const XT* x, int K, int j, bool valid, LnHold<XT, NT>& h) {
-  static_assert(NT >= 1 && NT <= 8, "at most 1024 elements");
-  const XT* xj = x + 8 * j;   // slab t of this lane starts 128 * t elements further on
+__device__ __forceinline__ void ln_row_load(LnRow<XT, NT>& h, const XT* x, int K, int lane, bool valid) {
+  h.live = 0u;
 #pragma unroll
   for (int t = 0; t < NT; ++t) {
-    if (valid && 8 * j + 128 * t < K) h.load(xj, t, 128 * t);
-    else h.clear(t);
+    const int k0 = 8 * lane + 512 * t;
+    const bool in = valid && k0 < K;
+    h.load_slab(x, t, in ? k0 : 0);
+    h.live |= (in ? 1u : 0u) << t;
   }
 }
 
+// Mean and 1 / sqrt(var + eps) of the row (two-pass variance).  All 64 lanes
+// must be active.
 template <typename XT, int NT>
-__device__ __forceinline__ void ln_stats_held(const LnHold<XT, NT>& h, int K, int j, float eps, float& mean,
-                                              float& rstd) {
+__device__ __forceinline__ void ln_row_stats(LnRow<XT, NT>& h, int K, float eps, float& mean, float& rstd) {
+  h.mask();
   float s = 0.f;
 #pragma unroll
   for (int t = 0; t < NT; ++t)
 #pragma unroll
     for (int e = 0; e < 8; ++e) s += h.get(t, e);
-#pragma unroll
-  for (int off = 1; off < 16; off <<= 1) s += __shfl_xor(s, off);
-  mean = s / static_cast<float>(K);
+  mean = wave_sum(s) / static_cast<float>(K);
   float q = 0.f;
 #pragma unroll
   for (int t = 0; t < NT; ++t) {
-    if (8 * j + 128 * t < K) {
+    if ((h.live >> t) & 1u) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const float d = h.get(t, e) - mean;
@@ -195,16 +236,7 @@ __device__ __forceinline__ void ln_stats_held(const LnHold<XT, NT>& h, int K, in
       }
     }
   }
-#pragma unroll
-  for (int off = 1; off < 16; off <<= 1) q += __shfl_xor(q, off);
-  rstd = 1.0f / sqrtf(q / static_cast<float>(K) + eps);
-}
-
-template <typename XT, int NT>
-__device__ __forceinline__ void ln_stats_g16(const XT* x, int K, int j, float eps, bool valid,
-                                             LnHold<XT, NT>& h, float& mean, float& rstd) {
-  ln_load_g16<XT, NT>(x, K, j, valid, h);
-  ln_stats_held<XT, NT>(h, K, j, eps, mean, rstd);
+  rstd = 1.0f / sqrtf(wave_sum(q) / static_cast<float>(K) + eps);
 }
 
 // LayerNorm of one element given its row statistics (same expression

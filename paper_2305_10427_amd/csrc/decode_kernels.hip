@@ -3,16 +3,13 @@
 #include "attn.h"
 #include "common.h"
 #include "kernels.h"
+#include "mma.h"
 
 namespace pdec {
 
 constexpr int kMaxKeys = 1024;
 constexpr int kMaxHeadDim = 128;
 
-__device__ __forceinline__ void row_place(const RowMap& m, int row, int& s, int& p) {
-  if (m.sent != nullptr) { s = m.sent[row]; p = m.pos[row]; }
-  else { s = row / m.per_sent; p = row - s * m.per_sent; }
-}
 
 // ---------------------------------------------------------------------------
 // Scaled dot-product attention, one wave per (row, head).
@@ -26,14 +23,14 @@ __device__ __forceinline__ void row_place(const RowMap& m, int row, int& s, int&
 template <typename AT, int DH>
 __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   __shared__ float s_q[4][DH];
-  __shared__ AttnSlot<DH> s_slot[4];
+  __shared__ AttnStage<AT, DH> s_stage[4];
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = threadIdx.x / kWave;
   const int R = a.n_rows_dev ? *a.n_rows_dev : a.n_rows;
   const int idx = blockIdx.x * 4 + wave;
   const int row = idx / a.H;
   const int hh = idx - row * a.H;
-  if (row >= R) return;   // no workgroup barrier below
+  if (row >= R) return;   // whole wave; no workgroup barrier below
   int s, p;
   row_place(a.rows, row, s, p);
   const int nk = a.causal ? p + 1 : a.klen[s];
@@ -44,20 +41,18 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   KeyRows<AT, DH> kr;
   kr.load(Kb, Vb, lane, lane < nk);
   const float* q = a.q + static_cast<size_t>(row) * a.ldq + hh * DH;
-  for (int d = lane; d < DH; d += kWave) s_q[wave][d] = q[d];
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+  for (int i = 0; i < (DH + kWave - 1) / kWave; ++i) {
+    const int d = lane + kWave * i;
+    const float v = q[d < DH ? d : 0];   // unconditional load
+    if (d < DH) s_q[wave][d] = v;
+  }
+  wave_lds_sync();
   RowState<DH> st;
   st.init();
   for (int key0 = 0; key0 < nk; key0 += kAttnChunk) {
     if (key0 > 0) kr.load(Kb, Vb, key0 + lane, key0 + lane < nk);
-    chunk_partial<AT, DH>(s_q[wave], kr, Vb, key0, nk, a.scale, lane, &s_slot[wave]);
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    merge_chunk<DH>(st, &s_slot[wave], lane);
-    __builtin_amdgcn_wave_barrier();
+    chunk_fold<AT, DH>(s_q[wave], kr, Vb, key0, nk, a.scale, lane, s_stage[wave], st);
   }
   row_output<AT, DH>(st, static_cast<AT*>(a.out) + static_cast<size_t>(row) * a.ldo + hh * DH, lane);
 }
@@ -89,35 +84,21 @@ __global__ __launch_bounds__(256) void k_embed(EmbedArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Row LayerNorm, 4 rows per wave with 16 lanes per row, statistics by
-// ln_stats_g16 (the same lane split and pairing as the LayerNorm prologue of
-// the matrix products).
+// Row LayerNorm, one wave per row, with the statistics and element split of
+// the LayerNorm prologue of the products (ln_row_stats, ln_row_apply), so a
+// row is normalised bitwise alike here and there.
 template <typename WT, typename XT, int NT>
 __global__ __launch_bounds__(256) void k_ln(LnArgs a) {
   const int lane = threadIdx.x & (kWave - 1);
-  const int wave = threadIdx.x / kWave;
-  const int j = lane & 15;
-  const int row = (blockIdx.x * 4 + wave) * 4 + (lane >> 4);
+  const int row = blockIdx.x * 4 + threadIdx.x / kWave;
   const int R = a.n_rows_dev ? *a.n_rows_dev : a.n_rows;
-  const bool ok = row < R;
-  const XT* x = static_cast<const XT*>(a.x) + static_cast<size_t>(ok ? row : 0) * a.d;
-  LnHold<XT, NT> h;
+  if (row >= R) return;   // whole wave
+  LnRow<XT, NT> h;
+  ln_row_load<XT, NT>(h, static_cast<const XT*>(a.x) + static_cast<size_t>(row) * a.d, a.d, lane, true);
   float mean, rstd;
-  ln_stats_g16<XT, NT>(x, a.d, j, a.eps, ok, h, mean, rstd);
-  if (!ok) return;
-#pragma unroll
-  for (int t = 0; t < NT; ++t) {
-    const int k0 = 8 * j + 128 * t;
-    if (k0 < a.d) {
-      float g[8], b[8];
-      load_n<WT, 8>(static_cast<const WT*>(a.g), k0, g);
-      load_n<WT, 8>(static_cast<const WT*>(a.b), k0, b);
-#pragma unroll
-      for (int e = 0; e < 8; ++e)
-        Elt<WT>::store(static_cast<WT*>(a.out), static_cast<size_t>(row) * a.d + k0 + e,
-                       ln_apply(h.get(t, e), mean, rstd, g[e], b[e]));
-    }
-  }
+  ln_row_stats<XT, NT>(h, a.d, a.eps, mean, rstd);
+  ln_row_apply<WT, XT, NT>(h, a.d, mean, rstd, static_cast<const WT*>(a.g), static_cast<const WT*>(a.b),
+                           static_cast<WT*>(a.out) + static_cast<size_t>(row) * a.d, nullptr, lane);
 }
 
 // ---------------------------------------------------------------------------
@@ -225,9 +206,8 @@ struct Best {
 // (larger key, then lower index) wins; the non-finite bits are or-ed.  The
 // order of combination does not change the result.
 __device__ __forceinline__ void best_merge(uint32_t& bk, uint32_t& bi, uint32_t& nf, uint32_t k2, uint32_t raw) {
-  const uint32_t i2 = raw & 0x7fffffffu;
   nf |= raw >> 31;
-  if (k2 > bk || (k2 == bk && i2 < bi)) { bk = k2; bi = i2; }
+  best_take(bk, bi, k2, raw & 0x7fffffffu);
 }
 
 // Best over partials p[t0 .. t1) by one wave, eight loads per lane in flight.
@@ -240,14 +220,17 @@ __device__ __forceinline__ Best reduce_span(const uint2* p, int t0, int t1, int 
 #pragma unroll
     for (int u = 0; u < 8; ++u) best_merge(bk, bi, nf, v[u].x, v[u].y);
   }
+  group16_best(bk, bi);
+  nf = group16_or(nf);
+  // the four rows of 16 lanes (all lanes are active here)
+  uint32_t rk = __builtin_amdgcn_readlane(bk, 0), ri = __builtin_amdgcn_readlane(bi, 0);
+  uint32_t rf = __builtin_amdgcn_readlane(nf, 0);
 #pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    const uint32_t ok = __shfl_xor(bk, off);
-    const uint32_t oi = __shfl_xor(bi, off);
-    nf |= __shfl_xor(nf, off);
-    if (ok > bk || (ok == bk && oi < bi)) { bk = ok; bi = oi; }
+  for (int r = 16; r < kWave; r += 16) {
+    best_take(rk, ri, __builtin_amdgcn_readlane(bk, r), __builtin_amdgcn_readlane(bi, r));
+    rf |= __builtin_amdgcn_readlane(nf, r);
   }
-  return Best{bk, bi | (nf << 31)};
+  return Best{rk, ri | (rf << 31)};
 }
 
 // Argmax of each of R rows over the per-workgroup partials of the fused
@@ -384,20 +367,20 @@ hipError_t launch_embed(int dtype, const EmbedArgs& a, int R_max, hipStream_t s)
 }
 
 hipError_t launch_ln(int dtype, const LnArgs& a, int R_max, hipStream_t s) {
-  const int grid = (R_max + 15) / 16;
+  const int grid = (R_max + 3) / 4;
   if (grid == 0) return hipSuccess;
   if (a.d % 8 != 0 || a.d > 1024) return hipErrorInvalidValue;
   if (dtype == DT_BF16) {
     if (a.d > 512) {
-      if (a.x_f32) hipLaunchKernelGGL((k_ln<bf16_t, float, 8>), dim3(grid), dim3(256), 0, s, a);
-      else hipLaunchKernelGGL((k_ln<bf16_t, bf16_t, 8>), dim3(grid), dim3(256), 0, s, a);
+      if (a.x_f32) hipLaunchKernelGGL((k_ln<bf16_t, float, 2>), dim3(grid), dim3(256), 0, s, a);
+      else hipLaunchKernelGGL((k_ln<bf16_t, bf16_t, 2>), dim3(grid), dim3(256), 0, s, a);
     } else {
-      if (a.x_f32) hipLaunchKernelGGL((k_ln<bf16_t, float, 4>), dim3(grid), dim3(256), 0, s, a);
-      else hipLaunchKernelGGL((k_ln<bf16_t, bf16_t, 4>), dim3(grid), dim3(256), 0, s, a);
+      if (a.x_f32) hipLaunchKernelGGL((k_ln<bf16_t, float, 1>), dim3(grid), dim3(256), 0, s, a);
+      else hipLaunchKernelGGL((k_ln<bf16_t, bf16_t, 1>), dim3(grid), dim3(256), 0, s, a);
     }
   } else {
     if (a.d > 512) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((k_ln<float, float, 4>), dim3(grid), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((k_ln<float, float, 1>), dim3(grid), dim3(256), 0, s, a);
   }
   return hipGetLastError();
 }

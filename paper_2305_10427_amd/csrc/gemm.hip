@@ -67,42 +67,48 @@ __global__ __launch_bounds__(KSPLIT == 8 ? 512 : 256) void k_gemm(GemmArgs a) {
   const int m_first = blockIdx.y * 16 * a.mt_per_wg;
   const int m_last = min(R_max, m_first + 16 * a.mt_per_wg);
 
-  // PRO_LN: the first tile's input rows and gamma / beta go out before the
-  // weights -- loads complete in issue order, and the LayerNorm must not
-  // wait for the weight stream.  Gamma and beta are staged through LDS (one
-  // 16-byte word per thread of the first 256).
-  LnTileRows<WT, XT, LNT> ln;
+  // Loads complete in issue order, so the small loads the prologue and the
+  // epilogue need go out before the weight stream: PRO_LN's input rows of the
+  // first tile and gamma / beta (staged through LDS, one 16-byte word per
+  // thread of the first 256), the bias, the residual of the first tile.
+  // Every load is unconditional (clamped to a valid address, unused values
+  // dropped later): a load under a branch makes the compiler wait for all
+  // earlier loads where the paths join.
+  LnTile<WT, XT, LNT / 4> ln;   // LNT: 128-element slabs of a 16-lane row group; 4 per 512
   __shared__ uint4 s_gb[PRO == PRO_LN ? 2 : 1][128];
   uint4 gb = make_uint4(0u, 0u, 0u, 0u);
   const int gw = threadIdx.x & 127;
-  const bool gb_lane = PRO == PRO_LN && threadIdx.x < 256 && gw < K * static_cast<int>(sizeof(WT)) / 16;
   if constexpr (PRO == PRO_LN) {
-    if (wave < 4) ln.load(X, a.ldx, K, m_first, R_max, wave, lane);
-    if (gb_lane) gb = static_cast<const uint4*>(threadIdx.x < 128 ? a.ln_g : a.ln_b)[gw];
+    ln.load(X, a.ldx, K, m_first, R_max, wave & 3, lane);
+    const bool gb_word = gw < K * static_cast<int>(sizeof(WT)) / 16;
+    gb = static_cast<const uint4*>((threadIdx.x & 128) ? a.ln_b : a.ln_g)[gb_word ? gw : 0];
   }
-
-  // Then the loads that do not depend on the previous kernel: the first
-  // weight batch, the bias, the residual of the first tile's outputs.
-  frag bcur[D];
-#pragma unroll
-  for (int u = 0; u < D; ++u) {
-    const int step = s_begin + u;
-    bcur[u] = (step < s_end && col < N) ? MM::load(wrow + step * KS) : MM::zero();
-  }
-  const float bias_v = (col < N) ? Elt<WT>::load(static_cast<const WT*>(a.bias), col) : 0.f;
+  const float bias_v = Elt<WT>::load(static_cast<const WT*>(a.bias), col < N ? col : 0);
   constexpr int NE = SPLIT ? 1 : 4;       // output elements finished per lane
   const bool epi_wave = !SPLIT || wave < 4;   // waves that finish outputs
   float rpre[NE];
   if constexpr (EPI == EPI_RESID) {
 #pragma unroll
     for (int e = 0; e < NE; ++e) {
-      const int row = m_first + 4 * lg + (SPLIT ? wave : e);
-      const size_t ri = static_cast<size_t>(row) * a.ldr + col;
-      rpre[e] = (epi_wave && row < R_max && col < N)
-                    ? (a.resid_f32 ? static_cast<const float*>(a.resid)[ri] : Elt<AT>::load(static_cast<const AT*>(a.resid), ri))
-                    : 0.f;
+      const int row = m_first + 4 * lg + (SPLIT ? (wave & 3) : e);
+      const size_t ri = static_cast<size_t>(row < R_max ? row : 0) * a.ldr + (col < N ? col : 0);
+      rpre[e] = Elt<AT>::load(static_cast<const AT*>(a.resid), ri);
     }
   }
+  int rs[NE], rp[NE];                     // EPI_QKV: (sentence, position) of the first tile's rows
+  if constexpr (EPI == EPI_QKV) {
+#pragma unroll
+    for (int e = 0; e < NE; ++e) {
+      const int row = m_first + 4 * lg + (SPLIT ? (wave & 3) : e);
+      row_place(a.rows, row < R_max ? row : 0, rs[e], rp[e]);
+    }
+  }
+  __builtin_amdgcn_sched_barrier(0);   // keep the loads above ahead of the weights
+
+  // the first weight batch
+  frag bcur[D];
+#pragma unroll
+  for (int u = 0; u < D; ++u) bcur[u] = MM::load(wrow + min(s_begin + u, n_steps - 1) * KS);
   const int R = a.n_rows_dev ? *a.n_rows_dev : a.n_rows;
 
   __shared__ float s_part[KSPLIT > 1 ? KSPLIT : 1][4][64];
@@ -113,7 +119,7 @@ __global__ __launch_bounds__(KSPLIT == 8 ? 512 : 256) void k_gemm(GemmArgs a) {
   AT* sA = reinterpret_cast<AT*>(s_dyn);
   const int lda = K + 16 / static_cast<int>(sizeof(AT));
   if constexpr (PRO == PRO_LN) {
-    if (gb_lane) s_gb[threadIdx.x >> 7][gw] = gb;
+    s_gb[(threadIdx.x >> 7) & 1][gw] = gb;   // words past the rows are never read
     __syncthreads();
   }
 
@@ -122,14 +128,9 @@ __global__ __launch_bounds__(KSPLIT == 8 ? 512 : 256) void k_gemm(GemmArgs a) {
     const int arow = m0 + lr;                 // X row fed by this lane
     const bool arow_ok = arow < R_max;
     if (m0 != m_first) {
-      if constexpr (PRO == PRO_LN) {
-        if (wave < 4) ln.load(X, a.ldx, K, m0, R_max, wave, lane);
-      }
+      if constexpr (PRO == PRO_LN) ln.load(X, a.ldx, K, m0, R_max, wave & 3, lane);
 #pragma unroll
-      for (int u = 0; u < D; ++u) {
-        const int step = s_begin + u;
-        bcur[u] = (step < s_end && col < N) ? MM::load(wrow + step * KS) : MM::zero();
-      }
+      for (int u = 0; u < D; ++u) bcur[u] = MM::load(wrow + min(s_begin + u, n_steps - 1) * KS);
     }
     if constexpr (PRO == PRO_LN) {
       if (wave < 4)
@@ -144,30 +145,29 @@ __global__ __launch_bounds__(KSPLIT == 8 ? 512 : 256) void k_gemm(GemmArgs a) {
       const bool more = s0 + D < s_end;
       if (more) {
 #pragma unroll
-        for (int u = 0; u < D; ++u) {
-          const int step = s0 + D + u;
-          bnext[u] = (step < s_end && col < N) ? MM::load(wrow + step * KS) : MM::zero();
-        }
+        for (int u = 0; u < D; ++u) bnext[u] = MM::load(wrow + min(s0 + D + u, n_steps - 1) * KS);
       }
       frag af[D];
 #pragma unroll
       for (int u = 0; u < D; ++u) {
-        const int k = (s0 + u) * KS + EPL * lg;
-        const bool ok = s0 + u < s_end;
+        const int k = min(s0 + u, n_steps - 1) * KS + EPL * lg;
         if constexpr (PRO == PRO_LN) {
-          af[u] = ok ? MM::load(sA + static_cast<size_t>(lr) * lda + k) : MM::zero();
+          af[u] = MM::load(sA + static_cast<size_t>(lr) * lda + k);
+        } else if constexpr (std::is_same<XT, AT>::value) {
+          af[u] = MM::load(X + static_cast<size_t>(arow_ok ? arow : 0) * a.ldx + k);
         } else {
-          if (ok && arow_ok) {
-            float xv[EPL];
-            load_n<XT, EPL>(X, static_cast<size_t>(arow) * a.ldx + k, xv);
-            af[u] = MM::pack(xv);
-          } else {
-            af[u] = MM::zero();
-          }
+          float xv[EPL];
+          load_n<XT, EPL>(X, static_cast<size_t>(arow_ok ? arow : 0) * a.ldx + k, xv);
+          af[u] = MM::pack(xv);
         }
       }
+      __builtin_amdgcn_sched_barrier(0);   // all loads of the batch before its products
+      // steps past the wave's K range contribute exact zeros
 #pragma unroll
-      for (int u = 0; u < D; ++u) acc = MM::step(af[u], bcur[u], acc);
+      for (int u = 0; u < D; ++u) {
+        const bool ok = s0 + u < s_end;
+        acc = MM::step(ok ? af[u] : MM::zero(), ok ? bcur[u] : MM::zero(), acc);
+      }
       if (more) {
 #pragma unroll
         for (int u = 0; u < D; ++u) bcur[u] = bnext[u];
@@ -191,9 +191,9 @@ __global__ __launch_bounds__(KSPLIT == 8 ? 512 : 256) void k_gemm(GemmArgs a) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) cv[i] = acc[i];
     }
-    uint32_t bk[4] = {0, 0, 0, 0};
-    int bi[4] = {0x7fffffff, 0x7fffffff, 0x7fffffff, 0x7fffffff};
-    int nf = 0;
+    uint32_t bk[4] = {0u, 0u, 0u, 0u};
+    uint32_t bi[4] = {0x7fffffffu, 0x7fffffffu, 0x7fffffffu, 0x7fffffffu};
+    uint32_t nf = 0;
 #pragma unroll
     for (int e = 0; e < NE; ++e) {
       const int i = SPLIT ? wave : e;
@@ -208,9 +208,7 @@ __global__ __launch_bounds__(KSPLIT == 8 ? 512 : 256) void k_gemm(GemmArgs a) {
         Elt<AT>::store(static_cast<AT*>(a.out), static_cast<size_t>(row) * a.ldo + col, t);
       } else if constexpr (EPI == EPI_RESID) {
         const size_t ri = static_cast<size_t>(row) * a.ldr + col;
-        const float rv = m0 == m_first ? rpre[e]
-                         : (a.resid_f32 ? static_cast<const float*>(a.resid)[ri]
-                                        : Elt<AT>::load(static_cast<const AT*>(a.resid), ri));
+        const float rv = m0 == m_first ? rpre[e] : Elt<AT>::load(static_cast<const AT*>(a.resid), ri);
         const float t = (v + bias_v) + rv;
         if (a.out_f32 != nullptr) a.out_f32[static_cast<size_t>(row) * a.ldo + col] = t;
         else Elt<AT>::store(static_cast<AT*>(a.out), static_cast<size_t>(row) * a.ldo + col, t);
@@ -224,9 +222,8 @@ __global__ __launch_bounds__(KSPLIT == 8 ? 512 : 256) void k_gemm(GemmArgs a) {
           const int cc = c - which * a.d;
           const int hh = cc / a.dh;
           const int dd = cc - hh * a.dh;
-          int s, p;
-          if (a.rows.sent != nullptr) { s = a.rows.sent[row]; p = a.rows.pos[row]; }
-          else { s = row / a.rows.per_sent; p = row - s * a.rows.per_sent; }
+          int s = rs[e], p = rp[e];
+          if (m0 != m_first) row_place(a.rows, row, s, p);
           const size_t idx = ((static_cast<size_t>(s) * a.H + hh) * a.T + p) * a.dh + dd;
           Elt<AT>::store(static_cast<AT*>(which == 0 ? a.kc : a.vc), idx, t);
         }
@@ -234,31 +231,21 @@ __global__ __launch_bounds__(KSPLIT == 8 ? 512 : 256) void k_gemm(GemmArgs a) {
         a.out_f32[static_cast<size_t>(row) * a.ldo + col] = fmaf(a.logit_scale, v, bias_v);
       } else if constexpr (EPI == EPI_ARGMAX) {
         const float logit = fmaf(a.logit_scale, v, bias_v);   // s * (h . E[col]) + bias[col]
-        if (!isfinite(logit)) nf |= 1 << e;   // bit e: a non-finite logit in row 4 lg + e
-        else { bk[e] = float_key(logit); bi[e] = col; }
+        if (!isfinite(logit)) nf |= 1u << e;   // bit e: a non-finite logit in row 4 lg + e
+        else { bk[e] = float_key(logit); bi[e] = static_cast<uint32_t>(col); }
       }
     }
     if constexpr (EPI == EPI_ARGMAX) {
       static_assert(KSPLIT == 1, "the fused argmax runs with whole-K waves");
       // best of each row over the 16 columns held by one 16-lane group
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-#pragma unroll
-        for (int off = 1; off < 16; off <<= 1) {
-          const uint32_t ok = __shfl_xor(bk[e], off);
-          const int oi = __shfl_xor(bi[e], off);
-          if (ok > bk[e] || (ok == bk[e] && oi < bi[e])) { bk[e] = ok; bi[e] = oi; }
-        }
-      }
-      nf |= __shfl_xor(nf, 1);
-      nf |= __shfl_xor(nf, 2);
-      nf |= __shfl_xor(nf, 4);
-      nf |= __shfl_xor(nf, 8);
+      for (int e = 0; e < 4; ++e) group16_best(bk[e], bi[e]);
+      nf = group16_or(nf);
       if (lr == 0) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           s_key[wave][4 * lg + e] = bk[e];
-          s_idx[wave][4 * lg + e] = bi[e] | (((nf >> e) & 1) << 31);
+          s_idx[wave][4 * lg + e] = static_cast<int>(bi[e] | (((nf >> e) & 1u) << 31));
         }
       }
       __syncthreads();

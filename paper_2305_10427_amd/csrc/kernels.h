@@ -17,6 +17,12 @@ struct RowMap {
   int per_sent;
 };
 
+// (sentence, position) of row `row`.
+__device__ __forceinline__ void row_place(const RowMap& m, int row, int& s, int& p) {
+  if (m.sent != nullptr) { s = m.sent[row]; p = m.pos[row]; }
+  else { s = row / m.per_sent; p = row - s * m.per_sent; }
+}
+
 enum Prologue { PRO_NONE = 0, PRO_LN = 1 };
 enum Epilogue {
   EPI_F32 = 0,     // out_f32 = acc + bias
@@ -49,9 +55,8 @@ struct GemmArgs {
   float* out_f32;
   void* out;
   int ldo;
-  const void* resid;
+  const void* resid;       // residual, storage type (EPI_RESID)
   int ldr;
-  int resid_f32;
   int act;                 // 1 relu, 2 gelu (EPI_ACT)
   int q_cols;              // EPI_QKV
   void* kc;                // EPI_QKV: K / V caches [S][H][T][dh] of one layer

@@ -56,49 +56,67 @@ __device__ __forceinline__ float gelu_erf(float v) {
   return 0.5f * v * (1.0f + erff(v * 0.70710678118654752f));
 }
 
-// LayerNorm of the 16-row input tile rows m0 .. m0+15 (rows >= R_max read as
-// zeros) into the LDS tile sA[16][lda] in the storage type, by waves 0..3:
-// wave w owns tile rows 4w .. 4w+3 with 16 lanes per row (statistics as in
-// ln_stats_g16).  load() issues the row loads and finish() computes the
-// statistics and writes the normalised rows (also to ln_out, rows below
-// R_out, when it is non-null), so a caller can issue other loads in between.
-// The caller synchronises the workgroup after finish().
-template <typename WT, typename XT, int LNT> struct LnTileRows {
-  LnHold<XT, LNT> h;
-  int lr, tr, row;
-  bool ok;
-  __device__ __forceinline__ void load(const XT* X, int ldx, int K, int m0, int R_max, int wave, int lane) {
-    lr = lane & 15;
-    tr = 4 * wave + (lane >> 4);
-    row = m0 + tr;
-    ok = row < R_max;
-    ln_load_g16<XT, LNT>(X + static_cast<size_t>(ok ? row : 0) * ldx, K, lr, ok, h);
+// Normalised values of a row (statistics from ln_row_stats) rounded to the
+// storage type and written to dst (one row; lane j writes elements
+// 8j + 512t .. +7) and, when out is non-null, also to out.  g, b: gamma and
+// beta, in global memory or LDS.
+template <typename WT, typename XT, int NT>
+__device__ __forceinline__ void ln_row_apply(const LnRow<XT, NT>& h, int K, float mean, float rstd, const WT* g,
+                                             const WT* b, WT* dst, WT* out, int lane) {
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    const int k0 = 8 * lane + 512 * t;
+    if (k0 < K) {
+      float gv[8], bv[8], y[8];
+      load_n<WT, 8>(g, k0, gv);
+      load_n<WT, 8>(b, k0, bv);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) y[e] = ln_apply(h.get(t, e), mean, rstd, gv[e], bv[e]);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) Elt<WT>::store(dst, k0 + e, y[e]);
+      if (out != nullptr) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) Elt<WT>::store(out, k0 + e, y[e]);
+      }
+    }
   }
-  // g, b: gamma and beta, in global memory or LDS
+}
+
+// LayerNorm of the 16-row input tile rows m0 .. m0+15 into the LDS tile
+// sA[16][lda] in the storage type, by 4 waves: wave w owns tile rows
+// w, w + 4, w + 8, w + 12 (one row per pass).  load() issues the loads of all
+// 16 rows (rows >= R_max read row 0 and are not used), so a caller can issue
+// other loads after it; finish() normalises the passes that hold rows below
+// R_max (rows of later passes are left unwritten: their products are
+// discarded) and also writes rows below R_out to ln_out when it is non-null.
+// The caller synchronises the workgroup after finish().
+template <typename WT, typename XT, int NT> struct LnTile {
+  LnRow<XT, NT> h[4];
+  int wave, lane, m0, R_max;
+  __device__ __forceinline__ void load(const XT* X, int ldx, int K, int m0_, int R_max_, int wave_, int lane_) {
+    wave = wave_;
+    lane = lane_;
+    m0 = m0_;
+    R_max = R_max_;
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      const int row = m0 + 4 * p + wave;
+      const bool ok = row < R_max;
+      ln_row_load<XT, NT>(h[p], X + static_cast<size_t>(ok ? row : 0) * ldx, K, lane, ok);
+    }
+  }
   __device__ __forceinline__ void finish(int K, float eps, const WT* g, const WT* b, WT* sA, int lda, WT* ln_out,
                                          int ldlo, int R_out) {
-    float mean, rstd;
-    ln_stats_held<XT, LNT>(h, K, lr, eps, mean, rstd);
-    const bool write_out = ln_out != nullptr && row < R_out;
-    // per-lane bases; slab t adds the constant 128 * t
-    const WT* gj = g + 8 * lr;
-    const WT* bj = b + 8 * lr;
-    WT* aj = sA + static_cast<size_t>(tr) * lda + 8 * lr;
-    WT* oj = write_out ? ln_out + static_cast<size_t>(row) * ldlo + 8 * lr : nullptr;
+    const int n_pass = min(4, (R_max - m0 + 3) / 4);
 #pragma unroll
-    for (int t = 0; t < LNT; ++t) {
-      if (8 * lr + 128 * t < K) {
-        float gv[8], bv[8], y[8];
-        load_n<WT, 8>(gj, 128 * t, gv);
-        load_n<WT, 8>(bj, 128 * t, bv);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) y[e] = Elt<WT>::round(ln_apply(h.get(t, e), mean, rstd, gv[e], bv[e]));
-#pragma unroll
-        for (int e = 0; e < 8; ++e) Elt<WT>::store(aj, 128 * t + e, y[e]);
-        if (write_out) {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) Elt<WT>::store(oj, 128 * t + e, y[e]);
-        }
+    for (int p = 0; p < 4; ++p) {
+      if (p < n_pass) {
+        const int tr = 4 * p + wave;
+        const int row = m0 + tr;
+        float mean, rstd;
+        ln_row_stats<XT, NT>(h[p], K, eps, mean, rstd);
+        WT* out = (ln_out != nullptr && row < R_out) ? ln_out + static_cast<size_t>(row) * ldlo : nullptr;
+        ln_row_apply<WT, XT, NT>(h[p], K, mean, rstd, g, b, sA + static_cast<size_t>(tr) * lda, out, lane);
       }
     }
   }

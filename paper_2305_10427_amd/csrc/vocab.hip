@@ -65,29 +65,29 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(VocabShape<
   // Loads complete in issue order, so everything the LayerNorm prologue reads
   // goes out before the weight ring: the rows (held in registers), then
   // gamma and beta (one 16-byte word per lane, staged through LDS).
-  LnTileRows<WT, XT, LNT> ln;
+  LnTile<WT, XT, LNT / 4> ln;
   ln.load(static_cast<const XT*>(a.x), a.ldx, K, 0, a.n_rows, wave, lane);
   __shared__ uint4 s_gb[2][128];                   // gamma, beta: up to 2 KB each
   const int gb_words = K * static_cast<int>(sizeof(WT)) / 16;
   const int gw = threadIdx.x & 127;
-  uint4 gb = make_uint4(0u, 0u, 0u, 0u);
-  if (gw < gb_words) gb = static_cast<const uint4*>(threadIdx.x < 128 ? a.ln_g : a.ln_b)[gw];
+  const uint4 gb = static_cast<const uint4*>(threadIdx.x < 128 ? a.ln_g : a.ln_b)[gw < gb_words ? gw : 0];
+  __builtin_amdgcn_sched_barrier(0);   // keep these loads ahead of the weight ring
 
-  // prime the ring: the first D (tile, step) loads
+  // prime the ring: the first D (tile, step) loads.  No load sits under a
+  // branch (that would make the compiler wait for every earlier load); a
+  // wave with fewer than D steps reads clamped rows it never uses.
   frag ring[D];
   int jn = 0, sn = 0;                // (tile, step) of the next load
   const WT* pn = wrow(0);
 #pragma unroll
   for (int u = 0; u < D; ++u) {
-    if (u < total) {
-      ring[u] = MM::load(pn + sn * KS);
-      if (++sn == n_steps) { sn = 0; ++jn; pn = wrow(jn); }
-    }
+    ring[u] = MM::load(pn + sn * KS);
+    if (++sn == n_steps) { sn = 0; ++jn; pn = wrow(jn); }
   }
-  float bias_v = my_tiles > 0 ? Elt<WT>::load(bias, min(w_id * 16 + lr, N - 1)) : 0.f;
+  float bias_v = Elt<WT>::load(bias, min(w_id * 16 + lr, N - 1));
 
   // LayerNorm of the (at most 16) rows into LDS while the weights arrive
-  if (gw < gb_words) s_gb[threadIdx.x >> 7][gw] = gb;
+  s_gb[threadIdx.x >> 7][gw] = gb;     // words past the rows are never read
   __syncthreads();
   extern __shared__ __align__(16) unsigned char s_dyn[];
   AT* sA = reinterpret_cast<AT*>(s_dyn);
@@ -99,8 +99,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(VocabShape<
 
   // stream: consume step g from ring[g % D], refill it with step g + D
   uint32_t bk[4] = {0u, 0u, 0u, 0u};
-  int bi[4] = {0x7fffffff, 0x7fffffff, 0x7fffffff, 0x7fffffff};
-  int nf = 0;                        // bit i: a non-finite logit in row 4 lg + i
+  uint32_t bi[4] = {0x7fffffffu, 0x7fffffffu, 0x7fffffffu, 0x7fffffffu};
+  uint32_t nf = 0;                   // bit i: a non-finite logit in row 4 lg + i
   floatx4_t acc = {0.f, 0.f, 0.f, 0.f};
   int j = 0, s = 0;                  // (tile, step) being consumed
   const AT* arow = sA + static_cast<size_t>(lr) * lda + EPL * lg;
@@ -121,12 +121,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(VocabShape<
           for (int i = 0; i < 4; ++i) {
             if (4 * lg + i >= R) continue;
             const float logit = fmaf(a.logit_scale, acc[i], bias_v);   // s * (h . E[col]) + bias[col]
-            if (!isfinite(logit)) {
-              nf |= 1 << i;
-            } else {
-              const uint32_t key = float_key(logit);
-              if (key > bk[i] || (key == bk[i] && col < bi[i])) { bk[i] = key; bi[i] = col; }
-            }
+            if (!isfinite(logit)) nf |= 1u << i;
+            else best_take(bk[i], bi[i], float_key(logit), static_cast<uint32_t>(col));
           }
         }
         acc = floatx4_t{0.f, 0.f, 0.f, 0.f};
@@ -139,23 +135,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(VocabShape<
 
   // best of each row over the 16 columns of a lane group, then over the waves
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-#pragma unroll
-    for (int off = 1; off < 16; off <<= 1) {
-      const uint32_t ok = __shfl_xor(bk[i], off);
-      const int oi = __shfl_xor(bi[i], off);
-      if (ok > bk[i] || (ok == bk[i] && oi < bi[i])) { bk[i] = ok; bi[i] = oi; }
-    }
-  }
-#pragma unroll
-  for (int off = 1; off < 16; off <<= 1) nf |= __shfl_xor(nf, off);
+  for (int i = 0; i < 4; ++i) group16_best(bk[i], bi[i]);
+  nf = group16_or(nf);
   __shared__ uint32_t s_key[4][16];
   __shared__ int s_idx[4][16];
   if (lr == 0) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       s_key[wave][4 * lg + i] = bk[i];
-      s_idx[wave][4 * lg + i] = bi[i] | (((nf >> i) & 1) << 31);
+      s_idx[wave][4 * lg + i] = static_cast<int>(bi[i] | (((nf >> i) & 1u) << 31));
     }
   }
   __syncthreads();
