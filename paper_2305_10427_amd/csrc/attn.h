@@ -4,8 +4,8 @@
 // For one chunk (keys key0 .. key0+63 that are < nk):
 //   s_k = (q . k_k) * scale          lane k scores key key0 + k
 //   m_c = max_k s_k,  p_k = exp(s_k - m_c),  l_c = sum_k p_k     (DPP trees)
-//   o_c[d] = sum_k p_k v_k[d]        lane d, keys in increasing order (p and
-//                                    the chunk's V rows staged through LDS)
+//   o_c[d] = sum_k p_k v_k[d]        lane d, four partial sums over the keys
+//                                    (p and the V rows staged through LDS)
 // and a row's chunks are folded in chunk order:
 //   m' = max(m, m_c),  o <- o exp(m - m') + o_c exp(m_c - m'),  l likewise,
 // the output being o / l.  Chunk boundaries depend only on the row's own key
@@ -32,8 +32,7 @@ template <int DH> struct RowState {
   }
 };
 
-// The K and V rows of the key a lane scores, as raw 16-byte words, loaded
-// ahead of the query.  V is held only when it fits comfortably in registers
+// The K and V rows of the key a lane scores, as raw 16-byte words.  V is held only when it fits comfortably in registers
 // (<= 256 bytes per row); otherwise it is read again when staged.
 template <typename AT, int DH> struct KeyRows {
   static constexpr int V16 = Vec16<AT>::N;        // elements per 16-byte word
@@ -97,14 +96,16 @@ __device__ __forceinline__ void chunk_fold(const float* q, const KeyRows<AT, DH>
   constexpr int V16 = KR::V16;
   const int key = key0 + lane;
   const bool valid = key < nk;
-  float acc = 0.f;
+  // q . k as four interleaved partial sums (element e of each word to sum e % 4)
+  float acc4[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int i = 0; i < KR::NW; ++i) {
     float kv[V16];
     unpack_word<AT>(kr.k[i], kv);
 #pragma unroll
-    for (int e = 0; e < V16; ++e) acc = fmaf(q[i * V16 + e], kv[e], acc);
+    for (int e = 0; e < V16; ++e) acc4[e & 3] = fmaf(q[i * V16 + e], kv[e], acc4[e & 3]);
   }
+  const float acc = (acc4[0] + acc4[1]) + (acc4[2] + acc4[3]);
   const float sc = valid ? acc * scale : -INFINITY;
   const float mc = wave_max(sc);
   const float p = valid ? expf(sc - mc) : 0.f;
@@ -112,26 +113,29 @@ __device__ __forceinline__ void chunk_fold(const float* q, const KeyRows<AT, DH>
   const float mn = fmaxf(st.m, mc);
   const float a1 = expf(st.m - mn);
   const float a2 = expf(mc - mn);
-  const int kc = min(kAttnChunk, nk - key0);       // keys of this chunk
-  sm.p[lane] = p;
+  sm.p[lane] = p;                                  // zero past the row's keys
 #pragma unroll
   for (int p0 = 0; p0 < DH; p0 += SM::DP) {
-    // stage dimensions p0 .. p0+DP of the lane's V row
+    // stage dimensions p0 .. p0+DP of the lane's V row (zeros past the row)
     uint4* dst = reinterpret_cast<uint4*>(sm.v + lane * SM::LDV);
 #pragma unroll
     for (int i = 0; i < SM::DP / V16; ++i) {
+      uint4 w;
       if constexpr (KR::HOLD_V) {
-        dst[i] = kr.v[p0 / V16 + i];
+        w = kr.v[p0 / V16 + i];
       } else {
-        dst[i] = reinterpret_cast<const uint4*>(Vb + static_cast<size_t>(valid ? key : 0) * DH + p0)[i];
+        w = reinterpret_cast<const uint4*>(Vb + static_cast<size_t>(valid ? key : 0) * DH + p0)[i];
       }
+      dst[i] = valid ? w : make_uint4(0u, 0u, 0u, 0u);
     }
     wave_lds_sync();
-    // lane (p0 + j) % 64 sums dimension p0 + j over the chunk's keys
+    // lane (p0 + j) % 64 sums dimension p0 + j over all 64 keys of the chunk
+    // (keys past the row have p = 0 and zero rows: exact zeros)
     const int j = lane - (p0 % kWave);
     if (j >= 0 && j < SM::DP) {
       float o4[4] = {0.f, 0.f, 0.f, 0.f};
-      for (int k = 0; k < kc; ++k)
+#pragma unroll
+      for (int k = 0; k < kAttnChunk; ++k)
         o4[k & 3] = fmaf(sm.p[k], Elt<AT>::load(sm.v, k * SM::LDV + j), o4[k & 3]);
       const float oc = (o4[0] + o4[1]) + (o4[2] + o4[3]);
       float& so = st.o[(p0 + j) / kWave];

@@ -31,21 +31,27 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   const int row = idx / a.H;
   const int hh = idx - row * a.H;
   if (row >= R) return;   // whole wave; no workgroup barrier below
+  // the query first (it does not depend on the row's placement), then the
+  // first chunk's K/V rows
+  const float* q = a.q + static_cast<size_t>(row) * a.ldq + hh * DH;
+  float qv[(DH + kWave - 1) / kWave];
+#pragma unroll
+  for (int i = 0; i < (DH + kWave - 1) / kWave; ++i) {
+    const int d = lane + kWave * i;
+    qv[i] = q[d < DH ? d : 0];           // unconditional load
+  }
   int s, p;
   row_place(a.rows, row, s, p);
   const int nk = a.causal ? p + 1 : a.klen[s];
   const size_t base = (static_cast<size_t>(s) * a.H + hh) * a.T * DH;
   const AT* Kb = static_cast<const AT*>(a.kc) + base;
   const AT* Vb = static_cast<const AT*>(a.vc) + base;
-  // the first chunk's K/V rows go out before the query
   KeyRows<AT, DH> kr;
   kr.load(Kb, Vb, lane, lane < nk);
-  const float* q = a.q + static_cast<size_t>(row) * a.ldq + hh * DH;
 #pragma unroll
   for (int i = 0; i < (DH + kWave - 1) / kWave; ++i) {
     const int d = lane + kWave * i;
-    const float v = q[d < DH ? d : 0];   // unconditional load
-    if (d < DH) s_q[wave][d] = v;
+    if (d < DH) s_q[wave][d] = qv[i];
   }
   wave_lds_sync();
   RowState<DH> st;
