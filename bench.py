@@ -99,10 +99,15 @@ def gpu_workload(wl_name, steps, warmup, modes, headline, n_sent=0):
         f"in {time.perf_counter() - t0:.1f}s")
     res = {}
     for mode, b in modes:
-        r = run_mode(ctxs, sents, outs, mode, b, steps, warmup, timing=(mode, b) == headline)
+        r = run_mode(ctxs, sents, outs, mode, b, steps, warmup)
         res[f"{mode}_b{b}"] = r
         log(f"[{wl_name}] {mode:9s} b={b}: {r['tokens_per_s']:9.1f} tok/s  {r['ms_per_step']:7.3f} ms/sentence  "
             f"k/m={r['k_over_m']:.3f}")
+    # the vocabulary kernel's launch time: a second pass of the headline mode
+    # with HIP events around that kernel (the events cost time of their own, so
+    # the throughput above comes from the pass without them)
+    t = run_mode(ctxs, sents, outs, headline[0], headline[1], steps, warmup, timing=True)
+    res[f"{headline[0]}_b{headline[1]}"].update(vocab_launches=t["vocab_launches"], vocab_ms=t["vocab_ms"])
     return cfg, w, sents, model, res
 
 

@@ -4,8 +4,8 @@
 // For one chunk (keys key0 .. key0+63 that are < nk):
 //   s_k = (q . k_k) * scale          lane k scores key key0 + k
 //   m_c = max_k s_k,  p_k = exp(s_k - m_c),  l_c = sum_k p_k     (DPP trees)
-//   o_c[d] = sum_k p_k v_k[d]        lane d, four partial sums over the keys
-//                                    (p and the V rows staged through LDS)
+//   o_c[d] = sum_k p_k v_k[d]        two dimensions per lane over a half of the
+//                                    keys (V read directly, p through LDS)
 // and a row's chunks are folded in chunk order:
 //   m' = max(m, m_c),  o <- o exp(m - m') + o_c exp(m_c - m'),  l likewise,
 // the output being o / l.  Chunk boundaries depend only on the row's own key
@@ -18,50 +18,48 @@ namespace pdec {
 
 constexpr int kAttnChunk = kWave;   // keys per chunk
 
-// Running state of one row: m, l wave-uniform; lane d owns output dimensions
-// d, d + 64, ...
+// Running state of one row: m, l wave-uniform; lane l < 32 owns output
+// dimensions 2l, 2l + 1 (+ 64 i).
 template <int DH> struct RowState {
-  static constexpr int NO = (DH + kWave - 1) / kWave;
+  static constexpr int NP = (DH + kWave - 1) / kWave;   // 64-dimension groups
   float m, l;
-  float o[NO];
+  float o[NP][2];
   __device__ __forceinline__ void init() {
     m = -INFINITY;
     l = 0.f;
 #pragma unroll
-    for (int i = 0; i < NO; ++i) o[i] = 0.f;
+    for (int i = 0; i < NP; ++i) o[i][0] = o[i][1] = 0.f;
   }
 };
 
-// The K and V rows of the key a lane scores, as raw 16-byte words.  V is held only when it fits comfortably in registers
-// (<= 256 bytes per row); otherwise it is read again when staged.
-template <typename AT, int DH> struct KeyRows {
+// One chunk of a row's keys, in registers: lane k holds the K row of key
+// key0 + k (raw 16-byte words), and lane l the V entries of dimensions
+// 2(l mod 32), 2(l mod 32) + 1 (+ 64 i) for the 32 keys key0 + 32(l / 32) + k'.
+// Keys past nk are loaded from key 0 (every load unconditional) and dropped.
+template <typename AT, int DH> struct KeyChunk {
   static constexpr int V16 = Vec16<AT>::N;        // elements per 16-byte word
-  static constexpr int NW = DH / V16;             // words per row
-  static constexpr bool HOLD_V = DH * sizeof(AT) <= 256;
+  static constexpr int NW = DH / V16;             // K words per row
+  static constexpr int NP = (DH + kWave - 1) / kWave;
+  using Pair = typename std::conditional<sizeof(AT) == 2, uint32_t, uint2>::type;   // two elements
   uint4 k[NW];
-  uint4 v[HOLD_V ? NW : 1];
-  // always loads (key 0 for an invalid lane): no load under a branch
-  __device__ __forceinline__ void load(const AT* Kb, const AT* Vb, int key, bool valid) {
-    key = valid ? key : 0;
+  Pair v[NP][32];
+  __device__ __forceinline__ void load(const AT* Kb, const AT* Vb, int key0, int nk, int lane) {
+    const int key = key0 + lane < nk ? key0 + lane : 0;
     const uint4* kr = reinterpret_cast<const uint4*>(Kb + static_cast<size_t>(key) * DH);
 #pragma unroll
     for (int i = 0; i < NW; ++i) k[i] = kr[i];
-    if constexpr (HOLD_V) {
-      const uint4* vr = reinterpret_cast<const uint4*>(Vb + static_cast<size_t>(key) * DH);
+    const int d0 = 2 * (lane & 31);
+    const int kh = key0 + 32 * (lane >> 5);
 #pragma unroll
-      for (int i = 0; i < NW; ++i) v[i] = vr[i];
+    for (int i = 0; i < NP; ++i) {
+      const int d = d0 + kWave * i < DH ? d0 + kWave * i : 0;
+#pragma unroll
+      for (int k2 = 0; k2 < 32; ++k2) {
+        const int kk = kh + k2 < nk ? kh + k2 : 0;
+        v[i][k2] = *reinterpret_cast<const Pair*>(Vb + static_cast<size_t>(kk) * DH + d);
+      }
     }
   }
-};
-
-// Per-wave LDS staging of one chunk: the weights p_k and DP dimensions of the
-// 64 V rows at a time (rows padded by 16 bytes).
-template <typename AT, int DH> struct AttnStage {
-  static constexpr int DP0 = 8192 / (kAttnChunk * static_cast<int>(sizeof(AT)));
-  static constexpr int DP = DH < DP0 ? DH : DP0;  // dimensions per pass: 64 (bf16), 32 (f32)
-  static constexpr int LDV = DP + 16 / static_cast<int>(sizeof(AT));
-  float p[kAttnChunk];
-  AT v[kAttnChunk * LDV];
 };
 
 template <typename AT> __device__ __forceinline__ void unpack_word(uint4 w, float* out);
@@ -77,6 +75,21 @@ template <> __device__ __forceinline__ void unpack_word<bf16_t>(uint4 w, float* 
     out[2 * j + 1] = __uint_as_float(u[j] & 0xffff0000u);
   }
 }
+__device__ __forceinline__ void unpack_pair(uint32_t w, float& a, float& b) {
+  a = __uint_as_float(w << 16);
+  b = __uint_as_float(w & 0xffff0000u);
+}
+__device__ __forceinline__ void unpack_pair(uint2 w, float& a, float& b) {
+  a = __uint_as_float(w.x);
+  b = __uint_as_float(w.y);
+}
+
+// Per-wave LDS of the chunk computation: the weights p_k and the upper
+// key-half partial outputs.
+struct AttnScratch {
+  float p[kAttnChunk];
+  float half[32][2];
+};
 
 // Orders the wave's LDS writes before its following reads.
 __device__ __forceinline__ void wave_lds_sync() {
@@ -85,61 +98,65 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// One chunk folded into the row state.  q: the row's query (DH floats, LDS);
-// kr: the lane's key (key0 + lane) when it is < nk; Vb: key 0 of the row's
-// [T][DH] V slice.  All 64 lanes must be active.
+// One chunk folded into the row state.  q: the row's query (DH floats, LDS).
+// All 64 lanes must be active.
 template <typename AT, int DH>
-__device__ __forceinline__ void chunk_fold(const float* q, const KeyRows<AT, DH>& kr, const AT* Vb, int key0, int nk,
-                                           float scale, int lane, AttnStage<AT, DH>& sm, RowState<DH>& st) {
-  using KR = KeyRows<AT, DH>;
-  using SM = AttnStage<AT, DH>;
-  constexpr int V16 = KR::V16;
-  const int key = key0 + lane;
-  const bool valid = key < nk;
-  // q . k as four interleaved partial sums (element e of each word to sum e % 4)
+__device__ __forceinline__ void chunk_fold(const float* q, const KeyChunk<AT, DH>& kc, int key0, int nk, float scale,
+                                           int lane, AttnScratch& sm, RowState<DH>& st) {
+  using KC = KeyChunk<AT, DH>;
+  constexpr int V16 = KC::V16;
+  const bool valid = key0 + lane < nk;
+  // q . k as four interleaved partial sums
   float acc4[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int i = 0; i < KR::NW; ++i) {
+  for (int i = 0; i < KC::NW; ++i) {
     float kv[V16];
-    unpack_word<AT>(kr.k[i], kv);
+    unpack_word<AT>(kc.k[i], kv);
 #pragma unroll
     for (int e = 0; e < V16; ++e) acc4[e & 3] = fmaf(q[i * V16 + e], kv[e], acc4[e & 3]);
   }
   const float acc = (acc4[0] + acc4[1]) + (acc4[2] + acc4[3]);
   const float sc = valid ? acc * scale : -INFINITY;
   const float mc = wave_max(sc);
-  const float p = valid ? expf(sc - mc) : 0.f;
+  const float p = valid ? expf(sc - mc) : 0.f;   // zero past the row's keys
   const float lc = wave_sum(p);
   const float mn = fmaxf(st.m, mc);
   const float a1 = expf(st.m - mn);
   const float a2 = expf(mc - mn);
-  sm.p[lane] = p;                                  // zero past the row's keys
+  sm.p[lane] = p;
+  wave_lds_sync();
+  // P.V: each lane sums its two dimensions over its half of the keys
+  // (keys past nk have p = 0; their V entries are dropped by the select)
+  const int kh = 32 * (lane >> 5);
+  float o[KC::NP][2];
 #pragma unroll
-  for (int p0 = 0; p0 < DH; p0 += SM::DP) {
-    // stage dimensions p0 .. p0+DP of the lane's V row (zeros past the row)
-    uint4* dst = reinterpret_cast<uint4*>(sm.v + lane * SM::LDV);
+  for (int i = 0; i < KC::NP; ++i) {
+    float oa[4] = {0.f, 0.f, 0.f, 0.f}, ob[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int i = 0; i < SM::DP / V16; ++i) {
-      uint4 w;
-      if constexpr (KR::HOLD_V) {
-        w = kr.v[p0 / V16 + i];
-      } else {
-        w = reinterpret_cast<const uint4*>(Vb + static_cast<size_t>(valid ? key : 0) * DH + p0)[i];
-      }
-      dst[i] = valid ? w : make_uint4(0u, 0u, 0u, 0u);
+    for (int k2 = 0; k2 < 32; ++k2) {
+      const bool kin = key0 + kh + k2 < nk;
+      float va, vb;
+      unpack_pair(kc.v[i][k2], va, vb);
+      const float pk = sm.p[kh + k2];
+      oa[k2 & 3] = fmaf(pk, kin ? va : 0.f, oa[k2 & 3]);
+      ob[k2 & 3] = fmaf(pk, kin ? vb : 0.f, ob[k2 & 3]);
+    }
+    o[i][0] = (oa[0] + oa[1]) + (oa[2] + oa[3]);
+    o[i][1] = (ob[0] + ob[1]) + (ob[2] + ob[3]);
+  }
+  // lower key half + upper key half, per dimension group
+#pragma unroll
+  for (int i = 0; i < KC::NP; ++i) {
+    if (lane >= 32) {
+      sm.half[lane - 32][0] = o[i][0];
+      sm.half[lane - 32][1] = o[i][1];
     }
     wave_lds_sync();
-    // lane (p0 + j) % 64 sums dimension p0 + j over all 64 keys of the chunk
-    // (keys past the row have p = 0 and zero rows: exact zeros)
-    const int j = lane - (p0 % kWave);
-    if (j >= 0 && j < SM::DP) {
-      float o4[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int k = 0; k < kAttnChunk; ++k)
-        o4[k & 3] = fmaf(sm.p[k], Elt<AT>::load(sm.v, k * SM::LDV + j), o4[k & 3]);
-      const float oc = (o4[0] + o4[1]) + (o4[2] + o4[3]);
-      float& so = st.o[(p0 + j) / kWave];
-      so = so * a1 + oc * a2;
+    if (lane < 32) {
+      const float oc0 = o[i][0] + sm.half[lane][0];
+      const float oc1 = o[i][1] + sm.half[lane][1];
+      st.o[i][0] = st.o[i][0] * a1 + oc0 * a2;
+      st.o[i][1] = st.o[i][1] * a1 + oc1 * a2;
     }
     wave_lds_sync();
   }
@@ -151,9 +168,12 @@ __device__ __forceinline__ void chunk_fold(const float* q, const KeyRows<AT, DH>
 template <typename AT, int DH>
 __device__ __forceinline__ void row_output(const RowState<DH>& st, AT* out, int lane) {
 #pragma unroll
-  for (int i = 0; i < RowState<DH>::NO; ++i) {
-    const int d = lane + kWave * i;
-    if (d < DH) Elt<AT>::store(out, d, st.o[i] / st.l);
+  for (int i = 0; i < RowState<DH>::NP; ++i) {
+    const int d = 2 * lane + kWave * i;
+    if (lane < 32 && d < DH) {
+      Elt<AT>::store(out, d, st.o[i][0] / st.l);
+      Elt<AT>::store(out, d + 1, st.o[i][1] / st.l);
+    }
   }
 }
 

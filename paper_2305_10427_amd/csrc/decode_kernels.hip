@@ -23,7 +23,7 @@ constexpr int kMaxHeadDim = 128;
 template <typename AT, int DH>
 __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   __shared__ float s_q[4][DH];
-  __shared__ AttnStage<AT, DH> s_stage[4];
+  __shared__ AttnScratch s_scr[4];
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = threadIdx.x / kWave;
   const int R = a.n_rows_dev ? *a.n_rows_dev : a.n_rows;
@@ -32,7 +32,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   const int hh = idx - row * a.H;
   if (row >= R) return;   // whole wave; no workgroup barrier below
   // the query first (it does not depend on the row's placement), then the
-  // first chunk's K/V rows
+  // first chunk's keys
   const float* q = a.q + static_cast<size_t>(row) * a.ldq + hh * DH;
   float qv[(DH + kWave - 1) / kWave];
 #pragma unroll
@@ -46,8 +46,8 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   const size_t base = (static_cast<size_t>(s) * a.H + hh) * a.T * DH;
   const AT* Kb = static_cast<const AT*>(a.kc) + base;
   const AT* Vb = static_cast<const AT*>(a.vc) + base;
-  KeyRows<AT, DH> kr;
-  kr.load(Kb, Vb, lane, lane < nk);
+  KeyChunk<AT, DH> kc;
+  kc.load(Kb, Vb, 0, nk, lane);
 #pragma unroll
   for (int i = 0; i < (DH + kWave - 1) / kWave; ++i) {
     const int d = lane + kWave * i;
@@ -57,8 +57,8 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   RowState<DH> st;
   st.init();
   for (int key0 = 0; key0 < nk; key0 += kAttnChunk) {
-    if (key0 > 0) kr.load(Kb, Vb, key0 + lane, key0 + lane < nk);
-    chunk_fold<AT, DH>(s_q[wave], kr, Vb, key0, nk, a.scale, lane, s_stage[wave], st);
+    if (key0 > 0) kc.load(Kb, Vb, key0, nk, lane);
+    chunk_fold<AT, DH>(s_q[wave], kc, key0, nk, a.scale, lane, s_scr[wave], st);
   }
   row_output<AT, DH>(st, static_cast<AT*>(a.out) + static_cast<size_t>(row) * a.ldo + hh * DH, lane);
 }

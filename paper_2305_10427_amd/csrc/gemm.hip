@@ -162,12 +162,10 @@ __global__ __launch_bounds__(KSPLIT == 8 ? 512 : 256) void k_gemm(GemmArgs a) {
         }
       }
       __builtin_amdgcn_sched_barrier(0);   // all loads of the batch before its products
-      // steps past the wave's K range contribute exact zeros
+      // only the steps of the wave's K range (a wave-uniform branch)
 #pragma unroll
-      for (int u = 0; u < D; ++u) {
-        const bool ok = s0 + u < s_end;
-        acc = MM::step(ok ? af[u] : MM::zero(), ok ? bcur[u] : MM::zero(), acc);
-      }
+      for (int u = 0; u < D; ++u)
+        if (s0 + u < s_end) acc = MM::step(af[u], bcur[u], acc);
       if (more) {
 #pragma unroll
         for (int u = 0; u < D; ++u) bcur[u] = bnext[u];

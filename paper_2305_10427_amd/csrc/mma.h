@@ -84,14 +84,15 @@ __device__ __forceinline__ void ln_row_apply(const LnRow<XT, NT>& h, int K, floa
 
 // LayerNorm of the 16-row input tile rows m0 .. m0+15 into the LDS tile
 // sA[16][lda] in the storage type, by 4 waves: wave w owns tile rows
-// w, w + 4, w + 8, w + 12 (one row per pass).  load() issues the loads of all
-// 16 rows (rows >= R_max read row 0 and are not used), so a caller can issue
-// other loads after it; finish() normalises the passes that hold rows below
+// w, w + 4, w + 8, w + 12 (one row per pass; NPASS passes, so rows
+// m0 .. m0 + 4 NPASS - 1).  load() issues the loads of those rows (rows
+// >= R_max read row 0 and are not used), so a caller can issue other loads
+// after it; finish() normalises the passes that hold rows below
 // R_max (rows of later passes are left unwritten: their products are
 // discarded) and also writes rows below R_out to ln_out when it is non-null.
 // The caller synchronises the workgroup after finish().
-template <typename WT, typename XT, int NT> struct LnTile {
-  LnRow<XT, NT> h[4];
+template <typename WT, typename XT, int NT, int NPASS = 4> struct LnTile {
+  LnRow<XT, NT> h[NPASS];
   int wave, lane, m0, R_max;
   __device__ __forceinline__ void load(const XT* X, int ldx, int K, int m0_, int R_max_, int wave_, int lane_) {
     wave = wave_;
@@ -99,7 +100,7 @@ template <typename WT, typename XT, int NT> struct LnTile {
     m0 = m0_;
     R_max = R_max_;
 #pragma unroll
-    for (int p = 0; p < 4; ++p) {
+    for (int p = 0; p < NPASS; ++p) {
       const int row = m0 + 4 * p + wave;
       const bool ok = row < R_max;
       ln_row_load<XT, NT>(h[p], X + static_cast<size_t>(ok ? row : 0) * ldx, K, lane, ok);
@@ -107,9 +108,9 @@ template <typename WT, typename XT, int NT> struct LnTile {
   }
   __device__ __forceinline__ void finish(int K, float eps, const WT* g, const WT* b, WT* sA, int lda, WT* ln_out,
                                          int ldlo, int R_out) {
-    const int n_pass = min(4, (R_max - m0 + 3) / 4);
+    const int n_pass = min(NPASS, (R_max - m0 + 3) / 4);
 #pragma unroll
-    for (int p = 0; p < 4; ++p) {
+    for (int p = 0; p < NPASS; ++p) {
       if (p < n_pass) {
         const int tr = 4 * p + wave;
         const int row = m0 + tr;
