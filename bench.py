@@ -32,6 +32,18 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+_MODELS = {}
+
+
+def load_model(cfg):
+    """Seed-0 weights of a model shape and their device copy, drawn once per run."""
+    from paper_2305_10427_amd import pdec, synth
+    if cfg not in _MODELS:
+        w = synth.make_weights(cfg, seed=0)
+        _MODELS[cfg] = (w, pdec.Model(cfg, w))
+    return _MODELS[cfg]
+
+
 def run_mode(ctxs, sents, outs, mode, block, steps, warmup, timing=False):
     import torch
     n = len(sents)
@@ -79,8 +91,7 @@ def gpu_workload(wl_name, steps, warmup, modes, headline, n_sent=0):
     wl = C.WORKLOADS[wl_name]
     cfg = wl.model
     t0 = time.perf_counter()
-    w = synth.make_weights(cfg, seed=0)
-    model = pdec.Model(cfg, w)
+    w, model = load_model(cfg)
     sents = synth.make_sentences(wl, seed=1)
     if n_sent:
         sents = sents[:n_sent]
@@ -109,6 +120,50 @@ def gpu_workload(wl_name, steps, warmup, modes, headline, n_sent=0):
     t = run_mode(ctxs, sents, outs, headline[0], headline[1], steps, warmup, timing=True)
     res[f"{headline[0]}_b{headline[1]}"].update(vocab_launches=t["vocab_launches"], vocab_ms=t["vocab_ms"])
     return cfg, w, sents, model, res
+
+
+def batched_workload(wl_name, n_batches, modes, repeats):
+    """Batched decoding (sentences padded to the batch maximum and decoded
+    together, each with its own iteration state): target tokens/s and k/m per
+    mode over the first n_batches batches of the workload."""
+    import torch
+    from paper_2305_10427_amd import configs as C, pdec, synth
+    wl = C.WORKLOADS[wl_name]
+    cfg = wl.model
+    _, model = load_model(cfg)
+    batches = synth.make_batches(synth.make_sentences(wl, seed=1)[: n_batches * wl.batch], wl.batch)
+    ctxs, outs = [], []
+    for bt in batches:
+        c = pdec.Context(model, wl.batch, bt.src.shape[1], wl.tgt_cap)
+        c.encode(torch.from_numpy(bt.src).cuda(), bt.src_len.tolist())
+        ctxs.append(c)
+        B = len(bt.src_len)
+        outs.append((torch.empty((B, wl.tgt_cap), dtype=torch.int32, device="cuda"),
+                     torch.empty(B, dtype=torch.int32, device="cuda"),
+                     torch.empty(B, dtype=torch.int32, device="cuda"),
+                     torch.empty(B, dtype=torch.int32, device="cuda")))
+    torch.cuda.synchronize()
+    res = {}
+    for mode, b in modes:
+        for c, bt, o in zip(ctxs, batches, outs):       # graph capture + warm-up
+            c.decode(mode, bt.tgt_m.tolist(), block=b, out=o)
+        torch.cuda.synchronize()
+        toks = ks = ms = 0
+        t0 = time.perf_counter()
+        for _ in range(repeats):
+            for c, bt, o in zip(ctxs, batches, outs):
+                c.decode(mode, bt.tgt_m.tolist(), block=b, out=o)
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t0
+        for bt, o in zip(batches, outs):
+            toks += int(o[1].sum()) * repeats
+            ks += int(o[2].sum()) * repeats
+            ms += int(bt.tgt_m.sum()) * repeats
+        res[f"{mode}_b{b}"] = {"tokens_per_s": round(toks / dt, 1), "k_over_m": round(ks / ms, 4),
+                               "ms_per_batch": round(1e3 * dt / (repeats * len(batches)), 3)}
+        log(f"[{wl_name}] {mode:9s} b={b:2d}: {toks / dt:10.1f} tok/s  k/m={ks / ms:.3f}  "
+            f"{1e3 * dt / (repeats * len(batches)):8.2f} ms/batch")
+    return res
 
 
 def cpu_baseline(cfg, weights, sents, mode, block, budget_s):
@@ -176,6 +231,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-f32", action="store_true")
     ap.add_argument("--no-large", action="store_true")
+    ap.add_argument("--no-batched", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
@@ -203,6 +259,19 @@ def main():
     if not args.no_large:
         _, _, _, _, large = gpu_workload("large", min(args.steps, 20), min(args.warmup, 2),
                                          [("ar", 1), ("gs_jacobi", 16)], ("gs_jacobi", 16), 20)
+
+    batched = None
+    if not args.no_batched:
+        batched = {
+            "mt_base_b64": {"workload": "mt_base bf16, batch 64, first 4 batches of 64 sources, n ~ clipped "
+                                        "log-normal (median 25, max 128), m = n + 10",
+                            **batched_workload("mt_base_b64", 4, [("ar", 1), ("hybrid", 2), ("hybrid", 3),
+                                                                  ("hybrid", 5), ("hybrid", 8)], 2)},
+            "large_b32": {"workload": "large bf16, batch 32, first 2 batches of 32 sources, n ~ U[20,120], "
+                                      "m = min(n + 10, 256)",
+                          **batched_workload("large_b32", 2, [("ar", 1)] + [(m, b) for m in ("gs_jacobi", "hybrid")
+                                                                          for b in (1, 2, 4, 8, 16, 32)], 1)},
+        }
 
     h = res[f"{headline[0]}_b{headline[1]}"]
     # roofline of the fused vocabulary projection + argmax (bytes: E [V][d] and the output bias, bf16)
@@ -255,6 +324,8 @@ def main():
         lavg = lv["vocab_ms"] / max(lv["vocab_launches"], 1)
         line["large_bf16"]["vocab_roofline"] = {"achieved": round(lb / (lavg * 1e-3) / 1e9, 1), "peak": HBM_PEAK_GBS,
                                                 "unit": "GB/s", "avg_launch_us": round(lavg * 1e3, 2)}
+    if batched is not None:
+        line["batched"] = batched
     print(json.dumps(line), flush=True)
 
 

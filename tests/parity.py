@@ -11,6 +11,7 @@ accepted as exact.
 from __future__ import annotations
 
 import dataclasses
+import functools
 from typing import List, Optional
 
 import numpy as np
@@ -70,3 +71,27 @@ def summarize(labels: List[str]) -> dict:
     for lab in labels:
         out["exact" if lab == "exact" else ("near_tie" if lab.startswith("near_tie") else "fail")] += 1
     return out
+
+
+@functools.lru_cache(maxsize=None)
+def workload_model(cfg: C.ModelConfig):
+    """(weights, GPU model, oracle model) of a workload's model with seed-0
+    weights, built once per test session (drawing the large model's weights
+    takes tens of seconds)."""
+    from paper_2305_10427_amd import pdec, synth
+    w = synth.make_weights(cfg, seed=0)
+    return w, pdec.Model(cfg, w), oracle.Model(cfg, w.values)
+
+
+def classify_ids(ids: np.ndarray, greedy: oracle.Result, tol: float) -> str:
+    """Token ids only (for modes whose iteration count the oracle does not
+    replay at this size): 'exact', 'near_tie:...' or 'FAIL:...' as in classify."""
+    if np.array_equal(ids, greedy.out):
+        return "exact"
+    n = min(len(ids), len(greedy.out))
+    diff = np.nonzero(ids[:n] != greedy.out[:n])[0]
+    t = int(diff[0]) if len(diff) else n
+    recs = [r for r in greedy.records if r.position == t]
+    if recs and recs[-1].top1 - recs[-1].top2 < 2 * tol * recs[-1].linf:
+        return f"near_tie:token@{t}"
+    return f"FAIL:tokens differ at {t}: gpu={ids[:t + 3].tolist()} oracle={greedy.out[:t + 3].tolist()}"

@@ -10,7 +10,7 @@ import pytest
 
 import oracle
 from paper_2305_10427_amd import configs as C, pdec, synth
-from tests.parity import TOL, classify, gpu_decode_batch, summarize
+from tests.parity import TOL, classify, gpu_decode_batch, summarize, workload_model
 
 pytestmark = pytest.mark.gpu
 
@@ -239,10 +239,8 @@ def test_error_paths_on_device():
 def _full_size(wl_name, n_sent, m_cap, modes):
     wl = C.WORKLOADS[wl_name]
     cfg = wl.model
-    w = synth.make_weights(cfg, seed=0)
-    gm = pdec.Model(cfg, w)
+    _, gm, M = workload_model(cfg)
     ctx = pdec.Context(gm, 1, 128, wl.tgt_cap)
-    M = oracle.Model(cfg, w.values)
     labels = []
     for src, m in synth.make_sentences(wl, seed=1, count=n_sent):
         m = min(m, m_cap)
