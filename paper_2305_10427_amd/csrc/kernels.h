@@ -161,6 +161,15 @@ struct ReduceArgs {
 hipError_t launch_gemm(int dtype, int pro, int epi, int ksplit, const GemmArgs& a, hipStream_t s);
 int gemm_grid(int epi, int N, int ksplit);
 size_t gemm_ln_lds_bytes(int K, size_t elt);
+// Products of many rows on LDS-staged MFMA tiles (bf16, no prologue, K a
+// multiple of 64); bitwise the same values as launch_gemm.  The vocabulary
+// argmax writes ceil(N / gemm_tiled_bn(EPI_ARGMAX, N, rows)) partials per row.
+bool gemm_tiled_ok(int dtype, int pro, const GemmArgs& a);
+int gemm_tiled_bn(int epi, int N, int rows);
+void gemm_tiled_init();
+hipError_t launch_gemm_tiled(int epi, int ksplit, const GemmArgs& a, hipStream_t s);
+int gemm_tiled_cfg(int epi, int N, int rows);
+hipError_t launch_gemm_tiled_cfg(int epi, int ksplit, int cfg, const GemmArgs& a, hipStream_t s);
 hipError_t launch_attn(int dtype, const AttnArgs& a, int R_max, hipStream_t s);
 // Fused vocabulary projection + argmax for at most 16 rows (streaming kernel);
 // writes vocab_grid(dtype, V, d) partials per row (at most ceil(V / 64)).

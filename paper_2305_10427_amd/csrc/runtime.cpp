@@ -33,6 +33,7 @@ pd_status fail(pd_status st, const std::string& msg) {
   } while (0)
 
 constexpr int kFuseLnMaxRows = 64;  // above this the LayerNorm runs as its own kernel
+constexpr int kTiledMinRows = 64;   // above this bf16 products run on the LDS-tiled kernel
 constexpr size_t kAlign = 256;
 
 int weight_count(const pd_config& c) {
@@ -239,6 +240,7 @@ hipError_t run_gemm(const pd_ctx& C, const Rows& r, GemmArgs g, int epi, bool pr
     }
   }
   const int ksplit = (epi == EPI_ARGMAX || epi == EPI_LOGITS) ? 1 : (g.K >= 2048 ? 8 : 4);
+  if (r.R_max > kTiledMinRows && gemm_tiled_ok(M.dt, pro, g)) return launch_gemm_tiled(epi, ksplit, g, s);
   return launch_gemm(M.dt, pro, epi, ksplit, g, s);
 }
 
@@ -247,7 +249,16 @@ hipError_t run_gemm(const pd_ctx& C, const Rows& r, GemmArgs g, int epi, bool pr
 // epilogue (one partial per 64-column workgroup).
 constexpr int kVocabStreamMaxRows = 16;
 int vocab_parts(const pd_model& M, int R_max) {
-  return R_max <= kVocabStreamMaxRows ? vocab_grid(M.dt, M.V, M.d) : gemm_grid(EPI_ARGMAX, M.V, 1);
+  if (R_max <= kVocabStreamMaxRows) return vocab_grid(M.dt, M.V, M.d);
+  GemmArgs g;
+  std::memset(&g, 0, sizeof(g));
+  g.N = M.V;
+  g.K = M.d;
+  if (R_max > kTiledMinRows && gemm_tiled_ok(M.dt, PRO_NONE, g)) {
+    const int bn = gemm_tiled_bn(EPI_ARGMAX, M.V, R_max);
+    return (M.V + bn - 1) / bn;
+  }
+  return gemm_grid(EPI_ARGMAX, M.V, 1);
 }
 
 // Decoder pass over the rows of one iteration (or the teacher-forced rows of
@@ -364,6 +375,12 @@ hipError_t decoder_pass(pd_ctx& C, const Rows& r, float* logits, hipStream_t s, 
   return launch_argmax_reduce(ra, r.R_max, s);
 }
 
+// Encoder products (no prologue): the tiled kernel for many rows.
+hipError_t enc_gemm(const pd_model& M, int epi, int ksplit, const GemmArgs& g, hipStream_t s) {
+  if (g.n_rows > kTiledMinRows && gemm_tiled_ok(M.dt, PRO_NONE, g)) return launch_gemm_tiled(epi, ksplit, g, s);
+  return launch_gemm(M.dt, PRO_NONE, epi, ksplit, g, s);
+}
+
 hipError_t encoder_pass(pd_ctx& C, const int32_t* src, int B, int n_max, hipStream_t s) {
   const pd_model& M = *C.M;
   const pd_config& cfg = M.cfg;
@@ -396,14 +413,14 @@ hipError_t encoder_pass(pd_ctx& C, const int32_t* src, int B, int n_max, hipStre
     g.out_f32 = q_buf; g.ldo = d; g.q_cols = d;
     g.kc = C.at<char>(C.L.enc_k); g.vc = C.at<char>(C.L.enc_v);
     g.H = M.H; g.dh = M.dh; g.T = C.max_src; g.d = d;
-    if ((e = launch_gemm(M.dt, PRO_NONE, EPI_QKV, 4, g, s)) != hipSuccess) return e;
+    if ((e = enc_gemm(M, EPI_QKV, 4, g, s)) != hipSuccess) return e;
     AttnArgs aa{nullptr, R, q_buf, d, g.kc, g.vc, M.H, M.dh, C.max_src, r.map, 0, klen, a_buf, d, scale};
     if ((e = launch_attn(M.dt, aa, R, s)) != hipSuccess) return e;
     g = gemm_base(r);
     g.x = a_buf; g.ldx = d; g.w = M.enc(l, E_WO); g.bias = M.enc(l, E_BO); g.N = d; g.K = d;
     g.resid = x_res; g.ldr = d; g.ldo = d;
     if (pre) g.out = x_res; else g.out_f32 = s_buf;
-    if ((e = launch_gemm(M.dt, PRO_NONE, EPI_RESID, 4, g, s)) != hipSuccess) return e;
+    if ((e = enc_gemm(M, EPI_RESID, 4, g, s)) != hipSuccess) return e;
     if (!pre) {
       LnArgs la{nullptr, R, s_buf, 1, M.enc(l, E_LN1G), M.enc(l, E_LN1B), cfg.ln_eps, d, x_res};
       if ((e = launch_ln(M.dt, la, R, s)) != hipSuccess) return e;
@@ -417,12 +434,12 @@ hipError_t encoder_pass(pd_ctx& C, const int32_t* src, int B, int n_max, hipStre
     g = gemm_base(r);
     g.x = in; g.ldx = d; g.w = M.enc(l, E_W1); g.bias = M.enc(l, E_B1); g.N = M.dff; g.K = d;
     g.out = h_buf; g.ldo = M.dff; g.act = cfg.act_gelu ? 2 : 1;
-    if ((e = launch_gemm(M.dt, PRO_NONE, EPI_ACT, 4, g, s)) != hipSuccess) return e;
+    if ((e = enc_gemm(M, EPI_ACT, 4, g, s)) != hipSuccess) return e;
     g = gemm_base(r);
     g.x = h_buf; g.ldx = M.dff; g.w = M.enc(l, E_W2); g.bias = M.enc(l, E_B2); g.N = d; g.K = M.dff;
     g.resid = x_res; g.ldr = d; g.ldo = d;
     if (pre) g.out = x_res; else g.out_f32 = s_buf;
-    if ((e = launch_gemm(M.dt, PRO_NONE, EPI_RESID, g.K >= 2048 ? 8 : 4, g, s)) != hipSuccess) return e;
+    if ((e = enc_gemm(M, EPI_RESID, g.K >= 2048 ? 8 : 4, g, s)) != hipSuccess) return e;
     if (!pre) {
       LnArgs la{nullptr, R, s_buf, 1, M.enc(l, E_LN2G), M.enc(l, E_LN2B), cfg.ln_eps, d, x_res};
       if ((e = launch_ln(M.dt, la, R, s)) != hipSuccess) return e;
@@ -440,7 +457,7 @@ hipError_t encoder_pass(pd_ctx& C, const int32_t* src, int B, int n_max, hipStre
     g.q_cols = 0;
     g.kc = C.at<char>(C.L.cross_k) + l * cross_layer; g.vc = C.at<char>(C.L.cross_v) + l * cross_layer;
     g.H = M.H; g.dh = M.dh; g.T = C.max_src; g.d = d;
-    if ((e = launch_gemm(M.dt, PRO_NONE, EPI_QKV, 4, g, s)) != hipSuccess) return e;
+    if ((e = enc_gemm(M, EPI_QKV, 4, g, s)) != hipSuccess) return e;
   }
   return hipSuccess;
 }
@@ -532,6 +549,7 @@ pd_status pd_model_create(const pd_config* cfg, const void* const* dev_weights, 
   for (int i = 0; i < n; ++i)
     if (dev_weights[i] == nullptr || !aligned(dev_weights[i], 16))
       return fail(PD_E_ARG, "weight " + std::to_string(i) + " is null or not 16-byte aligned");
+  gemm_tiled_init();
   pd_model* m = new pd_model();
   m->cfg = *cfg;
   m->w.assign(dev_weights, dev_weights + n);
