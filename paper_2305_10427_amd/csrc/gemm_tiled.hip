@@ -36,6 +36,9 @@ namespace {
 
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
+// Word 3 of a raw buffer resource (32-bit data format, no swizzle, no index).
+constexpr int kBufferWord3 = 0x00020000;
+
 constexpr int kBK = 64;            // k per LDS stage (two MFMA steps)
 constexpr int kLdsPad = 8;         // bf16 elements of padding per LDS row (rows 144 B apart: conflict-free b128 reads)
 constexpr int kLdsRow = kBK + kLdsPad;
@@ -86,19 +89,28 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_tiled(GemmArgs a, int n_r
   // global -> register staging: chunk c = tid + NT i covers row c / 8, k 8 (c % 8).
   // Two register sets: the loads of stage kt + 2 leave while stage kt is
   // multiplied and stage kt + 1 waits in the other set for its LDS store.
-  const bf16_t* ga[S::LA];
-  const bf16_t* gb[S::LB];
+  // Stage loads are buffer loads: a fixed 32-bit byte offset per lane plus the
+  // stage's k offset in a scalar register, so no per-stage address arithmetic
+  // writes a register that an earlier load may still be filling (the compiler
+  // would then wait for every outstanding load before issuing the next).
+  // Reads past the end of a buffer return zero instead of faulting.
+  const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<bf16_t*>(X), static_cast<short>(0), static_cast<int>(static_cast<uint32_t>(R_max) * a.ldx * 2),
+      kBufferWord3);
+  const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<bf16_t*>(W), static_cast<short>(0), static_cast<int>(static_cast<uint32_t>(N) * K * 2), kBufferWord3);
+  uint32_t oa[S::LA], ob[S::LB];
 #pragma unroll
   for (int i = 0; i < S::LA; ++i) {
     const int c = tid + NT * i;
     const int row = min(m0 + c / 8, R_max - 1);
-    ga[i] = X + static_cast<size_t>(row) * a.ldx + 8 * (c % 8);
+    oa[i] = (static_cast<uint32_t>(row) * a.ldx + 8 * (c % 8)) * 2;
   }
 #pragma unroll
   for (int i = 0; i < S::LB; ++i) {
     const int c = tid + NT * i;
     const int col = min(n0 + c / 8, N - 1);
-    gb[i] = W + static_cast<size_t>(col) * K + 8 * (c % 8);
+    ob[i] = (static_cast<uint32_t>(col) * K + 8 * (c % 8)) * 2;
   }
   struct Staged {
     u32x4_t a[S::LA];
@@ -110,9 +122,11 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_tiled(GemmArgs a, int n_r
   Staged st[NS];
   auto load_stage = [&](Staged& r, int k0) __attribute__((always_inline)) {
 #pragma unroll
-    for (int i = 0; i < S::LA; ++i) r.a[i] = *reinterpret_cast<const u32x4_t*>(ga[i] + k0);
+    for (int i = 0; i < S::LA; ++i)
+      r.a[i] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(xr, oa[i], 2 * k0, 0));
 #pragma unroll
-    for (int i = 0; i < S::LB; ++i) r.b[i] = *reinterpret_cast<const u32x4_t*>(gb[i] + k0);
+    for (int i = 0; i < S::LB; ++i)
+      r.b[i] = __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(wr, ob[i], 2 * k0, 0));
   };
   auto store_stage = [&](const Staged& r, int buf) __attribute__((always_inline)) {
 #pragma unroll
@@ -176,23 +190,35 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_tiled(GemmArgs a, int n_r
   };
 
   const int n_kt = K / kBK;
+  // Every load is issued unconditionally (stages past the end reload the last
+  // stage): a load under a branch makes the compiler wait for all outstanding
+  // loads where the paths join.
 #pragma unroll
-  for (int u = 0; u < NS; ++u)
-    if (u < n_kt) load_stage(st[u], u * kBK);
+  for (int u = 0; u < NS; ++u) load_stage(st[u], min(u, n_kt - 1) * kBK);
   store_stage(st[0], 0);
   __syncthreads();
-  for (int kt0 = 0; kt0 < n_kt; kt0 += NS) {
+  int kt0 = 0;
+  for (; kt0 + NS <= n_kt; kt0 += NS) {
 #pragma unroll
     for (int u = 0; u < NS; ++u) {
+      // st[u] held stage kt (already in LDS): refill it with stage kt + NS;
+      // st[u + 1] holds stage kt + 1, stored once this stage's products are
+      // issued (after the last stage the store fills the idle buffer, unread)
       const int kt = kt0 + u;
-      if (kt < n_kt) {
-        // st[u] held stage kt (already in LDS): refill it with stage kt + NS;
-        // st[u + 1] holds stage kt + 1, stored once this stage's products are issued
-        if (kt + NS < n_kt) load_stage(st[u], (kt + NS) * kBK);
-        compute_stage(kt);
-        if (kt + 1 < n_kt) store_stage(st[(u + 1) % NS], (kt + 1) & 1);
-        __syncthreads();
-      }
+      load_stage(st[u], min(kt + NS, n_kt - 1) * kBK);
+      compute_stage(kt);
+      store_stage(st[(u + 1) % NS], (kt + 1) & 1);
+      __syncthreads();
+    }
+  }
+  // the last n_kt mod NS stages: their loads have all been issued
+#pragma unroll
+  for (int u = 0; u < NS - 1; ++u) {
+    const int kt = kt0 + u;
+    if (kt < n_kt) {
+      compute_stage(kt);
+      if (kt + 1 < n_kt) store_stage(st[(u + 1) % NS], (kt + 1) & 1);
+      __syncthreads();
     }
   }
   while (w_cur < KSPLIT) fold();   // the last range, then any empty trailing ranges
@@ -318,18 +344,17 @@ hipError_t launch_shape(const GemmArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Tile configurations (rows x columns, waves, register sets in flight):
-// 0: 128 x 128, 2 x 2, 2;  1: 256 x 128, 4 x 2, 4;  2: 128 x 64, 2 x 2, 3;
-// 3: 64 x 64, 2 x 2, 4.
-constexpr int kTileCfgs = 4;
+// Tile configurations (rows x columns, waves, register sets in flight),
+// chosen by measurement on MI355X: 0: 128 x 128, 2 x 2 waves, 2 sets (the
+// vocabulary argmax: 711 TFLOP/s at 1024 rows); 1: 64 x 64, 2 x 2 waves,
+// 4 sets (decoder products: many workgroups for N of 1-4 K columns).
+constexpr int kTileCfgs = 2;
 
 template <int EPI, int KSPLIT>
 hipError_t launch_k(const GemmArgs& a, int cfg, hipStream_t s) {
   switch (cfg) {
     case 0: return launch_shape<EPI, 128, 128, 2, 2, 2, KSPLIT>(a, s);
-    case 1: return launch_shape<EPI, 256, 128, 4, 2, 4, KSPLIT>(a, s);
-    case 2: return launch_shape<EPI, 128, 64, 2, 2, 3, KSPLIT>(a, s);
-    case 3: return launch_shape<EPI, 64, 64, 2, 2, 4, KSPLIT>(a, s);
+    case 1: return launch_shape<EPI, 64, 64, 2, 2, 4, KSPLIT>(a, s);
     default: return hipErrorInvalidValue;
   }
 }
@@ -337,8 +362,6 @@ hipError_t launch_k(const GemmArgs& a, int cfg, hipStream_t s) {
 template <int EPI, int KSPLIT>
 void init_k() {
   allow_lds<EPI, 128, 128, 2, 2, 2, KSPLIT>();
-  allow_lds<EPI, 256, 128, 4, 2, 4, KSPLIT>();
-  allow_lds<EPI, 128, 64, 2, 2, 3, KSPLIT>();
   allow_lds<EPI, 64, 64, 2, 2, 4, KSPLIT>();
 }
 
@@ -353,7 +376,7 @@ hipError_t launch_e(const GemmArgs& a, int ksplit, int cfg, hipStream_t s) {
   }
 }
 
-int tile_bn(int cfg) { return cfg <= 1 ? 128 : 64; }
+int tile_bn(int cfg) { return cfg == 0 ? 128 : 64; }
 
 }  // namespace
 
@@ -370,20 +393,22 @@ void gemm_tiled_init() {
   init_k<EPI_LOGITS, 1>();
 }
 
-// Tile configuration of a product of `rows` rows and N columns (measured on
-// MI355X: 64 x 64 tiles, many workgroups, for the decoder products; 256 x 128
-// for the vocabulary).  The vocabulary argmax keeps 128-column tiles (its
-// partial count depends only on N).
+// Tile configuration of a product of `rows` rows and N columns.  The
+// vocabulary argmax keeps 128-column tiles (its partial count depends only
+// on N).
 int gemm_tiled_cfg(int epi, int N, int rows) {
   (void)N;
-  if (epi == EPI_ARGMAX || epi == EPI_LOGITS) return rows >= 256 ? 1 : 0;
-  return 3;
+  (void)rows;
+  return (epi == EPI_ARGMAX || epi == EPI_LOGITS) ? 0 : 1;
 }
 
 int gemm_tiled_bn(int epi, int N, int rows) { return tile_bn(gemm_tiled_cfg(epi, N, rows)); }
 
 bool gemm_tiled_ok(int dtype, int pro, const GemmArgs& a) {
-  return dtype == DT_BF16 && pro == PRO_NONE && !a.x_f32 && a.K % kBK == 0 && a.K > 0 && a.N > 0;
+  // byte offsets within the input rows and the weight matrix must fit 31 bits
+  const bool off32 = static_cast<uint64_t>(a.n_rows) * a.ldx * 2 < (1ull << 31) &&
+                     static_cast<uint64_t>(a.N) * a.K * 2 < (1ull << 31);
+  return dtype == DT_BF16 && pro == PRO_NONE && !a.x_f32 && a.K % kBK == 0 && a.K > 0 && a.N > 0 && off32;
 }
 
 hipError_t launch_gemm_tiled_cfg(int epi, int ksplit, int cfg, const GemmArgs& a, hipStream_t s) {
