@@ -26,6 +26,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0   # dense bf16 matrix peak of MI355X
 
 
 def log(*a):
@@ -159,10 +160,32 @@ def batched_workload(wl_name, n_batches, modes, repeats):
             toks += int(o[1].sum()) * repeats
             ks += int(o[2].sum()) * repeats
             ms += int(bt.tgt_m.sum()) * repeats
+        # a separate pass with HIP events around the fused vocabulary launch and
+        # the device count of rows evaluated: its MFMA rate
+        for c in ctxs:
+            c.set_timing(True)
+        for c, bt, o in zip(ctxs, batches, outs):
+            c.decode(mode, bt.tgt_m.tolist(), block=b, out=o)
+        torch.cuda.synchronize()
+        launches = rows = 0
+        vms = 0.0
+        for c in ctxs:
+            n_l, t_ms = c.vocab_timing()
+            launches += n_l
+            vms += t_ms
+            rows += c.rows_processed()
+            c.set_timing(False)
+        flops = 2.0 * rows * cfg.vocab * cfg.d_model
+        vocab_tf = flops / (vms * 1e-3) / 1e12 if vms > 0 else 0.0
         res[f"{mode}_b{b}"] = {"tokens_per_s": round(toks / dt, 1), "k_over_m": round(ks / ms, 4),
-                               "ms_per_batch": round(1e3 * dt / (repeats * len(batches)), 3)}
+                               "ms_per_batch": round(1e3 * dt / (repeats * len(batches)), 3),
+                               "rows_per_iteration": round(rows / max(launches, 1), 1),
+                               "vocab_mfma": {"achieved": round(vocab_tf, 1), "peak": MFMA_BF16_PEAK_TFLOPS,
+                                              "unit": "TFLOP/s", "frac": round(vocab_tf / MFMA_BF16_PEAK_TFLOPS, 4),
+                                              "avg_launch_us": round(1e3 * vms / max(launches, 1), 2)}}
         log(f"[{wl_name}] {mode:9s} b={b:2d}: {toks / dt:10.1f} tok/s  k/m={ks / ms:.3f}  "
-            f"{1e3 * dt / (repeats * len(batches)):8.2f} ms/batch")
+            f"{1e3 * dt / (repeats * len(batches)):8.2f} ms/batch  vocab {vocab_tf:6.1f} TFLOP/s "
+            f"({rows / max(launches, 1):.0f} rows/iteration)")
     return res
 
 

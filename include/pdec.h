@@ -204,9 +204,21 @@ pd_status pd_debug_logits(pd_ctx* ctx, const int32_t* tgt_in, int32_t T, float* 
  * launches and their total milliseconds since the last pd_ctx_set_timing.
  * Timing adds two event records per iteration; timed iterations are launched
  * kernel by kernel instead of replaying the captured iteration graph.
+ * pd_ctx_set_timing also resets the counter of pd_ctx_rows_processed
+ * (synchronously).
  */
 pd_status pd_ctx_set_timing(pd_ctx* ctx, int32_t enable);
 pd_status pd_ctx_vocab_timing(const pd_ctx* ctx, int64_t* launches, double* total_ms);
+
+/*
+ * Rows (decoder positions) evaluated by all iterations of pd_decode on this
+ * context since the context was created or pd_ctx_set_timing was last called:
+ * the sum over iterations of the rows laid out for that iteration (the work
+ * the fused vocabulary projection and every decoder product did).  Reads
+ * device memory synchronously: call it after the decode's stream has
+ * synchronised.
+ */
+pd_status pd_ctx_rows_processed(const pd_ctx* ctx, int64_t* rows);
 
 /* Message of the last failing call on this thread ("" if none). */
 const char* pd_last_error(void);

@@ -166,6 +166,7 @@ __device__ void emit_rows(const CtrlArgs& a) {
   const int total = s_total;
   if (threadIdx.x == 0) {
     *a.n_rows = total;
+    if (a.rows_total != nullptr) *a.rows_total += static_cast<unsigned long long>(total);
     if (a.host_done != nullptr)
       __hip_atomic_store(a.host_done, total == 0 ? 1 : 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
   }

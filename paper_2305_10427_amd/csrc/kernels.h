@@ -133,6 +133,7 @@ struct CtrlArgs {
   int* row_pos;
   int* row_tok;
   int* n_rows;             // device scalar
+  unsigned long long* rows_total;   // device counter: rows of every iteration laid out (may be null)
   int* host_done;          // mapped pinned host flag (may be null)
   int pad_id, bos_id, eos_id;
   int R_max;

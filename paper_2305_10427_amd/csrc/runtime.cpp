@@ -119,7 +119,7 @@ struct Layout {
   size_t x_res, s_buf, q_buf, a_buf, h_buf;
   size_t enc_k, enc_v, cross_k, cross_v, self_k, self_v;
   size_t partials, new_tok, row_flags, row_sent, row_pos, row_tok;
-  size_t st, y, tgt_m, src_len, n_rows;
+  size_t st, y, tgt_m, src_len, n_rows, rows_total;
   size_t total;
 };
 
@@ -160,6 +160,7 @@ Layout plan(const pd_model& M, int max_batch, int max_src, int max_tgt) {
   L.tgt_m = take(static_cast<size_t>(max_batch) * 4);
   L.src_len = take(static_cast<size_t>(max_batch) * 4);
   L.n_rows = take(4);
+  L.rows_total = take(8);
   L.total = off;
   return L;
 }
@@ -635,6 +636,11 @@ pd_status pd_ctx_create(const pd_model* model, int32_t max_batch, int32_t max_sr
     hipEventCreate(&c->tv1[i]);
   }
   hipStreamCreateWithFlags(&c->capture, hipStreamNonBlocking);
+  e = hipMemset(c->at<unsigned long long>(c->L.rows_total), 0, sizeof(unsigned long long));
+  if (e != hipSuccess) {
+    pd_ctx_destroy(c);
+    return fail(PD_E_DEVICE, std::string("hipMemset: ") + hipGetErrorString(e));
+  }
   const char* g = std::getenv("PDEC_GRAPHS");
   c->use_graphs = !(g != nullptr && g[0] == '0');
   *out = c;
@@ -723,6 +729,7 @@ pd_status pd_decode(pd_ctx* ctx, int32_t mode, int32_t block, int32_t horizon, i
   ca.row_pos = C.at<int>(C.L.row_pos);
   ca.row_tok = C.at<int>(C.L.row_tok);
   ca.n_rows = C.at<int>(C.L.n_rows);
+  ca.rows_total = C.at<unsigned long long>(C.L.rows_total);
   ca.host_done = C.host_done_dev;
   ca.pad_id = M.cfg.pad_id;
   ca.bos_id = M.cfg.bos_id;
@@ -784,6 +791,7 @@ pd_status pd_decode(pd_ctx* ctx, int32_t mode, int32_t block, int32_t horizon, i
 
 pd_status pd_ctx_set_timing(pd_ctx* ctx, int32_t enable) {
   if (ctx == nullptr) return fail(PD_E_ARG, "null context");
+  PD_HIP(hipMemset(ctx->at<unsigned long long>(ctx->L.rows_total), 0, sizeof(unsigned long long)));
   ctx->timing = enable != 0;
   ctx->tv_launches = 0;
   ctx->tv_ms = 0.0;
@@ -795,6 +803,14 @@ pd_status pd_ctx_vocab_timing(const pd_ctx* ctx, int64_t* launches, double* tota
   if (ctx == nullptr || launches == nullptr || total_ms == nullptr) return fail(PD_E_ARG, "null argument");
   *launches = ctx->tv_launches;
   *total_ms = ctx->tv_ms;
+  return PD_OK;
+}
+
+pd_status pd_ctx_rows_processed(const pd_ctx* ctx, int64_t* rows) {
+  if (ctx == nullptr || rows == nullptr) return fail(PD_E_ARG, "null argument");
+  unsigned long long v = 0;
+  PD_HIP(hipMemcpy(&v, ctx->at<unsigned long long>(ctx->L.rows_total), sizeof(v), hipMemcpyDeviceToHost));
+  *rows = static_cast<int64_t>(v);
   return PD_OK;
 }
 

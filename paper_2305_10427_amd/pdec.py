@@ -41,7 +41,8 @@ class pd_config(ctypes.Structure):
 
 EXPORTS = ("pd_weight_count", "pd_weight_shape", "pd_model_create", "pd_model_destroy",
            "pd_ctx_workspace_bytes", "pd_ctx_create", "pd_ctx_destroy", "pd_encode", "pd_decode",
-           "pd_debug_logits", "pd_ctx_set_timing", "pd_ctx_vocab_timing", "pd_last_error")
+           "pd_debug_logits", "pd_ctx_set_timing", "pd_ctx_vocab_timing", "pd_ctx_rows_processed",
+           "pd_last_error")
 
 _lib = None
 
@@ -79,6 +80,8 @@ def load_library(path: str = LIB_PATH):
     L.pd_ctx_set_timing.restype = I32
     L.pd_ctx_vocab_timing.argtypes = [VP, P(I64), P(ctypes.c_double)]
     L.pd_ctx_vocab_timing.restype = I32
+    L.pd_ctx_rows_processed.argtypes = [VP, P(I64)]
+    L.pd_ctx_rows_processed.restype = I32
     L.pd_last_error.argtypes = []
     L.pd_last_error.restype = ctypes.c_char_p
     _lib = L
@@ -217,6 +220,12 @@ class Context:
         n, ms = ctypes.c_int64(), ctypes.c_double()
         _check(load_library().pd_ctx_vocab_timing(self.handle, ctypes.byref(n), ctypes.byref(ms)))
         return n.value, ms.value
+
+    def rows_processed(self) -> int:
+        """Rows evaluated by all iterations since set_timing (synchronous)."""
+        n = ctypes.c_int64()
+        _check(load_library().pd_ctx_rows_processed(self.handle, ctypes.byref(n)))
+        return n.value
 
     def __del__(self):
         if getattr(self, "handle", None) and _lib is not None:

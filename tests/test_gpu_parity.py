@@ -266,3 +266,20 @@ def test_mt_base_sampled_sentences(wl):
 def test_large_sampled_sentence():
     labels = _full_size("large", 1, 24, [("ar", 1), ("jacobi", 0), ("gs_jacobi", 16)])
     say("large", summarize(labels))
+
+
+def test_rows_processed_counts_block_positions():
+    """The device row counter equals the positions the oracle's iterations
+    evaluated: k for greedy, the sum of the block lengths of every iteration for
+    the Jacobi modes."""
+    _, _, ctx, M = build(CHAIN, seed=1, bias_std=0.5, ln_std=0.3)
+    for src in sources(CHAIN.vocab, 2, seed=12):
+        enc = M.encode(src)
+        for mode, b in [("ar", 1), ("jacobi", 0), ("gs_jacobi", 3), ("hybrid", 4)]:
+            say(f"case rows mode={mode} b={b}")
+            want = oracle.decode(M, enc, 16, mode, b)
+            ctx.set_timing(False)                   # resets the counter
+            g = gpu_decode_batch(ctx, [src], [16], mode, b)[0]
+            assert g.k == want.k
+            expect = want.k if mode == "ar" else sum(len(blk) for _, _, blk in want.iterates)
+            assert ctx.rows_processed() == expect
