@@ -256,6 +256,9 @@ def main():
     ap.add_argument("--no-large", action="store_true")
     ap.add_argument("--no-batched", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true")
+    ap.add_argument("--batched-only", default="",
+                    help="WORKLOAD:MODE:B — decode one batch of a batched workload in one mode and exit "
+                         "(profiling driver; prints no JSON line)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); sentence-level data "
@@ -269,6 +272,10 @@ def main():
 
     if args.copy_calibration:
         copy_calibration()
+    if args.batched_only:
+        wl_name, mode, b = args.batched_only.split(":")
+        batched_workload(wl_name, 1, [(mode, int(b))], 1)
+        return
     headline = ("hybrid", 5)
     modes = [(m.split(":")[0], int(m.split(":")[1])) for m in args.modes.split(",")]
     if headline not in modes:
