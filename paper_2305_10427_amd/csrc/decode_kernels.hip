@@ -65,14 +65,26 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
 
 // ---------------------------------------------------------------------------
 // Token embedding x = E[tok] * scale + PE(pos), PE the interleaved sinusoid
-// (columns 2i, 2i+1 = sin, cos of pos * 10000^(-2i/d)), evaluated in double.
+// (columns 2i, 2i+1 = sin, cos of pos * 10000^(-2i/d)), evaluated in double
+// and rounded to float once per context into a table (k_pe_table), so that
+// embedding a row costs two loads per element instead of double-precision
+// transcendentals.
+__global__ __launch_bounds__(256) void k_pe_table(float* pe, int n_pos, int d) {
+  const size_t total = static_cast<size_t>(n_pos) * d;
+  for (size_t t = blockIdx.x * blockDim.x + threadIdx.x; t < total; t += static_cast<size_t>(gridDim.x) * blockDim.x) {
+    const int p = static_cast<int>(t / d);
+    const int c = static_cast<int>(t - static_cast<size_t>(p) * d);
+    const double freq = exp(-log(10000.0) * static_cast<double>(c & ~1) / d);
+    const double ang = static_cast<double>(p) * freq;
+    pe[t] = static_cast<float>((c & 1) ? cos(ang) : sin(ang));
+  }
+}
+
 template <typename WT>
-__device__ __forceinline__ float embed_elem(const WT* emb, int tok, int p, int c, int d, float scale, int vocab) {
+__device__ __forceinline__ float embed_elem(const WT* emb, const float* pe, int tok, int p, int c, int d, float scale,
+                                            int vocab) {
   tok = min(max(tok, 0), vocab - 1);
-  const double freq = exp(-log(10000.0) * static_cast<double>(c & ~1) / d);
-  const double ang = static_cast<double>(p) * freq;
-  const float pe = static_cast<float>((c & 1) ? cos(ang) : sin(ang));
-  return Elt<WT>::load(emb, static_cast<size_t>(tok) * d + c) * scale + pe;
+  return Elt<WT>::load(emb, static_cast<size_t>(tok) * d + c) * scale + pe[static_cast<size_t>(p) * d + c];
 }
 
 template <typename WT>
@@ -85,7 +97,7 @@ __global__ __launch_bounds__(256) void k_embed(EmbedArgs a) {
     int s, p;
     row_place(a.rows, row, s, p);
     Elt<WT>::store(static_cast<WT*>(a.out), t,
-                   embed_elem<WT>(static_cast<const WT*>(a.emb), a.tok[row], p, c, a.d, a.scale, a.vocab));
+                   embed_elem<WT>(static_cast<const WT*>(a.emb), a.pe, a.tok[row], p, c, a.d, a.scale, a.vocab));
   }
 }
 
@@ -177,7 +189,7 @@ __device__ void emit_rows(const CtrlArgs& a) {
       const int row = static_cast<int>(t / a.d);
       const int c = static_cast<int>(t - static_cast<size_t>(row) * a.d);
       Elt<WT>::store(static_cast<WT*>(a.x_out), t,
-                     embed_elem<WT>(static_cast<const WT*>(a.emb), a.row_tok[row], a.row_pos[row], c, a.d,
+                     embed_elem<WT>(static_cast<const WT*>(a.emb), a.pe, a.row_tok[row], a.row_pos[row], c, a.d,
                                     a.emb_scale, a.vocab));
     }
   }
@@ -272,6 +284,31 @@ __device__ void reduce_rows(const uint2* partials, int part_ld, int n_parts, int
   }
 }
 
+// State transition of a sentence after an iteration of its block:
+// changed = the block differs from its previous value (StopC, Eq. (3)),
+// eos = the new block holds [EOS], nf = a non-finite logit was seen.
+__device__ __forceinline__ void advance_state(const CtrlArgs& a, SentState& st, bool changed, bool eos, int nf) {
+  if (nf) st.flags |= FLAG_NONFINITE;
+  st.k += 1;
+  st.j += 1;
+  const bool converged = !changed || st.j >= st.L;
+  if (converged) {
+    if ((a.mode == MODE_AR || a.mode == MODE_HYBRID) && eos) {
+      st.done = 1;
+      st.flags |= FLAG_CONVERGED | FLAG_EOS;
+    }
+    if (!st.done) {
+      st.i += st.L;
+      st.j = 0;
+      if (st.i >= st.m) { st.done = 1; st.flags |= FLAG_CONVERGED; }
+      else st.L = block_len(a, st.i, st.m);
+    }
+  }
+  const int cap = a.max_iters > 0 ? a.max_iters : st.m;
+  if (!st.done && st.k >= cap) { st.done = 1; st.flags |= FLAG_MAX_ITERS; }
+  if (st.done) st.L = 0;
+}
+
 template <typename WT>
 __global__ __launch_bounds__(1024) void k_ctrl_step(CtrlArgs a) {
   const int R = *a.n_rows;
@@ -282,53 +319,148 @@ __global__ __launch_bounds__(1024) void k_ctrl_step(CtrlArgs a) {
     SentState st = a.st[s];
     if (st.done) continue;
     int* y = a.y + static_cast<size_t>(s) * a.ldy;
-    bool changed = false;
+    bool changed = false, eos = false;
     int nf = 0;
     for (int r = 0; r < st.L; ++r) {
       const int t = a.new_tok[st.row0 + r];
       nf |= a.row_flags[st.row0 + r];
       if (y[st.i + r] != t) changed = true;
+      eos |= t == a.eos_id;
       y[st.i + r] = t;
     }
-    if (nf) st.flags |= FLAG_NONFINITE;
-    st.k += 1;
-    st.j += 1;
-    const bool converged = !changed || st.j >= st.L;
-    if (converged) {
-      if (a.mode == MODE_AR || a.mode == MODE_HYBRID) {
-        for (int r = 0; r < st.L; ++r)
-          if (y[st.i + r] == a.eos_id) { st.done = 1; st.flags |= FLAG_CONVERGED | FLAG_EOS; break; }
-      }
-      if (!st.done) {
-        st.i += st.L;
-        st.j = 0;
-        if (st.i >= st.m) { st.done = 1; st.flags |= FLAG_CONVERGED; }
-        else st.L = block_len(a, st.i, st.m);
-      }
-    }
-    const int cap = a.max_iters > 0 ? a.max_iters : st.m;
-    if (!st.done && st.k >= cap) { st.done = 1; st.flags |= FLAG_MAX_ITERS; }
-    if (st.done) st.L = 0;
+    advance_state(a, st, changed, eos, nf);
     a.st[s] = st;
   }
   __syncthreads();
   emit_rows<WT>(a);
 }
 
+// The control step of iterations of at most 64 rows (so at most 64
+// sentences), with everything that does not leave the workgroup kept in LDS:
+// the sentence states, the new tokens, the previous block values and the next
+// rows.  Its global-memory round trips are (1) states, row count and argmax
+// partials, (2) the blocks' previous values, (3) the embedding rows of the
+// next tokens, against about seven in k_ctrl_step; the transitions are the
+// same (advance_state).  Draft positions beyond a sentence's current block
+// still hold their initial [PAD] (InitT), so the next block's shifted-left
+// inputs are the block's last new token followed by [PAD].
+constexpr int kCtrlSmallMax = 64;
+
+template <typename WT>
+__global__ __launch_bounds__(1024) void k_ctrl_small(CtrlArgs a) {
+  __shared__ SentState s_st[kCtrlSmallMax];
+  __shared__ int s_tok[kCtrlSmallMax], s_flag[kCtrlSmallMax], s_old[kCtrlSmallMax], s_prev[kCtrlSmallMax];
+  __shared__ int s_rpos[kCtrlSmallMax], s_rtok[kCtrlSmallMax];
+  __shared__ int s_total;
+  const int tid = threadIdx.x;
+  const bool sent = tid < a.B;
+  // (1) states and the row count; the partials of every row the launch may
+  // hold (rows past the device count are reduced too and ignored)
+  SentState st;
+  if (sent) st = a.st[tid];
+  const int R = *a.n_rows;
+  // (2) previous values of each live block and the token before it, issued
+  // before the reduction so that both round trips overlap
+  if (sent && !st.done) {
+    const int* y = a.y + static_cast<size_t>(tid) * a.ldy;
+    for (int r = 0; r < st.L; ++r) s_old[st.row0 + r] = y[st.i + r];
+    s_prev[tid] = st.i > 0 ? y[st.i - 1] : a.bos_id;
+  }
+  reduce_rows(a.partials, a.part_ld, a.n_parts, a.R_max, s_tok, s_flag);   // ends synchronised
+  if (R == 0) return;                          // workgroup-uniform: the decode had already finished
+  int i_old = 0, row0_old = 0, L_old = 0;
+  if (sent && !st.done) {
+    int* y = a.y + static_cast<size_t>(tid) * a.ldy;
+    bool changed = false, eos = false;
+    int nf = 0;
+    for (int r = 0; r < st.L; ++r) {
+      const int t = s_tok[st.row0 + r];
+      nf |= s_flag[st.row0 + r];
+      changed |= s_old[st.row0 + r] != t;
+      eos |= t == a.eos_id;
+      y[st.i + r] = t;
+    }
+    i_old = st.i;
+    row0_old = st.row0;
+    L_old = st.L;
+    advance_state(a, st, changed, eos, nf);
+  }
+  if (sent) s_st[tid] = st;
+  __syncthreads();
+  if (tid == 0) {
+    int acc = 0;
+    for (int s = 0; s < a.B; ++s) {
+      s_st[s].row0 = acc;
+      acc += s_st[s].done ? 0 : s_st[s].L;
+    }
+    s_total = acc;
+    *a.n_rows = acc;
+    if (a.rows_total != nullptr) *a.rows_total += static_cast<unsigned long long>(acc);
+    if (a.host_done != nullptr)
+      __hip_atomic_store(a.host_done, acc == 0 ? 1 : 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  }
+  __syncthreads();
+  // the next rows: sentence order, block order; the shifted-left input of
+  // position p is [BOS] at p = 0, else y[p - 1]: the value just written, the
+  // token before the old block, or [PAD] past the old block (InitT)
+  if (sent) {
+    st = s_st[tid];
+    a.st[tid] = st;
+    for (int r = 0; r < st.L; ++r) {
+      const int row = st.row0 + r;
+      const int p = st.i + r;
+      int tok;
+      if (p == 0) tok = a.bos_id;
+      else if (p - 1 < i_old) tok = s_prev[tid];
+      else if (p - 1 < i_old + L_old) tok = s_tok[row0_old + (p - 1 - i_old)];
+      else tok = a.pad_id;
+      s_rpos[row] = p;
+      s_rtok[row] = tok;
+      a.row_sent[row] = tid;
+      a.row_pos[row] = p;
+      a.row_tok[row] = tok;
+    }
+  }
+  __syncthreads();
+  // (3) the embedding of the next rows
+  const int total = s_total;
+  const size_t n = static_cast<size_t>(total) * a.d;
+  for (size_t t = tid; t < n; t += blockDim.x) {
+    const int row = static_cast<int>(t / a.d);
+    const int c = static_cast<int>(t - static_cast<size_t>(row) * a.d);
+    Elt<WT>::store(static_cast<WT*>(a.x_out), t,
+                   embed_elem<WT>(static_cast<const WT*>(a.emb), a.pe, s_rtok[row], s_rpos[row], c, a.d, a.emb_scale,
+                                  a.vocab));
+  }
+}
+
 // Outputs: ids cut after the first [EOS] (inclusive) and [PAD]-filled, the
 // output length, the iteration count k and the flags of each sentence.
 __global__ __launch_bounds__(256) void k_finalize(CtrlArgs a) {
-  for (int s = threadIdx.x; s < a.B; s += blockDim.x) {
+  // one wave per sentence; lanes stride over the positions
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = threadIdx.x / kWave;
+  for (int s = blockIdx.x * 4 + wave; s < a.B; s += gridDim.x * 4) {
     const SentState st = a.st[s];
     const int* y = a.y + static_cast<size_t>(s) * a.ldy;
-    int len = st.m;
-    for (int t = 0; t < st.m; ++t)
-      if (y[t] == a.eos_id) { len = t + 1; break; }
-    for (int t = 0; t < a.out_ld; ++t)
+    int first = st.m;                        // first [EOS] at or after this lane's positions
+    for (int t = lane; t < st.m; t += kWave)
+      if (y[t] == a.eos_id) { first = t; break; }
+    // wave minimum (DPP within rows of 16, then across the four rows)
+    first = min(first, __builtin_amdgcn_mov_dpp(first, kDppXor1, 0xF, 0xF, false));
+    first = min(first, __builtin_amdgcn_mov_dpp(first, kDppXor2, 0xF, 0xF, false));
+    first = min(first, __builtin_amdgcn_mov_dpp(first, kDppHalfMirror, 0xF, 0xF, false));
+    first = min(first, __builtin_amdgcn_mov_dpp(first, kDppMirror, 0xF, 0xF, false));
+    first = min(min(__builtin_amdgcn_readlane(first, 0), __builtin_amdgcn_readlane(first, 16)),
+                min(__builtin_amdgcn_readlane(first, 32), __builtin_amdgcn_readlane(first, 48)));
+    const int len = first < st.m ? first + 1 : st.m;
+    for (int t = lane; t < a.out_ld; t += kWave)
       a.out_ids[static_cast<size_t>(s) * a.out_ld + t] = (t < len && t < a.ldy) ? y[t] : a.pad_id;
-    a.out_len[s] = len;
-    a.out_k[s] = st.k;
-    a.out_flags[s] = st.flags;
+    if (lane == 0) {
+      a.out_len[s] = len;
+      a.out_k[s] = st.k;
+      a.out_flags[s] = st.flags;
+    }
   }
 }
 
@@ -362,6 +494,14 @@ hipError_t launch_attn(int dtype, const AttnArgs& a, int R_max, hipStream_t s) {
   const int grid = (R_max * a.H + 3) / 4;
   if (grid == 0) return hipSuccess;
   return dtype == DT_BF16 ? launch_attn_t<bf16_t>(a, grid, s) : launch_attn_t<float>(a, grid, s);
+}
+
+hipError_t launch_pe_table(float* pe, int n_pos, int d, hipStream_t s) {
+  const size_t total = static_cast<size_t>(n_pos) * d;
+  const int grid = static_cast<int>(std::min<size_t>((total + 255) / 256, 4096));
+  if (grid == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_pe_table, dim3(grid), dim3(256), 0, s, pe, n_pos, d);
+  return hipGetLastError();
 }
 
 hipError_t launch_embed(int dtype, const EmbedArgs& a, int R_max, hipStream_t s) {
@@ -406,13 +546,20 @@ hipError_t launch_ctrl_init(int dtype, const CtrlArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_ctrl_step(int dtype, const CtrlArgs& a, hipStream_t s) {
+  const bool small = a.partials != nullptr && a.x_out != nullptr && a.R_max <= kCtrlSmallMax && a.B <= kCtrlSmallMax;
+  if (small) {
+    if (dtype == DT_BF16) hipLaunchKernelGGL(k_ctrl_small<bf16_t>, dim3(1), dim3(1024), 0, s, a);
+    else hipLaunchKernelGGL(k_ctrl_small<float>, dim3(1), dim3(1024), 0, s, a);
+    return hipGetLastError();
+  }
   if (dtype == DT_BF16) hipLaunchKernelGGL(k_ctrl_step<bf16_t>, dim3(1), dim3(1024), 0, s, a);
   else hipLaunchKernelGGL(k_ctrl_step<float>, dim3(1), dim3(1024), 0, s, a);
   return hipGetLastError();
 }
 
 hipError_t launch_finalize(const CtrlArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(k_finalize, dim3(1), dim3(256), 0, s, a);
+  const int grid = std::max(1, std::min((a.B + 3) / 4, 256));
+  hipLaunchKernelGGL(k_finalize, dim3(grid), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

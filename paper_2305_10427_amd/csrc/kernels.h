@@ -90,6 +90,7 @@ struct EmbedArgs {
   const int* tok;          // [R] token of each row
   RowMap rows;             // position of each row
   const void* emb;         // E[V][d]
+  const float* pe;         // positional table [positions][d] (k_pe_table)
   float scale;
   int d;
   int vocab;               // ids outside [0, vocab) are clamped into it
@@ -143,6 +144,7 @@ struct CtrlArgs {
   int part_ld, n_parts;
   void* x_out;
   const void* emb;
+  const float* pe;         // positional table [positions][d]
   float emb_scale;
   int d, vocab;
   // finalize
@@ -177,6 +179,8 @@ hipError_t launch_attn(int dtype, const AttnArgs& a, int R_max, hipStream_t s);
 int vocab_grid(int dtype, int V, int d);
 hipError_t launch_vocab_argmax(int dtype, const GemmArgs& a, hipStream_t s);
 hipError_t launch_embed(int dtype, const EmbedArgs& a, int R_max, hipStream_t s);
+// Sinusoidal positional table pe[p][c] for p < n_pos (float of the double-precision value).
+hipError_t launch_pe_table(float* pe, int n_pos, int d, hipStream_t s);
 hipError_t launch_ln(int dtype, const LnArgs& a, int R_max, hipStream_t s);
 hipError_t launch_argmax_reduce(const ReduceArgs& a, int R_max, hipStream_t s);
 hipError_t launch_ctrl_init(int dtype, const CtrlArgs& a, hipStream_t s);

@@ -119,7 +119,7 @@ struct Layout {
   size_t x_res, s_buf, q_buf, a_buf, h_buf;
   size_t enc_k, enc_v, cross_k, cross_v, self_k, self_v;
   size_t partials, new_tok, row_flags, row_sent, row_pos, row_tok;
-  size_t st, y, tgt_m, src_len, n_rows, rows_total;
+  size_t st, y, tgt_m, src_len, n_rows, rows_total, pe;
   size_t total;
 };
 
@@ -161,6 +161,7 @@ Layout plan(const pd_model& M, int max_batch, int max_src, int max_tgt) {
   L.src_len = take(static_cast<size_t>(max_batch) * 4);
   L.n_rows = take(4);
   L.rows_total = take(8);
+  L.pe = take(static_cast<size_t>(std::max(max_src, max_tgt)) * d * sizeof(float));
   L.total = off;
   return L;
 }
@@ -289,7 +290,7 @@ hipError_t decoder_pass(pd_ctx& C, const Rows& r, float* logits, hipStream_t s, 
   hipError_t e;
 
   if (!fused) {   // otherwise the control step has embedded the rows already
-    EmbedArgs ea{r.n_dev, r.n_host, r.tok, r.map, M.w[0], M.dec_scale, d, M.V, x_res};
+    EmbedArgs ea{r.n_dev, r.n_host, r.tok, r.map, M.w[0], C.at<float>(C.L.pe), M.dec_scale, d, M.V, x_res};
     if ((e = launch_embed(M.dt, ea, r.R_max, s)) != hipSuccess) return e;
   }
 
@@ -420,7 +421,7 @@ hipError_t encoder_pass(pd_ctx& C, const int32_t* src, int B, int n_max, hipStre
   const float scale = 1.0f / std::sqrt(static_cast<float>(M.dh));
   hipError_t e;
 
-  EmbedArgs ea{nullptr, R, src, r.map, M.w[0], M.enc_scale, d, M.V, x_res};
+  EmbedArgs ea{nullptr, R, src, r.map, M.w[0], C.at<float>(C.L.pe), M.enc_scale, d, M.V, x_res};
   if ((e = launch_embed(M.dt, ea, R, s)) != hipSuccess) return e;
   for (int l = 0; l < cfg.n_enc; ++l) {
     const void* in = x_res;
@@ -637,9 +638,11 @@ pd_status pd_ctx_create(const pd_model* model, int32_t max_batch, int32_t max_sr
   }
   hipStreamCreateWithFlags(&c->capture, hipStreamNonBlocking);
   e = hipMemset(c->at<unsigned long long>(c->L.rows_total), 0, sizeof(unsigned long long));
+  if (e == hipSuccess) e = launch_pe_table(c->at<float>(c->L.pe), std::max(max_src, max_tgt), model->d, nullptr);
+  if (e == hipSuccess) e = hipDeviceSynchronize();
   if (e != hipSuccess) {
     pd_ctx_destroy(c);
-    return fail(PD_E_DEVICE, std::string("hipMemset: ") + hipGetErrorString(e));
+    return fail(PD_E_DEVICE, std::string("context set-up: ") + hipGetErrorString(e));
   }
   const char* g = std::getenv("PDEC_GRAPHS");
   c->use_graphs = !(g != nullptr && g[0] == '0');
@@ -748,6 +751,7 @@ pd_status pd_decode(pd_ctx* ctx, int32_t mode, int32_t block, int32_t horizon, i
     ca.n_parts = vocab_parts(M, R_max);
     ca.x_out = C.at<char>(C.L.x_res);
     ca.emb = M.w[0];
+    ca.pe = C.at<float>(C.L.pe);
     ca.emb_scale = M.dec_scale;
     ca.d = M.d;
     ca.vocab = M.V;
