@@ -189,6 +189,21 @@ pd_status pd_decode(pd_ctx* ctx, int32_t mode, int32_t block, int32_t horizon, i
                     int32_t* out_k, int32_t* out_flags, void* stream);
 
 /*
+ * pd_decode from a caller-supplied initial draft (InitT of Section 3.3)
+ * instead of all [PAD].
+ *   init_ids  device int32 [B][init_ld], init_ld >= max(tgt_m): the draft of
+ *             positions 0 .. tgt_m[b] - 1 of each sentence (ids outside
+ *             [0, vocab) are clamped into it where they enter the decoder)
+ * Every mode still returns the greedy solution in at most m iterations
+ * (Proposition 1 holds for any initialisation); only the iteration count k
+ * depends on the draft.  PD_AR ignores the draft's values (blocks of one
+ * position converge after one iteration).  init_ids == NULL is pd_decode.
+ */
+pd_status pd_decode_init(pd_ctx* ctx, int32_t mode, int32_t block, int32_t horizon, int32_t max_iters,
+                         const int32_t* tgt_m, const int32_t* init_ids, int32_t init_ld, int32_t* out_ids,
+                         int32_t out_ld, int32_t* out_len, int32_t* out_k, int32_t* out_flags, void* stream);
+
+/*
  * Verification only: teacher-forced logits of the encoded batch.
  *   tgt_in  device int32 [B][T] decoder inputs (BOS first), T <= max_tgt
  *   logits  device float [B][T][V]

@@ -210,7 +210,9 @@ __global__ __launch_bounds__(1024) void k_ctrl_init(CtrlArgs a) {
     st.row0 = 0;
     a.st[s] = st;
     int* y = a.y + static_cast<size_t>(s) * a.ldy;
-    for (int t = 0; t < a.ldy; ++t) y[t] = a.pad_id;      // InitT: all [PAD]
+    // InitT: the caller's draft over the m positions, else all [PAD]
+    const int* init = a.init != nullptr ? a.init + static_cast<size_t>(s) * a.init_ld : nullptr;
+    for (int t = 0; t < a.ldy; ++t) y[t] = (init != nullptr && t < m) ? init[t] : a.pad_id;
   }
   __syncthreads();
   emit_rows<WT>(a);
@@ -336,14 +338,13 @@ __global__ __launch_bounds__(1024) void k_ctrl_step(CtrlArgs a) {
 }
 
 // The control step of iterations of at most 64 rows (so at most 64
-// sentences), with everything that does not leave the workgroup kept in LDS:
-// the sentence states, the new tokens, the previous block values and the next
-// rows.  Its global-memory round trips are (1) states, row count and argmax
-// partials, (2) the blocks' previous values, (3) the embedding rows of the
-// next tokens, against about seven in k_ctrl_step; the transitions are the
-// same (advance_state).  Draft positions beyond a sentence's current block
-// still hold their initial [PAD] (InitT), so the next block's shifted-left
-// inputs are the block's last new token followed by [PAD].
+// sentences and blocks of at most 64 positions), with everything that does
+// not leave the workgroup kept in LDS: the sentence states, the new tokens,
+// the previous block values, the draft just past the block and the next rows.
+// Its global-memory round trips are (1) states, row count and argmax
+// partials, (2) the blocks' previous values and the draft after them, (3) the
+// embedding rows of the next tokens, against about seven in k_ctrl_step; the
+// transitions are the same (advance_state).
 constexpr int kCtrlSmallMax = 64;
 
 template <typename WT>
@@ -351,6 +352,7 @@ __global__ __launch_bounds__(1024) void k_ctrl_small(CtrlArgs a) {
   __shared__ SentState s_st[kCtrlSmallMax];
   __shared__ int s_tok[kCtrlSmallMax], s_flag[kCtrlSmallMax], s_old[kCtrlSmallMax], s_prev[kCtrlSmallMax];
   __shared__ int s_rpos[kCtrlSmallMax], s_rtok[kCtrlSmallMax];
+  __shared__ int s_after[kCtrlSmallMax][kCtrlSmallMax];   // draft values past each sentence's block
   __shared__ int s_total;
   const int tid = threadIdx.x;
   const bool sent = tid < a.B;
@@ -365,6 +367,10 @@ __global__ __launch_bounds__(1024) void k_ctrl_small(CtrlArgs a) {
     const int* y = a.y + static_cast<size_t>(tid) * a.ldy;
     for (int r = 0; r < st.L; ++r) s_old[st.row0 + r] = y[st.i + r];
     s_prev[tid] = st.i > 0 ? y[st.i - 1] : a.bos_id;
+    // inputs of a next block of up to 64 positions: y[i + L .. i + L + 62]
+    const int a0 = st.i + st.L;
+    const int n_after = min(kCtrlSmallMax - 1, st.m - a0);
+    for (int r = 0; r < n_after; ++r) s_after[tid][r] = y[a0 + r];
   }
   reduce_rows(a.partials, a.part_ld, a.n_parts, a.R_max, s_tok, s_flag);   // ends synchronised
   if (R == 0) return;                          // workgroup-uniform: the decode had already finished
@@ -402,7 +408,7 @@ __global__ __launch_bounds__(1024) void k_ctrl_small(CtrlArgs a) {
   __syncthreads();
   // the next rows: sentence order, block order; the shifted-left input of
   // position p is [BOS] at p = 0, else y[p - 1]: the value just written, the
-  // token before the old block, or [PAD] past the old block (InitT)
+  // token before the old block, or the draft past the old block
   if (sent) {
     st = s_st[tid];
     a.st[tid] = st;
@@ -413,7 +419,7 @@ __global__ __launch_bounds__(1024) void k_ctrl_small(CtrlArgs a) {
       if (p == 0) tok = a.bos_id;
       else if (p - 1 < i_old) tok = s_prev[tid];
       else if (p - 1 < i_old + L_old) tok = s_tok[row0_old + (p - 1 - i_old)];
-      else tok = a.pad_id;
+      else tok = s_after[tid][p - 1 - (i_old + L_old)];
       s_rpos[row] = p;
       s_rtok[row] = tok;
       a.row_sent[row] = tid;

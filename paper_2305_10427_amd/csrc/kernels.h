@@ -138,6 +138,8 @@ struct CtrlArgs {
   int* host_done;          // mapped pinned host flag (may be null)
   int pad_id, bos_id, eos_id;
   int R_max;
+  const int* init;         // initial draft [B][init_ld] (nullptr: all [PAD])
+  int init_ld;
   // fused into the control step when non-null: the argmax over the vocabulary
   // partials of the rows just computed, and the embedding of the next rows
   const uint2* partials;

@@ -688,6 +688,13 @@ pd_status pd_encode(pd_ctx* ctx, const int32_t* src_ids, const int32_t* src_len,
 pd_status pd_decode(pd_ctx* ctx, int32_t mode, int32_t block, int32_t horizon, int32_t max_iters,
                     const int32_t* tgt_m, int32_t* out_ids, int32_t out_ld, int32_t* out_len,
                     int32_t* out_k, int32_t* out_flags, void* stream) {
+  return pd_decode_init(ctx, mode, block, horizon, max_iters, tgt_m, nullptr, 0, out_ids, out_ld, out_len, out_k,
+                        out_flags, stream);
+}
+
+pd_status pd_decode_init(pd_ctx* ctx, int32_t mode, int32_t block, int32_t horizon, int32_t max_iters,
+                         const int32_t* tgt_m, const int32_t* init_ids, int32_t init_ld, int32_t* out_ids,
+                         int32_t out_ld, int32_t* out_len, int32_t* out_k, int32_t* out_flags, void* stream) {
   if (ctx == nullptr || tgt_m == nullptr || out_ids == nullptr || out_len == nullptr || out_k == nullptr ||
       out_flags == nullptr)
     return fail(PD_E_ARG, "null argument");
@@ -702,6 +709,7 @@ pd_status pd_decode(pd_ctx* ctx, int32_t mode, int32_t block, int32_t horizon, i
     m_max = std::max(m_max, tgt_m[b]);
   }
   if (out_ld < m_max) return fail(PD_E_ARG, "out_ld must be >= max(tgt_m)");
+  if (init_ids != nullptr && init_ld < m_max) return fail(PD_E_ARG, "init_ld must be >= max(tgt_m)");
   hipStream_t s = static_cast<hipStream_t>(stream);
   pd_ctx& C = *ctx;
   const pd_model& M = *C.M;
@@ -738,6 +746,8 @@ pd_status pd_decode(pd_ctx* ctx, int32_t mode, int32_t block, int32_t horizon, i
   ca.bos_id = M.cfg.bos_id;
   ca.eos_id = M.cfg.eos_id;
   ca.R_max = R_max;
+  ca.init = init_ids;
+  ca.init_ld = init_ld;
   ca.out_ids = out_ids;
   ca.out_ld = out_ld;
   ca.out_len = out_len;

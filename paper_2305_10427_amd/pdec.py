@@ -40,7 +40,7 @@ class pd_config(ctypes.Structure):
 
 
 EXPORTS = ("pd_weight_count", "pd_weight_shape", "pd_model_create", "pd_model_destroy",
-           "pd_ctx_workspace_bytes", "pd_ctx_create", "pd_ctx_destroy", "pd_encode", "pd_decode",
+           "pd_ctx_workspace_bytes", "pd_ctx_create", "pd_ctx_destroy", "pd_encode", "pd_decode", "pd_decode_init",
            "pd_debug_logits", "pd_ctx_set_timing", "pd_ctx_vocab_timing", "pd_ctx_rows_processed",
            "pd_last_error")
 
@@ -74,6 +74,8 @@ def load_library(path: str = LIB_PATH):
     L.pd_encode.restype = I32
     L.pd_decode.argtypes = [VP, I32, I32, I32, I32, P(I32), VP, I32, VP, VP, VP, VP]
     L.pd_decode.restype = I32
+    L.pd_decode_init.argtypes = [VP, I32, I32, I32, I32, P(I32), VP, I32, VP, I32, VP, VP, VP, VP]
+    L.pd_decode_init.restype = I32
     L.pd_debug_logits.argtypes = [VP, VP, I32, VP, VP]
     L.pd_debug_logits.restype = I32
     L.pd_ctx_set_timing.argtypes = [VP, I32]
@@ -180,8 +182,9 @@ class Context:
         self.B = B
 
     def decode(self, mode, tgt_m: Sequence[int], block: int = 1, max_iters: int = 0, horizon: int = 0,
-               stream=None, out=None):
-        """Returns (ids [B, m_max], lengths [B], k [B], flags [B]) as device int32 tensors."""
+               stream=None, out=None, init=None):
+        """Returns (ids [B, m_max], lengths [B], k [B], flags [B]) as device int32 tensors.
+        init: optional int32 tensor [B, >= max(tgt_m)], the initial draft (default all [PAD])."""
         import torch
         mode_id = MODE_IDS[mode] if isinstance(mode, str) else int(mode)
         tgt_m = [int(x) for x in tgt_m]
@@ -195,10 +198,22 @@ class Context:
                    torch.empty(B, dtype=torch.int32, device=self.device),
                    torch.empty(B, dtype=torch.int32, device=self.device))
         ids, ln, k, fl = out
-        _check(load_library().pd_decode(self.handle, mode_id, int(block), int(horizon), int(max_iters),
-                                        _host_i32(tgt_m), ctypes.c_void_p(ids.data_ptr()), ids.shape[1],
-                                        ctypes.c_void_p(ln.data_ptr()), ctypes.c_void_p(k.data_ptr()),
-                                        ctypes.c_void_p(fl.data_ptr()), ctypes.c_void_p(_stream_handle(stream))))
+        if init is None:
+            _check(load_library().pd_decode(self.handle, mode_id, int(block), int(horizon), int(max_iters),
+                                            _host_i32(tgt_m), ctypes.c_void_p(ids.data_ptr()), ids.shape[1],
+                                            ctypes.c_void_p(ln.data_ptr()), ctypes.c_void_p(k.data_ptr()),
+                                            ctypes.c_void_p(fl.data_ptr()), ctypes.c_void_p(_stream_handle(stream))))
+        else:
+            init = init.to(device=self.device, dtype=torch.int32).contiguous()
+            if init.dim() != 2 or init.shape[0] != B:
+                raise PdError(1, f"init must be [B, >= m_max], got {tuple(init.shape)}")
+            self._init = init                # keep alive until the kernels have read it
+            _check(load_library().pd_decode_init(self.handle, mode_id, int(block), int(horizon), int(max_iters),
+                                                 _host_i32(tgt_m), ctypes.c_void_p(init.data_ptr()), init.shape[1],
+                                                 ctypes.c_void_p(ids.data_ptr()), ids.shape[1],
+                                                 ctypes.c_void_p(ln.data_ptr()), ctypes.c_void_p(k.data_ptr()),
+                                                 ctypes.c_void_p(fl.data_ptr()),
+                                                 ctypes.c_void_p(_stream_handle(stream))))
         return ids, ln, k, fl
 
     def debug_logits(self, tgt_in, stream=None):

@@ -29,7 +29,8 @@ class GpuResult:
     flags: int
 
 
-def gpu_decode_batch(ctx, srcs, ms, mode, block=1, max_iters=0, horizon=0) -> List[GpuResult]:
+def gpu_decode_batch(ctx, srcs, ms, mode, block=1, max_iters=0, horizon=0, init=None) -> List[GpuResult]:
+    """init: optional list of initial drafts (one int array of length >= m per sentence)."""
     import torch
     B = len(srcs)
     n_max = max(len(s) for s in srcs)
@@ -37,7 +38,14 @@ def gpu_decode_batch(ctx, srcs, ms, mode, block=1, max_iters=0, horizon=0) -> Li
     for r, s in enumerate(srcs):
         src[r, :len(s)] = s
     ctx.encode(torch.from_numpy(src).cuda(), [len(s) for s in srcs])
-    ids, ln, k, fl = ctx.decode(mode, ms, block=block, max_iters=max_iters, horizon=horizon)
+    init_t = None
+    if init is not None:
+        w = max(len(d) for d in init)
+        arr = np.zeros((B, w), np.int32)
+        for r, d in enumerate(init):
+            arr[r, :len(d)] = d
+        init_t = torch.from_numpy(arr).cuda()
+    ids, ln, k, fl = ctx.decode(mode, ms, block=block, max_iters=max_iters, horizon=horizon, init=init_t)
     torch.cuda.synchronize()
     ids, ln, k, fl = (t.cpu().numpy() for t in (ids, ln, k, fl))
     out = []

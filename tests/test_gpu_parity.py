@@ -283,3 +283,35 @@ def test_rows_processed_counts_block_positions():
             assert g.k == want.k
             expect = want.k if mode == "ar" else sum(len(blk) for _, _, blk in want.iterates)
             assert ctx.rows_processed() == expect
+
+
+def test_initial_draft_variants_match_oracle():
+    """pd_decode_init (InitT of Section 3.3): random drafts give the oracle's ids
+    and k; the greedy solution as the draft is a fixed point recognised at once
+    (Jacobi k = 1, GS-Jacobi k = number of blocks); batched drafts equal
+    single-sentence decodes."""
+    for cfg, wkw in [(TINY, {}), (CHAIN, dict(bias_std=0.5, ln_std=0.3))]:
+        _, _, ctx, M = build(cfg, seed=5, **wkw)
+        srcs = sources(cfg.vocab, 3, seed=14)
+        for si, src in enumerate(srcs):
+            enc = M.encode(src)
+            greedy = oracle.greedy(M, enc, 16)
+            for m in (7, 16):
+                draft = synth.random_draft(m, cfg.vocab, 200 + si)
+                for mode, b in [("jacobi", 0), ("gs_jacobi", 3), ("gs_jacobi", 4), ("hybrid", 4)]:
+                    say(f"case init cfg={cfg.name} mode={mode} b={b} m={m}")
+                    want = oracle.decode(M, enc, m, mode, b, init=draft)
+                    g = gpu_decode_batch(ctx, [src], [m], mode, b, init=[draft])[0]
+                    lab = classify(g, want, oracle.greedy(M, enc, m), TOL[cfg.dtype])
+                    assert not lab.startswith("FAIL"), f"{mode} b={b} m={m}: {lab}"
+            y_star = oracle.greedy(M, enc, 16, stop_at_eos=False).y
+            say(f"case init fixed point cfg={cfg.name}")
+            assert gpu_decode_batch(ctx, [src], [16], "jacobi", init=[y_star])[0].k == 1
+            for b in (3, 4, 16):
+                assert gpu_decode_batch(ctx, [src], [16], "gs_jacobi", b, init=[y_star])[0].k == -(-16 // b)
+        drafts = [synth.random_draft(16, cfg.vocab, 300 + r) for r in range(3)]
+        batch = gpu_decode_batch(ctx, srcs, [16, 11, 16], "gs_jacobi", 4, init=drafts)
+        for r in range(3):
+            one = gpu_decode_batch(ctx, [srcs[r]], [[16, 11, 16][r]], "gs_jacobi", 4, init=[drafts[r]])[0]
+            np.testing.assert_array_equal(batch[r].ids, one.ids)
+            assert batch[r].k == one.k

@@ -272,3 +272,22 @@ def test_max_iters_cap():
         assert r.k == 3 and r.hit_max_iters, mode
         r = oracle.decode(M, enc, m, mode, b, max_iters=m)
         assert not r.hit_max_iters
+
+
+@pytest.mark.parametrize("cfg,seed,kw", CASES, ids=["tiny", "tiny_bias", "chain"])
+def test_greedy_solution_as_draft_is_a_fixed_point(cfg, seed, kw):
+    """Initialised with the greedy solution y* (the unique solution of the
+    triangular system, Eq. (2)), every iteration reproduces its block: Jacobi
+    stops after one iteration and GS-Jacobi after one iteration per block."""
+    M = _model(cfg, seed, **kw)
+    for src in _sources(cfg, 3, seed=seed + 20):
+        enc = M.encode(src)
+        for m in (1, 7, 16):
+            y_star = oracle.greedy(M, enc, m, stop_at_eos=False).y
+            r = oracle.jacobi(M, enc, m, init=y_star)
+            assert r.k == 1
+            np.testing.assert_array_equal(r.y, y_star)
+            for b in (1, 3, 4, m):
+                r = oracle.gs_jacobi(M, enc, m, b, init=y_star)
+                assert r.k == -(-m // b)
+                np.testing.assert_array_equal(r.y, y_star)
