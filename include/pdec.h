@@ -235,6 +235,51 @@ pd_status pd_ctx_vocab_timing(const pd_ctx* ctx, int64_t* launches, double* tota
  */
 pd_status pd_ctx_rows_processed(const pd_ctx* ctx, int64_t* rows);
 
+/*
+ * Decoding trace: the data behind the DDGviz view (Section 3.5, and Figure 3
+ * in Section 4.3), which shows for every Jacobi iteration the token each
+ * evaluated position received and its probability under p_theta.
+ *
+ * With a trace buffer set, every iteration of pd_decode / pd_decode_init
+ * appends one record per evaluated row (decoder position), in the order of
+ * the iteration's rows (sentence by sentence, positions increasing):
+ *   iteration  the sentence's iteration count after this iteration (1-based,
+ *              the k of that sentence at that point)
+ *   sentence   index of the sentence in the batch
+ *   position   0-based target position (the record predicts y[position])
+ *   token      argmax over the vocabulary (the value written to the iterate)
+ *   top1       the largest logit of the row
+ *   lse        log sum_v exp(logit_v) of the row, so that the token's
+ *              probability is exp(top1 - lse)
+ * Records are appended at index = number of records so far; the buffer keeps
+ * the first `capacity` of them and pd_ctx_trace_count returns the full count
+ * (which may exceed capacity).  Tracing stores each iteration's full logits
+ * (rows x V floats) into a caller-owned scratch of at least
+ * pd_trace_scratch_bytes(model, rows) bytes, where rows is the largest number
+ * of rows one iteration lays out (B * block for the block modes, B * m for
+ * PD_JACOBI); a decode whose iteration needs more rows than the scratch holds
+ * fails with PD_E_WORKSPACE before launching anything.  Traced iterations are
+ * launched kernel by kernel (no graph replay).  Tracing changes no token,
+ * count or flag of the decode.
+ *
+ * pd_ctx_set_trace(ctx, records, capacity, scratch, scratch_bytes): records:
+ *   device buffer of `capacity` records (pd_trace_record, 16-byte aligned), scratch:
+ *   device float buffer (16-byte aligned).  Both stay owned by the caller and
+ *   must outlive every traced decode.  records == NULL turns tracing off.
+ *   Resets the record count (synchronously).
+ * pd_ctx_trace_count: records appended since pd_ctx_set_trace (synchronous
+ *   device read; call after the decode's stream has synchronised).
+ */
+typedef struct {
+  int32_t iteration, sentence, position, token;
+  float top1, lse;
+} pd_trace_record;
+
+pd_status pd_trace_scratch_bytes(const pd_model* model, int32_t max_rows, size_t* bytes);
+pd_status pd_ctx_set_trace(pd_ctx* ctx, void* dev_records, int64_t capacity, void* dev_logits_scratch,
+                           size_t scratch_bytes);
+pd_status pd_ctx_trace_count(const pd_ctx* ctx, int64_t* records);
+
 /* Message of the last failing call on this thread ("" if none). */
 const char* pd_last_error(void);
 

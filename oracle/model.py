@@ -120,6 +120,7 @@ class ArgmaxRecord:
     top1: float
     top2: float            # largest logit among the other indices
     linf: float            # max |logit|
+    lse: float = 0.0       # log sum_v exp(logit_v): p(token) = exp(top1 - lse)
 
 
 class Model:
@@ -233,5 +234,6 @@ def argmax_rows(logits: np.ndarray, p0: int) -> List[ArgmaxRecord]:
         t = int(np.argmax(row))              # first maximal index
         top1 = float(row[t])
         rest = np.delete(row, t)
-        out.append(ArgmaxRecord(p0 + r, t, top1, float(rest.max()), float(np.abs(row).max())))
+        lse = top1 + float(np.log(np.sum(np.exp(row - top1))))    # log-sum-exp, shifted by the maximum
+        out.append(ArgmaxRecord(p0 + r, t, top1, float(rest.max()), float(np.abs(row).max()), lse))
     return out

@@ -120,6 +120,35 @@ __global__ __launch_bounds__(256) void k_ln(LnArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// Trace statistics of stored logits: per row the largest logit m and
+// lse = m + log sum_v exp(logit_v - m), one workgroup per row.
+__global__ __launch_bounds__(256) void k_row_lse(const float* logits, int ld, int V, const int* n_rows_dev,
+                                                 float* row_max, float* row_lse) {
+  const int row = blockIdx.x;
+  const int R = n_rows_dev ? *n_rows_dev : gridDim.x;
+  if (row >= R) return;
+  const float* x = logits + static_cast<size_t>(row) * ld;
+  __shared__ float s_red[4];
+  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+  float m = -INFINITY;
+  for (int v = threadIdx.x; v < V; v += blockDim.x) m = fmaxf(m, x[v]);
+  m = wave_max(m);
+  if (lane == 0) s_red[wave] = m;
+  __syncthreads();
+  m = fmaxf(fmaxf(s_red[0], s_red[1]), fmaxf(s_red[2], s_red[3]));
+  __syncthreads();
+  float sum = 0.f;
+  for (int v = threadIdx.x; v < V; v += blockDim.x) sum += expf(x[v] - m);
+  sum = wave_sum(sum);
+  if (lane == 0) s_red[wave] = sum;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    row_max[row] = m;
+    row_lse[row] = m + logf((s_red[0] + s_red[1]) + (s_red[2] + s_red[3]));
+  }
+}
+
+// ---------------------------------------------------------------------------
 // On-device control of the fixed-point iteration.
 //
 // Every mode is a sequence of blocks [i, i+L) solved by Jacobi iterations:
@@ -311,6 +340,15 @@ __device__ __forceinline__ void advance_state(const CtrlArgs& a, SentState& st, 
   if (st.done) st.L = 0;
 }
 
+// Trace record of row `row` of the iteration (the caller's buffer keeps the
+// first trace_cap records; the count keeps growing).
+__device__ __forceinline__ void trace_row(const CtrlArgs& a, unsigned long long base, int row, int it, int s, int p,
+                                          int tok) {
+  const unsigned long long idx = base + static_cast<unsigned long long>(row);
+  if (idx < static_cast<unsigned long long>(a.trace_cap))
+    a.trace[idx] = TraceRec{it, s, p, tok, a.row_max[row], a.row_lse[row]};
+}
+
 template <typename WT>
 __global__ __launch_bounds__(1024) void k_ctrl_step(CtrlArgs a) {
   const int R = *a.n_rows;
@@ -329,11 +367,13 @@ __global__ __launch_bounds__(1024) void k_ctrl_step(CtrlArgs a) {
       if (y[st.i + r] != t) changed = true;
       eos |= t == a.eos_id;
       y[st.i + r] = t;
+      if (a.trace != nullptr) trace_row(a, *a.trace_count, st.row0 + r, st.k + 1, s, st.i + r, t);
     }
     advance_state(a, st, changed, eos, nf);
     a.st[s] = st;
   }
   __syncthreads();
+  if (a.trace != nullptr && threadIdx.x == 0) *a.trace_count += static_cast<unsigned long long>(R);
   emit_rows<WT>(a);
 }
 
@@ -379,12 +419,14 @@ __global__ __launch_bounds__(1024) void k_ctrl_small(CtrlArgs a) {
     int* y = a.y + static_cast<size_t>(tid) * a.ldy;
     bool changed = false, eos = false;
     int nf = 0;
+    const unsigned long long tbase = a.trace != nullptr ? *a.trace_count : 0ull;
     for (int r = 0; r < st.L; ++r) {
       const int t = s_tok[st.row0 + r];
       nf |= s_flag[st.row0 + r];
       changed |= s_old[st.row0 + r] != t;
       eos |= t == a.eos_id;
       y[st.i + r] = t;
+      if (a.trace != nullptr) trace_row(a, tbase, st.row0 + r, st.k + 1, tid, st.i + r, t);
     }
     i_old = st.i;
     row0_old = st.row0;
@@ -394,6 +436,7 @@ __global__ __launch_bounds__(1024) void k_ctrl_small(CtrlArgs a) {
   if (sent) s_st[tid] = st;
   __syncthreads();
   if (tid == 0) {
+    if (a.trace != nullptr) *a.trace_count += static_cast<unsigned long long>(R);
     int acc = 0;
     for (int s = 0; s < a.B; ++s) {
       s_st[s].row0 = acc;
@@ -500,6 +543,13 @@ hipError_t launch_attn(int dtype, const AttnArgs& a, int R_max, hipStream_t s) {
   const int grid = (R_max * a.H + 3) / 4;
   if (grid == 0) return hipSuccess;
   return dtype == DT_BF16 ? launch_attn_t<bf16_t>(a, grid, s) : launch_attn_t<float>(a, grid, s);
+}
+
+hipError_t launch_row_lse(const float* logits, int ld, int V, const int* n_rows_dev, int R_max, float* row_max,
+                          float* row_lse, hipStream_t s) {
+  if (R_max <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_row_lse, dim3(R_max), dim3(256), 0, s, logits, ld, V, n_rows_dev, row_max, row_lse);
+  return hipGetLastError();
 }
 
 hipError_t launch_pe_table(float* pe, int n_pos, int d, hipStream_t s) {

@@ -109,6 +109,18 @@ struct LnArgs {
   void* out;               // storage type
 };
 
+// One record of the decoding trace: the token an iteration produced at a
+// target position, its logit and the log-sum-exp of the row's logits
+// (probability exp(top1 - lse)).  Same layout as pd_trace_record.
+struct TraceRec {
+  int iteration;   // 1-based iteration count of the sentence that produced the token
+  int sentence;
+  int position;    // 0-based target position
+  int token;
+  float top1;
+  float lse;
+};
+
 // Per-sentence decoding state kept on the device.
 struct SentState {
   int m;          // target length (number of equations)
@@ -140,6 +152,12 @@ struct CtrlArgs {
   int R_max;
   const int* init;         // initial draft [B][init_ld] (nullptr: all [PAD])
   int init_ld;
+  // decoding trace (nullptr: off): one record per evaluated row
+  TraceRec* trace;
+  long long trace_cap;
+  unsigned long long* trace_count;
+  const float* row_max;    // [R] largest logit of each row of the iteration
+  const float* row_lse;    // [R] log-sum-exp of each row
   // fused into the control step when non-null: the argmax over the vocabulary
   // partials of the rows just computed, and the embedding of the next rows
   const uint2* partials;
@@ -181,6 +199,10 @@ hipError_t launch_attn(int dtype, const AttnArgs& a, int R_max, hipStream_t s);
 int vocab_grid(int dtype, int V, int d);
 hipError_t launch_vocab_argmax(int dtype, const GemmArgs& a, hipStream_t s);
 hipError_t launch_embed(int dtype, const EmbedArgs& a, int R_max, hipStream_t s);
+// Trace: largest logit and log-sum-exp of each of the iteration's rows of
+// stored logits [R][ld] (rows counted on the device, at most R_max).
+hipError_t launch_row_lse(const float* logits, int ld, int V, const int* n_rows_dev, int R_max, float* row_max,
+                          float* row_lse, hipStream_t s);
 // Sinusoidal positional table pe[p][c] for p < n_pos (float of the double-precision value).
 hipError_t launch_pe_table(float* pe, int n_pos, int d, hipStream_t s);
 hipError_t launch_ln(int dtype, const LnArgs& a, int R_max, hipStream_t s);

@@ -119,7 +119,7 @@ struct Layout {
   size_t x_res, s_buf, q_buf, a_buf, h_buf;
   size_t enc_k, enc_v, cross_k, cross_v, self_k, self_v;
   size_t partials, new_tok, row_flags, row_sent, row_pos, row_tok;
-  size_t st, y, tgt_m, src_len, n_rows, rows_total, pe;
+  size_t st, y, tgt_m, src_len, n_rows, rows_total, pe, trace_count, row_max, row_lse;
   size_t total;
 };
 
@@ -161,6 +161,9 @@ Layout plan(const pd_model& M, int max_batch, int max_src, int max_tgt) {
   L.src_len = take(static_cast<size_t>(max_batch) * 4);
   L.n_rows = take(4);
   L.rows_total = take(8);
+  L.trace_count = take(8);
+  L.row_max = take(rows_dec * 4);
+  L.row_lse = take(rows_dec * 4);
   L.pe = take(static_cast<size_t>(std::max(max_src, max_tgt)) * d * sizeof(float));
   L.total = off;
   return L;
@@ -196,6 +199,11 @@ struct pd_ctx {
   bool tv_pending[2] = {false, false};
   int64_t tv_launches = 0;
   double tv_ms = 0.0;
+  // decoding trace (off while trace == nullptr): caller-owned records and logits scratch
+  TraceRec* trace = nullptr;
+  long long trace_cap = 0;
+  float* trace_logits = nullptr;
+  long long trace_rows = 0;            // rows the scratch holds
   int enc_B = 0, enc_nmax = 0;
   bool encoded = false;
 
@@ -390,6 +398,20 @@ hipError_t decoder_pass(pd_ctx& C, const Rows& r, float* logits, hipStream_t s, 
   if (slot >= 0) {
     if ((e = hipEventRecord(C.tv1[slot], s)) != hipSuccess) return e;
     C.tv_pending[slot] = true;
+  }
+  if (C.trace != nullptr) {
+    // trace: the same logits stored (verification-path product from the
+    // un-normalised rows), then each row's maximum and log-sum-exp
+    GemmArgs gl = gemm_base(r);
+    if (pre) { gl.x = x_res; gl.x_f32 = 0; gl.ln_g = M.dec_ln(0); gl.ln_b = M.dec_ln(1); }
+    else { gl.x = s_buf; gl.x_f32 = 1; gl.ln_g = M.dec(cfg.n_dec - 1, D_LN3G); gl.ln_b = M.dec(cfg.n_dec - 1, D_LN3B); }
+    gl.ldx = d; gl.ln_eps = cfg.ln_eps;
+    gl.w = M.w[0]; gl.bias = M.w[1]; gl.N = M.V; gl.K = d; gl.logit_scale = cfg.logit_scale;
+    gl.out_f32 = C.trace_logits; gl.ldo = M.V;
+    if ((e = run_gemm(C, r, gl, EPI_LOGITS, true, a_buf, s)) != hipSuccess) return e;
+    if ((e = launch_row_lse(C.trace_logits, M.V, M.V, r.n_dev, r.R_max, C.at<float>(C.L.row_max),
+                            C.at<float>(C.L.row_lse), s)) != hipSuccess)
+      return e;
   }
   if (fused) return hipSuccess;   // the control step reduces the partials
   ReduceArgs ra{r.n_dev, C.at<uint2>(C.L.partials), g.part_ld, n_parts, C.at<int>(C.L.new_tok),
@@ -713,15 +735,17 @@ pd_status pd_decode_init(pd_ctx* ctx, int32_t mode, int32_t block, int32_t horiz
   hipStream_t s = static_cast<hipStream_t>(stream);
   pd_ctx& C = *ctx;
   const pd_model& M = *C.M;
-  pd_status st = stage_lengths(ctx, C.stage_tgt, tgt_m, B, C.at<int>(C.L.tgt_m), s);
-  if (st != PD_OK) return st;
-
   int Lmax = 1;
   if (mode == PD_JACOBI) Lmax = m_max;
   else if (mode == PD_GS_JACOBI || mode == PD_HYBRID) Lmax = std::min(block, m_max);
   const int R_max = B * Lmax;
   int iters = m_max;
   if (max_iters > 0) iters = std::min(iters, max_iters);
+  if (C.trace != nullptr && R_max > C.trace_rows)
+    return fail(PD_E_WORKSPACE, "trace logits scratch holds " + std::to_string(C.trace_rows) +
+                                    " rows, the decode needs " + std::to_string(R_max));
+  pd_status st = stage_lengths(ctx, C.stage_tgt, tgt_m, B, C.at<int>(C.L.tgt_m), s);
+  if (st != PD_OK) return st;
 
   CtrlArgs ca;
   std::memset(&ca, 0, sizeof(ca));
@@ -748,6 +772,13 @@ pd_status pd_decode_init(pd_ctx* ctx, int32_t mode, int32_t block, int32_t horiz
   ca.R_max = R_max;
   ca.init = init_ids;
   ca.init_ld = init_ld;
+  if (C.trace != nullptr) {
+    ca.trace = C.trace;
+    ca.trace_cap = C.trace_cap;
+    ca.trace_count = C.at<unsigned long long>(C.L.trace_count);
+    ca.row_max = C.at<float>(C.L.row_max);
+    ca.row_lse = C.at<float>(C.L.row_lse);
+  }
   ca.out_ids = out_ids;
   ca.out_ld = out_ld;
   ca.out_len = out_len;
@@ -774,7 +805,7 @@ pd_status pd_decode_init(pd_ctx* ctx, int32_t mode, int32_t block, int32_t horiz
     const int slot = C.timing ? (it & 1) : -1;
     if (slot >= 0 && (e = take_timing(C, slot)) != hipSuccess)
       return fail(PD_E_DEVICE, std::string("timing: ") + hipGetErrorString(e));
-    if (C.use_graphs && slot < 0) {   // event-timed iterations are launched directly
+    if (C.use_graphs && slot < 0 && C.trace == nullptr) {   // timed and traced iterations are launched directly
       hipGraphExec_t ex = nullptr;
       const GraphKey key{mode, block, horizon, max_iters, B, R_max, slot, fused ? 1 : 0};
       e = iteration_graph(C, key, r, ca, &ex);
@@ -817,6 +848,46 @@ pd_status pd_ctx_vocab_timing(const pd_ctx* ctx, int64_t* launches, double* tota
   if (ctx == nullptr || launches == nullptr || total_ms == nullptr) return fail(PD_E_ARG, "null argument");
   *launches = ctx->tv_launches;
   *total_ms = ctx->tv_ms;
+  return PD_OK;
+}
+
+static_assert(sizeof(TraceRec) == sizeof(pd_trace_record), "trace record layouts differ");
+
+pd_status pd_trace_scratch_bytes(const pd_model* model, int32_t max_rows, size_t* bytes) {
+  if (model == nullptr || bytes == nullptr) return fail(PD_E_ARG, "null argument");
+  if (max_rows < 1) return fail(PD_E_ARG, "max_rows must be >= 1");
+  *bytes = static_cast<size_t>(max_rows) * model->V * sizeof(float);
+  return PD_OK;
+}
+
+pd_status pd_ctx_set_trace(pd_ctx* ctx, void* dev_records, int64_t capacity, void* dev_logits_scratch,
+                           size_t scratch_bytes) {
+  if (ctx == nullptr) return fail(PD_E_ARG, "null context");
+  if (dev_records == nullptr) {
+    ctx->trace = nullptr;
+    ctx->trace_cap = 0;
+    ctx->trace_logits = nullptr;
+    ctx->trace_rows = 0;
+    return PD_OK;
+  }
+  if (capacity < 1 || dev_logits_scratch == nullptr) return fail(PD_E_ARG, "capacity must be >= 1 and scratch non-null");
+  if (!aligned(dev_records, 16) || !aligned(dev_logits_scratch, 16))
+    return fail(PD_E_ARG, "trace buffers must be 16-byte aligned");
+  const size_t row_bytes = static_cast<size_t>(ctx->M->V) * sizeof(float);
+  if (scratch_bytes < row_bytes) return fail(PD_E_WORKSPACE, "trace logits scratch holds no row");
+  PD_HIP(hipMemset(ctx->at<unsigned long long>(ctx->L.trace_count), 0, sizeof(unsigned long long)));
+  ctx->trace = static_cast<TraceRec*>(dev_records);
+  ctx->trace_cap = capacity;
+  ctx->trace_logits = static_cast<float*>(dev_logits_scratch);
+  ctx->trace_rows = static_cast<long long>(scratch_bytes / row_bytes);
+  return PD_OK;
+}
+
+pd_status pd_ctx_trace_count(const pd_ctx* ctx, int64_t* records) {
+  if (ctx == nullptr || records == nullptr) return fail(PD_E_ARG, "null argument");
+  unsigned long long v = 0;
+  PD_HIP(hipMemcpy(&v, ctx->at<unsigned long long>(ctx->L.trace_count), sizeof(v), hipMemcpyDeviceToHost));
+  *records = static_cast<int64_t>(v);
   return PD_OK;
 }
 

@@ -42,7 +42,7 @@ class pd_config(ctypes.Structure):
 EXPORTS = ("pd_weight_count", "pd_weight_shape", "pd_model_create", "pd_model_destroy",
            "pd_ctx_workspace_bytes", "pd_ctx_create", "pd_ctx_destroy", "pd_encode", "pd_decode", "pd_decode_init",
            "pd_debug_logits", "pd_ctx_set_timing", "pd_ctx_vocab_timing", "pd_ctx_rows_processed",
-           "pd_last_error")
+           "pd_trace_scratch_bytes", "pd_ctx_set_trace", "pd_ctx_trace_count", "pd_last_error")
 
 _lib = None
 
@@ -84,6 +84,12 @@ def load_library(path: str = LIB_PATH):
     L.pd_ctx_vocab_timing.restype = I32
     L.pd_ctx_rows_processed.argtypes = [VP, P(I64)]
     L.pd_ctx_rows_processed.restype = I32
+    L.pd_trace_scratch_bytes.argtypes = [VP, I32, P(SZ)]
+    L.pd_trace_scratch_bytes.restype = I32
+    L.pd_ctx_set_trace.argtypes = [VP, VP, I64, VP, SZ]
+    L.pd_ctx_set_trace.restype = I32
+    L.pd_ctx_trace_count.argtypes = [VP, P(I64)]
+    L.pd_ctx_trace_count.restype = I32
     L.pd_last_error.argtypes = []
     L.pd_last_error.restype = ctypes.c_char_p
     _lib = L
@@ -241,6 +247,36 @@ class Context:
         n = ctypes.c_int64()
         _check(load_library().pd_ctx_rows_processed(self.handle, ctypes.byref(n)))
         return n.value
+
+    TRACE_DTYPE = [("iteration", "<i4"), ("sentence", "<i4"), ("position", "<i4"), ("token", "<i4"),
+                   ("top1", "<f4"), ("lse", "<f4")]
+
+    def set_trace(self, capacity: int, max_rows: int):
+        """Turn the decoding trace on (capacity records, iterations of up to
+        max_rows rows; both buffers allocated here) or off (capacity 0)."""
+        import torch
+        L = load_library()
+        if capacity <= 0:
+            _check(L.pd_ctx_set_trace(self.handle, None, 0, None, 0))
+            self._trace = None
+            return
+        nbytes = ctypes.c_size_t()
+        _check(L.pd_trace_scratch_bytes(self.model.handle, int(max_rows), ctypes.byref(nbytes)))
+        rec = torch.empty(capacity * 6, dtype=torch.int32, device=self.device)
+        scratch = torch.empty(nbytes.value // 4, dtype=torch.float32, device=self.device)
+        _check(L.pd_ctx_set_trace(self.handle, ctypes.c_void_p(rec.data_ptr()), int(capacity),
+                                  ctypes.c_void_p(scratch.data_ptr()), nbytes.value))
+        self._trace = (rec, scratch)
+
+    def trace(self):
+        """Records appended since set_trace, as a numpy structured array
+        (fields of TRACE_DTYPE), and the full count (may exceed capacity)."""
+        n = ctypes.c_int64()
+        _check(load_library().pd_ctx_trace_count(self.handle, ctypes.byref(n)))
+        rec = self._trace[0]
+        kept = min(n.value, rec.numel() // 6)
+        raw = rec[: kept * 6].cpu().numpy()
+        return raw.view(np.dtype(self.TRACE_DTYPE)), n.value
 
     def __del__(self):
         if getattr(self, "handle", None) and _lib is not None:

@@ -1,0 +1,146 @@
+"""Decoding trace (the data of DDGviz, Section 3.5 and Figure 3) through the
+C ABI, against the oracle's argmax records.
+
+For every evaluated row the oracle keeps (position, token, top1, lse) in
+evaluation order; its iterates give the iteration that produced each block.
+The GPU trace must list the same rows in the same order, with the same token
+and iteration, and top1 / lse within the logits tolerance (tol * max|logit|).
+A near tie on the oracle's side (margin below 2 tol max|logit|) ends the
+comparison there: past it both trajectories are valid but may differ."""
+import dataclasses
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2305_10427_amd import configs as C, pdec, synth
+from tests.parity import TOL, gpu_decode_batch
+
+pytestmark = pytest.mark.gpu
+
+TINY = C.TINY
+CHAIN = dataclasses.replace(C.TINY, name="chain", logit_scale=-3.0)
+SMALL_PRE_BF16 = dataclasses.replace(C.TINY, name="small_pre", pre_ln=True, act_gelu=True, dtype=C.BF16)
+MODES = [("ar", 1), ("jacobi", 0), ("gs_jacobi", 3), ("hybrid", 4)]
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+def build(cfg, seed=0, max_batch=4, max_src=32, max_tgt=32, **wkw):
+    w = synth.make_weights(cfg, seed=seed, **wkw)
+    gm = pdec.Model(cfg, w)
+    return gm, pdec.Context(gm, max_batch, max_src, max_tgt), oracle.Model(cfg, w.values)
+
+
+def sources(vocab, count, n=16, seed=1):
+    g = np.random.default_rng(seed)
+    return [g.integers(4, vocab, n).astype(np.int32) for _ in range(count)]
+
+
+def oracle_trace(res: oracle.Result, mode: str):
+    """(iteration, position, token, top1, lse, top1 - top2, max|logit|) per evaluated row,
+    in evaluation order."""
+    its = []
+    if mode == "ar":
+        its = list(range(1, len(res.records) + 1))
+    else:
+        for k, _, blk in res.iterates:
+            its += [k] * len(blk)
+    assert len(its) == len(res.records)
+    return [(it, r.position, r.token, r.top1, r.lse, r.top1 - r.top2, r.linf) for it, r in zip(its, res.records)]
+
+
+def compare(got, want, tol, sentence=0):
+    """Compares until the end or the first oracle near tie; returns the rows compared."""
+    n = 0
+    for g, (it, pos, tok, top1, lse, margin, linf) in zip(got, want):
+        assert (int(g["iteration"]), int(g["sentence"]), int(g["position"])) == (it, sentence, pos), (g, it, pos)
+        if margin < 2 * tol * linf:
+            return n
+        assert int(g["token"]) == tok, (g, tok)
+        assert abs(float(g["top1"]) - top1) <= tol * linf, (g, top1)
+        assert abs(float(g["lse"]) - lse) <= tol * linf, (g, lse)
+        n += 1
+    assert len(got) == len(want)
+    return n
+
+
+@pytest.mark.parametrize("cfg,wkw", [(TINY, {}), (CHAIN, dict(bias_std=0.5, ln_std=0.3)),
+                                     (SMALL_PRE_BF16, dict(bias_std=0.3, ln_std=0.2))],
+                         ids=["tiny", "chain", "small_pre_bf16"])
+def test_trace_matches_oracle_records(cfg, wkw):
+    gm, ctx, M = build(cfg, seed=3, **wkw)
+    tol = TOL[cfg.dtype]
+    for src in sources(cfg.vocab, 2, seed=21):
+        enc = M.encode(src)
+        for mode, b in MODES:
+            for m in (9, 16):
+                say(f"case trace cfg={cfg.name} mode={mode} b={b} m={m}")
+                want = oracle.decode(M, enc, m, mode, b)
+                ctx.set_trace(4096, m)
+                ctx.set_timing(False)                 # resets the row counter
+                g = gpu_decode_batch(ctx, [src], [m], mode, b)[0]
+                rec, count = ctx.trace()
+                assert count == ctx.rows_processed()
+                assert count == len(rec)
+                compare(rec, oracle_trace(want, mode), tol)
+    ctx.set_trace(0, 0)
+
+
+def test_trace_changes_no_result_and_batches_agree():
+    """Traced decodes return the untraced ids, k and flags; the records of a
+    batch, sentence by sentence, equal (bitwise) those of single-sentence
+    decodes."""
+    gm, ctx, M = build(CHAIN, seed=4, bias_std=0.5, ln_std=0.3)
+    srcs = sources(CHAIN.vocab, 3, seed=22)
+    ms = [16, 11, 14]
+    for mode, b in MODES:
+        say(f"case trace batch mode={mode} b={b}")
+        ctx.set_trace(0, 0)
+        plain = gpu_decode_batch(ctx, srcs, ms, mode, b)
+        ctx.set_trace(8192, 3 * 16)
+        traced = gpu_decode_batch(ctx, srcs, ms, mode, b)
+        rec, count = ctx.trace()
+        assert count == len(rec)
+        for p, t in zip(plain, traced):
+            np.testing.assert_array_equal(p.ids, t.ids)
+            assert (p.k, p.flags) == (t.k, t.flags)
+        for s in range(3):
+            mine = rec[rec["sentence"] == s]
+            assert np.all(np.diff(mine["iteration"]) >= 0)
+            assert mine["iteration"].max() == traced[s].k
+            ctx.set_trace(4096, 16)
+            gpu_decode_batch(ctx, [srcs[s]], [ms[s]], mode, b)
+            one, _ = ctx.trace()
+            cols = ["iteration", "position", "token"]
+            for c in cols:
+                np.testing.assert_array_equal(mine[c], one[c])
+            np.testing.assert_array_equal(mine["top1"].view(np.uint32), one["top1"].view(np.uint32))
+            np.testing.assert_array_equal(mine["lse"].view(np.uint32), one["lse"].view(np.uint32))
+    ctx.set_trace(0, 0)
+
+
+def test_trace_capacity_and_scratch_limits():
+    """The buffer keeps the first `capacity` records while the count keeps
+    growing; a scratch too small for the iteration's rows is refused before
+    anything runs, and the context stays usable."""
+    gm, ctx, M = build(TINY, seed=5)
+    src = sources(TINY.vocab, 1, seed=23)[0]
+    ctx.set_trace(4096, 16)
+    gpu_decode_batch(ctx, [src], [16], "jacobi")
+    full, n_full = ctx.trace()
+    ctx.set_trace(5, 16)
+    gpu_decode_batch(ctx, [src], [16], "jacobi")
+    head, n = ctx.trace()
+    assert n == n_full and len(head) == 5
+    np.testing.assert_array_equal(head, full[:5])
+    ctx.set_trace(16, 4)                              # 4 rows of scratch, Jacobi needs 16
+    with pytest.raises(pdec.PdError) as ei:
+        gpu_decode_batch(ctx, [src], [16], "jacobi")
+    assert ei.value.status == 3
+    ctx.set_trace(0, 0)
+    want = oracle.decode(M, M.encode(src), 16, "jacobi")
+    g = gpu_decode_batch(ctx, [src], [16], "jacobi")[0]
+    np.testing.assert_array_equal(g.ids, want.out)

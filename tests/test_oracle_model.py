@@ -193,3 +193,18 @@ def test_logit_scale_gives_std_near_three():
     M = oracle.Model(cfg, w.values)
     lg = M.teacher_forced_logits(M.encode(np.arange(4, 20)), np.array([1] + list(range(30, 45))))
     assert 2.5 < lg.std() < 3.5
+
+
+def test_argmax_records_log_sum_exp():
+    """The records' log-sum-exp is scipy's, and exp(top1 - lse) is the softmax
+    probability of the argmax token (the quantity a decoding trace reports)."""
+    from scipy.special import logsumexp, softmax
+    from oracle.model import argmax_rows
+    g = np.random.default_rng(7)
+    logits = g.normal(0, 3, size=(5, 257))
+    logits[2, 17] = logits[2].max() + 0.5
+    recs = argmax_rows(logits, 3)
+    for r, rec in enumerate(recs):
+        assert rec.position == 3 + r
+        assert rec.lse == pytest.approx(float(logsumexp(logits[r])), rel=1e-12, abs=1e-12)
+        assert np.exp(rec.top1 - rec.lse) == pytest.approx(float(softmax(logits[r]).max()), rel=1e-12)
