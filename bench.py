@@ -86,7 +86,7 @@ def run_mode(ctxs, sents, outs, mode, block, steps, warmup, timing=False):
     return res
 
 
-def gpu_workload(wl_name, steps, warmup, modes, headline, n_sent=0):
+def gpu_workload(wl_name, steps, warmup, modes, headline, n_sent=0, trace=False):
     import torch
     from paper_2305_10427_amd import configs as C, pdec, synth
     wl = C.WORKLOADS[wl_name]
@@ -120,6 +120,17 @@ def gpu_workload(wl_name, steps, warmup, modes, headline, n_sent=0):
     # the throughput above comes from the pass without them)
     t = run_mode(ctxs, sents, outs, headline[0], headline[1], steps, warmup, timing=True)
     res[f"{headline[0]}_b{headline[1]}"].update(vocab_launches=t["vocab_launches"], vocab_ms=t["vocab_ms"])
+    if trace:
+        # the same decodes with the DDGviz trace on (records and log-sum-exp
+        # partials; iterations launched kernel by kernel)
+        for c in ctxs:
+            c.set_trace(4 * wl.tgt_cap, max(headline[1], 1))
+        t = run_mode(ctxs, sents, outs, headline[0], headline[1], steps, warmup)
+        for c in ctxs:
+            c.set_trace(0, 0)
+        res["trace"] = {"mode": f"{headline[0]}_b{headline[1]}", "tokens_per_s": t["tokens_per_s"],
+                        "ms_per_step": t["ms_per_step"]}
+        log(f"[{wl_name}] traced {headline[0]} b={headline[1]}: {t['tokens_per_s']:9.1f} tok/s")
     return cfg, w, sents, model, res
 
 
@@ -281,7 +292,8 @@ def main():
     if headline not in modes:
         modes.append(headline)
     cfg, w, sents, model, res = gpu_workload("mt_base_bf16", args.steps, args.warmup, modes, headline,
-                                             args.sentences)
+                                             args.sentences, trace=True)
+    traced = res.pop("trace")
     f32 = None
     if not args.no_f32:
         _, _, _, _, f32 = gpu_workload("mt_base_f32", args.steps, args.warmup, modes, headline, args.sentences)
@@ -339,6 +351,8 @@ def main():
         "speedup_vs_ar": (round(h["tokens_per_s"] / res["ar_b1"]["tokens_per_s"], 3) if "ar_b1" in res else None),
         "roofline": roof,
         "cpu_baseline": cpu,
+        "trace": {"mode": traced["mode"], "tokens_per_s": round(traced["tokens_per_s"], 1),
+                  "slowdown": round(h["tokens_per_s"] / traced["tokens_per_s"], 3)},
     }
     if f32 is not None:
         line["f32"] = {k: {"tokens_per_s": round(v["tokens_per_s"], 1), "k_over_m": round(v["k_over_m"], 4)}

@@ -253,19 +253,23 @@ pd_status pd_ctx_rows_processed(const pd_ctx* ctx, int64_t* rows);
  *              probability is exp(top1 - lse)
  * Records are appended at index = number of records so far; the buffer keeps
  * the first `capacity` of them and pd_ctx_trace_count returns the full count
- * (which may exceed capacity).  Tracing stores each iteration's full logits
- * (rows x V floats) into a caller-owned scratch of at least
- * pd_trace_scratch_bytes(model, rows) bytes, where rows is the largest number
- * of rows one iteration lays out (B * block for the block modes, B * m for
- * PD_JACOBI); a decode whose iteration needs more rows than the scratch holds
- * fails with PD_E_WORKSPACE before launching anything.  Traced iterations are
- * launched kernel by kernel (no graph replay).  Tracing changes no token,
- * count or flag of the decode.
+ * (which may exceed capacity).  The logits are still never stored: the fused
+ * vocabulary kernel also keeps a running log-sum-exp per row and returns, per
+ * workgroup, a (max, sum of exp(logit - max)) pair, which a small kernel
+ * folds into top1 and lse.  Those pairs go to a caller-owned scratch of at
+ * least pd_trace_scratch_bytes(model, rows) bytes, where rows is the largest
+ * number of rows one iteration lays out (B * block for the block modes, B * m
+ * for PD_JACOBI, B for PD_AR); a decode whose iteration needs more rows than
+ * the scratch holds fails with PD_E_WORKSPACE before launching anything.
+ * Traced iterations are launched kernel by kernel (no graph replay).  Tracing
+ * changes no token, count or flag of the decode.  top1 is the exact largest
+ * logit; lse is rounded in float and its summation order follows the kernel
+ * that ran (it may differ in the last bits between batch sizes).
  *
  * pd_ctx_set_trace(ctx, records, capacity, scratch, scratch_bytes): records:
- *   device buffer of `capacity` records (pd_trace_record, 16-byte aligned), scratch:
- *   device float buffer (16-byte aligned).  Both stay owned by the caller and
- *   must outlive every traced decode.  records == NULL turns tracing off.
+ *   device buffer of `capacity` records (pd_trace_record, 16-byte aligned),
+ *   scratch: device buffer (16-byte aligned).  Both stay owned by the caller
+ *   and must outlive every traced decode.  records == NULL turns tracing off.
  *   Resets the record count (synchronously).
  * pd_ctx_trace_count: records appended since pd_ctx_set_trace (synchronous
  *   device read; call after the decode's stream has synchronised).
@@ -276,7 +280,7 @@ typedef struct {
 } pd_trace_record;
 
 pd_status pd_trace_scratch_bytes(const pd_model* model, int32_t max_rows, size_t* bytes);
-pd_status pd_ctx_set_trace(pd_ctx* ctx, void* dev_records, int64_t capacity, void* dev_logits_scratch,
+pd_status pd_ctx_set_trace(pd_ctx* ctx, void* dev_records, int64_t capacity, void* dev_scratch,
                            size_t scratch_bytes);
 pd_status pd_ctx_trace_count(const pd_ctx* ctx, int64_t* records);
 

@@ -127,6 +127,30 @@ __device__ __forceinline__ void group16_best(uint32_t& bk, uint32_t& bi) {
   best_take(bk, bi, dpp_u<kDppMirror>(bk), dpp_u<kDppMirror>(bi));
 }
 
+// Running log-sum-exp of a row as (m, s): m the largest value seen, s the sum
+// of exp(x - m) over the values seen; log-sum-exp = m + log(s).  The empty
+// state is (-inf, 0).
+__device__ __forceinline__ void lse_take(float& m, float& s, float x) {
+  if (x > m) {
+    s = s * expf(m - x) + 1.f;
+    m = x;
+  } else {
+    s += expf(x - m);
+  }
+}
+__device__ __forceinline__ void lse_merge(float& m, float& s, float m2, float s2) {
+  const float mn = fmaxf(m, m2);
+  if (mn == -INFINITY) return;   // both empty
+  s = s * expf(m - mn) + s2 * expf(m2 - mn);
+  m = mn;
+}
+__device__ __forceinline__ void group16_lse(float& m, float& s) {
+  lse_merge(m, s, dpp_f<kDppXor1>(m), dpp_f<kDppXor1>(s));
+  lse_merge(m, s, dpp_f<kDppXor2>(m), dpp_f<kDppXor2>(s));
+  lse_merge(m, s, dpp_f<kDppHalfMirror>(m), dpp_f<kDppHalfMirror>(s));
+  lse_merge(m, s, dpp_f<kDppMirror>(m), dpp_f<kDppMirror>(s));
+}
+
 // Whole-wave sum / max: the four row results (lanes 0, 16, 32, 48) are read
 // into scalars and combined as (r0 + r1) + (r2 + r3), the same in every lane.
 // All 64 lanes must be active.

@@ -119,32 +119,27 @@ __global__ __launch_bounds__(256) void k_ln(LnArgs a) {
                            static_cast<WT*>(a.out) + static_cast<size_t>(row) * a.d, nullptr, lane);
 }
 
-// ---------------------------------------------------------------------------
-// Trace statistics of stored logits: per row the largest logit m and
-// lse = m + log sum_v exp(logit_v - m), one workgroup per row.
-__global__ __launch_bounds__(256) void k_row_lse(const float* logits, int ld, int V, const int* n_rows_dev,
-                                                 float* row_max, float* row_lse) {
-  const int row = blockIdx.x;
-  const int R = n_rows_dev ? *n_rows_dev : gridDim.x;
-  if (row >= R) return;
-  const float* x = logits + static_cast<size_t>(row) * ld;
-  __shared__ float s_red[4];
-  const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
-  float m = -INFINITY;
-  for (int v = threadIdx.x; v < V; v += blockDim.x) m = fmaxf(m, x[v]);
-  m = wave_max(m);
-  if (lane == 0) s_red[wave] = m;
-  __syncthreads();
-  m = fmaxf(fmaxf(s_red[0], s_red[1]), fmaxf(s_red[2], s_red[3]));
-  __syncthreads();
-  float sum = 0.f;
-  for (int v = threadIdx.x; v < V; v += blockDim.x) sum += expf(x[v] - m);
-  sum = wave_sum(sum);
-  if (lane == 0) s_red[wave] = sum;
-  __syncthreads();
-  if (threadIdx.x == 0) {
+// Largest logit and log-sum-exp of each row from the vocabulary kernel's
+// per-workgroup (max, sum of exp(logit - max)) pairs: one wave per row, lane
+// l merging the pairs l, l + 64, ... in order, then the lanes as a fixed tree.
+__global__ __launch_bounds__(256) void k_lse_reduce(const float2* part, int part_ld, int n_parts,
+                                                    const int* n_rows_dev, int R_max, float* row_max,
+                                                    float* row_lse) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int row = blockIdx.x * 4 + static_cast<int>(threadIdx.x / kWave);
+  const int R = n_rows_dev ? *n_rows_dev : R_max;
+  if (row >= R) return;   // wave-uniform
+  const float2* p = part + static_cast<size_t>(row) * part_ld;
+  float m = -INFINITY, sm = 0.f;
+  for (int q = lane; q < n_parts; q += kWave) lse_merge(m, sm, p[q].x, p[q].y);
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    const float m2 = __shfl_xor(m, off), s2 = __shfl_xor(sm, off);
+    lse_merge(m, sm, m2, s2);
+  }
+  if (lane == 0) {
     row_max[row] = m;
-    row_lse[row] = m + logf((s_red[0] + s_red[1]) + (s_red[2] + s_red[3]));
+    row_lse[row] = m + logf(sm);
   }
 }
 
@@ -545,10 +540,11 @@ hipError_t launch_attn(int dtype, const AttnArgs& a, int R_max, hipStream_t s) {
   return dtype == DT_BF16 ? launch_attn_t<bf16_t>(a, grid, s) : launch_attn_t<float>(a, grid, s);
 }
 
-hipError_t launch_row_lse(const float* logits, int ld, int V, const int* n_rows_dev, int R_max, float* row_max,
-                          float* row_lse, hipStream_t s) {
+hipError_t launch_lse_reduce(const float2* part, int part_ld, int n_parts, const int* n_rows_dev, int R_max,
+                             float* row_max, float* row_lse, hipStream_t s) {
   if (R_max <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_row_lse, dim3(R_max), dim3(256), 0, s, logits, ld, V, n_rows_dev, row_max, row_lse);
+  hipLaunchKernelGGL(k_lse_reduce, dim3((R_max + 3) / 4), dim3(256), 0, s, part, part_ld, n_parts, n_rows_dev, R_max,
+                     row_max, row_lse);
   return hipGetLastError();
 }
 

@@ -114,6 +114,7 @@ __global__ __launch_bounds__(KSPLIT == 8 ? 512 : 256) void k_gemm(GemmArgs a) {
   __shared__ float s_part[KSPLIT > 1 ? KSPLIT : 1][4][64];
   __shared__ uint32_t s_key[4][16];
   __shared__ int s_idx[4][16];
+  __shared__ float2 s_lse[EPI == EPI_ARGMAX ? 4 : 1][16];
   // PRO_LN: the normalised 16-row input tile, rows padded by 16 bytes
   extern __shared__ __align__(16) unsigned char s_dyn[];
   AT* sA = reinterpret_cast<AT*>(s_dyn);
@@ -192,6 +193,7 @@ __global__ __launch_bounds__(KSPLIT == 8 ? 512 : 256) void k_gemm(GemmArgs a) {
     uint32_t bk[4] = {0u, 0u, 0u, 0u};
     uint32_t bi[4] = {0x7fffffffu, 0x7fffffffu, 0x7fffffffu, 0x7fffffffu};
     uint32_t nf = 0;
+    float lm[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY}, ls[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int e = 0; e < NE; ++e) {
       const int i = SPLIT ? wave : e;
@@ -230,7 +232,12 @@ __global__ __launch_bounds__(KSPLIT == 8 ? 512 : 256) void k_gemm(GemmArgs a) {
       } else if constexpr (EPI == EPI_ARGMAX) {
         const float logit = fmaf(a.logit_scale, v, bias_v);   // s * (h . E[col]) + bias[col]
         if (!isfinite(logit)) nf |= 1u << e;   // bit e: a non-finite logit in row 4 lg + e
-        else { bk[e] = float_key(logit); bi[e] = static_cast<uint32_t>(col); }
+        else {
+          bk[e] = float_key(logit);
+          bi[e] = static_cast<uint32_t>(col);
+          lm[e] = logit;
+          ls[e] = 1.f;
+        }
       }
     }
     if constexpr (EPI == EPI_ARGMAX) {
@@ -239,11 +246,17 @@ __global__ __launch_bounds__(KSPLIT == 8 ? 512 : 256) void k_gemm(GemmArgs a) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) group16_best(bk[e], bi[e]);
       nf = group16_or(nf);
+      const bool want_lse = a.part_lse != nullptr;
+      if (want_lse) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) group16_lse(lm[e], ls[e]);
+      }
       if (lr == 0) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           s_key[wave][4 * lg + e] = bk[e];
           s_idx[wave][4 * lg + e] = static_cast<int>(bi[e] | (((nf >> e) & 1u) << 31));
+          if (want_lse) s_lse[wave][4 * lg + e] = make_float2(lm[e], ls[e]);
         }
       }
       __syncthreads();
@@ -258,9 +271,15 @@ __global__ __launch_bounds__(KSPLIT == 8 ? 512 : 256) void k_gemm(GemmArgs a) {
           ff |= (raw >> 31) & 1;
           if (k2 > kk || (k2 == kk && i2 < ii)) { kk = k2; ii = i2; }
         }
-        if (m0 + r < R)
+        if (m0 + r < R) {
           a.partials[static_cast<size_t>(m0 + r) * a.part_ld + blockIdx.x] =
               make_uint2(kk, static_cast<uint32_t>(ii) | (static_cast<uint32_t>(ff) << 31));
+          if (want_lse) {
+            float m = s_lse[0][r].x, sm = s_lse[0][r].y;
+            for (int w = 1; w < 4; ++w) lse_merge(m, sm, s_lse[w][r].x, s_lse[w][r].y);   // wave order
+            a.part_lse[static_cast<size_t>(m0 + r) * a.part_ld + blockIdx.x] = make_float2(m, sm);
+          }
+        }
       }
       __syncthreads();
     }

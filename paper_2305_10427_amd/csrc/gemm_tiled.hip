@@ -236,26 +236,35 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_tiled(GemmArgs a, int n_r
   if constexpr (EPI == EPI_ARGMAX) {
     uint32_t bk[FM][4], bi[FM][4];
     uint32_t nf = 0;   // bit 4 i + e: a non-finite logit in row (i, e)
+    const bool want_lse = a.part_lse != nullptr;
+    float lm[FM][4], ls[FM][4];
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         bk[i][e] = 0u;
         bi[i][e] = 0x7fffffffu;
+        lm[i][e] = -INFINITY;
+        ls[i][e] = 0.f;
 #pragma unroll
         for (int j = 0; j < FN; ++j) {
           const int col = n0 + wn * S::TN + j * 16 + lr;
           const float logit = fmaf(a.logit_scale, res(i, j)[e], bias_v[j]);   // s * (h . E[col]) + bias[col]
           if (col < N) {
             if (!isfinite(logit)) nf |= 1u << (4 * i + e);
-            else best_take(bk[i][e], bi[i][e], float_key(logit), static_cast<uint32_t>(col));
+            else {
+              best_take(bk[i][e], bi[i][e], float_key(logit), static_cast<uint32_t>(col));
+              if (want_lse) lse_take(lm[i][e], ls[i][e], logit);
+            }
           }
         }
         group16_best(bk[i][e], bi[i][e]);
+        if (want_lse) group16_lse(lm[i][e], ls[i][e]);
       }
     nf = group16_or(nf);
     __shared__ uint32_t s_key[WN][BM];
     __shared__ uint32_t s_idx[WN][BM];
+    __shared__ float2 s_lse[WN][BM];
     if (lr == 0) {
 #pragma unroll
       for (int i = 0; i < FM; ++i)
@@ -264,6 +273,7 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_tiled(GemmArgs a, int n_r
           const int rl = wm * S::TM + i * 16 + 4 * lg + e;
           s_key[wn][rl] = bk[i][e];
           s_idx[wn][rl] = bi[i][e] | (((nf >> (4 * i + e)) & 1u) << 31);
+          if (want_lse) s_lse[wn][rl] = make_float2(lm[i][e], ls[i][e]);
         }
     }
     __syncthreads();
@@ -276,6 +286,12 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_tiled(GemmArgs a, int n_r
         ff |= s_idx[w][t] >> 31;
       }
       a.partials[static_cast<size_t>(m0 + t) * a.part_ld + cb] = make_uint2(kk, ii | (ff << 31));
+      if (want_lse) {
+        float m = s_lse[0][t].x, sm = s_lse[0][t].y;
+#pragma unroll
+        for (int w = 1; w < WN; ++w) lse_merge(m, sm, s_lse[w][t].x, s_lse[w][t].y);   // wave order
+        a.part_lse[static_cast<size_t>(m0 + t) * a.part_ld + cb] = make_float2(m, sm);
+      }
     }
     return;
   } else {

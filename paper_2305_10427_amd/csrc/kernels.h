@@ -66,6 +66,9 @@ struct GemmArgs {
   float logit_scale;       // EPI_ARGMAX
   uint2* partials;         // [row][part_ld] = (order key of best logit, index | nonfinite << 31)
   int part_ld;
+  // argmax epilogues, optional: [row][part_ld] = (max, sum of exp(logit - max))
+  // over the same columns as partials (finite logits only)
+  float2* part_lse;
 };
 
 struct AttnArgs {
@@ -199,10 +202,11 @@ hipError_t launch_attn(int dtype, const AttnArgs& a, int R_max, hipStream_t s);
 int vocab_grid(int dtype, int V, int d);
 hipError_t launch_vocab_argmax(int dtype, const GemmArgs& a, hipStream_t s);
 hipError_t launch_embed(int dtype, const EmbedArgs& a, int R_max, hipStream_t s);
-// Trace: largest logit and log-sum-exp of each of the iteration's rows of
-// stored logits [R][ld] (rows counted on the device, at most R_max).
-hipError_t launch_row_lse(const float* logits, int ld, int V, const int* n_rows_dev, int R_max, float* row_max,
-                          float* row_lse, hipStream_t s);
+// Trace: largest logit and log-sum-exp of each of the iteration's rows (rows
+// counted on the device, at most R_max) from the argmax kernels' per-part
+// (max, sum of exp(logit - max)) pairs part[row][part_ld], n_parts per row.
+hipError_t launch_lse_reduce(const float2* part, int part_ld, int n_parts, const int* n_rows_dev, int R_max,
+                             float* row_max, float* row_lse, hipStream_t s);
 // Sinusoidal positional table pe[p][c] for p < n_pos (float of the double-precision value).
 hipError_t launch_pe_table(float* pe, int n_pos, int d, hipStream_t s);
 hipError_t launch_ln(int dtype, const LnArgs& a, int R_max, hipStream_t s);

@@ -199,10 +199,11 @@ struct pd_ctx {
   bool tv_pending[2] = {false, false};
   int64_t tv_launches = 0;
   double tv_ms = 0.0;
-  // decoding trace (off while trace == nullptr): caller-owned records and logits scratch
+  // decoding trace (off while trace == nullptr): caller-owned records and the
+  // scratch of the vocabulary kernel's log-sum-exp partials
   TraceRec* trace = nullptr;
   long long trace_cap = 0;
-  float* trace_logits = nullptr;
+  float2* trace_part = nullptr;
   long long trace_rows = 0;            // rows the scratch holds
   int enc_B = 0, enc_nmax = 0;
   bool encoded = false;
@@ -379,6 +380,7 @@ hipError_t decoder_pass(pd_ctx& C, const Rows& r, float* logits, hipStream_t s, 
   }
   g.partials = C.at<uint2>(C.L.partials);
   g.part_ld = gemm_grid(EPI_ARGMAX, M.V, 1);
+  g.part_lse = C.trace_part;   // nullptr unless tracing
   const int n_parts = vocab_parts(M, r.R_max);
   const bool tiled = r.R_max > kVocabStreamMaxRows && vocab_tiled(M, r.R_max);
   if (tiled) {   // the final LayerNorm as its own kernel, outside the timed vocabulary launch
@@ -399,18 +401,9 @@ hipError_t decoder_pass(pd_ctx& C, const Rows& r, float* logits, hipStream_t s, 
     if ((e = hipEventRecord(C.tv1[slot], s)) != hipSuccess) return e;
     C.tv_pending[slot] = true;
   }
-  if (C.trace != nullptr) {
-    // trace: the same logits stored (verification-path product from the
-    // un-normalised rows), then each row's maximum and log-sum-exp
-    GemmArgs gl = gemm_base(r);
-    if (pre) { gl.x = x_res; gl.x_f32 = 0; gl.ln_g = M.dec_ln(0); gl.ln_b = M.dec_ln(1); }
-    else { gl.x = s_buf; gl.x_f32 = 1; gl.ln_g = M.dec(cfg.n_dec - 1, D_LN3G); gl.ln_b = M.dec(cfg.n_dec - 1, D_LN3B); }
-    gl.ldx = d; gl.ln_eps = cfg.ln_eps;
-    gl.w = M.w[0]; gl.bias = M.w[1]; gl.N = M.V; gl.K = d; gl.logit_scale = cfg.logit_scale;
-    gl.out_f32 = C.trace_logits; gl.ldo = M.V;
-    if ((e = run_gemm(C, r, gl, EPI_LOGITS, true, a_buf, s)) != hipSuccess) return e;
-    if ((e = launch_row_lse(C.trace_logits, M.V, M.V, r.n_dev, r.R_max, C.at<float>(C.L.row_max),
-                            C.at<float>(C.L.row_lse), s)) != hipSuccess)
+  if (C.trace != nullptr) {   // each row's largest logit and log-sum-exp from the partials
+    if ((e = launch_lse_reduce(C.trace_part, g.part_ld, n_parts, r.n_dev, r.R_max, C.at<float>(C.L.row_max),
+                               C.at<float>(C.L.row_lse), s)) != hipSuccess)
       return e;
   }
   if (fused) return hipSuccess;   // the control step reduces the partials
@@ -742,7 +735,7 @@ pd_status pd_decode_init(pd_ctx* ctx, int32_t mode, int32_t block, int32_t horiz
   int iters = m_max;
   if (max_iters > 0) iters = std::min(iters, max_iters);
   if (C.trace != nullptr && R_max > C.trace_rows)
-    return fail(PD_E_WORKSPACE, "trace logits scratch holds " + std::to_string(C.trace_rows) +
+    return fail(PD_E_WORKSPACE, "trace scratch holds " + std::to_string(C.trace_rows) +
                                     " rows, the decode needs " + std::to_string(R_max));
   pd_status st = stage_lengths(ctx, C.stage_tgt, tgt_m, B, C.at<int>(C.L.tgt_m), s);
   if (st != PD_OK) return st;
@@ -853,32 +846,37 @@ pd_status pd_ctx_vocab_timing(const pd_ctx* ctx, int64_t* launches, double* tota
 
 static_assert(sizeof(TraceRec) == sizeof(pd_trace_record), "trace record layouts differ");
 
+// Bytes of trace scratch per row: one (max, sum) pair per vocabulary workgroup.
+static size_t trace_row_bytes(const pd_model& M) {
+  return static_cast<size_t>(gemm_grid(EPI_ARGMAX, M.V, 1)) * sizeof(float2);
+}
+
 pd_status pd_trace_scratch_bytes(const pd_model* model, int32_t max_rows, size_t* bytes) {
   if (model == nullptr || bytes == nullptr) return fail(PD_E_ARG, "null argument");
   if (max_rows < 1) return fail(PD_E_ARG, "max_rows must be >= 1");
-  *bytes = static_cast<size_t>(max_rows) * model->V * sizeof(float);
+  *bytes = static_cast<size_t>(max_rows) * trace_row_bytes(*model);
   return PD_OK;
 }
 
-pd_status pd_ctx_set_trace(pd_ctx* ctx, void* dev_records, int64_t capacity, void* dev_logits_scratch,
+pd_status pd_ctx_set_trace(pd_ctx* ctx, void* dev_records, int64_t capacity, void* dev_scratch,
                            size_t scratch_bytes) {
   if (ctx == nullptr) return fail(PD_E_ARG, "null context");
   if (dev_records == nullptr) {
     ctx->trace = nullptr;
     ctx->trace_cap = 0;
-    ctx->trace_logits = nullptr;
+    ctx->trace_part = nullptr;
     ctx->trace_rows = 0;
     return PD_OK;
   }
-  if (capacity < 1 || dev_logits_scratch == nullptr) return fail(PD_E_ARG, "capacity must be >= 1 and scratch non-null");
-  if (!aligned(dev_records, 16) || !aligned(dev_logits_scratch, 16))
+  if (capacity < 1 || dev_scratch == nullptr) return fail(PD_E_ARG, "capacity must be >= 1 and scratch non-null");
+  if (!aligned(dev_records, 16) || !aligned(dev_scratch, 16))
     return fail(PD_E_ARG, "trace buffers must be 16-byte aligned");
-  const size_t row_bytes = static_cast<size_t>(ctx->M->V) * sizeof(float);
-  if (scratch_bytes < row_bytes) return fail(PD_E_WORKSPACE, "trace logits scratch holds no row");
+  const size_t row_bytes = trace_row_bytes(*ctx->M);
+  if (scratch_bytes < row_bytes) return fail(PD_E_WORKSPACE, "trace scratch holds no row");
   PD_HIP(hipMemset(ctx->at<unsigned long long>(ctx->L.trace_count), 0, sizeof(unsigned long long)));
   ctx->trace = static_cast<TraceRec*>(dev_records);
   ctx->trace_cap = capacity;
-  ctx->trace_logits = static_cast<float*>(dev_logits_scratch);
+  ctx->trace_part = static_cast<float2*>(dev_scratch);
   ctx->trace_rows = static_cast<long long>(scratch_bytes / row_bytes);
   return PD_OK;
 }

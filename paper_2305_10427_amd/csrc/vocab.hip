@@ -16,6 +16,10 @@
 // Every logit is accumulated exactly as in the general product kernel with
 // whole-K waves (MFMA steps in increasing k from zero, then s * acc + b), so
 // both kernels pick the same token for a row.
+//
+// The LSE variant also keeps, per row, a running log-sum-exp of the logits it
+// streams (for the decoding trace's token probabilities), returned beside
+// the argmax partials; the logits are still never stored.
 #include "common.h"
 #include "kernels.h"
 #include "mma.h"
@@ -33,7 +37,7 @@ template <int LNT, int XF32> struct VocabShape {
   static constexpr int MAX_WGS = 256 * OCC;
 };
 
-template <typename WT, int XF32, int LNT, int D = VocabShape<LNT, XF32>::D>
+template <typename WT, int XF32, int LNT, int LSE, int D = VocabShape<LNT, XF32>::D>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(VocabShape<LNT, XF32>::OCC))) void k_vocab(GemmArgs a) {
   using AT = WT;
   using XT = typename std::conditional<XF32 != 0, float, AT>::type;
@@ -101,6 +105,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(VocabShape<
   uint32_t bk[4] = {0u, 0u, 0u, 0u};
   uint32_t bi[4] = {0x7fffffffu, 0x7fffffffu, 0x7fffffffu, 0x7fffffffu};
   uint32_t nf = 0;                   // bit i: a non-finite logit in row 4 lg + i
+  float lm[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY}, ls[4] = {0.f, 0.f, 0.f, 0.f};
   floatx4_t acc = {0.f, 0.f, 0.f, 0.f};
   int j = 0, s = 0;                  // (tile, step) being consumed
   const AT* arow = sA + static_cast<size_t>(lr) * lda + EPL * lg;
@@ -122,7 +127,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(VocabShape<
             if (4 * lg + i >= R) continue;
             const float logit = fmaf(a.logit_scale, acc[i], bias_v);   // s * (h . E[col]) + bias[col]
             if (!isfinite(logit)) nf |= 1u << i;
-            else best_take(bk[i], bi[i], float_key(logit), static_cast<uint32_t>(col));
+            else {
+              best_take(bk[i], bi[i], float_key(logit), static_cast<uint32_t>(col));
+              if constexpr (LSE != 0) lse_take(lm[i], ls[i], logit);
+            }
           }
         }
         acc = floatx4_t{0.f, 0.f, 0.f, 0.f};
@@ -139,11 +147,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(VocabShape<
   nf = group16_or(nf);
   __shared__ uint32_t s_key[4][16];
   __shared__ int s_idx[4][16];
+  __shared__ float2 s_lse[LSE != 0 ? 4 : 1][16];
+  if constexpr (LSE != 0) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) group16_lse(lm[i], ls[i]);
+  }
   if (lr == 0) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       s_key[wave][4 * lg + i] = bk[i];
       s_idx[wave][4 * lg + i] = static_cast<int>(bi[i] | (((nf >> i) & 1u) << 31));
+      if constexpr (LSE != 0) s_lse[wave][4 * lg + i] = make_float2(lm[i], ls[i]);
     }
   }
   __syncthreads();
@@ -160,6 +174,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(VocabShape<
     }
     a.partials[static_cast<size_t>(r) * a.part_ld + blockIdx.x] =
         make_uint2(kk, static_cast<uint32_t>(ii) | (static_cast<uint32_t>(ff) << 31));
+    if constexpr (LSE != 0) {
+      float m = s_lse[0][r].x, sm = s_lse[0][r].y;
+      for (int w = 1; w < 4; ++w) lse_merge(m, sm, s_lse[w][r].x, s_lse[w][r].y);   // wave order
+      a.part_lse[static_cast<size_t>(r) * a.part_ld + blockIdx.x] = make_float2(m, sm);
+    }
   }
 }
 
@@ -171,18 +190,24 @@ int vocab_grid(int dtype, int V, int d) {
 
 namespace {
 
-template <typename WT, int XF32>
+template <typename WT, int XF32, int LSE>
 hipError_t launch_x(const GemmArgs& a, hipStream_t s) {
   const size_t lds = gemm_ln_lds_bytes(a.K, sizeof(WT));
   const dim3 grid(vocab_grid(std::is_same<WT, bf16_t>::value ? DT_BF16 : DT_F32, a.N, a.K));
   if constexpr (std::is_same<WT, bf16_t>::value) {
     if (a.K > 512) {
-      hipLaunchKernelGGL((k_vocab<WT, XF32, 8>), grid, dim3(256), lds, s, a);
+      hipLaunchKernelGGL((k_vocab<WT, XF32, 8, LSE>), grid, dim3(256), lds, s, a);
       return hipGetLastError();
     }
   }
-  hipLaunchKernelGGL((k_vocab<WT, XF32, 4>), grid, dim3(256), lds, s, a);
+  hipLaunchKernelGGL((k_vocab<WT, XF32, 4, LSE>), grid, dim3(256), lds, s, a);
   return hipGetLastError();
+}
+
+template <typename WT>
+hipError_t launch_w(const GemmArgs& a, hipStream_t s) {
+  if (a.part_lse != nullptr) return a.x_f32 ? launch_x<WT, 1, 1>(a, s) : launch_x<WT, 0, 1>(a, s);
+  return a.x_f32 ? launch_x<WT, 1, 0>(a, s) : launch_x<WT, 0, 0>(a, s);
 }
 
 }  // namespace
@@ -194,8 +219,7 @@ hipError_t launch_vocab_argmax(int dtype, const GemmArgs& a, hipStream_t s) {
   if (a.K % ks != 0 || a.K % 32 != 0 || a.K > (dtype == DT_BF16 ? 1024 : 512) ||
       a.part_ld < vocab_grid(dtype, a.N, a.K))
     return hipErrorInvalidValue;
-  if (dtype == DT_BF16) return a.x_f32 ? launch_x<bf16_t, 1>(a, s) : launch_x<bf16_t, 0>(a, s);
-  return a.x_f32 ? launch_x<float, 1>(a, s) : launch_x<float, 0>(a, s);
+  return dtype == DT_BF16 ? launch_w<bf16_t>(a, s) : launch_w<float>(a, s);
 }
 
 }  // namespace pdec

@@ -263,7 +263,7 @@ class Context:
         nbytes = ctypes.c_size_t()
         _check(L.pd_trace_scratch_bytes(self.model.handle, int(max_rows), ctypes.byref(nbytes)))
         rec = torch.empty(capacity * 6, dtype=torch.int32, device=self.device)
-        scratch = torch.empty(nbytes.value // 4, dtype=torch.float32, device=self.device)
+        scratch = torch.empty(nbytes.value // 8, dtype=torch.float64, device=self.device)
         _check(L.pd_ctx_set_trace(self.handle, ctypes.c_void_p(rec.data_ptr()), int(capacity),
                                   ctypes.c_void_p(scratch.data_ptr()), nbytes.value))
         self._trace = (rec, scratch)

@@ -5,8 +5,9 @@ For every evaluated row the oracle keeps (position, token, top1, lse) in
 evaluation order; its iterates give the iteration that produced each block.
 The GPU trace must list the same rows in the same order, with the same token
 and iteration, and top1 / lse within the logits tolerance (tol * max|logit|).
-A near tie on the oracle's side (margin below 2 tol max|logit|) ends the
-comparison there: past it both trajectories are valid but may differ."""
+A token that differs at a near tie on the oracle's side (margin below
+2 tol max|logit|) ends the comparison there: past it both trajectories are
+valid but may differ."""
 import dataclasses
 
 import numpy as np
@@ -53,13 +54,15 @@ def oracle_trace(res: oracle.Result, mode: str):
 
 
 def compare(got, want, tol, sentence=0):
-    """Compares until the end or the first oracle near tie; returns the rows compared."""
+    """Compares row by row until the end, or until a token differs at an
+    oracle near tie (a differing token anywhere else fails); returns the rows
+    compared."""
     n = 0
     for g, (it, pos, tok, top1, lse, margin, linf) in zip(got, want):
         assert (int(g["iteration"]), int(g["sentence"]), int(g["position"])) == (it, sentence, pos), (g, it, pos)
-        if margin < 2 * tol * linf:
+        if int(g["token"]) != tok:
+            assert margin < 2 * tol * linf, (g, tok, margin, linf)
             return n
-        assert int(g["token"]) == tok, (g, tok)
         assert abs(float(g["top1"]) - top1) <= tol * linf, (g, top1)
         assert abs(float(g["lse"]) - lse) <= tol * linf, (g, lse)
         n += 1
@@ -73,6 +76,7 @@ def compare(got, want, tol, sentence=0):
 def test_trace_matches_oracle_records(cfg, wkw):
     gm, ctx, M = build(cfg, seed=3, **wkw)
     tol = TOL[cfg.dtype]
+    rows = compared = 0
     for src in sources(cfg.vocab, 2, seed=21):
         enc = M.encode(src)
         for mode, b in MODES:
@@ -85,14 +89,46 @@ def test_trace_matches_oracle_records(cfg, wkw):
                 rec, count = ctx.trace()
                 assert count == ctx.rows_processed()
                 assert count == len(rec)
-                compare(rec, oracle_trace(want, mode), tol)
+                rows += len(want.records)
+                compared += compare(rec, oracle_trace(want, mode), tol)
+    say(f"case trace cfg={cfg.name}: {compared} of {rows} rows compared")
+    assert compared >= 0.9 * rows
+    ctx.set_trace(0, 0)
+
+
+@pytest.mark.parametrize("cfg,wkw", [(CHAIN, dict(bias_std=0.5, ln_std=0.3)),
+                                     (SMALL_PRE_BF16, dict(bias_std=0.3, ln_std=0.2))],
+                         ids=["chain_f32", "small_pre_bf16"])
+def test_batched_trace_matches_oracle_per_sentence(cfg, wkw):
+    """Iterations of more than one 16-row tile: the product kernel's argmax
+    epilogue (float) and the tiled kernel's (bf16: up to 64 rows and above 64
+    rows) also return the log-sum-exp partials; each sentence's records equal
+    the oracle's."""
+    gm, ctx, M = build(cfg, seed=7, **wkw)
+    tol = TOL[cfg.dtype]
+    srcs = sources(cfg.vocab, 4, seed=24)
+    ms = [24, 19, 24, 22]
+    rows = compared = 0
+    for B, mode, b in [(1, "jacobi", 0), (4, "jacobi", 0), (4, "gs_jacobi", 8), (4, "hybrid", 6)]:
+        say(f"case trace rows cfg={cfg.name} B={B} mode={mode} b={b}")
+        ctx.set_trace(16384, B * 24)
+        gpu_decode_batch(ctx, srcs[:B], ms[:B], mode, b)
+        rec, count = ctx.trace()
+        assert count == len(rec)
+        for s in range(B):
+            want = oracle.decode(M, M.encode(srcs[s]), ms[s], mode, b)
+            rows += len(want.records)
+            compared += compare(rec[rec["sentence"] == s], oracle_trace(want, mode), tol, sentence=s)
+    say(f"case trace rows cfg={cfg.name}: {compared} of {rows} rows compared")
+    assert compared >= 0.9 * rows
     ctx.set_trace(0, 0)
 
 
 def test_trace_changes_no_result_and_batches_agree():
     """Traced decodes return the untraced ids, k and flags; the records of a
-    batch, sentence by sentence, equal (bitwise) those of single-sentence
-    decodes."""
+    batch, sentence by sentence, equal those of single-sentence decodes
+    (top1 bitwise; lse to float rounding, its summation order following the
+    kernel that ran)."""
     gm, ctx, M = build(CHAIN, seed=4, bias_std=0.5, ln_std=0.3)
     srcs = sources(CHAIN.vocab, 3, seed=22)
     ms = [16, 11, 14]
@@ -118,7 +154,7 @@ def test_trace_changes_no_result_and_batches_agree():
             for c in cols:
                 np.testing.assert_array_equal(mine[c], one[c])
             np.testing.assert_array_equal(mine["top1"].view(np.uint32), one["top1"].view(np.uint32))
-            np.testing.assert_array_equal(mine["lse"].view(np.uint32), one["lse"].view(np.uint32))
+            np.testing.assert_allclose(mine["lse"], one["lse"], rtol=1e-6, atol=1e-6)
     ctx.set_trace(0, 0)
 
 
