@@ -213,12 +213,15 @@ pd_status pd_debug_logits(pd_ctx* ctx, const int32_t* tgt_in, int32_t T, float* 
 
 /*
  * Timing of the fused vocabulary projection + argmax kernel, the kernel that
- * moves most bytes per iteration.  With timing enabled, pd_decode records a
- * pair of HIP events on its stream around every launch of that kernel and
- * accumulates their elapsed times; pd_ctx_vocab_timing returns the number of
- * launches and their total milliseconds since the last pd_ctx_set_timing.
- * Timing adds two event records per iteration; timed iterations are launched
- * kernel by kernel instead of replaying the captured iteration graph.
+ * moves most bytes per iteration.  With timing enabled, pd_decode times every
+ * launch of that kernel with a pair of HIP events and accumulates their
+ * elapsed times; pd_ctx_vocab_timing returns the number of launches and their
+ * total milliseconds since the last pd_ctx_set_timing.  For iterations of at
+ * most 16 rows (the streaming kernel) the events carry the kernel dispatch's
+ * own start and end timestamps (hipExtLaunchKernel); for larger iterations
+ * they are recorded on the stream just before and after the launch, which
+ * adds the event markers' own time.  Timed iterations are launched kernel by
+ * kernel instead of replaying the captured iteration graph.
  * pd_ctx_set_timing also resets the counter of pd_ctx_rows_processed
  * (synchronously).
  */

@@ -199,8 +199,10 @@ hipError_t launch_gemm_tiled_cfg(int epi, int ksplit, int cfg, const GemmArgs& a
 hipError_t launch_attn(int dtype, const AttnArgs& a, int R_max, hipStream_t s);
 // Fused vocabulary projection + argmax for at most 16 rows (streaming kernel);
 // writes vocab_grid(dtype, V, d) partials per row (at most ceil(V / 64)).
+// Optional events ev0 / ev1 receive the kernel's own start and end times.
 int vocab_grid(int dtype, int V, int d);
-hipError_t launch_vocab_argmax(int dtype, const GemmArgs& a, hipStream_t s);
+hipError_t launch_vocab_argmax(int dtype, const GemmArgs& a, hipStream_t s, hipEvent_t ev0 = nullptr,
+                               hipEvent_t ev1 = nullptr);
 hipError_t launch_embed(int dtype, const EmbedArgs& a, int R_max, hipStream_t s);
 // Trace: largest logit and log-sum-exp of each of the iteration's rows (rows
 // counted on the device, at most R_max) from the argmax kernels' per-part

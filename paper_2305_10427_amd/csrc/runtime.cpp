@@ -388,19 +388,16 @@ hipError_t decoder_pass(pd_ctx& C, const Rows& r, float* logits, hipStream_t s, 
     if ((e = launch_ln(M.dt, la, r.R_max, s)) != hipSuccess) return e;
     g.x = a_buf; g.x_f32 = 0; g.ldx = d;
   }
-  if (slot >= 0 && (e = hipEventRecord(C.tv0[slot], s)) != hipSuccess) return e;
   if (r.R_max <= kVocabStreamMaxRows) {
-    e = launch_vocab_argmax(M.dt, g, s);   // one row tile: streaming kernel
-  } else if (tiled) {
-    e = launch_gemm_tiled(EPI_ARGMAX, 1, g, s);
+    // one row tile: streaming kernel, timed by its own dispatch timestamps
+    e = launch_vocab_argmax(M.dt, g, s, slot >= 0 ? C.tv0[slot] : nullptr, slot >= 0 ? C.tv1[slot] : nullptr);
   } else {
-    e = run_gemm(C, r, g, EPI_ARGMAX, true, a_buf, s);
+    if (slot >= 0 && (e = hipEventRecord(C.tv0[slot], s)) != hipSuccess) return e;
+    e = tiled ? launch_gemm_tiled(EPI_ARGMAX, 1, g, s) : run_gemm(C, r, g, EPI_ARGMAX, true, a_buf, s);
+    if (e == hipSuccess && slot >= 0) e = hipEventRecord(C.tv1[slot], s);
   }
   if (e != hipSuccess) return e;
-  if (slot >= 0) {
-    if ((e = hipEventRecord(C.tv1[slot], s)) != hipSuccess) return e;
-    C.tv_pending[slot] = true;
-  }
+  if (slot >= 0) C.tv_pending[slot] = true;
   if (C.trace != nullptr) {   // each row's largest logit and log-sum-exp from the partials
     if ((e = launch_lse_reduce(C.trace_part, g.part_ld, n_parts, r.n_dev, r.R_max, C.at<float>(C.L.row_max),
                                C.at<float>(C.L.row_lse), s)) != hipSuccess)

@@ -20,6 +20,8 @@
 // The LSE variant also keeps, per row, a running log-sum-exp of the logits it
 // streams (for the decoding trace's token probabilities), returned beside
 // the argmax partials; the logits are still never stored.
+#include <hip/hip_ext.h>
+
 #include "common.h"
 #include "kernels.h"
 #include "mma.h"
@@ -190,36 +192,43 @@ int vocab_grid(int dtype, int V, int d) {
 
 namespace {
 
-template <typename WT, int XF32, int LSE>
-hipError_t launch_x(const GemmArgs& a, hipStream_t s) {
-  const size_t lds = gemm_ln_lds_bytes(a.K, sizeof(WT));
-  const dim3 grid(vocab_grid(std::is_same<WT, bf16_t>::value ? DT_BF16 : DT_F32, a.N, a.K));
-  if constexpr (std::is_same<WT, bf16_t>::value) {
-    if (a.K > 512) {
-      hipLaunchKernelGGL((k_vocab<WT, XF32, 8, LSE>), grid, dim3(256), lds, s, a);
-      return hipGetLastError();
-    }
-  }
-  hipLaunchKernelGGL((k_vocab<WT, XF32, 4, LSE>), grid, dim3(256), lds, s, a);
+// With events, the launch records the kernel's own start and end in them
+// (hipExtLaunchKernel: timestamps of the dispatch itself, no marker packets).
+template <typename K>
+hipError_t launch_ev(K kernel, dim3 grid, size_t lds, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1,
+                     const GemmArgs& a) {
+  if (ev0 != nullptr) hipExtLaunchKernelGGL(kernel, grid, dim3(256), static_cast<uint32_t>(lds), s, ev0, ev1, 0u, a);
+  else hipLaunchKernelGGL(kernel, grid, dim3(256), lds, s, a);
   return hipGetLastError();
 }
 
+template <typename WT, int XF32, int LSE>
+hipError_t launch_x(const GemmArgs& a, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+  const size_t lds = gemm_ln_lds_bytes(a.K, sizeof(WT));
+  const dim3 grid(vocab_grid(std::is_same<WT, bf16_t>::value ? DT_BF16 : DT_F32, a.N, a.K));
+  if constexpr (std::is_same<WT, bf16_t>::value) {
+    if (a.K > 512) return launch_ev(k_vocab<WT, XF32, 8, LSE>, grid, lds, s, ev0, ev1, a);
+  }
+  return launch_ev(k_vocab<WT, XF32, 4, LSE>, grid, lds, s, ev0, ev1, a);
+}
+
 template <typename WT>
-hipError_t launch_w(const GemmArgs& a, hipStream_t s) {
-  if (a.part_lse != nullptr) return a.x_f32 ? launch_x<WT, 1, 1>(a, s) : launch_x<WT, 0, 1>(a, s);
-  return a.x_f32 ? launch_x<WT, 1, 0>(a, s) : launch_x<WT, 0, 0>(a, s);
+hipError_t launch_w(const GemmArgs& a, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+  if (a.part_lse != nullptr)
+    return a.x_f32 ? launch_x<WT, 1, 1>(a, s, ev0, ev1) : launch_x<WT, 0, 1>(a, s, ev0, ev1);
+  return a.x_f32 ? launch_x<WT, 1, 0>(a, s, ev0, ev1) : launch_x<WT, 0, 0>(a, s, ev0, ev1);
 }
 
 }  // namespace
 
-hipError_t launch_vocab_argmax(int dtype, const GemmArgs& a, hipStream_t s) {
+hipError_t launch_vocab_argmax(int dtype, const GemmArgs& a, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   if (a.n_rows <= 0) return hipSuccess;
   if (a.n_rows > 16 || a.N <= 0) return hipErrorInvalidValue;
   const int ks = dtype == DT_BF16 ? Mma<bf16_t>::KS : Mma<float>::KS;
   if (a.K % ks != 0 || a.K % 32 != 0 || a.K > (dtype == DT_BF16 ? 1024 : 512) ||
       a.part_ld < vocab_grid(dtype, a.N, a.K))
     return hipErrorInvalidValue;
-  return dtype == DT_BF16 ? launch_w<bf16_t>(a, s) : launch_w<float>(a, s);
+  return dtype == DT_BF16 ? launch_w<bf16_t>(a, s, ev0, ev1) : launch_w<float>(a, s, ev0, ev1);
 }
 
 }  // namespace pdec
