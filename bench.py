@@ -86,7 +86,42 @@ def run_mode(ctxs, sents, outs, mode, block, steps, warmup, timing=False):
     return res
 
 
-def gpu_workload(wl_name, steps, warmup, modes, headline, n_sent=0, trace=False):
+def encode_rate(ctxs, sents, cfg, steps, warmup):
+    """pd_encode of one source per call (batch 1), the step before the
+    decoding iterations: wall time per sentence over `steps` calls, against
+    the weights it must read (encoder layers and every decoder layer's
+    cross-attention K/V projection, bf16/f32 storage)."""
+    import torch
+    n = len(sents)
+    srcs = [torch.from_numpy(src[None]).cuda() for src, _ in sents]
+    torch.cuda.synchronize()
+    for i in range(warmup):
+        ctxs[i % n].encode(srcs[i % n], [len(sents[i % n][0])])
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        ctxs[i % n].encode(srcs[i % n], [len(sents[i % n][0])])
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / steps
+    es = 2 if cfg.dtype == "bf16" else 4
+    d, f = cfg.d_model, cfg.d_ff
+    wbytes = (cfg.n_enc * (4 * d * d + 2 * d * f + 9 * d + f) + cfg.n_dec * (2 * d * d + 2 * d)) * es
+    return {"us_per_sentence": 1e6 * dt, "weight_bytes": wbytes, "achieved_GBs": wbytes / dt / 1e9,
+            "frac": wbytes / dt / 1e9 / HBM_PEAK_GBS}
+
+
+def encode_only(steps, warmup):
+    import torch
+    from paper_2305_10427_amd import configs as C, pdec, synth
+    wl = C.WORKLOADS["mt_base_bf16"]
+    w, model = load_model(wl.model)
+    sents = synth.make_sentences(wl, seed=1)
+    ctx = pdec.Context(model, 1, max(len(s) for s, _ in sents), wl.tgt_cap)
+    e = encode_rate([ctx] * len(sents), sents, wl.model, steps, warmup)
+    log(f"[mt_base_bf16] encode: {e['us_per_sentence']:.1f} us/sentence, {e['achieved_GBs']:.0f} GB/s of weights")
+
+
+def gpu_workload(wl_name, steps, warmup, modes, headline, n_sent=0, trace=False, encode=False):
     import torch
     from paper_2305_10427_amd import configs as C, pdec, synth
     wl = C.WORKLOADS[wl_name]
@@ -120,6 +155,10 @@ def gpu_workload(wl_name, steps, warmup, modes, headline, n_sent=0, trace=False)
     # the throughput above comes from the pass without them)
     t = run_mode(ctxs, sents, outs, headline[0], headline[1], steps, warmup, timing=True)
     res[f"{headline[0]}_b{headline[1]}"].update(vocab_launches=t["vocab_launches"], vocab_ms=t["vocab_ms"])
+    if encode:
+        res["encode"] = encode_rate(ctxs, sents, cfg, steps, warmup)
+        e = res["encode"]
+        log(f"[{wl_name}] encode: {e['us_per_sentence']:.1f} us/sentence, {e['achieved_GBs']:.0f} GB/s of weights")
     if trace:
         # the same decodes with the DDGviz trace on (records and log-sum-exp
         # partials; iterations launched kernel by kernel)
@@ -267,6 +306,9 @@ def main():
     ap.add_argument("--no-large", action="store_true")
     ap.add_argument("--no-batched", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true")
+    ap.add_argument("--encode-only", action="store_true",
+                    help="encode the MT-base bf16 sources one by one (batch 1) and exit (profiling driver; "
+                         "prints no JSON line)")
     ap.add_argument("--batched-only", default="",
                     help="WORKLOAD:MODE:B — decode one batch of a batched workload in one mode and exit "
                          "(profiling driver; prints no JSON line)")
@@ -283,6 +325,9 @@ def main():
 
     if args.copy_calibration:
         copy_calibration()
+    if args.encode_only:
+        encode_only(args.steps, args.warmup)
+        return
     if args.batched_only:
         wl_name, mode, b = args.batched_only.split(":")
         batched_workload(wl_name, 1, [(mode, int(b))], 1)
@@ -292,15 +337,16 @@ def main():
     if headline not in modes:
         modes.append(headline)
     cfg, w, sents, model, res = gpu_workload("mt_base_bf16", args.steps, args.warmup, modes, headline,
-                                             args.sentences, trace=True)
+                                             args.sentences, trace=True, encode=True)
     traced = res.pop("trace")
+    enc = res.pop("encode")
     f32 = None
     if not args.no_f32:
         _, _, _, _, f32 = gpu_workload("mt_base_f32", args.steps, args.warmup, modes, headline, args.sentences)
     large = None
     if not args.no_large:
         _, _, _, _, large = gpu_workload("large", min(args.steps, 20), min(args.warmup, 2),
-                                         [("ar", 1), ("gs_jacobi", 16)], ("gs_jacobi", 16), 20)
+                                         [("ar", 1), ("jacobi", 0), ("gs_jacobi", 16)], ("gs_jacobi", 16), 20)
 
     batched = None
     if not args.no_batched:
@@ -351,6 +397,9 @@ def main():
         "speedup_vs_ar": (round(h["tokens_per_s"] / res["ar_b1"]["tokens_per_s"], 3) if "ar_b1" in res else None),
         "roofline": roof,
         "cpu_baseline": cpu,
+        "encode": {"us_per_sentence": round(enc["us_per_sentence"], 2), "weight_bytes": enc["weight_bytes"],
+                   "achieved": round(enc["achieved_GBs"], 1), "unit": "GB/s", "frac": round(enc["frac"], 4),
+                   "note": "pd_encode at batch 1 over the workload's sources (not in the decode timing)"},
         "trace": {"mode": traced["mode"], "tokens_per_s": round(traced["tokens_per_s"], 1),
                   "slowdown": round(h["tokens_per_s"] / traced["tokens_per_s"], 3)},
     }

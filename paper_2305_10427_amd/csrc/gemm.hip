@@ -42,6 +42,7 @@ constexpr int kDepth = 8;   // MFMA steps per weight batch; two batches are in f
 
 template <typename WT, int PRO, int EPI, int XF32, int KSPLIT, int LNT>
 __global__ __launch_bounds__(KSPLIT == 8 ? 512 : 256) void k_gemm(GemmArgs a) {
+  if constexpr (EPI == EPI_QKV) layer_select(a, blockIdx.z);
   using AT = WT;
   using XT = typename std::conditional<XF32 != 0, float, AT>::type;
   using MM = Mma<WT>;
@@ -294,13 +295,17 @@ hipError_t launch_k(GemmArgs a, int ksplit, hipStream_t s) {
   const int gy = tiles < 64 ? tiles : 64;
   a.mt_per_wg = (tiles + gy - 1) / gy;
   const size_t lds = PRO == PRO_LN ? gemm_ln_lds_bytes(a.K, sizeof(WT)) : 0;
+  const int gz = EPI == EPI_QKV && a.n_layers > 1 ? a.n_layers : 1;
   if (EPI == EPI_ARGMAX || ksplit == 1) {
-    hipLaunchKernelGGL((k_gemm<WT, PRO, EPI, XF32, 1, LNT>), dim3(gemm_grid(EPI, a.N, 1), gy), dim3(256), lds, s, a);
+    hipLaunchKernelGGL((k_gemm<WT, PRO, EPI, XF32, 1, LNT>), dim3(gemm_grid(EPI, a.N, 1), gy, gz), dim3(256), lds, s,
+                       a);
   } else if constexpr (EPI != EPI_ARGMAX) {
     if (ksplit == 8)
-      hipLaunchKernelGGL((k_gemm<WT, PRO, EPI, XF32, 8, LNT>), dim3(gemm_grid(EPI, a.N, 8), gy), dim3(512), lds, s, a);
+      hipLaunchKernelGGL((k_gemm<WT, PRO, EPI, XF32, 8, LNT>), dim3(gemm_grid(EPI, a.N, 8), gy, gz), dim3(512), lds,
+                         s, a);
     else
-      hipLaunchKernelGGL((k_gemm<WT, PRO, EPI, XF32, 4, LNT>), dim3(gemm_grid(EPI, a.N, 4), gy), dim3(256), lds, s, a);
+      hipLaunchKernelGGL((k_gemm<WT, PRO, EPI, XF32, 4, LNT>), dim3(gemm_grid(EPI, a.N, 4), gy, gz), dim3(256), lds,
+                         s, a);
   }
   return hipGetLastError();
 }

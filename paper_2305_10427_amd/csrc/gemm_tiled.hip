@@ -59,6 +59,7 @@ template <int BM, int BN, int WM, int WN> struct TileShape {
 
 template <int EPI, int BM, int BN, int WM, int WN, int NS, int KSPLIT>
 __global__ __launch_bounds__(64 * WM * WN) void k_gemm_tiled(GemmArgs a, int n_rb, int n_tiles) {
+  if constexpr (EPI == EPI_QKV) layer_select(a, blockIdx.y);
   using S = TileShape<BM, BN, WM, WN>;
   using MM = Mma<bf16_t>;
   using frag = MM::frag;
@@ -355,8 +356,9 @@ hipError_t launch_shape(const GemmArgs& a, hipStream_t s) {
   const int n_rb = (a.n_rows + BM - 1) / BM;
   const int n_tiles = n_rb * ((a.N + BN - 1) / BN);
   const size_t lds = TileShape<BM, BN, WM, WN>::LDS;
-  hipLaunchKernelGGL((k_gemm_tiled<EPI, BM, BN, WM, WN, NS, KSPLIT>), dim3(n_tiles), dim3(64 * WM * WN), lds, s, a, n_rb,
-                     n_tiles);
+  const int gy = EPI == EPI_QKV && a.n_layers > 1 ? a.n_layers : 1;
+  hipLaunchKernelGGL((k_gemm_tiled<EPI, BM, BN, WM, WN, NS, KSPLIT>), dim3(n_tiles, gy), dim3(64 * WM * WN), lds, s, a,
+                     n_rb, n_tiles);
   return hipGetLastError();
 }
 

@@ -33,6 +33,8 @@ enum Epilogue {
   EPI_LOGITS = 5,  // out_f32 = scale * acc + bias (verification only)
 };
 
+constexpr int kMaxLayers = 16;   // layers of one multi-layer product launch
+
 struct GemmArgs {
   const int* n_rows_dev;   // row count read on device (nullptr: n_rows is exact)
   int n_rows;              // launch bound on the rows (rows >= the device count are discarded)
@@ -69,7 +71,33 @@ struct GemmArgs {
   // argmax epilogues, optional: [row][part_ld] = (max, sum of exp(logit - max))
   // over the same columns as partials (finite logits only)
   float2* part_lse;
+  // EPI_QKV of several layers in one launch (n_layers > 1; the last grid
+  // dimension indexes the layer): layer z reads lw[z], lb[z] and writes the
+  // caches kc / vc + z * kv_stride bytes
+  int n_layers;
+  long long kv_stride;
+  const void* lw[kMaxLayers];
+  const void* lb[kMaxLayers];
 };
+
+// The weights and caches of layer z of a multi-layer EPI_QKV launch.  The
+// tables are read with constant indices only (a selection chain on the
+// uniform z): indexing them with z would copy the argument block to scratch.
+__device__ __forceinline__ void layer_select(GemmArgs& a, int z) {
+  if (a.n_layers > 1) {
+    const void* w = a.lw[0];
+    const void* b = a.lb[0];
+#pragma unroll
+    for (int i = 1; i < kMaxLayers; ++i) {
+      w = z == i ? a.lw[i] : w;
+      b = z == i ? a.lb[i] : b;
+    }
+    a.w = w;
+    a.bias = b;
+    a.kc = static_cast<char*>(a.kc) + z * a.kv_stride;
+    a.vc = static_cast<char*>(a.vc) + z * a.kv_stride;
+  }
+}
 
 struct AttnArgs {
   const int* n_rows_dev;

@@ -409,12 +409,6 @@ hipError_t decoder_pass(pd_ctx& C, const Rows& r, float* logits, hipStream_t s, 
   return launch_argmax_reduce(ra, r.R_max, s);
 }
 
-// Encoder products (no prologue): the tiled kernel for many rows.
-hipError_t enc_gemm(const pd_model& M, int epi, int ksplit, const GemmArgs& g, hipStream_t s) {
-  if (g.n_rows > kTiledMinRows && gemm_tiled_ok(M.dt, PRO_NONE, g)) return launch_gemm_tiled(epi, ksplit, g, s);
-  return launch_gemm(M.dt, PRO_NONE, epi, ksplit, g, s);
-}
-
 hipError_t encoder_pass(pd_ctx& C, const int32_t* src, int B, int n_max, hipStream_t s) {
   const pd_model& M = *C.M;
   const pd_config& cfg = M.cfg;
@@ -435,63 +429,76 @@ hipError_t encoder_pass(pd_ctx& C, const int32_t* src, int B, int n_max, hipStre
 
   EmbedArgs ea{nullptr, R, src, r.map, M.w[0], C.at<float>(C.L.pe), M.enc_scale, d, M.V, x_res};
   if ((e = launch_embed(M.dt, ea, R, s)) != hipSuccess) return e;
+  // Every LayerNorm feeding a product runs in that product's prologue (a
+  // separate kernel above 64 rows, run_gemm); post-LN stores the normalised
+  // rows to x_res as the next residual.
   for (int l = 0; l < cfg.n_enc; ++l) {
-    const void* in = x_res;
-    if (pre) {
-      LnArgs la{nullptr, R, x_res, 0, M.enc(l, E_LN1G), M.enc(l, E_LN1B), cfg.ln_eps, d, a_buf};
-      if ((e = launch_ln(M.dt, la, R, s)) != hipSuccess) return e;
-      in = a_buf;
-    }
     GemmArgs g = gemm_base(r);
-    g.x = in; g.ldx = d; g.w = M.enc(l, E_WQKV); g.bias = M.enc(l, E_BQKV); g.N = 3 * d; g.K = d;
+    bool ln = true;
+    void* ln_tmp = a_buf;
+    if (pre) {
+      g.x = x_res; g.x_f32 = 0; g.ln_g = M.enc(l, E_LN1G); g.ln_b = M.enc(l, E_LN1B);
+    } else if (l > 0) {
+      g.x = s_buf; g.x_f32 = 1; g.ln_g = M.enc(l - 1, E_LN2G); g.ln_b = M.enc(l - 1, E_LN2B);
+      g.ln_out = x_res; g.ldlo = d; ln_tmp = x_res;
+    } else {
+      g.x = x_res; g.x_f32 = 0; ln = false;   // the embedding
+    }
+    g.ldx = d; g.ln_eps = cfg.ln_eps;
+    g.w = M.enc(l, E_WQKV); g.bias = M.enc(l, E_BQKV); g.N = 3 * d; g.K = d;
     g.out_f32 = q_buf; g.ldo = d; g.q_cols = d;
     g.kc = C.at<char>(C.L.enc_k); g.vc = C.at<char>(C.L.enc_v);
     g.H = M.H; g.dh = M.dh; g.T = C.max_src; g.d = d;
-    if ((e = enc_gemm(M, EPI_QKV, 4, g, s)) != hipSuccess) return e;
+    if ((e = run_gemm(C, r, g, EPI_QKV, ln, ln_tmp, s)) != hipSuccess) return e;
     AttnArgs aa{nullptr, R, q_buf, d, g.kc, g.vc, M.H, M.dh, C.max_src, r.map, 0, klen, a_buf, d, scale};
     if ((e = launch_attn(M.dt, aa, R, s)) != hipSuccess) return e;
     g = gemm_base(r);
     g.x = a_buf; g.ldx = d; g.w = M.enc(l, E_WO); g.bias = M.enc(l, E_BO); g.N = d; g.K = d;
     g.resid = x_res; g.ldr = d; g.ldo = d;
     if (pre) g.out = x_res; else g.out_f32 = s_buf;
-    if ((e = enc_gemm(M, EPI_RESID, 4, g, s)) != hipSuccess) return e;
-    if (!pre) {
-      LnArgs la{nullptr, R, s_buf, 1, M.enc(l, E_LN1G), M.enc(l, E_LN1B), cfg.ln_eps, d, x_res};
-      if ((e = launch_ln(M.dt, la, R, s)) != hipSuccess) return e;
-    }
-    in = x_res;
-    if (pre) {
-      LnArgs la{nullptr, R, x_res, 0, M.enc(l, E_LN2G), M.enc(l, E_LN2B), cfg.ln_eps, d, a_buf};
-      if ((e = launch_ln(M.dt, la, R, s)) != hipSuccess) return e;
-      in = a_buf;
-    }
+    if ((e = run_gemm(C, r, g, EPI_RESID, false, nullptr, s)) != hipSuccess) return e;
     g = gemm_base(r);
-    g.x = in; g.ldx = d; g.w = M.enc(l, E_W1); g.bias = M.enc(l, E_B1); g.N = M.dff; g.K = d;
+    if (pre) {
+      g.x = x_res; g.x_f32 = 0; g.ln_g = M.enc(l, E_LN2G); g.ln_b = M.enc(l, E_LN2B);
+      ln_tmp = a_buf;
+    } else {
+      g.x = s_buf; g.x_f32 = 1; g.ln_g = M.enc(l, E_LN1G); g.ln_b = M.enc(l, E_LN1B);
+      g.ln_out = x_res; g.ldlo = d; ln_tmp = x_res;
+    }
+    g.ldx = d; g.ln_eps = cfg.ln_eps;
+    g.w = M.enc(l, E_W1); g.bias = M.enc(l, E_B1); g.N = M.dff; g.K = d;
     g.out = h_buf; g.ldo = M.dff; g.act = cfg.act_gelu ? 2 : 1;
-    if ((e = enc_gemm(M, EPI_ACT, 4, g, s)) != hipSuccess) return e;
+    if ((e = run_gemm(C, r, g, EPI_ACT, true, ln_tmp, s)) != hipSuccess) return e;
     g = gemm_base(r);
     g.x = h_buf; g.ldx = M.dff; g.w = M.enc(l, E_W2); g.bias = M.enc(l, E_B2); g.N = d; g.K = M.dff;
     g.resid = x_res; g.ldr = d; g.ldo = d;
     if (pre) g.out = x_res; else g.out_f32 = s_buf;
-    if ((e = enc_gemm(M, EPI_RESID, g.K >= 2048 ? 8 : 4, g, s)) != hipSuccess) return e;
-    if (!pre) {
-      LnArgs la{nullptr, R, s_buf, 1, M.enc(l, E_LN2G), M.enc(l, E_LN2B), cfg.ln_eps, d, x_res};
-      if ((e = launch_ln(M.dt, la, R, s)) != hipSuccess) return e;
-    }
+    if ((e = run_gemm(C, r, g, EPI_RESID, false, nullptr, s)) != hipSuccess) return e;
   }
-  const void* mem = x_res;
-  if (pre) {
-    LnArgs la{nullptr, R, x_res, 0, M.enc_ln(0), M.enc_ln(1), cfg.ln_eps, d, a_buf};
+  // the memory: the last LayerNorm (post-LN: the last layer's second; pre-LN:
+  // the encoder's final one), stored once for every cross-attention product
+  const void* mem = pre ? a_buf : x_res;
+  {
+    LnArgs la = pre ? LnArgs{nullptr, R, x_res, 0, M.enc_ln(0), M.enc_ln(1), cfg.ln_eps, d, a_buf}
+                    : LnArgs{nullptr, R, s_buf, 1, M.enc(cfg.n_enc - 1, E_LN2G), M.enc(cfg.n_enc - 1, E_LN2B),
+                             cfg.ln_eps, d, x_res};
     if ((e = launch_ln(M.dt, la, R, s)) != hipSuccess) return e;
-    mem = a_buf;
   }
-  for (int l = 0; l < cfg.n_dec; ++l) {
+  // cross-attention K / V of every decoder layer, up to kMaxLayers layers per launch
+  for (int l0 = 0; l0 < cfg.n_dec; l0 += kMaxLayers) {
+    const int nl = std::min(kMaxLayers, cfg.n_dec - l0);
     GemmArgs g = gemm_base(r);
-    g.x = mem; g.ldx = d; g.w = M.dec(l, D_CWKV); g.bias = M.dec(l, D_CBKV); g.N = 2 * d; g.K = d;
+    g.x = mem; g.ldx = d; g.w = M.dec(l0, D_CWKV); g.bias = M.dec(l0, D_CBKV); g.N = 2 * d; g.K = d;
     g.q_cols = 0;
-    g.kc = C.at<char>(C.L.cross_k) + l * cross_layer; g.vc = C.at<char>(C.L.cross_v) + l * cross_layer;
+    g.kc = C.at<char>(C.L.cross_k) + l0 * cross_layer; g.vc = C.at<char>(C.L.cross_v) + l0 * cross_layer;
     g.H = M.H; g.dh = M.dh; g.T = C.max_src; g.d = d;
-    if ((e = enc_gemm(M, EPI_QKV, 4, g, s)) != hipSuccess) return e;
+    g.n_layers = nl;
+    g.kv_stride = static_cast<long long>(cross_layer);
+    for (int z = 0; z < nl; ++z) {
+      g.lw[z] = M.dec(l0 + z, D_CWKV);
+      g.lb[z] = M.dec(l0 + z, D_CBKV);
+    }
+    if ((e = run_gemm(C, r, g, EPI_QKV, false, nullptr, s)) != hipSuccess) return e;
   }
   return hipSuccess;
 }
