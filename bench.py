@@ -371,6 +371,15 @@ def main():
             "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(),
             "avg_launch_us": round(avg_ms * 1e3, 2), "launches": h["vocab_launches"],
             "bytes_per_launch": bytes_per_launch}
+    # the whole batch-1 iteration against the bytes it must move: decoder
+    # weights + vocabulary (the K/V cache reads are a few hundred KB)
+    d, f, L = cfg.d_model, cfg.d_ff, cfg.n_dec
+    iter_bytes = (L * (6 * d * d + 2 * d * f + 13 * d + f) + cfg.vocab * (d + 1)) * 2
+    iter_us = 1e6 * h["seconds"] / h["k"]
+    iteration = {"us": round(iter_us, 2), "bytes": iter_bytes, "achieved": round(iter_bytes / iter_us / 1e3, 1),
+                 "unit": "GB/s", "frac": round(iter_bytes / iter_us / 1e3 / HBM_PEAK_GBS, 4),
+                 "note": "one decoding iteration (every kernel of the decoder pass, vocabulary and control step) "
+                         "at batch 1: latency-bound"}
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(cfg, w, sents, headline[0], headline[1], args.cpu_seconds)
@@ -396,6 +405,7 @@ def main():
                       "ms_per_sentence": round(v["ms_per_step"], 4)} for k, v in res.items()},
         "speedup_vs_ar": (round(h["tokens_per_s"] / res["ar_b1"]["tokens_per_s"], 3) if "ar_b1" in res else None),
         "roofline": roof,
+        "iteration_roofline": iteration,
         "cpu_baseline": cpu,
         "encode": {"us_per_sentence": round(enc["us_per_sentence"], 2), "weight_bytes": enc["weight_bytes"],
                    "achieved": round(enc["achieved_GBs"], 1), "unit": "GB/s", "frac": round(enc["frac"], 4),

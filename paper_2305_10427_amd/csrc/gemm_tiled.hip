@@ -367,8 +367,11 @@ hipError_t launch_shape(const GemmArgs& a, hipStream_t s) {
 // vocabulary argmax above 64 rows: 712 TFLOP/s at 1024 rows); 1: 64 x 64,
 // 2 x 2 waves, 4 sets (decoder products: many workgroups for N of 1-4 K
 // columns); 2: 64 x 128, 2 x 2 waves, 3 sets (the vocabulary argmax of
-// 17-64 rows: 94 us for 250,027 x 1024 at 64 rows).
-constexpr int kTileCfgs = 3;
+// 17-64 rows: 94 us for 250,027 x 1024 at 64 rows); 3: 32 x 64 and 4: 32 x 32,
+// 2 x 2 waves, 4 sets (decoder products of a few hundred rows).  Every
+// configuration accumulates each output element in the same order, so all
+// give bitwise the same products.
+constexpr int kTileCfgs = 5;
 
 template <int EPI, int KSPLIT>
 hipError_t launch_k(const GemmArgs& a, int cfg, hipStream_t s) {
@@ -376,13 +379,20 @@ hipError_t launch_k(const GemmArgs& a, int cfg, hipStream_t s) {
     case 0: return launch_shape<EPI, 128, 128, 2, 2, 2, KSPLIT>(a, s);
     case 1: return launch_shape<EPI, 64, 64, 2, 2, 4, KSPLIT>(a, s);
     case 2: return launch_shape<EPI, 64, 128, 2, 2, 3, KSPLIT>(a, s);
+    case 3:
+    case 4:
+      if constexpr (EPI != EPI_ARGMAX && EPI != EPI_LOGITS) {
+        if (cfg == 3) return launch_shape<EPI, 32, 64, 2, 2, 4, KSPLIT>(a, s);
+        return launch_shape<EPI, 32, 32, 2, 2, 4, KSPLIT>(a, s);
+      }
+      return hipErrorInvalidValue;
     default: return hipErrorInvalidValue;
   }
 }
 
 template <int EPI, int KSPLIT>
 void init_k() {
-  allow_lds<EPI, 128, 128, 2, 2, 2, KSPLIT>();
+  allow_lds<EPI, 128, 128, 2, 2, 2, KSPLIT>();   // the smaller tiles fit the default LDS limit
   allow_lds<EPI, 64, 64, 2, 2, 4, KSPLIT>();
   allow_lds<EPI, 64, 128, 2, 2, 3, KSPLIT>();
 }
@@ -398,7 +408,7 @@ hipError_t launch_e(const GemmArgs& a, int ksplit, int cfg, hipStream_t s) {
   }
 }
 
-int tile_bn(int cfg) { return cfg == 1 ? 64 : 128; }
+int tile_bn(int cfg) { return cfg == 1 || cfg == 3 ? 64 : (cfg == 4 ? 32 : 128); }
 
 }  // namespace
 
@@ -419,9 +429,14 @@ void gemm_tiled_init() {
 // vocabulary argmax keeps 128-column tiles (its partial count depends only
 // on N).
 int gemm_tiled_cfg(int epi, int N, int rows) {
-  (void)N;
   if (epi == EPI_ARGMAX || epi == EPI_LOGITS) return rows > 64 ? 0 : 2;
-  return 1;
+  // decoder products: the largest tile that still gives 1024 workgroups (a
+  // few per CU), else 32 x 32 (measured at 100, 200, 631 and 1024 rows, N of
+  // 512-4096: the smaller tiles win whenever the larger ones leave CUs idle)
+  const auto wgs = [&](int bm, int bn) { return ((rows + bm - 1) / bm) * ((N + bn - 1) / bn); };
+  if (wgs(64, 64) >= 1024) return 1;
+  if (wgs(32, 64) >= 1024) return 3;
+  return 4;
 }
 
 int gemm_tiled_bn(int epi, int N, int rows) { return tile_bn(gemm_tiled_cfg(epi, N, rows)); }
