@@ -379,13 +379,8 @@ hipError_t launch_k(const GemmArgs& a, int cfg, hipStream_t s) {
     case 0: return launch_shape<EPI, 128, 128, 2, 2, 2, KSPLIT>(a, s);
     case 1: return launch_shape<EPI, 64, 64, 2, 2, 4, KSPLIT>(a, s);
     case 2: return launch_shape<EPI, 64, 128, 2, 2, 3, KSPLIT>(a, s);
-    case 3:
-    case 4:
-      if constexpr (EPI != EPI_ARGMAX && EPI != EPI_LOGITS) {
-        if (cfg == 3) return launch_shape<EPI, 32, 64, 2, 2, 4, KSPLIT>(a, s);
-        return launch_shape<EPI, 32, 32, 2, 2, 4, KSPLIT>(a, s);
-      }
-      return hipErrorInvalidValue;
+    case 3: return launch_shape<EPI, 32, 64, 2, 2, 4, KSPLIT>(a, s);
+    case 4: return launch_shape<EPI, 32, 32, 2, 2, 4, KSPLIT>(a, s);
     default: return hipErrorInvalidValue;
   }
 }
@@ -429,7 +424,11 @@ void gemm_tiled_init() {
 // vocabulary argmax keeps 128-column tiles (its partial count depends only
 // on N).
 int gemm_tiled_cfg(int epi, int N, int rows) {
-  if (epi == EPI_ARGMAX || epi == EPI_LOGITS) return rows > 64 ? 0 : 2;
+  if (epi == EPI_ARGMAX || epi == EPI_LOGITS) {
+    // 128- or 64-row tiles (128 columns), whichever pads the rows less (ties: 128)
+    const int pad128 = (rows + 127) / 128 * 128, pad64 = (rows + 63) / 64 * 64;
+    return rows > 64 && pad128 <= pad64 ? 0 : 2;
+  }
   // decoder products: the largest tile that still gives 1024 workgroups (a
   // few per CU), else 32 x 32 (measured at 100, 200, 631 and 1024 rows, N of
   // 512-4096: the smaller tiles win whenever the larger ones leave CUs idle)
@@ -451,7 +450,8 @@ bool gemm_tiled_ok(int dtype, int pro, const GemmArgs& a) {
 hipError_t launch_gemm_tiled_cfg(int epi, int ksplit, int cfg, const GemmArgs& a, hipStream_t s) {
   if (a.n_rows <= 0) return hipSuccess;
   if (a.K % kBK != 0 || a.x_f32 || cfg < 0 || cfg >= kTileCfgs) return hipErrorInvalidValue;
-  if ((epi == EPI_ARGMAX || epi == EPI_LOGITS) && tile_bn(cfg) != 128) return hipErrorInvalidValue;
+  // the argmax partials are laid out per column tile: at most ceil(N / 32) per row
+  if (epi == EPI_ARGMAX && a.part_ld < (a.N + tile_bn(cfg) - 1) / tile_bn(cfg)) return hipErrorInvalidValue;
   switch (epi) {
     case EPI_F32: return launch_e<EPI_F32>(a, ksplit, cfg, s);
     case EPI_ACT: return launch_e<EPI_ACT>(a, ksplit, cfg, s);
