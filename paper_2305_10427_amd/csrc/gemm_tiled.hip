@@ -368,10 +368,11 @@ hipError_t launch_shape(const GemmArgs& a, hipStream_t s) {
 // 2 x 2 waves, 4 sets (decoder products: many workgroups for N of 1-4 K
 // columns); 2: 64 x 128, 2 x 2 waves, 3 sets (the vocabulary argmax of
 // 17-64 rows: 94 us for 250,027 x 1024 at 64 rows); 3: 32 x 64 and 4: 32 x 32,
-// 2 x 2 waves, 4 sets (decoder products of a few hundred rows).  Every
+// 2 x 2 waves, 4 sets (decoder products of a few hundred rows); 5: 32 x 128,
+// 2 x 2 waves, 3 sets (the vocabulary argmax of 17-32 rows).  Every
 // configuration accumulates each output element in the same order, so all
 // give bitwise the same products.
-constexpr int kTileCfgs = 5;
+constexpr int kTileCfgs = 6;
 
 template <int EPI, int KSPLIT>
 hipError_t launch_k(const GemmArgs& a, int cfg, hipStream_t s) {
@@ -381,6 +382,7 @@ hipError_t launch_k(const GemmArgs& a, int cfg, hipStream_t s) {
     case 2: return launch_shape<EPI, 64, 128, 2, 2, 3, KSPLIT>(a, s);
     case 3: return launch_shape<EPI, 32, 64, 2, 2, 4, KSPLIT>(a, s);
     case 4: return launch_shape<EPI, 32, 32, 2, 2, 4, KSPLIT>(a, s);
+    case 5: return launch_shape<EPI, 32, 128, 2, 2, 3, KSPLIT>(a, s);
     default: return hipErrorInvalidValue;
   }
 }
@@ -403,7 +405,7 @@ hipError_t launch_e(const GemmArgs& a, int ksplit, int cfg, hipStream_t s) {
   }
 }
 
-int tile_bn(int cfg) { return cfg == 1 || cfg == 3 ? 64 : (cfg == 4 ? 32 : 128); }
+int tile_bn(int cfg) { return cfg == 1 || cfg == 3 ? 64 : (cfg == 4 ? 32 : 128); }   // 0, 2, 5: 128
 
 }  // namespace
 
@@ -425,7 +427,9 @@ void gemm_tiled_init() {
 // on N).
 int gemm_tiled_cfg(int epi, int N, int rows) {
   if (epi == EPI_ARGMAX || epi == EPI_LOGITS) {
-    // 128- or 64-row tiles (128 columns), whichever pads the rows less (ties: 128)
+    // 128 columns; 32 rows up to 32 rows, then 128- or 64-row tiles,
+    // whichever pads the rows less (ties: 128)
+    if (rows <= 32) return 5;
     const int pad128 = (rows + 127) / 128 * 128, pad64 = (rows + 63) / 64 * 64;
     return rows > 64 && pad128 <= pad64 ? 0 : 2;
   }

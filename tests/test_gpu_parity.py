@@ -268,6 +268,16 @@ def test_large_sampled_sentence():
     say("large", summarize(labels))
 
 
+def test_more_decoder_layers_than_one_cross_kv_launch_holds():
+    """17 decoder layers: the cross-attention K/V products of pd_encode run as
+    a 16-layer launch and a 1-layer launch; decodes still match the oracle."""
+    cfg = dataclasses.replace(C.TINY, name="deep17", n_enc=1, n_dec=17)
+    _, _, ctx, M = build(cfg, seed=8, bias_std=0.3, ln_std=0.2)
+    labels = run_modes(cfg, ctx, M, sources(cfg.vocab, 2, seed=15), 12,
+                       [("ar", 1), ("jacobi", 0), ("gs_jacobi", 4), ("hybrid", 3)], TOL[cfg.dtype])
+    say(f"deep17: {summarize(labels)}")
+
+
 def test_rows_processed_counts_block_positions():
     """The device row counter equals the positions the oracle's iterations
     evaluated: k for greedy, the sum of the block lengths of every iteration for
