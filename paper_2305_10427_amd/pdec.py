@@ -271,6 +271,8 @@ class Context:
     def trace(self):
         """Records appended since set_trace, as a numpy structured array
         (fields of TRACE_DTYPE), and the full count (may exceed capacity)."""
+        if getattr(self, "_trace", None) is None:
+            raise PdError(6, "tracing is off: call set_trace first")
         n = ctypes.c_int64()
         _check(load_library().pd_ctx_trace_count(self.handle, ctypes.byref(n)))
         rec = self._trace[0]
