@@ -372,6 +372,106 @@ __global__ __launch_bounds__(1024) void k_ctrl_step(CtrlArgs a) {
   emit_rows<WT>(a);
 }
 
+// The control step with one thread per row instead of one per sentence (up
+// to 1024 sentences; k_ctrl_step above is the fallback for more): the rows'
+// loads go out together rather than one block position after another.  The
+// per-sentence results of Eq. (3) (changed, [EOS], non-finite) are gathered
+// with LDS atomic ORs, the states advance exactly as in k_ctrl_step
+// (advance_state), the next layout's first rows come from a prefix sum over
+// the sentences, and the next rows are written one thread per row.
+constexpr int kCtrlRowsMaxB = 1024;
+
+template <typename WT>
+__global__ __launch_bounds__(1024) void k_ctrl_rows(CtrlArgs a) {
+  __shared__ int s_acc[kCtrlRowsMaxB];         // bit 0 changed, bit 1 [EOS], bit 2 non-finite
+  __shared__ int s_k[kCtrlRowsMaxB];           // iterations so far (trace)
+  __shared__ int s_i[kCtrlRowsMaxB];           // next block start
+  __shared__ int s_scan[2][kCtrlRowsMaxB + 1]; // next block lengths -> first rows (exclusive prefix)
+  const int tid = threadIdx.x;
+  const int R = *a.n_rows;
+  if (R == 0) return;                          // workgroup-uniform: the decode had already finished
+  if (a.partials != nullptr)
+    reduce_rows(a.partials, a.part_ld, a.n_parts, R, const_cast<int*>(a.new_tok), const_cast<int*>(a.row_flags));
+  SentState st;
+  const bool sent = tid < a.B;
+  if (sent) {
+    st = a.st[tid];
+    s_acc[tid] = 0;
+    s_k[tid] = st.k;
+  }
+  __syncthreads();
+  const unsigned long long tbase = a.trace != nullptr ? *a.trace_count : 0ull;
+  for (int row = tid; row < R; row += blockDim.x) {
+    const int s = a.row_sent[row], p = a.row_pos[row];
+    const int t = a.new_tok[row];
+    int* yp = a.y + static_cast<size_t>(s) * a.ldy + p;
+    const int bits = (*yp != t ? 1 : 0) | (t == a.eos_id ? 2 : 0) | (a.row_flags[row] != 0 ? 4 : 0);
+    *yp = t;
+    if (bits != 0) atomicOr(&s_acc[s], bits);
+    if (a.trace != nullptr) trace_row(a, tbase, row, s_k[s] + 1, s, p, t);
+  }
+  __syncthreads();
+  int len = 0;
+  if (sent) {
+    if (!st.done) {
+      const int acc = s_acc[tid];
+      advance_state(a, st, (acc & 1) != 0, (acc & 2) != 0, (acc & 4) ? 1 : 0);
+    }
+    len = st.done ? 0 : st.L;
+    s_i[tid] = st.i;
+    s_scan[0][tid + 1] = len;
+  }
+  if (tid == 0) s_scan[0][0] = 0;
+  __syncthreads();
+  // inclusive scan of s_scan[.][1..B] (Hillis-Steele), s_scan[.][0] = 0
+  int src = 0;
+  for (int off = 1; off < a.B; off <<= 1) {
+    if (tid < a.B) {
+      const int v = s_scan[src][tid + 1];
+      s_scan[src ^ 1][tid + 1] = tid >= off ? v + s_scan[src][tid + 1 - off] : v;
+    }
+    if (tid == 0) s_scan[src ^ 1][0] = 0;
+    __syncthreads();
+    src ^= 1;
+  }
+  const int* first = s_scan[src];               // first[s] = first row of sentence s, first[B] = total
+  if (sent) {
+    st.row0 = first[tid];
+    a.st[tid] = st;
+  }
+  const int total = first[a.B];
+  for (int row = tid; row < total; row += blockDim.x) {
+    int lo = 0, hi = a.B - 1;                    // the sentence s with first[s] <= row < first[s + 1]
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (first[mid] <= row) lo = mid;
+      else hi = mid - 1;
+    }
+    const int p = s_i[lo] + (row - first[lo]);
+    a.row_sent[row] = lo;
+    a.row_pos[row] = p;
+    a.row_tok[row] = p == 0 ? a.bos_id : a.y[static_cast<size_t>(lo) * a.ldy + p - 1];
+  }
+  if (tid == 0) {
+    if (a.trace != nullptr) *a.trace_count += static_cast<unsigned long long>(R);
+    *a.n_rows = total;
+    if (a.rows_total != nullptr) *a.rows_total += static_cast<unsigned long long>(total);
+    if (a.host_done != nullptr)
+      __hip_atomic_store(a.host_done, total == 0 ? 1 : 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  }
+  if (a.x_out != nullptr) {
+    __syncthreads();
+    const size_t n = static_cast<size_t>(total) * a.d;
+    for (size_t t = tid; t < n; t += blockDim.x) {
+      const int row = static_cast<int>(t / a.d);
+      const int c = static_cast<int>(t - static_cast<size_t>(row) * a.d);
+      Elt<WT>::store(static_cast<WT*>(a.x_out), t,
+                     embed_elem<WT>(static_cast<const WT*>(a.emb), a.pe, a.row_tok[row], a.row_pos[row], c, a.d,
+                                    a.emb_scale, a.vocab));
+    }
+  }
+}
+
 // The control step of iterations of at most 64 rows (so at most 64
 // sentences and blocks of at most 64 positions), with everything that does
 // not leave the workgroup kept in LDS: the sentence states, the new tokens,
@@ -602,6 +702,11 @@ hipError_t launch_ctrl_step(int dtype, const CtrlArgs& a, hipStream_t s) {
   if (small) {
     if (dtype == DT_BF16) hipLaunchKernelGGL(k_ctrl_small<bf16_t>, dim3(1), dim3(1024), 0, s, a);
     else hipLaunchKernelGGL(k_ctrl_small<float>, dim3(1), dim3(1024), 0, s, a);
+    return hipGetLastError();
+  }
+  if (a.B <= kCtrlRowsMaxB) {
+    if (dtype == DT_BF16) hipLaunchKernelGGL(k_ctrl_rows<bf16_t>, dim3(1), dim3(1024), 0, s, a);
+    else hipLaunchKernelGGL(k_ctrl_rows<float>, dim3(1), dim3(1024), 0, s, a);
     return hipGetLastError();
   }
   if (dtype == DT_BF16) hipLaunchKernelGGL(k_ctrl_step<bf16_t>, dim3(1), dim3(1024), 0, s, a);
