@@ -26,13 +26,14 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   __shared__ AttnScratch s_scr[4];
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = threadIdx.x / kWave;
-  const int R = a.n_rows_dev ? *a.n_rows_dev : a.n_rows;
   const int idx = blockIdx.x * 4 + wave;
   const int row = idx / a.H;
   const int hh = idx - row * a.H;
-  if (row >= R) return;   // whole wave; no workgroup barrier below
-  // the query first (it does not depend on the row's placement), then the
-  // first chunk's keys
+  if (row >= a.rows_max) return;         // padding waves of the last workgroup; no workgroup barrier below
+  // the device row count, the query and the row's placement go out together
+  // (rows below the launch bound have valid query and placement slots); rows
+  // at or past the count leave before touching the keys
+  const int R = a.n_rows_dev ? *a.n_rows_dev : a.n_rows;
   const float* q = a.q + static_cast<size_t>(row) * a.ldq + hh * DH;
   float qv[(DH + kWave - 1) / kWave];
 #pragma unroll
@@ -42,6 +43,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   }
   int s, p;
   row_place(a.rows, row, s, p);
+  if (row >= R) return;
   const int nk = a.causal ? p + 1 : a.klen[s];
   const size_t base = (static_cast<size_t>(s) * a.H + hh) * a.T * DH;
   const AT* Kb = static_cast<const AT*>(a.kc) + base;
@@ -633,10 +635,12 @@ static hipError_t launch_attn_t(const AttnArgs& a, int grid, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_attn(int dtype, const AttnArgs& a, int R_max, hipStream_t s) {
-  if (a.dh > kMaxHeadDim || a.T > kMaxKeys) return hipErrorInvalidValue;
-  const int grid = (R_max * a.H + 3) / 4;
+hipError_t launch_attn(int dtype, const AttnArgs& args, int R_max, hipStream_t s) {
+  if (args.dh > kMaxHeadDim || args.T > kMaxKeys) return hipErrorInvalidValue;
+  const int grid = (R_max * args.H + 3) / 4;
   if (grid == 0) return hipSuccess;
+  AttnArgs a = args;
+  a.rows_max = R_max;
   return dtype == DT_BF16 ? launch_attn_t<bf16_t>(a, grid, s) : launch_attn_t<float>(a, grid, s);
 }
 

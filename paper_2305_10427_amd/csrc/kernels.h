@@ -113,6 +113,7 @@ struct AttnArgs {
   void* out;               // [R][ldo] storage type
   int ldo;
   float scale;             // 1/sqrt(dh)
+  int rows_max;            // launch bound on the rows (set by launch_attn)
 };
 
 struct EmbedArgs {
