@@ -191,11 +191,11 @@ struct pd_ctx {
   int* host_done_dev;     // device view of host_pinned[0]
   int* stage_src;         // pinned staging copies of host length arrays
   int* stage_tgt;
-  hipEvent_t stage_ev;
+  hipEvent_t stage_ev = nullptr;
   std::vector<hipEvent_t> it_ev;
   // vocabulary-kernel timing: event pairs per in-flight iteration slot
   bool timing = false;
-  hipEvent_t tv0[2], tv1[2];
+  hipEvent_t tv0[2] = {nullptr, nullptr}, tv1[2] = {nullptr, nullptr};
   bool tv_pending[2] = {false, false};
   int64_t tv_launches = 0;
   double tv_ms = 0.0;
@@ -648,15 +648,16 @@ pd_status pd_ctx_create(const pd_model* model, int32_t max_batch, int32_t max_sr
   }
   c->stage_src = c->host_pinned + 1;
   c->stage_tgt = c->host_pinned + 1 + max_batch;
-  hipEventCreateWithFlags(&c->stage_ev, hipEventDisableTiming);
-  c->it_ev.resize(2);
-  for (auto& ev : c->it_ev) hipEventCreateWithFlags(&ev, hipEventDisableTiming);
-  for (int i = 0; i < 2; ++i) {
-    hipEventCreate(&c->tv0[i]);
-    hipEventCreate(&c->tv1[i]);
+  c->it_ev.resize(2, nullptr);
+  e = hipEventCreateWithFlags(&c->stage_ev, hipEventDisableTiming);
+  for (auto& ev : c->it_ev)
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+  for (int i = 0; i < 2 && e == hipSuccess; ++i) {
+    e = hipEventCreate(&c->tv0[i]);
+    if (e == hipSuccess) e = hipEventCreate(&c->tv1[i]);
   }
-  hipStreamCreateWithFlags(&c->capture, hipStreamNonBlocking);
-  e = hipMemset(c->at<unsigned long long>(c->L.rows_total), 0, sizeof(unsigned long long));
+  if (e == hipSuccess) e = hipStreamCreateWithFlags(&c->capture, hipStreamNonBlocking);
+  if (e == hipSuccess) e = hipMemset(c->at<unsigned long long>(c->L.rows_total), 0, sizeof(unsigned long long));
   if (e == hipSuccess) e = launch_pe_table(c->at<float>(c->L.pe), std::max(max_src, max_tgt), model->d, nullptr);
   if (e == hipSuccess) e = hipDeviceSynchronize();
   if (e != hipSuccess) {
@@ -671,14 +672,14 @@ pd_status pd_ctx_create(const pd_model* model, int32_t max_batch, int32_t max_sr
 
 void pd_ctx_destroy(pd_ctx* ctx) {
   if (ctx == nullptr) return;
-  hipEventSynchronize(ctx->stage_ev);
-  for (auto ev : ctx->it_ev) { hipEventSynchronize(ev); hipEventDestroy(ev); }
+  if (ctx->stage_ev) hipEventSynchronize(ctx->stage_ev);
+  for (auto ev : ctx->it_ev)
+    if (ev) { hipEventSynchronize(ev); hipEventDestroy(ev); }
   for (int i = 0; i < 2; ++i) {
-    hipEventSynchronize(ctx->tv1[i]);
-    hipEventDestroy(ctx->tv0[i]);
-    hipEventDestroy(ctx->tv1[i]);
+    if (ctx->tv1[i]) { hipEventSynchronize(ctx->tv1[i]); hipEventDestroy(ctx->tv1[i]); }
+    if (ctx->tv0[i]) hipEventDestroy(ctx->tv0[i]);
   }
-  hipEventDestroy(ctx->stage_ev);
+  if (ctx->stage_ev) hipEventDestroy(ctx->stage_ev);
   for (auto& kv : ctx->graphs) hipGraphExecDestroy(kv.second);
   if (ctx->capture) hipStreamDestroy(ctx->capture);
   hipHostFree(ctx->host_pinned);
