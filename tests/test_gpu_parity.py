@@ -213,25 +213,28 @@ def test_max_iters_and_horizon():
         assert classify(g, want, greedy, TOL[C.F32]) == "exact"
 
 
-def test_degenerate_and_extreme_shapes_match_oracle():
+@pytest.mark.parametrize("cfg", [CHAIN, SMALL_PRE_BF16], ids=["chain_f32", "small_pre_bf16"])
+def test_degenerate_and_extreme_shapes_match_oracle(cfg):
     """One-token targets and sources, blocks longer than the target, ragged
     batches mixing them with full-length sentences, and the context's maximum
     batch, source and target sizes: every mode against the oracle, and each
-    batched sentence against its own single decode."""
-    _, _, ctx, M = build(CHAIN, seed=9, max_batch=4, max_src=32, max_tgt=32, bias_std=0.5, ln_std=0.3)
+    batched sentence against its own single decode (bf16: the batched
+    iterations of up to 128 rows run on the tiled products and the
+    row-parallel control step)."""
+    _, _, ctx, M = build(cfg, seed=9, max_batch=4, max_src=32, max_tgt=32, bias_std=0.5, ln_std=0.3)
     g = np.random.default_rng(16)
     modes = [("ar", 1), ("jacobi", 0), ("gs_jacobi", 4), ("gs_jacobi", 40), ("hybrid", 3), ("hybrid", 40)]
     cases = [([1], [1]), ([1], [2]), ([2], [1]), ([32], [32]), ([1, 16, 5, 32], [1, 16, 3, 32]),
              ([32, 32, 32, 32], [32, 1, 32, 2])]
     for lens, ms in cases:
-        srcs = [g.integers(4, CHAIN.vocab, n).astype(np.int32) for n in lens]
+        srcs = [g.integers(4, cfg.vocab, n).astype(np.int32) for n in lens]
         for mode, b in modes:
             say(f"case shapes lens={lens} m={ms} mode={mode} b={b}")
             got = gpu_decode_batch(ctx, srcs, ms, mode, b)
             for r, (src, m) in enumerate(zip(srcs, ms)):
                 enc = M.encode(src)
                 want = oracle.decode(M, enc, m, mode, b)
-                lab = classify(got[r], want, oracle.greedy(M, enc, m), TOL[CHAIN.dtype])
+                lab = classify(got[r], want, oracle.greedy(M, enc, m), TOL[cfg.dtype])
                 assert not lab.startswith("FAIL"), f"{lens} {ms} {mode} b={b} sentence {r}: {lab}"
                 assert got[r].k <= m
                 if len(srcs) > 1:
