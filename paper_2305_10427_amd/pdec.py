@@ -198,8 +198,8 @@ class Context:
             raise PdError(1, f"tgt_m has {len(tgt_m)} entries, the encoded batch has {self.B}")
         m_max = max(tgt_m)
         B = len(tgt_m)
-        if out is None:
-            out = (torch.empty((B, m_max), dtype=torch.int32, device=self.device),
+        if out is None:   # at least one column, so that the library itself reports a bad tgt_m
+            out = (torch.empty((B, max(m_max, 1)), dtype=torch.int32, device=self.device),
                    torch.empty(B, dtype=torch.int32, device=self.device),
                    torch.empty(B, dtype=torch.int32, device=self.device),
                    torch.empty(B, dtype=torch.int32, device=self.device))

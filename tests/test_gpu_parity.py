@@ -254,6 +254,7 @@ def test_error_paths_on_device():
     assert e.value.status == 6                          # decode before encode
     ctx.encode(torch.ones((1, 8), dtype=torch.int32).cuda() * 7, [8])
     for kw, status in [(dict(mode=9, tgt_m=[4]), 1), (dict(mode="ar", tgt_m=[17]), 2),
+                       (dict(mode="ar", tgt_m=[0]), 2),
                        (dict(mode="gs_jacobi", tgt_m=[4], block=0), 1)]:
         with pytest.raises(pdec.PdError) as e:
             ctx.decode(**kw)
@@ -264,6 +265,17 @@ def test_error_paths_on_device():
     with pytest.raises(pdec.PdError) as e:
         ctx.encode(torch.ones((1, 8), dtype=torch.int32).cuda(), [9])         # length > n_max
     assert e.value.status == 1
+    with pytest.raises(pdec.PdError) as e:
+        ctx.encode(torch.ones((1, 8), dtype=torch.int32).cuda(), [0])         # empty source
+    assert e.value.status == 1
+    with pytest.raises(pdec.PdError) as e:
+        ctx.encode(torch.ones((0, 8), dtype=torch.int32).cuda(), [])          # empty batch
+    assert e.value.status == 1
+    # the context still decodes after the refused calls
+    ctx.encode(torch.ones((1, 8), dtype=torch.int32).cuda() * 7, [8])
+    ids, ln, k, fl = ctx.decode("gs_jacobi", [6], block=3)
+    torch.cuda.synchronize()
+    assert 1 <= int(ln[0]) <= 6 and 1 <= int(k[0]) <= 6
 
 
 def _full_size(wl_name, n_sent, m_cap, modes):
