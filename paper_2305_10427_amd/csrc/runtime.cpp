@@ -32,8 +32,13 @@ pd_status fail(pd_status st, const std::string& msg) {
       return fail(PD_E_DEVICE, std::string(#call " failed: ") + hipGetErrorString(e_));     \
   } while (0)
 
-constexpr int kFuseLnMaxRows = 64;  // above this the LayerNorm runs as its own kernel
-constexpr int kTiledMinRows = 64;   // above this bf16 products run on the LDS-tiled kernel
+// Up to this many rows a product runs on the streaming kernel with the
+// LayerNorm in its prologue; above it the LayerNorm runs as its own kernel and
+// bf16 products on the LDS-tiled kernel.  Both choices give bitwise the same
+// rows.  For d <= 512 the streaming kernel stays ahead up to 128 rows; for
+// wider models its per-workgroup LayerNorm costs more than the separate pass
+// from 65 rows on.
+int stream_max_rows(int d) { return d <= 512 ? 128 : 64; }
 constexpr size_t kAlign = 256;
 
 int weight_count(const pd_config& c) {
@@ -238,7 +243,7 @@ hipError_t run_gemm(const pd_ctx& C, const Rows& r, GemmArgs g, int epi, bool pr
   const pd_model& M = *C.M;
   int pro = PRO_NONE;
   if (pro_ln) {
-    if (r.R_max <= kFuseLnMaxRows) {
+    if (r.R_max <= stream_max_rows(M.d)) {
       pro = PRO_LN;
     } else {
       LnArgs la{r.n_dev, r.n_host, g.x, g.x_f32, g.ln_g, g.ln_b, M.cfg.ln_eps, g.K, ln_tmp};
@@ -251,7 +256,7 @@ hipError_t run_gemm(const pd_ctx& C, const Rows& r, GemmArgs g, int epi, bool pr
     }
   }
   const int ksplit = (epi == EPI_ARGMAX || epi == EPI_LOGITS) ? 1 : (g.K >= 2048 ? 8 : 4);
-  if (r.R_max > kTiledMinRows && gemm_tiled_ok(M.dt, pro, g)) return launch_gemm_tiled(epi, ksplit, g, s);
+  if (r.R_max > stream_max_rows(M.d) && gemm_tiled_ok(M.dt, pro, g)) return launch_gemm_tiled(epi, ksplit, g, s);
   return launch_gemm(M.dt, pro, epi, ksplit, g, s);
 }
 

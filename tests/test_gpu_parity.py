@@ -164,8 +164,10 @@ def test_rows_are_invariant_to_block_and_batch(cfg):
     g = np.random.default_rng(9)
     tgt = np.concatenate([np.ones((3, 1), np.int32), g.integers(0, cfg.vocab, (3, 89)).astype(np.int32)], 1)
     ctx.encode(torch.from_numpy(np.stack(srcs)).cuda(), [10, 10, 10])
-    full = ctx.debug_logits(torch.from_numpy(tgt)).cpu().numpy()           # 3 x 90 rows (> 64: separate LN)
-    for T in (1, 3, 8):
+    full = ctx.debug_logits(torch.from_numpy(tgt)).cpu().numpy()           # 270 rows: separate LN, tiled products
+    # 3, 9 and 24 rows: streaming products with the LayerNorm prologue; 90 rows:
+    # the same for d <= 512, separate LN and tiled products for wider models
+    for T in (1, 3, 8, 30):
         say(f"case row-invariance T={T}")
         part = ctx.debug_logits(torch.from_numpy(np.ascontiguousarray(tgt[:, :T]))).cpu().numpy()
         np.testing.assert_array_equal(part, full[:, :T])
