@@ -477,39 +477,59 @@ __global__ __launch_bounds__(1024) void k_ctrl_rows(CtrlArgs a) {
 // The control step of iterations of at most 64 rows (so at most 64
 // sentences and blocks of at most 64 positions), with everything that does
 // not leave the workgroup kept in LDS: the sentence states, the new tokens,
-// the previous block values, the draft just past the block and the next rows.
-// Its global-memory round trips are (1) states, row count and argmax
-// partials, (2) the blocks' previous values and the draft after them, (3) the
-// embedding rows of the next tokens, against about seven in k_ctrl_step; the
-// transitions are the same (advance_state).
+// a window of each sentence's draft and the next rows.  Its global-memory
+// round trips are (1) states and row count, (2) the draft windows together
+// with the argmax partials, (3) the embedding rows of the next tokens,
+// against about seven in k_ctrl_step; the transitions are the same
+// (advance_state).
+//
+// The window of sentence s is y[i - 1 .. i + 126] around its current block
+// [i, i + L): the token before the block, the block's previous values and the
+// draft after it.  Every position the next rows read as input lies in it:
+// the next block starts at most L <= 64 positions later and holds at most 64.
+// All 1024 threads load it, (sentence, offset) items 8 per thread, with every
+// load in flight before the first wait.
 constexpr int kCtrlSmallMax = 64;
+constexpr int kCtrlWindow = 2 * kCtrlSmallMax;
+constexpr int kCtrlSmallThreads = 1024;
 
 template <typename WT>
 __global__ __launch_bounds__(1024) void k_ctrl_small(CtrlArgs a) {
   __shared__ SentState s_st[kCtrlSmallMax];
-  __shared__ int s_tok[kCtrlSmallMax], s_flag[kCtrlSmallMax], s_old[kCtrlSmallMax], s_prev[kCtrlSmallMax];
+  __shared__ int s_tok[kCtrlSmallMax], s_flag[kCtrlSmallMax];
   __shared__ int s_rpos[kCtrlSmallMax], s_rtok[kCtrlSmallMax];
-  __shared__ int s_after[kCtrlSmallMax][kCtrlSmallMax];   // draft values past each sentence's block
+  __shared__ int s_win[kCtrlSmallMax][kCtrlWindow];   // s_win[s][r] = y_s[i_s - 1 + r]
   __shared__ int s_total;
+  constexpr int kItems = kCtrlSmallMax * kCtrlWindow / kCtrlSmallThreads;
   const int tid = threadIdx.x;
   const bool sent = tid < a.B;
-  // (1) states and the row count; the partials of every row the launch may
-  // hold (rows past the device count are reduced too and ignored)
+  // (1) states and the row count
   SentState st;
-  if (sent) st = a.st[tid];
+  if (sent) {
+    st = a.st[tid];
+    s_st[tid] = st;
+  }
   const int R = *a.n_rows;
-  // (2) previous values of each live block and the token before it, issued
-  // before the reduction so that both round trips overlap
-  if (sent && !st.done) {
-    const int* y = a.y + static_cast<size_t>(tid) * a.ldy;
-    for (int r = 0; r < st.L; ++r) s_old[st.row0 + r] = y[st.i + r];
-    s_prev[tid] = st.i > 0 ? y[st.i - 1] : a.bos_id;
-    // inputs of a next block of up to 64 positions: y[i + L .. i + L + 62]
-    const int a0 = st.i + st.L;
-    const int n_after = min(kCtrlSmallMax - 1, st.m - a0);
-    for (int r = 0; r < n_after; ++r) s_after[tid][r] = y[a0 + r];
+  __syncthreads();
+  // (2) the draft windows (positions clamped into the row; values outside
+  // [0, m) are never used), then the argmax partials of every row the launch
+  // may hold (rows past the device count are reduced too and ignored): the
+  // reduction's wait covers both
+  int wv[kItems];
+#pragma unroll
+  for (int u = 0; u < kItems; ++u) {
+    const int it = tid + kCtrlSmallThreads * u;
+    const int s = it / kCtrlWindow < a.B ? it / kCtrlWindow : 0;
+    const int p = min(max(s_st[s].i - 1 + it % kCtrlWindow, 0), a.ldy - 1);
+    wv[u] = a.y[static_cast<size_t>(s) * a.ldy + p];
   }
   reduce_rows(a.partials, a.part_ld, a.n_parts, a.R_max, s_tok, s_flag);   // ends synchronised
+#pragma unroll
+  for (int u = 0; u < kItems; ++u) {
+    const int it = tid + kCtrlSmallThreads * u;
+    if (it / kCtrlWindow < a.B) s_win[it / kCtrlWindow][it % kCtrlWindow] = wv[u];
+  }
+  __syncthreads();
   if (R == 0) return;                          // workgroup-uniform: the decode had already finished
   int i_old = 0, row0_old = 0, L_old = 0;
   if (sent && !st.done) {
@@ -520,7 +540,7 @@ __global__ __launch_bounds__(1024) void k_ctrl_small(CtrlArgs a) {
     for (int r = 0; r < st.L; ++r) {
       const int t = s_tok[st.row0 + r];
       nf |= s_flag[st.row0 + r];
-      changed |= s_old[st.row0 + r] != t;
+      changed |= s_win[tid][1 + r] != t;      // previous value y[i + r]
       eos |= t == a.eos_id;
       y[st.i + r] = t;
       if (a.trace != nullptr) trace_row(a, tbase, st.row0 + r, st.k + 1, tid, st.i + r, t);
@@ -557,9 +577,8 @@ __global__ __launch_bounds__(1024) void k_ctrl_small(CtrlArgs a) {
       const int p = st.i + r;
       int tok;
       if (p == 0) tok = a.bos_id;
-      else if (p - 1 < i_old) tok = s_prev[tid];
-      else if (p - 1 < i_old + L_old) tok = s_tok[row0_old + (p - 1 - i_old)];
-      else tok = s_after[tid][p - 1 - (i_old + L_old)];
+      else if (p - 1 < i_old || p - 1 >= i_old + L_old) tok = s_win[tid][p - i_old];   // y[p - 1], unchanged
+      else tok = s_tok[row0_old + (p - 1 - i_old)];
       s_rpos[row] = p;
       s_rtok[row] = tok;
       a.row_sent[row] = tid;
@@ -704,8 +723,8 @@ hipError_t launch_ctrl_init(int dtype, const CtrlArgs& a, hipStream_t s) {
 hipError_t launch_ctrl_step(int dtype, const CtrlArgs& a, hipStream_t s) {
   const bool small = a.partials != nullptr && a.x_out != nullptr && a.R_max <= kCtrlSmallMax && a.B <= kCtrlSmallMax;
   if (small) {
-    if (dtype == DT_BF16) hipLaunchKernelGGL(k_ctrl_small<bf16_t>, dim3(1), dim3(1024), 0, s, a);
-    else hipLaunchKernelGGL(k_ctrl_small<float>, dim3(1), dim3(1024), 0, s, a);
+    if (dtype == DT_BF16) hipLaunchKernelGGL(k_ctrl_small<bf16_t>, dim3(1), dim3(kCtrlSmallThreads), 0, s, a);
+    else hipLaunchKernelGGL(k_ctrl_small<float>, dim3(1), dim3(kCtrlSmallThreads), 0, s, a);
     return hipGetLastError();
   }
   if (a.B <= kCtrlRowsMaxB) {
