@@ -205,8 +205,7 @@ __device__ void emit_rows(const CtrlArgs& a) {
   if (threadIdx.x == 0) {
     *a.n_rows = total;
     if (a.rows_total != nullptr) *a.rows_total += static_cast<unsigned long long>(total);
-    if (a.host_done != nullptr)
-      __hip_atomic_store(a.host_done, total == 0 ? 1 : 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    if (a.host_rows != nullptr) __hip_atomic_store(a.host_rows, total, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
   }
   if (a.x_out != nullptr) {
     __syncthreads();
@@ -458,8 +457,7 @@ __global__ __launch_bounds__(1024) void k_ctrl_rows(CtrlArgs a) {
     if (a.trace != nullptr) *a.trace_count += static_cast<unsigned long long>(R);
     *a.n_rows = total;
     if (a.rows_total != nullptr) *a.rows_total += static_cast<unsigned long long>(total);
-    if (a.host_done != nullptr)
-      __hip_atomic_store(a.host_done, total == 0 ? 1 : 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    if (a.host_rows != nullptr) __hip_atomic_store(a.host_rows, total, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
   }
   if (a.x_out != nullptr) {
     __syncthreads();
@@ -562,8 +560,7 @@ __global__ __launch_bounds__(1024) void k_ctrl_small(CtrlArgs a) {
     s_total = acc;
     *a.n_rows = acc;
     if (a.rows_total != nullptr) *a.rows_total += static_cast<unsigned long long>(acc);
-    if (a.host_done != nullptr)
-      __hip_atomic_store(a.host_done, acc == 0 ? 1 : 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    if (a.host_rows != nullptr) __hip_atomic_store(a.host_rows, acc, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
   }
   __syncthreads();
   // the next rows: sentence order, block order; the shifted-left input of

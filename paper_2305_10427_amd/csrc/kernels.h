@@ -179,7 +179,8 @@ struct CtrlArgs {
   int* row_tok;
   int* n_rows;             // device scalar
   unsigned long long* rows_total;   // device counter: rows of every iteration laid out (may be null)
-  int* host_done;          // mapped pinned host flag (may be null)
+  int* host_rows;          // mapped pinned host word (may be null): the next iteration's row count, 0 when every
+                           // sentence is done
   int pad_id, bos_id, eos_id;
   int R_max;
   const int* init;         // initial draft [B][init_ld] (nullptr: all [PAD])

@@ -192,8 +192,8 @@ struct pd_ctx {
   int max_batch, max_src, max_tgt;
   char* ws;
   Layout L;
-  int* host_pinned;       // [0]: done word (device-written); [1 .. ]: staging for lengths
-  int* host_done_dev;     // device view of host_pinned[0]
+  int* host_pinned;       // [0]: next iteration's row count (device-written, 0: done); [1 .. ]: staging for lengths
+  int* host_rows_dev;     // device view of host_pinned[0]
   int* stage_src;         // pinned staging copies of host length arrays
   int* stage_tgt;
   hipEvent_t stage_ev = nullptr;
@@ -288,6 +288,14 @@ int vocab_parts(const pd_model& M, int R_max) {
 
 // Decoder pass over the rows of one iteration (or the teacher-forced rows of
 // pd_debug_logits), ending in the fused vocabulary argmax or a logits store.
+// Token + positional embedding of the iteration's rows into the residual stream.
+hipError_t embed_rows(pd_ctx& C, const Rows& r, hipStream_t s) {
+  const pd_model& M = *C.M;
+  EmbedArgs ea{r.n_dev, r.n_host, r.tok, r.map, M.w[0], C.at<float>(C.L.pe), M.dec_scale, M.d, M.V,
+               C.at<char>(C.L.x_res)};
+  return launch_embed(M.dt, ea, r.R_max, s);
+}
+
 hipError_t decoder_pass(pd_ctx& C, const Rows& r, float* logits, hipStream_t s, int slot = -1, bool fused = false) {
   const pd_model& M = *C.M;
   const pd_config& cfg = M.cfg;
@@ -303,10 +311,7 @@ hipError_t decoder_pass(pd_ctx& C, const Rows& r, float* logits, hipStream_t s, 
   const size_t cross_layer = static_cast<size_t>(C.max_batch) * C.max_src * d * es;
   hipError_t e;
 
-  if (!fused) {   // otherwise the control step has embedded the rows already
-    EmbedArgs ea{r.n_dev, r.n_host, r.tok, r.map, M.w[0], C.at<float>(C.L.pe), M.dec_scale, d, M.V, x_res};
-    if ((e = launch_embed(M.dt, ea, r.R_max, s)) != hipSuccess) return e;
-  }
+  if (!fused && (e = embed_rows(C, r, s)) != hipSuccess) return e;   // else the control step has embedded them
 
   for (int l = 0; l < cfg.n_dec; ++l) {
     // self-attention: Q -> q_buf, K/V of the block -> cache (layer l)
@@ -510,6 +515,41 @@ hipError_t encoder_pass(pd_ctx& C, const int32_t* src, int B, int n_max, hipStre
 
 constexpr int kFuseCtrlMaxRows = 64;   // above this the argmax reduction and embedding run as own kernels
 
+// Launch bound of an iteration: the smallest power of two at or above a known
+// upper bound on its rows, at most the decode's maximum.  Rows never grow from
+// one iteration to the next (sentences only finish; a new block is never
+// longer than the one before it: min(b, m - i), then 1 past the hybrid
+// horizon), so a row count published by an earlier iteration bounds every
+// later one.  Every kernel choice a bound selects gives bitwise the same rows,
+// so the bound changes speed only: the last iterations of a batch, where few
+// sentences are left, run the kernels of small iterations.
+int launch_bound(int rows, int R_full) {
+  int b = 1;
+  while (b < rows && b < R_full) b <<= 1;
+  return std::min(b, R_full);
+}
+
+// The control arguments of an iteration launched with bound R: with at most
+// kFuseCtrlMaxRows rows the control step also reduces the argmax partials and
+// embeds the next rows.
+CtrlArgs ctrl_for_bound(const pd_ctx& C, const CtrlArgs& base, int R) {
+  const pd_model& M = *C.M;
+  CtrlArgs c = base;
+  c.R_max = R;
+  if (R <= kFuseCtrlMaxRows) {
+    c.partials = C.at<uint2>(C.L.partials);
+    c.part_ld = gemm_grid(EPI_ARGMAX, M.V, 1);
+    c.n_parts = vocab_parts(M, R);
+    c.x_out = C.at<char>(C.L.x_res);
+    c.emb = M.w[0];
+    c.pe = C.at<float>(C.L.pe);
+    c.emb_scale = M.dec_scale;
+    c.d = M.d;
+    c.vocab = M.V;
+  }
+  return c;
+}
+
 // One decoding iteration: decoder pass over the current rows, fused
 // vocabulary argmax, control step.
 hipError_t iteration(pd_ctx& C, const Rows& r, const CtrlArgs& ca, hipStream_t s, int slot, bool fused) {
@@ -645,7 +685,7 @@ pd_status pd_ctx_create(const pd_model* model, int32_t max_batch, int32_t max_sr
                                hipHostMallocMapped);
   if (e != hipSuccess) { delete c; return fail(PD_E_DEVICE, std::string("hipHostMalloc: ") + hipGetErrorString(e)); }
   c->host_pinned[0] = 0;
-  e = hipHostGetDevicePointer(reinterpret_cast<void**>(&c->host_done_dev), c->host_pinned, 0);
+  e = hipHostGetDevicePointer(reinterpret_cast<void**>(&c->host_rows_dev), c->host_pinned, 0);
   if (e != hipSuccess) {
     hipHostFree(c->host_pinned);
     delete c;
@@ -768,7 +808,7 @@ pd_status pd_decode_init(pd_ctx* ctx, int32_t mode, int32_t block, int32_t horiz
   ca.row_tok = C.at<int>(C.L.row_tok);
   ca.n_rows = C.at<int>(C.L.n_rows);
   ca.rows_total = C.at<unsigned long long>(C.L.rows_total);
-  ca.host_done = C.host_done_dev;
+  ca.host_rows = C.host_rows_dev;
   ca.pad_id = M.cfg.pad_id;
   ca.bos_id = M.cfg.bos_id;
   ca.eos_id = M.cfg.eos_id;
@@ -788,44 +828,50 @@ pd_status pd_decode_init(pd_ctx* ctx, int32_t mode, int32_t block, int32_t horiz
   ca.out_k = out_k;
   ca.out_flags = out_flags;
 
-  const bool fused = R_max <= kFuseCtrlMaxRows;
-  if (fused) {
-    ca.partials = C.at<uint2>(C.L.partials);
-    ca.part_ld = gemm_grid(EPI_ARGMAX, M.V, 1);
-    ca.n_parts = vocab_parts(M, R_max);
-    ca.x_out = C.at<char>(C.L.x_res);
-    ca.emb = M.w[0];
-    ca.pe = C.at<float>(C.L.pe);
-    ca.emb_scale = M.dec_scale;
-    ca.d = M.d;
-    ca.vocab = M.V;
-  }
-  Rows r{ca.n_rows, 0, RowMap{ca.row_sent, ca.row_pos, 0}, ca.row_tok, R_max};
-  hipError_t e = launch_ctrl_init(M.dt, ca, s);
+  // the first rows (at most R_max) are laid out, and embedded when the first
+  // iteration's control step is the fused one, by the initial step
+  bool prev_fused = R_max <= kFuseCtrlMaxRows;
+  const CtrlArgs c0 = ctrl_for_bound(C, ca, R_max);
+  hipError_t e = launch_ctrl_init(M.dt, c0, s);
   if (e != hipSuccess) return fail(PD_E_DEVICE, std::string("init launch: ") + hipGetErrorString(e));
-  volatile int* done = C.host_pinned;
+  volatile int* host_rows = C.host_pinned;
+  int bound = R_max;   // rows of the next iteration launched are at most this
   for (int it = 0; it < iters; ++it) {
     const int slot = C.timing ? (it & 1) : -1;
     if (slot >= 0 && (e = take_timing(C, slot)) != hipSuccess)
       return fail(PD_E_DEVICE, std::string("timing: ") + hipGetErrorString(e));
-    if (C.use_graphs && slot < 0 && C.trace == nullptr) {   // timed and traced iterations are launched directly
-      hipGraphExec_t ex = nullptr;
-      const GraphKey key{mode, block, horizon, max_iters, B, R_max, slot, fused ? 1 : 0};
-      e = iteration_graph(C, key, r, ca, &ex);
-      if (e == hipSuccess) e = hipGraphLaunch(ex, s);
-    } else {
-      e = iteration(C, r, ca, s, slot, fused);
+    const int Rb = launch_bound(bound, R_max);
+    const bool fused = Rb <= kFuseCtrlMaxRows;
+    const CtrlArgs cb = ctrl_for_bound(C, ca, Rb);
+    const Rows r{ca.n_rows, 0, RowMap{ca.row_sent, ca.row_pos, 0}, ca.row_tok, Rb};
+    // the first iteration under a fused control step after unfused ones: its
+    // rows were laid out but not embedded
+    e = fused && !prev_fused ? embed_rows(C, r, s) : hipSuccess;
+    prev_fused = fused;
+    if (e == hipSuccess) {
+      if (C.use_graphs && slot < 0 && C.trace == nullptr) {   // timed and traced iterations are launched directly
+        hipGraphExec_t ex = nullptr;
+        const GraphKey key{mode, block, horizon, max_iters, B, Rb, slot, fused ? 1 : 0};
+        e = iteration_graph(C, key, r, cb, &ex);
+        if (e == hipSuccess) e = hipGraphLaunch(ex, s);
+      } else {
+        e = iteration(C, r, cb, s, slot, fused);
+      }
     }
     if (e == hipSuccess) e = hipEventRecord(C.it_ev[it & 1], s);
     if (e != hipSuccess) return fail(PD_E_DEVICE, std::string("iteration launch: ") + hipGetErrorString(e));
     if (it >= 1) {
       // the previous iteration has finished when its event completes; its
-      // control step has published whether every sentence is done
+      // control step (or a later one) has published the row count of the
+      // iteration after it: 0 when every sentence is done, else a bound on
+      // the rows of every iteration not launched yet
       hipEvent_t ev = C.it_ev[(it - 1) & 1];
       while ((e = hipEventQuery(ev)) == hipErrorNotReady) {
       }
       if (e != hipSuccess) return fail(PD_E_DEVICE, std::string("iteration: ") + hipGetErrorString(e));
-      if (*done) break;
+      const int rows = *host_rows;
+      if (rows <= 0) break;
+      bound = std::min(bound, rows);
     }
   }
   e = launch_finalize(ca, s);

@@ -193,6 +193,31 @@ def test_batched_sentences_equal_single_decodes():
             assert not lab.startswith("FAIL"), lab
 
 
+@pytest.mark.parametrize("cfg,wkw", [(TINY, {}), (SMALL_PRE_BF16, dict(bias_std=0.5, ln_std=0.3))],
+                         ids=["tiny_f32", "small_pre_bf16"])
+def test_launch_bound_shrinks_with_the_rows(cfg, wkw):
+    """A batch whose rows fall, as sentences finish, from above 128 through 128
+    and 64: its iterations are launched with shrinking bounds (separate
+    LayerNorm and tiled products, then LayerNorm prologues, then the control
+    step that also embeds the next rows), and every sentence still equals its
+    single decode bitwise and the oracle."""
+    _, _, ctx, M = build(cfg, seed=5, max_batch=4, max_src=16, max_tgt=48, **wkw)
+    srcs = sources(cfg.vocab, 4, n=12, seed=11)
+    ms = [44, 6, 14, 33]   # Jacobi: 97 rows, then 91, 77 and 44 as sentences finish (k = 6, 14, 33, 37-44)
+    for mode, b in [("jacobi", 0), ("gs_jacobi", 40), ("hybrid", 24)]:
+        say(f"case launch-bound cfg={cfg.name} mode={mode} b={b} ms={ms}")
+        batch = gpu_decode_batch(ctx, srcs, ms, mode, b)
+        for r in range(4):
+            one = gpu_decode_batch(ctx, [srcs[r]], [ms[r]], mode, b)[0]
+            np.testing.assert_array_equal(batch[r].ids, one.ids)
+            assert batch[r].k == one.k
+            enc = M.encode(srcs[r])
+            want = oracle.decode(M, enc, ms[r], mode, b)
+            lab = classify(batch[r], want, oracle.greedy(M, enc, ms[r]), TOL[cfg.dtype])
+            say(f"  sentence {r} m={ms[r]}: {lab} k={batch[r].k}")
+            assert not lab.startswith("FAIL"), lab
+
+
 def test_max_iters_and_horizon():
     _, _, ctx, M = build(CHAIN, seed=1, bias_std=0.5, ln_std=0.3)
     src = sources(CHAIN.vocab, 1, seed=3)[0]
