@@ -179,14 +179,17 @@ __device__ __forceinline__ int block_len(const CtrlArgs& a, int i, int m) {
 // write the embedded rows.  Single workgroup.
 template <typename WT>
 __device__ void emit_rows(const CtrlArgs& a) {
-  __shared__ int s_total;
+  __shared__ int s_total, s_near;
   if (threadIdx.x == 0) {
     int acc = 0;
+    bool near = true;
     for (int s = 0; s < a.B; ++s) {
       a.st[s].row0 = acc;
       acc += a.st[s].done ? 0 : a.st[s].L;
+      near = near && near_end(a.st[s]);
     }
     s_total = acc;
+    s_near = near ? 1 : 0;
   }
   __syncthreads();
   for (int s = threadIdx.x; s < a.B; s += blockDim.x) {
@@ -205,7 +208,8 @@ __device__ void emit_rows(const CtrlArgs& a) {
   if (threadIdx.x == 0) {
     *a.n_rows = total;
     if (a.rows_total != nullptr) *a.rows_total += static_cast<unsigned long long>(total);
-    if (a.host_rows != nullptr) __hip_atomic_store(a.host_rows, total, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    if (a.host_rows != nullptr)
+      __hip_atomic_store(a.host_rows, host_word(total, s_near != 0), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
   }
   if (a.x_out != nullptr) {
     __syncthreads();
@@ -388,9 +392,11 @@ __global__ __launch_bounds__(1024) void k_ctrl_rows(CtrlArgs a) {
   __shared__ int s_k[kCtrlRowsMaxB];           // iterations so far (trace)
   __shared__ int s_i[kCtrlRowsMaxB];           // next block start
   __shared__ int s_scan[2][kCtrlRowsMaxB + 1]; // next block lengths -> first rows (exclusive prefix)
+  __shared__ int s_far;                        // some live sentence is not near its end (near_end)
   const int tid = threadIdx.x;
   const int R = *a.n_rows;
   if (R == 0) return;                          // workgroup-uniform: the decode had already finished
+  if (tid == 0) s_far = 0;
   if (a.partials != nullptr)
     reduce_rows(a.partials, a.part_ld, a.n_parts, R, const_cast<int*>(a.new_tok), const_cast<int*>(a.row_flags));
   SentState st;
@@ -418,6 +424,7 @@ __global__ __launch_bounds__(1024) void k_ctrl_rows(CtrlArgs a) {
       const int acc = s_acc[tid];
       advance_state(a, st, (acc & 1) != 0, (acc & 2) != 0, (acc & 4) ? 1 : 0);
     }
+    if (!near_end(st)) s_far = 1;
     len = st.done ? 0 : st.L;
     s_i[tid] = st.i;
     s_scan[0][tid + 1] = len;
@@ -457,7 +464,8 @@ __global__ __launch_bounds__(1024) void k_ctrl_rows(CtrlArgs a) {
     if (a.trace != nullptr) *a.trace_count += static_cast<unsigned long long>(R);
     *a.n_rows = total;
     if (a.rows_total != nullptr) *a.rows_total += static_cast<unsigned long long>(total);
-    if (a.host_rows != nullptr) __hip_atomic_store(a.host_rows, total, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    if (a.host_rows != nullptr)
+      __hip_atomic_store(a.host_rows, host_word(total, s_far == 0), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
   }
   if (a.x_out != nullptr) {
     __syncthreads();
@@ -553,14 +561,17 @@ __global__ __launch_bounds__(1024) void k_ctrl_small(CtrlArgs a) {
   if (tid == 0) {
     if (a.trace != nullptr) *a.trace_count += static_cast<unsigned long long>(R);
     int acc = 0;
+    bool near = true;
     for (int s = 0; s < a.B; ++s) {
       s_st[s].row0 = acc;
       acc += s_st[s].done ? 0 : s_st[s].L;
+      near = near && near_end(s_st[s]);
     }
     s_total = acc;
     *a.n_rows = acc;
     if (a.rows_total != nullptr) *a.rows_total += static_cast<unsigned long long>(acc);
-    if (a.host_rows != nullptr) __hip_atomic_store(a.host_rows, acc, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    if (a.host_rows != nullptr)
+      __hip_atomic_store(a.host_rows, host_word(acc, near), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
   }
   __syncthreads();
   // the next rows: sentence order, block order; the shifted-left input of

@@ -179,8 +179,7 @@ struct CtrlArgs {
   int* row_tok;
   int* n_rows;             // device scalar
   unsigned long long* rows_total;   // device counter: rows of every iteration laid out (may be null)
-  int* host_rows;          // mapped pinned host word (may be null): the next iteration's row count, 0 when every
-                           // sentence is done
+  int* host_rows;          // mapped pinned host word (may be null): host_word(rows of the next iteration, near_end)
   int pad_id, bos_id, eos_id;
   int R_max;
   const int* init;         // initial draft [B][init_ld] (nullptr: all [PAD])
@@ -203,6 +202,19 @@ struct CtrlArgs {
   // finalize
   int* out_ids; int out_ld; int* out_len; int* out_k; int* out_flags;
 };
+
+// The word the control step publishes to the host after laying out the next
+// iteration: its row count (0 when every sentence is done) and, in bit 30,
+// whether that iteration may be the last one: every live sentence is in its
+// last block, the iteration is not the first of a block of several positions
+// (which compares with an unrefined draft), and the block's cap of L
+// iterations leaves at most kNearEndIters more.  The bit only paces the host.
+constexpr int kNearEndBit = 1 << 30;
+constexpr int kNearEndIters = 8;
+__device__ __forceinline__ bool near_end(const SentState& st) {
+  return st.done || (st.i + st.L >= st.m && (st.j >= 1 || st.L == 1) && st.L - st.j <= kNearEndIters);
+}
+__host__ __device__ __forceinline__ int host_word(int rows, bool near) { return rows | (near && rows > 0 ? kNearEndBit : 0); }
 
 struct ReduceArgs {
   const int* n_rows_dev;

@@ -588,6 +588,15 @@ pd_status stage_lengths(pd_ctx* C, int* stage, const int32_t* host, int B, int* 
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
+// Spin until the event has completed (the iteration loop polls rather than
+// blocking: a blocking wait adds a wake-up latency to every iteration).
+hipError_t wait_event(hipEvent_t ev) {
+  hipError_t e;
+  while ((e = hipEventQuery(ev)) == hipErrorNotReady) {
+  }
+  return e;
+}
+
 // Fold a completed event pair of the vocabulary kernel into the totals.
 hipError_t take_timing(pd_ctx& C, int slot) {
   if (!C.tv_pending[slot]) return hipSuccess;
@@ -863,13 +872,20 @@ pd_status pd_decode_init(pd_ctx* ctx, int32_t mode, int32_t block, int32_t horiz
     if (it >= 1) {
       // the previous iteration has finished when its event completes; its
       // control step (or a later one) has published the row count of the
-      // iteration after it: 0 when every sentence is done, else a bound on
-      // the rows of every iteration not launched yet
-      hipEvent_t ev = C.it_ev[(it - 1) & 1];
-      while ((e = hipEventQuery(ev)) == hipErrorNotReady) {
+      // iteration after it (0 when every sentence is done, else a bound on
+      // the rows of every iteration not launched yet) and whether that
+      // iteration, the one in flight, may be the last: then it is waited for
+      // too, rather than launching one more iteration that may find nothing
+      // to do
+      if ((e = wait_event(C.it_ev[(it - 1) & 1])) != hipSuccess)
+        return fail(PD_E_DEVICE, std::string("iteration: ") + hipGetErrorString(e));
+      int word = *host_rows;
+      if ((word & kNearEndBit) != 0) {
+        if ((e = wait_event(C.it_ev[it & 1])) != hipSuccess)
+          return fail(PD_E_DEVICE, std::string("iteration: ") + hipGetErrorString(e));
+        word = *host_rows;
       }
-      if (e != hipSuccess) return fail(PD_E_DEVICE, std::string("iteration: ") + hipGetErrorString(e));
-      const int rows = *host_rows;
+      const int rows = word & ~kNearEndBit;
       if (rows <= 0) break;
       bound = std::min(bound, rows);
     }
