@@ -181,8 +181,9 @@ pd_status pd_encode(pd_ctx* ctx, const int32_t* src_ids, const int32_t* src_len,
  * The initial draft is all [PAD] (Section 3.3, "Initialization").  Sentences
  * of a batch iterate independently; a sentence's result does not depend on
  * the other sentences.  The call blocks the host until the iteration has
- * converged (it polls a completion word once per iteration), then enqueues
- * the output writes on the stream.
+ * converged (it polls a word the device writes once per iteration: the next
+ * iteration's row count, which also sizes later launches), then enqueues the
+ * output writes on the stream.
  */
 pd_status pd_decode(pd_ctx* ctx, int32_t mode, int32_t block, int32_t horizon, int32_t max_iters,
                     const int32_t* tgt_m, int32_t* out_ids, int32_t out_ld, int32_t* out_len,
