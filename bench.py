@@ -161,7 +161,7 @@ def gpu_workload(wl_name, steps, warmup, modes, headline, n_sent=0, trace=False,
         log(f"[{wl_name}] encode: {e['us_per_sentence']:.1f} us/sentence, {e['achieved_GBs']:.0f} GB/s of weights")
     if trace:
         # the same decodes with the DDGviz trace on (records and log-sum-exp
-        # partials; iterations launched kernel by kernel)
+        # partials)
         for c in ctxs:
             c.set_trace(4 * wl.tgt_cap, max(headline[1], 1))
         t = run_mode(ctxs, sents, outs, headline[0], headline[1], steps, warmup)

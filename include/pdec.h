@@ -265,8 +265,9 @@ pd_status pd_ctx_rows_processed(const pd_ctx* ctx, int64_t* rows);
  * number of rows one iteration lays out (B * block for the block modes, B * m
  * for PD_JACOBI, B for PD_AR); a decode whose iteration needs more rows than
  * the scratch holds fails with PD_E_WORKSPACE before launching anything.
- * Traced iterations are launched kernel by kernel (no graph replay).  Tracing
- * changes no token, count or flag of the decode.  top1 is the exact largest
+ * Traced iterations are replayed from HIP graphs like untraced ones (one
+ * capture per set of trace buffers).  Tracing changes no token, count or flag
+ * of the decode.  top1 is the exact largest
  * logit; lse is rounded in float and its summation order follows the kernel
  * that ran (it may differ in the last bits between batch sizes).
  *

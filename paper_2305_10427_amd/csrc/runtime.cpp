@@ -178,9 +178,14 @@ Layout plan(const pd_model& M, int max_batch, int max_src, int max_tgt) {
 
 struct GraphKey {
   int mode, block, horizon, max_iters, B, R_max, slot, fused;
+  // the trace buffers are kernel arguments of a traced iteration
+  const void* trace;
+  long long trace_cap;
+  const void* trace_part;
   bool operator==(const GraphKey& o) const {
     return mode == o.mode && block == o.block && horizon == o.horizon && max_iters == o.max_iters && B == o.B &&
-           R_max == o.R_max && slot == o.slot && fused == o.fused;
+           R_max == o.R_max && slot == o.slot && fused == o.fused && trace == o.trace && trace_cap == o.trace_cap &&
+           trace_part == o.trace_part;
   }
 };
 
@@ -858,9 +863,10 @@ pd_status pd_decode_init(pd_ctx* ctx, int32_t mode, int32_t block, int32_t horiz
     e = fused && !prev_fused ? embed_rows(C, r, s) : hipSuccess;
     prev_fused = fused;
     if (e == hipSuccess) {
-      if (C.use_graphs && slot < 0 && C.trace == nullptr) {   // timed and traced iterations are launched directly
+      if (C.use_graphs && slot < 0) {   // iterations timed with events are launched directly
         hipGraphExec_t ex = nullptr;
-        const GraphKey key{mode, block, horizon, max_iters, B, Rb, slot, fused ? 1 : 0};
+        const GraphKey key{mode, block, horizon, max_iters, B, Rb, slot, fused ? 1 : 0, C.trace, C.trace_cap,
+                           C.trace_part};
         e = iteration_graph(C, key, r, cb, &ex);
         if (e == hipSuccess) e = hipGraphLaunch(ex, s);
       } else {
