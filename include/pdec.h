@@ -136,7 +136,8 @@ void pd_model_destroy(pd_model* model);
 /*
  * Device workspace needed by a context that decodes up to max_batch sentences
  * with sources of at most max_src tokens and targets of at most max_tgt
- * positions (max_tgt <= 1024).  Covers every mode, including PD_JACOBI with
+ * positions (max_src, max_tgt <= 1024; max_batch * max(max_src, max_tgt)
+ * below 2^24, else PD_E_SHAPE).  Covers every mode, including PD_JACOBI with
  * blocks of max_tgt positions.
  */
 pd_status pd_ctx_workspace_bytes(const pd_model* model, int32_t max_batch, int32_t max_src,

@@ -40,6 +40,7 @@ pd_status fail(pd_status st, const std::string& msg) {
 // from 65 rows on.
 int stream_max_rows(int d) { return d <= 512 ? 128 : 64; }
 constexpr size_t kAlign = 256;
+constexpr long long kMaxCtxRows = 1LL << 24;   // rows of the largest launch a context may need
 
 int weight_count(const pd_config& c) {
   return 2 + 12 * c.n_enc + (c.pre_ln ? 2 : 0) + 20 * c.n_dec + (c.pre_ln ? 2 : 0);
@@ -673,6 +674,9 @@ pd_status pd_ctx_workspace_bytes(const pd_model* model, int32_t max_batch, int32
   if (model == nullptr || bytes == nullptr) return fail(PD_E_ARG, "null argument");
   if (max_batch < 1 || max_src < 1 || max_tgt < 1) return fail(PD_E_SHAPE, "limits must be positive");
   if (max_tgt > 1024 || max_src > 1024) return fail(PD_E_SHAPE, "max_src and max_tgt must be <= 1024");
+  // rows of one launch are counted in int and published to the host below the near-end bit
+  if (static_cast<long long>(max_batch) * std::max(max_src, max_tgt) >= kMaxCtxRows)
+    return fail(PD_E_SHAPE, "max_batch * max(max_src, max_tgt) must be below " + std::to_string(kMaxCtxRows));
   *bytes = plan(*model, max_batch, max_src, max_tgt).total;
   return PD_OK;
 }

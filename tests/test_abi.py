@@ -75,6 +75,8 @@ def test_model_create_checks_pointers_and_workspace_size():
     assert sz.value > small
     assert L.pd_ctx_workspace_bytes(h, 1, 16, 2048, ctypes.byref(sz)) == 2
     assert L.pd_ctx_workspace_bytes(h, 0, 16, 16, ctypes.byref(sz)) == 2
+    assert L.pd_ctx_workspace_bytes(h, (1 << 24) // 16, 16, 16, ctypes.byref(sz)) == 2   # 2^24 rows
+    assert L.pd_ctx_workspace_bytes(h, (1 << 24) // 16 - 1, 16, 16, ctypes.byref(sz)) == 0
     ctx = ctypes.c_void_p()
     assert L.pd_ctx_create(h, 1, 16, 16, ctypes.c_void_p(0x10080), small, ctypes.byref(ctx)) == 3   # misaligned
     assert L.pd_ctx_create(h, 1, 16, 16, ctypes.c_void_p(0x10000), small - 256, ctypes.byref(ctx)) == 3
