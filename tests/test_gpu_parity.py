@@ -218,6 +218,29 @@ def test_launch_bound_shrinks_with_the_rows(cfg, wkw):
             assert not lab.startswith("FAIL"), lab
 
 
+def test_more_than_64_sentences_under_a_fused_control_step():
+    """80 sentences of different lengths: once fewer than 65 rows are left,
+    the bound selects the control step that also reduces the argmax partials
+    and embeds the next rows, here the row-parallel one (more than 64
+    sentences).  Every sentence equals its single decode bitwise."""
+    _, _, ctx, M = build(TINY, seed=3, max_batch=80, max_src=16, max_tgt=24)
+    g = np.random.default_rng(31)
+    srcs = [g.integers(4, TINY.vocab, int(n)).astype(np.int32) for n in g.integers(4, 17, 80)]
+    ms = [int(m) for m in g.integers(1, 25, 80)]
+    for mode, b in [("ar", 1), ("hybrid", 2), ("gs_jacobi", 3)]:
+        say(f"case 80 sentences mode={mode} b={b}")
+        batch = gpu_decode_batch(ctx, srcs, ms, mode, b)
+        for r in range(80):
+            one = gpu_decode_batch(ctx, [srcs[r]], [ms[r]], mode, b)[0]
+            np.testing.assert_array_equal(batch[r].ids, one.ids)
+            assert batch[r].k == one.k
+        for r in (0, 41, 79):
+            enc = M.encode(srcs[r])
+            want = oracle.decode(M, enc, ms[r], mode, b)
+            lab = classify(batch[r], want, oracle.greedy(M, enc, ms[r]), TOL[C.F32])
+            assert not lab.startswith("FAIL"), lab
+
+
 def test_max_iters_and_horizon():
     _, _, ctx, M = build(CHAIN, seed=1, bias_std=0.5, ln_std=0.3)
     src = sources(CHAIN.vocab, 1, seed=3)[0]
