@@ -125,8 +125,9 @@ __device__ __forceinline__ void chunk_fold(const float* q, const KeyChunk<AT, DH
   const float a2 = expf(mc - mn);
   sm.p[lane] = p;
   wave_lds_sync();
-  // P.V: each lane sums its two dimensions over its half of the keys
-  // (keys past nk have p = 0; their V entries are dropped by the select)
+  // P.V: each lane sums its two dimensions over its half of the keys.  Keys
+  // past nk have p = 0 and hold key 0's V entries (a value every row
+  // attends to), so they add exact zeros: fmaf(0, v, acc) = acc for finite v.
   const int kh = 32 * (lane >> 5);
   float o[KC::NP][2];
 #pragma unroll
@@ -134,12 +135,11 @@ __device__ __forceinline__ void chunk_fold(const float* q, const KeyChunk<AT, DH
     float oa[4] = {0.f, 0.f, 0.f, 0.f}, ob[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int k2 = 0; k2 < 32; ++k2) {
-      const bool kin = key0 + kh + k2 < nk;
       float va, vb;
       unpack_pair(kc.v[i][k2], va, vb);
       const float pk = sm.p[kh + k2];
-      oa[k2 & 3] = fmaf(pk, kin ? va : 0.f, oa[k2 & 3]);
-      ob[k2 & 3] = fmaf(pk, kin ? vb : 0.f, ob[k2 & 3]);
+      oa[k2 & 3] = fmaf(pk, va, oa[k2 & 3]);
+      ob[k2 & 3] = fmaf(pk, vb, ob[k2 & 3]);
     }
     o[i][0] = (oa[0] + oa[1]) + (oa[2] + oa[3]);
     o[i][1] = (ob[0] + ob[1]) + (ob[2] + ob[3]);
