@@ -8,7 +8,25 @@ system of Eq. (2), f(y_i, y_{1:i-1}, x) = y_i - argmax p_theta(y_i | y_{1:i-1}, 
 Here y is a 0-based numpy array, so y[t] is y_{t+1}.  The decoder input at
 position p is [BOS] for p = 0 and y[p-1] otherwise, and its prediction is the
 new value of y[p]; this is the "shift left" of predictions that Appendix A
-mentions.  One iteration is one decoder forward over the active block.
+mentions.  F(y)[p] denotes that prediction.  One iteration is one decoder
+forward over the active block.
+
+Greedy decoding (Eq. (1)) is written out on its own, as the plain definition
+of the result every parallel mode must reproduce (Proposition 1).
+
+The three parallel algorithms of Section 3.2 (Algorithms 1-3 of Appendix A)
+are one procedure with different block schedules.  The m positions are cut
+into consecutive blocks, solved one after another (Gauss-Seidel from block
+to block); inside the current block [i, i + L) every iteration recomputes
+all L positions at once from the committed prefix y[0..i-1] and the block's
+previous values (Jacobi), and the block is committed as soon as an iteration
+leaves it unchanged (the stopping condition of Eq. (3)):
+
+    mode       block lengths                            stop at [EOS]
+    jacobi     one block of all m positions (PJ)        no
+    gs_jacobi  b, b, ..., the rest (PGJ)                no
+    hybrid     b, b, ... up to the horizon h, then      yes, after a committed
+               blocks of one position (HGJ)             block that holds [EOS]
 
 Readings where the paper leaves a detail open (each is listed in the design
 notes of the repository as well):
@@ -43,7 +61,7 @@ PAD, BOS, EOS = 0, 1, 2
 
 @dataclasses.dataclass
 class Result:
-    y: np.ndarray                 # final iterate (length m; AR/HGJ: up to the stop)
+    y: np.ndarray                 # final iterate: length m, or cut after the [EOS] decoding stopped at
     out: np.ndarray               # output ids, cut after the first EOS (inclusive)
     k: int                        # decoder forwards (iterations) used
     hit_max_iters: bool = False
@@ -96,11 +114,15 @@ def _init(m: int, init: Optional[np.ndarray]) -> np.ndarray:
     return np.full(m, PAD, np.int32) if init is None else np.array(init, np.int32).copy()
 
 
+def _cap(m: int, max_iters: Optional[int]) -> int:
+    return m if max_iters is None or max_iters <= 0 else max_iters
+
+
 def greedy(model: Model, enc: Encoded, m: int, stop_at_eos: bool = True,
            max_iters: Optional[int] = None, recompute: bool = False) -> Result:
     """Greedy autoregressive decoding, Eq. (1): y[t] = argmax p(. | y[0..t-1], x), t = 0..m-1."""
     s = Solver(model, enc, m, recompute)
-    cap = m if max_iters is None or max_iters <= 0 else max_iters
+    cap = _cap(m, max_iters)
     y = np.full(m, PAD, np.int32)
     k, t = 0, 0
     while t < m:
@@ -114,100 +136,82 @@ def greedy(model: Model, enc: Encoded, m: int, stop_at_eos: bool = True,
     return Result(y[:t].copy(), cut_at_eos(y[:t]), k, False, s.records)
 
 
-def jacobi(model: Model, enc: Encoded, m: int, init=None, max_iters: Optional[int] = None,
-           recompute: bool = False) -> Result:
-    """Parallel Jacobi decoding, Algorithm 1: update all m positions from the previous iterate."""
-    s = Solver(model, enc, m, recompute)
-    cap = m if max_iters is None or max_iters <= 0 else min(m, max_iters)
-    y = _init(m, init)
-    res = Result(y, y, 0)
-    for j in range(1, m + 1):
-        if j > cap:
-            res.hit_max_iters = True
-            break
-        o = y.copy()
-        y = s.block(y, 0, m)
-        res.k = j
-        res.iterates.append((j, 0, y.copy()))
-        if np.array_equal(y, o):          # StopC, Eq. (3)
-            break
-    res.y, res.out, res.records = y, cut_at_eos(y), s.records
-    return res
+def block_length(mode: str, i: int, m: int, b: int, h: int) -> int:
+    """Length of the block that starts at position i (see the table above)."""
+    if mode == "jacobi":
+        return m - i
+    if mode == "gs_jacobi":
+        return min(b, m - i)
+    if mode == "hybrid":
+        return min(b, h - i) if i < h else 1
+    raise ValueError(mode)
 
 
-def gs_jacobi(model: Model, enc: Encoded, m: int, b: int, init=None,
-              max_iters: Optional[int] = None, recompute: bool = False) -> Result:
-    """Parallel GS-Jacobi decoding, Algorithm 2: Jacobi inside b-blocks, Gauss-Seidel across them."""
-    s = Solver(model, enc, m, recompute)
-    cap = m if max_iters is None or max_iters <= 0 else max_iters
+def solve_by_blocks(model: Model, enc: Encoded, m: int, mode: str, b: int = 1, h: Optional[int] = None,
+                    init=None, max_iters: Optional[int] = None, recompute: bool = False,
+                    evaluator=None) -> Result:
+    """The block fixed-point procedure shared by PJ, PGJ and HGJ (Section 3.2).
+
+    evaluator: optional stand-in for the model's Solver (an object with the
+    same ``block(y, i, L)`` and ``records``), so that a recorded sequence of
+    evaluations of F can be replayed through exactly this control flow.
+    """
+    F = Solver(model, enc, m, recompute) if evaluator is None else evaluator
+    cap = _cap(m, max_iters)
+    h = m if h is None else min(h, m)
     y = _init(m, init)
     res = Result(y, y, 0)
     i = 0
     while i < m:
-        L = min(b, m - i)
-        for j in range(1, L + 1):
+        L = block_length(mode, i, m, b, h)
+        committed = False
+        for j in range(1, L + 1):                 # at most L iterations per block
             if res.k >= cap:
                 res.hit_max_iters = True
                 break
-            o = y[i:i + L].copy()
-            y[i:i + L] = s.block(y, i, L)
+            before = y[i:i + L].copy()
+            y[i:i + L] = F.block(y, i, L)
             res.k += 1
             res.iterates.append((res.k, i, y[i:i + L].copy()))
-            if np.array_equal(y[i:i + L], o):
+            if np.array_equal(y[i:i + L], before) or j == L:   # Eq. (3), or exact after L iterations
+                committed = True
                 break
-        if res.hit_max_iters:
+        if not committed:                         # the iteration budget ran out inside the block
             break
+        if mode == "hybrid":
+            hit = np.nonzero(y[i:i + L] == EOS)[0]
+            if len(hit):                          # CheckEOS: stop at the block's first [EOS]
+                y = y[: i + int(hit[0]) + 1].copy()
+                break
         i += L
-    res.y, res.out, res.records = y, cut_at_eos(y), s.records
+    res.y, res.out, res.records = y, cut_at_eos(y), F.records
     return res
 
 
+def jacobi(model: Model, enc: Encoded, m: int, init=None, max_iters: Optional[int] = None,
+           recompute: bool = False, evaluator=None) -> Result:
+    """Parallel Jacobi decoding (Algorithm 1): one block of all m positions."""
+    return solve_by_blocks(model, enc, m, "jacobi", init=init, max_iters=max_iters, recompute=recompute,
+                           evaluator=evaluator)
+
+
+def gs_jacobi(model: Model, enc: Encoded, m: int, b: int, init=None,
+              max_iters: Optional[int] = None, recompute: bool = False, evaluator=None) -> Result:
+    """Parallel GS-Jacobi decoding (Algorithm 2): Jacobi inside b-blocks, Gauss-Seidel across them."""
+    return solve_by_blocks(model, enc, m, "gs_jacobi", b, init=init, max_iters=max_iters, recompute=recompute,
+                           evaluator=evaluator)
+
+
 def hybrid(model: Model, enc: Encoded, m: int, b: int, h: Optional[int] = None, init=None,
-           max_iters: Optional[int] = None, recompute: bool = False) -> Result:
-    """Hybrid GS-Jacobi decoding, Algorithm 3.
+           max_iters: Optional[int] = None, recompute: bool = False, evaluator=None) -> Result:
+    """Hybrid GS-Jacobi decoding (Algorithm 3).
 
     GS-Jacobi blocks up to the horizon h; a converged block that holds [EOS]
     ends decoding at its first [EOS].  Without [EOS] before h, decoding goes on
     autoregressively from position h until [EOS] or m.
     """
-    s = Solver(model, enc, m, recompute)
-    cap = m if max_iters is None or max_iters <= 0 else max_iters
-    h = m if h is None else min(h, m)
-    y = _init(m, init)
-    res = Result(y, y, 0)
-    i = 0
-    eos_cond = False
-    while i < h and not eos_cond and not res.hit_max_iters:
-        L = min(b, h - i)
-        for j in range(1, L + 1):
-            if res.k >= cap:
-                res.hit_max_iters = True
-                break
-            o = y[i:i + L].copy()
-            y[i:i + L] = s.block(y, i, L)
-            res.k += 1
-            res.iterates.append((res.k, i, y[i:i + L].copy()))
-            stop = np.array_equal(y[i:i + L], o) or j == L
-            hit = np.nonzero(y[i:i + L] == EOS)[0]
-            if stop and len(hit):
-                y = y[: i + int(hit[0]) + 1].copy()
-                eos_cond = True
-                break
-            if stop:
-                break
-        if not eos_cond and not res.hit_max_iters:
-            i += L
-    while not eos_cond and not res.hit_max_iters and i < m:
-        if res.k >= cap:
-            res.hit_max_iters = True
-            break
-        y[i] = s.block(y, i, 1)[0]
-        res.k += 1
-        res.iterates.append((res.k, i, y[i:i + 1].copy()))
-        i += 1
-        eos_cond = bool(y[i - 1] == EOS)
-    res.y, res.out, res.records = y, cut_at_eos(y), s.records
-    return res
+    return solve_by_blocks(model, enc, m, "hybrid", b, h, init=init, max_iters=max_iters, recompute=recompute,
+                           evaluator=evaluator)
 
 
 def decode(model: Model, enc: Encoded, m: int, mode: str, block: int = 1, **kw) -> Result:

@@ -24,6 +24,9 @@ bf16 models follow a storage contract: values are rounded to bfloat16
 attention output, the FFN hidden after the activation, the residual stream
 after each sublayer and every LayerNorm output that feeds a matrix product;
 all other arithmetic is float64 here.  float32 models round nowhere.
+
+Model(..., dtype=np.float32) runs the same code in float32 arithmetic; it is
+used only to time the CPU baseline, never for parity.
 """
 from __future__ import annotations
 
@@ -87,7 +90,7 @@ def attention(q, k, v, n_heads, key_limit=None):
     """
     Lq, d = q.shape
     dh = d // n_heads
-    out = np.zeros((Lq, d), np.float64)
+    out = np.zeros((Lq, d), q.dtype)
     for h in range(n_heads):
         sl = slice(h * dh, (h + 1) * dh)
         scores = (q[:, sl] @ k[:, sl].T) / math.sqrt(dh)          # [Lq, Lk]
@@ -126,19 +129,20 @@ class ArgmaxRecord:
 class Model:
     """p_theta with weights given as a {name: array} dict (canonical names)."""
 
-    def __init__(self, cfg, weights: Dict[str, np.ndarray]):
+    def __init__(self, cfg, weights: Dict[str, np.ndarray], dtype=np.float64):
         self.cfg = cfg
         self.d = cfg.d_model
         self.H = cfg.n_heads
         self.bf16 = cfg.dtype == "bf16"
-        self.w = {k: np.asarray(v, dtype=np.float64) for k, v in weights.items()}
+        self.dt = np.dtype(dtype)
+        self.w = {k: np.asarray(v, dtype=self.dt) for k, v in weights.items()}
         self.enc_scale = math.sqrt(self.d)
         des = getattr(cfg, "dec_emb_scale", None)
         self.dec_scale = math.sqrt(self.d) if des is None else float(des)
 
     # -- helpers -------------------------------------------------------------
     def _r(self, x):
-        return round_bf16(x) if self.bf16 else x
+        return round_bf16(x).astype(self.dt, copy=False) if self.bf16 else x
 
     def _lin(self, x, name_w, name_b):
         return x @ self.w[name_w].T + self.w[name_b]
@@ -150,7 +154,8 @@ class Model:
         return gelu(x) if self.cfg.act_gelu else np.maximum(x, 0.0)
 
     def embed(self, tokens, positions, scale):
-        return self._r(self.w["emb"][np.asarray(tokens)] * scale + sinusoid(positions, self.d))
+        pe = sinusoid(positions, self.d).astype(self.dt, copy=False)
+        return self._r(self.w["emb"][np.asarray(tokens)] * self.dt.type(scale) + pe)
 
     # -- encoder ---------------------------------------------------------------
     def encode(self, src) -> Encoded:
@@ -179,8 +184,8 @@ class Model:
 
     # -- decoder ---------------------------------------------------------------
     def new_cache(self, T: int) -> Cache:
-        return Cache([np.zeros((T, self.d)) for _ in range(self.cfg.n_dec)],
-                     [np.zeros((T, self.d)) for _ in range(self.cfg.n_dec)])
+        return Cache([np.zeros((T, self.d), self.dt) for _ in range(self.cfg.n_dec)],
+                     [np.zeros((T, self.d), self.dt) for _ in range(self.cfg.n_dec)])
 
     def decode_rows(self, enc: Encoded, cache: Cache, tokens, p0: int) -> np.ndarray:
         """Final hidden states of input positions p0 .. p0+L-1.
@@ -216,7 +221,7 @@ class Model:
 
     def logits(self, h: np.ndarray) -> np.ndarray:
         """Tied output projection s * h . E^T + out_bias, one row per hidden state."""
-        return self.cfg.logit_scale * (h @ self.w["emb"].T) + self.w["out_bias"]
+        return self.dt.type(self.cfg.logit_scale) * (h @ self.w["emb"].T) + self.w["out_bias"]
 
     def teacher_forced_logits(self, enc: Encoded, tgt_in) -> np.ndarray:
         """Logits of every position for decoder inputs tgt_in (BOS first), recomputed from scratch."""

@@ -211,11 +211,12 @@ def eos_bias_for(cfg, seed, wkw, src, m, q):
 
 def eos_cases(cfg, seed, wkw, b, m=16, tries=40):
     """One (bias, source, q) per kind: first EOS at a block start, inside a block,
-    at a block's last position, or absent."""
+    at a block's last position, or absent.  Positions past the first block are
+    tried first, so that the EOS's block index and its absolute position differ."""
     found = {}
     for t in range(tries):
         src = np.random.default_rng(1000 + t).integers(4, cfg.vocab, 16)
-        for q in [-1] + list(range(m)):
+        for q in [-1] + list(range(b, m)) + list(range(min(b, m))):
             if q < 0:
                 kind = "absent"
             else:

@@ -208,3 +208,50 @@ def test_argmax_records_log_sum_exp():
         assert rec.position == 3 + r
         assert rec.lse == pytest.approx(float(logsumexp(logits[r])), rel=1e-12, abs=1e-12)
         assert np.exp(rec.top1 - rec.lse) == pytest.approx(float(softmax(logits[r]).max()), rel=1e-12)
+
+
+# --- the bf16 storage contract, against an independent functional model ----------
+
+def test_reference_bf16_rounding_matches_torch_and_breaks_ties_to_even():
+    """tests/bf16_ref.bf16 (integer rounding of the float64 pattern) agrees with
+    torch's float32 -> bfloat16 conversion on float32 values, and on float64
+    values next to a tie it rounds by the exact value, not by a float32 copy."""
+    from tests.bf16_ref import bf16
+    g = np.random.default_rng(4)
+    x32 = (g.standard_normal(50000) * 10.0 ** g.integers(-30, 30, 50000)).astype(np.float32)
+    x32 = np.concatenate([x32, ((g.integers(1, 2 ** 15, 4000).astype(np.uint32) << 16) | 0x8000).view(np.float32)])
+    x32 = x32[np.isfinite(x32) & (np.abs(x32) >= 2.0 ** -126) & (np.abs(x32) < 3.3e38)]
+    want = torch.from_numpy(x32).to(torch.bfloat16).to(torch.float64)
+    np.testing.assert_array_equal(bf16(torch.from_numpy(x32.astype(np.float64))).numpy(), want.numpy())
+    # 1 + 2^-8 is a tie between 1 and 1 + 2^-7: a hair larger in magnitude rounds away from zero, a hair smaller towards it
+    for tie in (1.0 + 2.0 ** -8, -(1.0 + 2.0 ** -8), 1.5 + 2.0 ** -8, 3.0 + 2.0 ** -7):
+        r = bf16(torch.tensor([tie * (1 + 2.0 ** -40), tie * (1 - 2.0 ** -40), tie], dtype=torch.float64)).numpy()
+        assert abs(r[0]) > abs(tie) > abs(r[1])
+        assert r[2] in (r[0], r[1])
+        assert (torch.tensor([r[2]], dtype=torch.float64).view(torch.int64).item() >> 45) & 1 == 0   # the even one
+    np.testing.assert_array_equal(bf16(torch.tensor([0.0, -0.0], dtype=torch.float64)).numpy(), [0.0, -0.0])
+
+
+@pytest.mark.parametrize("cfg", [SMALL_POST.with_dtype(C.BF16), SMALL_PRE.with_dtype(C.BF16)],
+                         ids=["post_ln_relu_bf16", "pre_ln_gelu_bf16"])
+def test_bf16_storage_contract_matches_functional_reference(cfg):
+    """The oracle's bf16 model rounds at exactly the points of the storage
+    contract: its teacher-forced logits equal those of tests/bf16_ref (torch
+    functional layers, its own rounding) to 1e-12 relative, so one rounding
+    more or less anywhere (each moves logits by about 1e-3) fails."""
+    from tests.bf16_ref import Bf16Seq2Seq
+    w = synth.make_weights(cfg, seed=15, bias_std=0.3, ln_std=0.2)
+    M = oracle.Model(cfg, w.values)
+    ref = Bf16Seq2Seq(cfg, w.values)
+    g = np.random.default_rng(8)
+    for n, T in [(11, 9), (5, 14)]:
+        src = g.integers(4, cfg.vocab, n)
+        tgt = np.concatenate([[1], g.integers(0, cfg.vocab, T - 1)])
+        got = M.teacher_forced_logits(M.encode(src), tgt)
+        want = ref.logits(src, tgt)
+        rel = np.abs(got - want).max(-1) / np.abs(want).max(-1)
+        assert rel.max() < 1e-12, rel.max()
+    # the same model with no rounding at all differs at the 1e-3 level (the pin has power)
+    Mf = oracle.Model(dataclasses.replace(cfg, dtype=C.F32), w.values)
+    lf = Mf.teacher_forced_logits(Mf.encode(src), tgt)
+    assert (np.abs(lf - want).max(-1) / np.abs(want).max(-1)).max() > 1e-4
