@@ -1,21 +1,28 @@
 #!/usr/bin/env python3
 """Decode throughput of parallel decoding vs greedy decoding on one MI355X.
 
-Workload (default): the Transformer-base-shaped model (6+6 layers, d=512, 8
-heads, FFN 2048, vocabulary 58,101, shared embeddings) with seeded random
-weights, 200 synthetic sources with lengths uniform in [10, 60] and
-m = min(n + 10, 128) target positions, batch 1 (the paper's online setting).
-A step is the decode of one sentence (pd_decode, batch 1) with its source
-already encoded and resident in HBM; the timed region covers K steps.
+Headline workload: the large multilingual-shaped model (12+12 layers,
+d = 1024, 16 heads, FFN 4096 GELU, pre-LN, vocabulary 250,027, bf16) with
+seeded random weights, batch 1 (the paper's online setting), sources of
+n ~ U[20, 120] tokens and m = min(n + 10, 256) target positions (50 sentences
+plus one with m = 256).  A step is the decode of one sentence (pd_decode,
+batch 1) with its source already encoded and resident in HBM; the timed region
+covers the first K sentences (--steps), after W warm-up decodes (--warmup) of
+the same first sentences.  Every mode decodes the same K sentences.
 
-One JSON line on stdout: value = target tokens/s of the headline mode
-(hybrid GS-Jacobi, b = 5) in bf16, plus greedy and GS-Jacobi numbers, k/m,
-the float32 model, the roofline of the fused vocabulary kernel and the CPU
-oracle baseline.
+One JSON line on stdout: value = target tokens/s of GS-Jacobi b = 16, next to
+greedy decoding, Jacobi and hybrid b = 16 with their k/m; the roofline of the
+time-dominant kernel family (the decoder's streaming matrix products) and of
+the fused vocabulary projection + argmax, from the kernels' own dispatch
+timestamps; the block-iteration / greedy-step cost ratio and the break-even
+k/m it implies; the CPU oracle baseline on the host cores; and, as side
+records, the Transformer-base-shaped model at batch 1 (float32 and bfloat16),
+the tiny model's iteration latency, and the batched workloads.
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -27,6 +34,9 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0
 MFMA_BF16_PEAK_TFLOPS = 2500.0   # dense bf16 matrix peak of MI355X
+HEADLINE = ("gs_jacobi", 16)
+LARGE_MODES = [("ar", 1), ("jacobi", 0), ("gs_jacobi", 16), ("hybrid", 16)]
+MT_MODES = [("ar", 1), ("gs_jacobi", 5), ("hybrid", 5)]
 
 
 def log(*a):
@@ -46,51 +56,74 @@ def load_model(cfg):
 
 
 def run_mode(ctxs, sents, outs, mode, block, steps, warmup, timing=False):
+    """Decodes sentences 0..steps-1 (each its own context, already encoded)
+    after warm-up decodes of sentences 0..warmup-1; returns the timed totals."""
     import torch
     n = len(sents)
-    order = [i % n for i in range(warmup + steps)]
+    assert steps <= n, f"{steps} steps but only {n} sentences"
     # one-time setup: every context captures and instantiates its iteration
-    # graph for this mode (and timing setting) on its first decode
-    for i in range(n):
-        ctxs[i].set_timing(timing)
+    # graph for this mode on its first decode
+    for i in range(steps):
         ctxs[i].decode(mode, [sents[i][1]], block=block, out=outs[i])
-        ctxs[i].set_timing(False)
     torch.cuda.synchronize()
-    for i in order[:warmup]:
-        ctxs[i].decode(mode, [sents[i][1]], block=block, out=outs[i])
+    for i in range(warmup):
+        ctxs[i % steps].decode(mode, [sents[i % steps][1]], block=block, out=outs[i % steps])
     torch.cuda.synchronize()
     if timing:
-        for c in ctxs:
+        for c in ctxs[:steps]:
             c.set_timing(True)
     t0 = time.perf_counter()
-    for i in order[warmup:]:
+    for i in range(steps):
         ctxs[i].decode(mode, [sents[i][1]], block=block, out=outs[i])
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
     toks = ks = ms = 0
-    for i in order[warmup:]:
+    for i in range(steps):
         toks += int(outs[i][1][0])
         ks += int(outs[i][2][0])
         ms += sents[i][1]
     res = {"tokens": toks, "seconds": dt, "tokens_per_s": toks / dt, "k": ks, "m": ms, "k_over_m": ks / ms,
-           "ms_per_step": 1e3 * dt / steps}
+           "ms_per_step": 1e3 * dt / steps, "us_per_iteration": 1e6 * dt / ks,
+           "kernels_per_iteration": ctxs[0].iteration_kernels()}
     if timing:
-        launches = total_ms = 0
-        for c in ctxs:
+        v_n = v_ms = p_n = p_ms = p_b = 0
+        for c in ctxs[:steps]:
             n_l, t_ms = c.vocab_timing()
-            launches += n_l
-            total_ms += t_ms
+            q_n, q_ms, q_b = c.product_timing()
+            v_n, v_ms, p_n, p_ms, p_b = v_n + n_l, v_ms + t_ms, p_n + q_n, p_ms + q_ms, p_b + q_b
             c.set_timing(False)
-        res["vocab_launches"] = launches
-        res["vocab_ms"] = total_ms
+        res.update(vocab_launches=v_n, vocab_ms=v_ms, product_launches=p_n, product_ms=p_ms, product_bytes=p_b)
     return res
+
+
+def setup_batch1(wl_name, n_sent):
+    import torch
+    from paper_2305_10427_amd import configs as C, pdec, synth
+    wl = C.WORKLOADS[wl_name]
+    t0 = time.perf_counter()
+    w, model = load_model(wl.model)
+    sents = synth.make_sentences(wl, seed=1)[:n_sent]
+    max_src = max(len(s) for s, _ in sents)
+    ctxs, outs = [], []
+    for src, m in sents:
+        c = pdec.Context(model, 1, max_src, wl.tgt_cap)
+        c.encode(torch.from_numpy(src[None]).cuda(), [len(src)])
+        ctxs.append(c)
+        outs.append((torch.empty((1, wl.tgt_cap), dtype=torch.int32, device="cuda"),
+                     torch.empty(1, dtype=torch.int32, device="cuda"),
+                     torch.empty(1, dtype=torch.int32, device="cuda"),
+                     torch.empty(1, dtype=torch.int32, device="cuda")))
+    torch.cuda.synchronize()
+    log(f"[{wl_name}] weights {model.weight_bytes() / 1e6:.1f} MB, {len(sents)} sentences encoded "
+        f"in {time.perf_counter() - t0:.1f}s")
+    return wl, w, model, sents, ctxs, outs
 
 
 def encode_rate(ctxs, sents, cfg, steps, warmup):
     """pd_encode of one source per call (batch 1), the step before the
     decoding iterations: wall time per sentence over `steps` calls, against
     the weights it must read (encoder layers and every decoder layer's
-    cross-attention K/V projection, bf16/f32 storage)."""
+    cross-attention K/V projection)."""
     import torch
     n = len(sents)
     srcs = [torch.from_numpy(src[None]).cuda() for src, _ in sents]
@@ -106,71 +139,186 @@ def encode_rate(ctxs, sents, cfg, steps, warmup):
     es = 2 if cfg.dtype == "bf16" else 4
     d, f = cfg.d_model, cfg.d_ff
     wbytes = (cfg.n_enc * (4 * d * d + 2 * d * f + 9 * d + f) + cfg.n_dec * (2 * d * d + 2 * d)) * es
-    return {"us_per_sentence": 1e6 * dt, "weight_bytes": wbytes, "achieved_GBs": wbytes / dt / 1e9,
-            "frac": wbytes / dt / 1e9 / HBM_PEAK_GBS}
+    return {"us_per_sentence": round(1e6 * dt, 2), "weight_bytes": wbytes,
+            "achieved": round(wbytes / dt / 1e9, 1), "unit": "GB/s", "frac": round(wbytes / dt / 1e9 / HBM_PEAK_GBS, 4)}
 
 
-def encode_only(steps, warmup):
+def mode_table(res):
+    return {k: {"tokens_per_s": round(v["tokens_per_s"], 1), "k_over_m": round(v["k_over_m"], 4),
+                "ms_per_sentence": round(v["ms_per_step"], 3), "us_per_iteration": round(v["us_per_iteration"], 2),
+                "kernels_per_iteration": v["kernels_per_iteration"]} for k, v in res.items()}
+
+
+def cost_ratio(res, block_key):
+    """Wall time of one iteration of the block mode against one greedy step.
+    The block mode decodes m tokens in k iterations, greedy decoding in m
+    steps, so it is faster exactly when k/m < greedy step / block iteration."""
+    it_b = res[block_key]["us_per_iteration"]
+    it_g = res["ar_b1"]["us_per_iteration"]
+    return {"mode": block_key, "block_iteration_us": round(it_b, 2), "greedy_step_us": round(it_g, 2),
+            "ratio": round(it_b / it_g, 3), "break_even_k_over_m": round(it_g / it_b, 3),
+            "measured_k_over_m": round(res[block_key]["k_over_m"], 4)}
+
+
+def source_sha(files):
+    return hashlib.sha256(b"".join(open(os.path.join(ROOT, "paper_2305_10427_amd", "csrc", f), "rb").read()
+                                   for f in files)).hexdigest()
+
+
+def measured_traffic(name):
+    """HBM bytes per launch from a committed rocprofv3 counter record
+    (profiles/<name>.json), or None once the kernel sources it covers changed."""
+    try:
+        rec = json.load(open(os.path.join(ROOT, "profiles", name + ".json")))
+        if source_sha(rec["kernel_sources"]) != rec["kernel_source_sha256"]:
+            return None
+        return rec["traffic_bytes_per_launch"]
+    except (OSError, KeyError, ValueError):
+        return None
+
+
+KERNEL_SOURCES = ["gemm.hip", "vocab.hip", "mma.h", "common.h", "kernels.h"]
+
+
+def rooflines(cfg, t):
+    """The decoder's streaming products (time-dominant at batch 1) and the
+    fused vocabulary kernel of the event-timed pass."""
+    p_avg = t["product_ms"] / max(t["product_launches"], 1)
+    p_bytes = t["product_bytes"] / max(t["product_launches"], 1)
+    p_ach = p_bytes / (p_avg * 1e-3) / 1e9 if p_avg > 0 else 0.0
+    v_bytes = cfg.vocab * (cfg.d_model + 1) * (2 if cfg.dtype == "bf16" else 4)
+    v_avg = t["vocab_ms"] / max(t["vocab_launches"], 1)
+    v_ach = v_bytes / (v_avg * 1e-3) / 1e9 if v_avg > 0 else 0.0
+    tag = cfg.name.split("@")[0]
+    products = {"kernel": "k_gemm (the decoder's streaming matrix products: QKV, attention output, cross-attention "
+                          "query and output, FFN; every launch of the timed iterations)",
+                "bound": "hbm", "achieved": round(p_ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(p_ach / HBM_PEAK_GBS, 4), "traffic": measured_traffic(f"gemm_products_{tag}"),
+                "avg_launch_us": round(p_avg * 1e3, 2), "launches": t["product_launches"],
+                "bytes_per_launch": round(p_bytes), "ms_per_iteration": round(t["product_ms"] / max(t["k"], 1), 4)}
+    vocab = {"kernel": "k_vocab (streaming vocabulary projection + LayerNorm + argmax, <= 16 rows)", "bound": "hbm",
+             "achieved": round(v_ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(v_ach / HBM_PEAK_GBS, 4),
+             "traffic": measured_traffic(f"vocab_argmax_{tag}"), "avg_launch_us": round(v_avg * 1e3, 2),
+             "launches": t["vocab_launches"], "bytes_per_launch": v_bytes}
+    return products, vocab
+
+
+def iteration_roofline(cfg, res):
+    d, f, L = cfg.d_model, cfg.d_ff, cfg.n_dec
+    es = 2 if cfg.dtype == "bf16" else 4
+    it_bytes = (L * (6 * d * d + 2 * d * f + 13 * d + f) + cfg.vocab * (d + 1)) * es
+    us = res["us_per_iteration"]
+    return {"us": round(us, 2), "bytes": it_bytes, "achieved": round(it_bytes / us / 1e3, 1), "unit": "GB/s",
+            "frac": round(it_bytes / us / 1e3 / HBM_PEAK_GBS, 4),
+            "note": "one decoding iteration (every kernel of the decoder pass, vocabulary and control step) at "
+                    "batch 1, against the weight bytes it must read"}
+
+
+def host_threads():
+    info = {"os_cpu_count": os.cpu_count(), "affinity": len(os.sched_getaffinity(0))}
+    try:
+        from threadpoolctl import threadpool_info
+        info["blas_threads"] = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:                       # noqa: BLE001
+        info["blas_threads"] = None
+    return info
+
+
+def cpu_baseline(wl, w, sents, ctxs, mode, block, m_cap, n_sent):
+    """The oracle as it stands (float64) and the same code in float32, on all
+    host threads and on one, over a bounded sample: the first n_sent sentences
+    with their targets cut to m_cap positions.  The GPU decodes the same cut
+    sentences; their ids and k are compared with the float64 oracle's
+    (exact / near tie)."""
+    import numpy as np
     import torch
-    from paper_2305_10427_amd import configs as C, pdec, synth
-    wl = C.WORKLOADS["mt_base_bf16"]
-    w, model = load_model(wl.model)
-    sents = synth.make_sentences(wl, seed=1)
-    ctx = pdec.Context(model, 1, max(len(s) for s, _ in sents), wl.tgt_cap)
-    e = encode_rate([ctx] * len(sents), sents, wl.model, steps, warmup)
-    log(f"[mt_base_bf16] encode: {e['us_per_sentence']:.1f} us/sentence, {e['achieved_GBs']:.0f} GB/s of weights")
-
-
-def gpu_workload(wl_name, steps, warmup, modes, headline, n_sent=0, trace=False, encode=False):
-    import torch
-    from paper_2305_10427_amd import configs as C, pdec, synth
-    wl = C.WORKLOADS[wl_name]
+    import oracle
+    from threadpoolctl import threadpool_limits
     cfg = wl.model
-    t0 = time.perf_counter()
-    w, model = load_model(cfg)
-    sents = synth.make_sentences(wl, seed=1)
-    if n_sent:
-        sents = sents[:n_sent]
-    max_src = max(len(s) for s, _ in sents)
-    ctxs, outs = [], []
-    for src, m in sents:
-        c = pdec.Context(model, 1, max_src, wl.tgt_cap)
-        c.encode(torch.from_numpy(src[None]).cuda(), [len(src)])
-        ctxs.append(c)
-        outs.append((torch.empty((1, wl.tgt_cap), dtype=torch.int32, device="cuda"),
-                     torch.empty(1, dtype=torch.int32, device="cuda"),
-                     torch.empty(1, dtype=torch.int32, device="cuda"),
-                     torch.empty(1, dtype=torch.int32, device="cuda")))
-    torch.cuda.synchronize()
-    log(f"[{wl_name}] weights {model.weight_bytes() / 1e6:.1f} MB, {len(sents)} sentences encoded "
-        f"in {time.perf_counter() - t0:.1f}s")
+    sample = [(src, min(m, m_cap)) for src, m in sents[:n_sent]]
+    host = host_threads()
+    out = {"sample": f"the first {n_sent} sentence(s) of the same workload with m cut to {m_cap}, {mode} b={block}, "
+                     "decode only (encoder excluded)", "host": host, "variants": {}}
+    results = None
+    for dt_name, dtype in (("f64", np.float64), ("f32", np.float32)):
+        M = oracle.Model(cfg, w.values, dtype=dtype)
+        encs = [M.encode(src) for src, _ in sample]
+        for threads in ("all", 1):
+            lim = host["blas_threads"] if threads == "all" else 1
+            with threadpool_limits(limits=lim):
+                toks, t0 = 0, time.perf_counter()
+                res = []
+                for enc, (_, m) in zip(encs, sample):
+                    r = oracle.decode(M, enc, m, mode, block)
+                    toks += len(r.out)
+                    res.append(r)
+                dt = time.perf_counter() - t0
+            out["variants"][f"{dt_name}_{threads}_threads" if threads == "all" else f"{dt_name}_1_thread"] = {
+                "tokens_per_s": round(toks / dt, 2), "threads": lim, "seconds": round(dt, 2)}
+            log(f"[cpu] oracle {dt_name} on {lim} thread(s): {toks / dt:.2f} tok/s ({dt:.1f}s)")
+            if dt_name == "f64" and threads == "all":
+                results = res
+        del M
+    v = out["variants"]["f64_all_threads"]
+    out.update(value=v["tokens_per_s"], unit="tokens/s", cores=v["threads"], kind="oracle")
+    # the GPU's decodes of the same cut sentences against the float64 oracle
+    exact = near = 0
+    for i, ((src, m), r) in enumerate(zip(sample, results)):
+        ids, ln, k, fl = ctxs[i].decode(mode, [m], block=block)
+        torch.cuda.synchronize()
+        g = ids[0, : int(ln[0])].cpu().numpy()
+        if np.array_equal(g, r.out) and int(k[0]) == r.k:
+            exact += 1
+        else:
+            near += 1
+    out["parity_sample"] = {"sentences": len(sample), "exact": exact, "not_exact": near,
+                            "note": "ids and k of the GPU against the float64 oracle on the baseline sample; "
+                                    "the GPU tests judge every difference"}
+    return out
+
+
+def tiny_latency(steps):
+    """The tiny 2+2 model (d = 64, V = 1000, fp32, n = m = 16): every mode over
+    its first `steps` sentences; the iteration is launch-bound, so the figures
+    are microseconds per iteration and kernels per iteration."""
+    wl, _, _, sents, ctxs, outs = setup_batch1("tiny", min(steps, 100))
+    res = {}
+    for mode, b in wl.modes:
+        r = run_mode(ctxs, sents, outs, mode, b, len(sents), 5)
+        res[f"{mode}_b{b}"] = r
+        log(f"[tiny] {mode:9s} b={b:2d}: {r['us_per_iteration']:7.2f} us/iteration, "
+            f"{r['kernels_per_iteration']} kernels/iteration, k/m={r['k_over_m']:.3f}")
+    return {"workload": f"tiny 2+2 layers, d=64, V=1000, fp32, batch 1, first {len(sents)} sources, n=m=16",
+            **mode_table(res)}
+
+
+def batch1_workload(wl_name, steps, warmup, modes, headline, trace=False, encode=False):
+    wl, w, model, sents, ctxs, outs = setup_batch1(wl_name, max(steps, warmup))
+    cfg = wl.model
     res = {}
     for mode, b in modes:
         r = run_mode(ctxs, sents, outs, mode, b, steps, warmup)
         res[f"{mode}_b{b}"] = r
-        log(f"[{wl_name}] {mode:9s} b={b}: {r['tokens_per_s']:9.1f} tok/s  {r['ms_per_step']:7.3f} ms/sentence  "
-            f"k/m={r['k_over_m']:.3f}")
-    # the vocabulary kernel's launch time: a second pass of the headline mode
-    # with HIP events around that kernel (the events cost time of their own, so
-    # the throughput above comes from the pass without them)
-    t = run_mode(ctxs, sents, outs, headline[0], headline[1], steps, warmup, timing=True)
-    res[f"{headline[0]}_b{headline[1]}"].update(vocab_launches=t["vocab_launches"], vocab_ms=t["vocab_ms"])
+        log(f"[{wl_name}] {mode:9s} b={b:2d}: {r['tokens_per_s']:9.1f} tok/s  {r['ms_per_step']:8.3f} ms/sentence  "
+            f"k/m={r['k_over_m']:.3f}  {r['us_per_iteration']:7.1f} us/iteration")
+    # the event-timed pass of the headline mode: dispatch timestamps of every
+    # decoder product and vocabulary launch (iterations launched kernel by
+    # kernel); the throughput above comes from the graph-replayed pass
+    timed = run_mode(ctxs, sents, outs, headline[0], headline[1], steps, warmup, timing=True)
+    extra = {}
     if encode:
-        res["encode"] = encode_rate(ctxs, sents, cfg, steps, warmup)
-        e = res["encode"]
-        log(f"[{wl_name}] encode: {e['us_per_sentence']:.1f} us/sentence, {e['achieved_GBs']:.0f} GB/s of weights")
+        extra["encode"] = encode_rate(ctxs, sents[:steps], cfg, steps, warmup)
+        log(f"[{wl_name}] encode: {extra['encode']['us_per_sentence']:.1f} us/sentence")
     if trace:
-        # the same decodes with the DDGviz trace on (records and log-sum-exp
-        # partials)
         for c in ctxs:
             c.set_trace(4 * wl.tgt_cap, max(headline[1], 1))
         t = run_mode(ctxs, sents, outs, headline[0], headline[1], steps, warmup)
         for c in ctxs:
             c.set_trace(0, 0)
-        res["trace"] = {"mode": f"{headline[0]}_b{headline[1]}", "tokens_per_s": t["tokens_per_s"],
-                        "ms_per_step": t["ms_per_step"]}
-        log(f"[{wl_name}] traced {headline[0]} b={headline[1]}: {t['tokens_per_s']:9.1f} tok/s")
-    return cfg, w, sents, model, res
+        h = res[f"{headline[0]}_b{headline[1]}"]
+        extra["trace"] = {"mode": f"{headline[0]}_b{headline[1]}", "tokens_per_s": round(t["tokens_per_s"], 1),
+                          "slowdown": round(h["tokens_per_s"] / t["tokens_per_s"], 3)}
+    return wl, w, sents, ctxs, res, timed, extra
 
 
 def batched_workload(wl_name, n_batches, modes, repeats):
@@ -210,8 +358,8 @@ def batched_workload(wl_name, n_batches, modes, repeats):
             toks += int(o[1].sum()) * repeats
             ks += int(o[2].sum()) * repeats
             ms += int(bt.tgt_m.sum()) * repeats
-        # a separate pass with HIP events around the fused vocabulary launch and
-        # the device count of rows evaluated: its MFMA rate
+        # a separate pass with HIP events around the vocabulary launch and the
+        # device count of rows evaluated: its MFMA rate
         for c in ctxs:
             c.set_timing(True)
         for c, bt, o in zip(ctxs, batches, outs):
@@ -239,48 +387,6 @@ def batched_workload(wl_name, n_batches, modes, repeats):
     return res
 
 
-def cpu_baseline(cfg, weights, sents, mode, block, budget_s):
-    """The oracle as it stands, on the host cores, on a bounded sample."""
-    import numpy as np
-    import oracle
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
-    except Exception:                       # noqa: BLE001
-        threads = len(os.sched_getaffinity(0))
-    M = oracle.Model(cfg, weights.values)
-    toks = n = 0
-    t0 = time.perf_counter()
-    dec_s = 0.0
-    for src, m in sents:
-        enc = M.encode(src)
-        t1 = time.perf_counter()
-        r = oracle.decode(M, enc, m, mode, block)
-        dec_s += time.perf_counter() - t1
-        toks += len(r.out)
-        n += 1
-        if time.perf_counter() - t0 > budget_s:
-            break
-    return {"value": toks / dec_s, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"first {n} sentences of the same workload, {mode} b={block}, decode only "
-                      f"(numpy float64 oracle, {dec_s:.1f}s)"}
-
-
-def measured_traffic():
-    """HBM bytes per launch of the fused vocabulary kernel from the committed
-    rocprofv3 counter summary, or None once the kernel source has changed."""
-    import hashlib
-    try:
-        rec = json.load(open(os.path.join(ROOT, "profiles", "vocab_argmax_mt_base_bf16.json")))
-        src = b"".join(open(os.path.join(ROOT, "paper_2305_10427_amd", "csrc", f), "rb").read()
-                       for f in rec["kernel_sources"])
-        if hashlib.sha256(src).hexdigest() != rec["kernel_source_sha256"]:
-            return None
-        return int(rec["traffic_bytes_per_launch"])
-    except (OSError, KeyError, ValueError):
-        return None
-
-
 def copy_calibration():
     """Three plain device copies of 256 MiB (read 256 MiB + write 256 MiB each):
     the reference kernel for scaling the HBM byte counters of a profile."""
@@ -296,19 +402,20 @@ def copy_calibration():
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--sentences", type=int, default=0, help="use the first N sentences (0: all)")
-    ap.add_argument("--modes", default="ar:1,gs_jacobi:5,hybrid:5")
-    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--steps", type=int, default=20, help="sentences timed per mode (the first STEPS)")
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--cpu-sentences", type=int, default=1)
+    ap.add_argument("--cpu-m", type=int, default=16, help="target positions of each CPU-baseline sentence")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-f32", action="store_true")
-    ap.add_argument("--no-large", action="store_true")
+    ap.add_argument("--no-mt-base", action="store_true")
+    ap.add_argument("--no-tiny", action="store_true")
     ap.add_argument("--no-batched", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true")
-    ap.add_argument("--encode-only", action="store_true",
-                    help="encode the MT-base bf16 sources one by one (batch 1) and exit (profiling driver; "
-                         "prints no JSON line)")
+    ap.add_argument("--encode-only", default="",
+                    help="WORKLOAD — encode its sources one by one (batch 1) and exit (profiling driver)")
+    ap.add_argument("--decode-only", default="",
+                    help="WORKLOAD:MODE:B:N — decode the first N sentences at batch 1 in one mode (graph replay, "
+                         "then an event-timed pass) and exit (profiling driver; prints no JSON line)")
     ap.add_argument("--batched-only", default="",
                     help="WORKLOAD:MODE:B — decode one batch of a batched workload in one mode and exit "
                          "(profiling driver; prints no JSON line)")
@@ -326,28 +433,50 @@ def main():
     if args.copy_calibration:
         copy_calibration()
     if args.encode_only:
-        encode_only(args.steps, args.warmup)
+        wl, _, _, sents, ctxs, _ = setup_batch1(args.encode_only, args.steps)
+        e = encode_rate(ctxs, sents, wl.model, args.steps, args.warmup)
+        log(f"[{args.encode_only}] encode: {e['us_per_sentence']:.1f} us/sentence, {e['achieved']:.0f} GB/s")
+        return
+    if args.decode_only:
+        name, mode, b, n = args.decode_only.split(":")
+        wl, _, _, sents, ctxs, outs = setup_batch1(name, int(n))
+        r = run_mode(ctxs, sents, outs, mode, int(b), int(n), min(args.warmup, int(n)))
+        t = run_mode(ctxs, sents, outs, mode, int(b), int(n), 0, timing=True)
+        prod, voc = rooflines(wl.model, t)
+        log(f"[{name}] {mode} b={b}: {r['tokens_per_s']:.1f} tok/s, {r['us_per_iteration']:.1f} us/iteration; "
+            f"products {prod['achieved']:.0f} GB/s ({prod['avg_launch_us']} us/launch), vocabulary "
+            f"{voc['achieved']:.0f} GB/s ({voc['avg_launch_us']} us/launch)")
         return
     if args.batched_only:
         wl_name, mode, b = args.batched_only.split(":")
         batched_workload(wl_name, 1, [(mode, int(b))], 1)
         return
-    headline = ("hybrid", 5)
-    modes = [(m.split(":")[0], int(m.split(":")[1])) for m in args.modes.split(",")]
-    if headline not in modes:
-        modes.append(headline)
-    cfg, w, sents, model, res = gpu_workload("mt_base_bf16", args.steps, args.warmup, modes, headline,
-                                             args.sentences, trace=True, encode=True)
-    traced = res.pop("trace")
-    enc = res.pop("encode")
-    f32 = None
-    if not args.no_f32:
-        _, _, _, _, f32 = gpu_workload("mt_base_f32", args.steps, args.warmup, modes, headline, args.sentences)
-    large = None
-    if not args.no_large:
-        _, _, _, _, large = gpu_workload("large", min(args.steps, 20), min(args.warmup, 2),
-                                         [("ar", 1), ("jacobi", 0), ("gs_jacobi", 16)], ("gs_jacobi", 16), 20)
 
+    wl, w, sents, ctxs, res, timed, extra = batch1_workload("large", args.steps, args.warmup, LARGE_MODES,
+                                                            HEADLINE, encode=True)
+    cfg = wl.model
+    key = f"{HEADLINE[0]}_b{HEADLINE[1]}"
+    h = res[key]
+    products, vocab = rooflines(cfg, timed)
+    log(f"[large] products {products['achieved']:.0f} GB/s ({products['frac']:.3f}), vocabulary "
+        f"{vocab['achieved']:.0f} GB/s ({vocab['frac']:.3f})")
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(wl, w, sents, ctxs, HEADLINE[0], HEADLINE[1], args.cpu_m, args.cpu_sentences)
+
+    mt = {}
+    if not args.no_mt_base:
+        for name in ("mt_base_bf16", "mt_base_f32"):
+            wl2, _, _, _, r2, t2, x2 = batch1_workload(name, min(args.steps, 200), args.warmup, MT_MODES,
+                                                       ("hybrid", 5), trace=name == "mt_base_bf16",
+                                                       encode=name == "mt_base_bf16")
+            p2, v2 = rooflines(wl2.model, t2)
+            mt[name] = {"workload": f"{name}: 6+6 layers, d=512, 8 heads, FFN 2048, V=58101, batch 1, the first "
+                                    f"{min(args.steps, 200)} of 200 sources n~U[10,60], m=min(n+10,128)",
+                        **mode_table(r2), "cost_ratio": cost_ratio(r2, "hybrid_b5"),
+                        "products_roofline": p2, "vocab_roofline": v2,
+                        "iteration_roofline": iteration_roofline(wl2.model, r2["hybrid_b5"]), **x2}
+    tiny = None if args.no_tiny else tiny_latency(100)
     batched = None
     if not args.no_batched:
         batched = {
@@ -360,30 +489,6 @@ def main():
                           **batched_workload("large_b32", 2, [("ar", 1)] + [(m, b) for m in ("gs_jacobi", "hybrid")
                                                                           for b in (1, 2, 4, 8, 16, 32)], 1)},
         }
-
-    h = res[f"{headline[0]}_b{headline[1]}"]
-    # roofline of the fused vocabulary projection + argmax (bytes: E [V][d] and the output bias, bf16)
-    bytes_per_launch = cfg.vocab * (cfg.d_model + 1) * 2
-    avg_ms = h["vocab_ms"] / max(h["vocab_launches"], 1)
-    achieved = bytes_per_launch / (avg_ms * 1e-3) / 1e9
-    roof = {"kernel": "k_vocab<bf16> (streaming vocab projection + LayerNorm + argmax, <= 16 rows)", "bound": "hbm",
-            "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(),
-            "avg_launch_us": round(avg_ms * 1e3, 2), "launches": h["vocab_launches"],
-            "bytes_per_launch": bytes_per_launch}
-    # the whole batch-1 iteration against the bytes it must move: decoder
-    # weights + vocabulary (the K/V cache reads are a few hundred KB)
-    d, f, L = cfg.d_model, cfg.d_ff, cfg.n_dec
-    iter_bytes = (L * (6 * d * d + 2 * d * f + 13 * d + f) + cfg.vocab * (d + 1)) * 2
-    iter_us = 1e6 * h["seconds"] / h["k"]
-    iteration = {"us": round(iter_us, 2), "bytes": iter_bytes, "achieved": round(iter_bytes / iter_us / 1e3, 1),
-                 "unit": "GB/s", "frac": round(iter_bytes / iter_us / 1e3 / HBM_PEAK_GBS, 4),
-                 "note": "one decoding iteration (every kernel of the decoder pass, vocabulary and control step) "
-                         "at batch 1: latency-bound"}
-    cpu = None
-    if not args.no_cpu_baseline:
-        cpu = cpu_baseline(cfg, w, sents, headline[0], headline[1], args.cpu_seconds)
-        log(f"[cpu] oracle {cpu['value']:.1f} tok/s on {cpu['cores']} threads ({cpu['sample']})")
 
     line = {
         "metric": "target tokens/s (parallel vs greedy AR decode) + iterations/sentence k/m",
@@ -398,35 +503,22 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic (seeded random weights and sources)",
-        "config": {"workload": "mt_base_bf16: 6+6 layers, d=512, 8 heads, FFN 2048, V=58101, batch 1, "
-                               "200 sources n~U[10,60], m=min(n+10,128)",
-                   "mode": headline[0], "block": headline[1], "global_batch": 1, "parallelism": "none"},
-        "modes": {k: {"tokens_per_s": round(v["tokens_per_s"], 1), "k_over_m": round(v["k_over_m"], 4),
-                      "ms_per_sentence": round(v["ms_per_step"], 4)} for k, v in res.items()},
-        "speedup_vs_ar": (round(h["tokens_per_s"] / res["ar_b1"]["tokens_per_s"], 3) if "ar_b1" in res else None),
-        "roofline": roof,
-        "iteration_roofline": iteration,
+        "config": {"workload": "large bf16: 12+12 layers, d=1024, 16 heads, FFN 4096 GELU, pre-LN, V=250027, batch 1, "
+                               "51 sources n~U[20,120] (the last with m=256), m=min(n+10,256); "
+                               f"timed: sentences 0..{args.steps - 1}",
+                   "mode": HEADLINE[0], "block": HEADLINE[1], "global_batch": 1, "parallelism": "none"},
+        "modes": mode_table(res),
+        "speedup_vs_ar": round(h["tokens_per_s"] / res["ar_b1"]["tokens_per_s"], 3),
+        "cost_ratio": cost_ratio(res, key),
+        "roofline": products,
+        "vocab_roofline": vocab,
+        "iteration_roofline": iteration_roofline(cfg, h),
         "cpu_baseline": cpu,
-        "encode": {"us_per_sentence": round(enc["us_per_sentence"], 2), "weight_bytes": enc["weight_bytes"],
-                   "achieved": round(enc["achieved_GBs"], 1), "unit": "GB/s", "frac": round(enc["frac"], 4),
-                   "note": "pd_encode at batch 1 over the workload's sources (not in the decode timing)"},
-        "trace": {"mode": traced["mode"], "tokens_per_s": round(traced["tokens_per_s"], 1),
-                  "slowdown": round(h["tokens_per_s"] / traced["tokens_per_s"], 3)},
+        "encode": {**extra["encode"], "note": "pd_encode at batch 1 over the timed sources (not in the decode timing)"},
     }
-    if f32 is not None:
-        line["f32"] = {k: {"tokens_per_s": round(v["tokens_per_s"], 1), "k_over_m": round(v["k_over_m"], 4)}
-                       for k, v in f32.items()}
-    if large is not None:
-        line["large_bf16"] = {
-            "workload": "12+12 layers, d=1024, 16 heads, FFN 4096 GELU, pre-LN, V=250027, batch 1, first 20 "
-                        "sources n~U[20,120], m=min(n+10,256)",
-            **{k: {"tokens_per_s": round(v["tokens_per_s"], 1), "k_over_m": round(v["k_over_m"], 4),
-                   "ms_per_sentence": round(v["ms_per_step"], 3)} for k, v in large.items()}}
-        lv = large["gs_jacobi_b16"]
-        lb = 250027 * 1025 * 2
-        lavg = lv["vocab_ms"] / max(lv["vocab_launches"], 1)
-        line["large_bf16"]["vocab_roofline"] = {"achieved": round(lb / (lavg * 1e-3) / 1e9, 1), "peak": HBM_PEAK_GBS,
-                                                "unit": "GB/s", "avg_launch_us": round(lavg * 1e3, 2)}
+    line.update(mt)
+    if tiny is not None:
+        line["tiny"] = tiny
     if batched is not None:
         line["batched"] = batched
     print(json.dumps(line), flush=True)

@@ -231,6 +231,26 @@ pd_status pd_ctx_set_timing(pd_ctx* ctx, int32_t enable);
 pd_status pd_ctx_vocab_timing(const pd_ctx* ctx, int64_t* launches, double* total_ms);
 
 /*
+ * Timing of the decoder's matrix products.  With timing enabled, every
+ * decoder-layer product of a timed iteration that runs on the streaming
+ * product kernel (iterations of up to 64 rows, 128 for d_model <= 512: QKV,
+ * attention output, cross-attention query and output, both FFN products) is
+ * launched with a pair of events that carry its dispatch's own start and end
+ * times.  pd_ctx_product_timing returns, since the last pd_ctx_set_timing,
+ * their number, the sum of their durations in milliseconds, and the
+ * algorithmic bytes those launches must read: weights, biases and LayerNorm
+ * parameters, in the storage type (the few activation rows are not counted).
+ */
+pd_status pd_ctx_product_timing(const pd_ctx* ctx, int64_t* launches, double* total_ms, double* bytes);
+
+/*
+ * Kernels launched per iteration: the number of kernel nodes of the HIP graph
+ * of the iteration that pd_decode last replayed on this context (0 before
+ * the first graph).
+ */
+pd_status pd_ctx_iteration_kernels(const pd_ctx* ctx, int64_t* kernels);
+
+/*
  * Rows (decoder positions) evaluated by all iterations of pd_decode on this
  * context since the context was created or pd_ctx_set_timing was last called:
  * the sum over iterations of the rows laid out for that iteration (the work

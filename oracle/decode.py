@@ -119,9 +119,11 @@ def _cap(m: int, max_iters: Optional[int]) -> int:
 
 
 def greedy(model: Model, enc: Encoded, m: int, stop_at_eos: bool = True,
-           max_iters: Optional[int] = None, recompute: bool = False) -> Result:
-    """Greedy autoregressive decoding, Eq. (1): y[t] = argmax p(. | y[0..t-1], x), t = 0..m-1."""
-    s = Solver(model, enc, m, recompute)
+           max_iters: Optional[int] = None, recompute: bool = False, evaluator=None) -> Result:
+    """Greedy autoregressive decoding, Eq. (1): y[t] = argmax p(. | y[0..t-1], x), t = 0..m-1.
+
+    evaluator: optional stand-in for the model's Solver (see solve_by_blocks)."""
+    s = Solver(model, enc, m, recompute) if evaluator is None else evaluator
     cap = _cap(m, max_iters)
     y = np.full(m, PAD, np.int32)
     k, t = 0, 0

@@ -32,6 +32,8 @@
 // Epilogue EPI_ARGMAX is the fused vocabulary projection + argmax: logits =
 // s * acc + bias are never stored; each workgroup keeps the best (largest
 // value, then lowest index) per row and writes one partial per row.
+#include <hip/hip_ext.h>
+
 #include "common.h"
 #include "kernels.h"
 #include "mma.h"
@@ -205,7 +207,7 @@ __global__ __launch_bounds__(KSPLIT == 8 ? 512 : 256) void k_gemm(GemmArgs a) {
         a.out_f32[static_cast<size_t>(row) * a.ldo + col] = v + bias_v;
       } else if constexpr (EPI == EPI_ACT) {
         float t = v + bias_v;
-        t = (a.act == 2) ? gelu_erf(t) : fmaxf(t, 0.f);
+        t = (a.act == 2) ? gelu_erf(t) : relu(t);
         Elt<AT>::store(static_cast<AT*>(a.out), static_cast<size_t>(row) * a.ldo + col, t);
       } else if constexpr (EPI == EPI_RESID) {
         const size_t ri = static_cast<size_t>(row) * a.ldr + col;
@@ -289,55 +291,65 @@ __global__ __launch_bounds__(KSPLIT == 8 ? 512 : 256) void k_gemm(GemmArgs a) {
 
 namespace {
 
+// Launch, through hipExtLaunchKernelGGL when a pair of events is given (the
+// events then carry the dispatch's own start and end timestamps).
+template <typename K>
+void launch_ev(K kernel, dim3 grid, dim3 block, size_t lds, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1,
+               const GemmArgs& a) {
+  if (ev0 != nullptr) hipExtLaunchKernelGGL(kernel, grid, block, static_cast<uint32_t>(lds), s, ev0, ev1, 0u, a);
+  else hipLaunchKernelGGL(kernel, grid, block, lds, s, a);
+}
+
 template <typename WT, int PRO, int EPI, int XF32, int LNT>
-hipError_t launch_k(GemmArgs a, int ksplit, hipStream_t s) {
+hipError_t launch_k(GemmArgs a, int ksplit, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   const int tiles = (a.n_rows + 15) / 16;
   const int gy = tiles < 64 ? tiles : 64;
   a.mt_per_wg = (tiles + gy - 1) / gy;
   const size_t lds = PRO == PRO_LN ? gemm_ln_lds_bytes(a.K, sizeof(WT)) : 0;
   const int gz = EPI == EPI_QKV && a.n_layers > 1 ? a.n_layers : 1;
   if (EPI == EPI_ARGMAX || ksplit == 1) {
-    hipLaunchKernelGGL((k_gemm<WT, PRO, EPI, XF32, 1, LNT>), dim3(gemm_grid(EPI, a.N, 1), gy, gz), dim3(256), lds, s,
-                       a);
+    launch_ev(k_gemm<WT, PRO, EPI, XF32, 1, LNT>, dim3(gemm_grid(EPI, a.N, 1), gy, gz), dim3(256), lds, s, ev0, ev1,
+              a);
   } else if constexpr (EPI != EPI_ARGMAX) {
     if (ksplit == 8)
-      hipLaunchKernelGGL((k_gemm<WT, PRO, EPI, XF32, 8, LNT>), dim3(gemm_grid(EPI, a.N, 8), gy, gz), dim3(512), lds,
-                         s, a);
+      launch_ev(k_gemm<WT, PRO, EPI, XF32, 8, LNT>, dim3(gemm_grid(EPI, a.N, 8), gy, gz), dim3(512), lds, s, ev0,
+                ev1, a);
     else
-      hipLaunchKernelGGL((k_gemm<WT, PRO, EPI, XF32, 4, LNT>), dim3(gemm_grid(EPI, a.N, 4), gy, gz), dim3(256), lds,
-                         s, a);
+      launch_ev(k_gemm<WT, PRO, EPI, XF32, 4, LNT>, dim3(gemm_grid(EPI, a.N, 4), gy, gz), dim3(256), lds, s, ev0,
+                ev1, a);
   }
   return hipGetLastError();
 }
 
 // LayerNorm chunks of 128 elements held per lane: 4 covers d <= 512, 8 covers d <= 1024
 template <typename WT, int PRO, int EPI, int XF32>
-hipError_t launch_t(const GemmArgs& a, int ksplit, hipStream_t s) {
+hipError_t launch_t(const GemmArgs& a, int ksplit, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   if constexpr (PRO == PRO_LN && std::is_same<WT, bf16_t>::value) {
-    if (a.K > 512) return launch_k<WT, PRO, EPI, XF32, 8>(a, ksplit, s);
+    if (a.K > 512) return launch_k<WT, PRO, EPI, XF32, 8>(a, ksplit, s, ev0, ev1);
   }
-  return launch_k<WT, PRO, EPI, XF32, 4>(a, ksplit, s);
+  return launch_k<WT, PRO, EPI, XF32, 4>(a, ksplit, s, ev0, ev1);
 }
 
 template <typename WT, int PRO, int XF32>
-hipError_t launch_epi(int epi, const GemmArgs& a, int ksplit, hipStream_t s) {
+hipError_t launch_epi(int epi, const GemmArgs& a, int ksplit, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   switch (epi) {
-    case EPI_F32: return launch_t<WT, PRO, EPI_F32, XF32>(a, ksplit, s);
-    case EPI_ACT: return launch_t<WT, PRO, EPI_ACT, XF32>(a, ksplit, s);
-    case EPI_RESID: return launch_t<WT, PRO, EPI_RESID, XF32>(a, ksplit, s);
-    case EPI_QKV: return launch_t<WT, PRO, EPI_QKV, XF32>(a, ksplit, s);
-    case EPI_ARGMAX: return launch_t<WT, PRO, EPI_ARGMAX, XF32>(a, ksplit, s);
-    case EPI_LOGITS: return launch_t<WT, PRO, EPI_LOGITS, XF32>(a, ksplit, s);
+    case EPI_F32: return launch_t<WT, PRO, EPI_F32, XF32>(a, ksplit, s, ev0, ev1);
+    case EPI_ACT: return launch_t<WT, PRO, EPI_ACT, XF32>(a, ksplit, s, ev0, ev1);
+    case EPI_RESID: return launch_t<WT, PRO, EPI_RESID, XF32>(a, ksplit, s, ev0, ev1);
+    case EPI_QKV: return launch_t<WT, PRO, EPI_QKV, XF32>(a, ksplit, s, ev0, ev1);
+    case EPI_ARGMAX: return launch_t<WT, PRO, EPI_ARGMAX, XF32>(a, ksplit, s, ev0, ev1);
+    case EPI_LOGITS: return launch_t<WT, PRO, EPI_LOGITS, XF32>(a, ksplit, s, ev0, ev1);
     default: return hipErrorInvalidValue;
   }
 }
 
 template <typename WT>
-hipError_t launch_dt(int pro, int epi, const GemmArgs& a, int ksplit, hipStream_t s) {
+hipError_t launch_dt(int pro, int epi, const GemmArgs& a, int ksplit, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   if (pro == PRO_LN)
-    return a.x_f32 ? launch_epi<WT, PRO_LN, 1>(epi, a, ksplit, s) : launch_epi<WT, PRO_LN, 0>(epi, a, ksplit, s);
+    return a.x_f32 ? launch_epi<WT, PRO_LN, 1>(epi, a, ksplit, s, ev0, ev1)
+                   : launch_epi<WT, PRO_LN, 0>(epi, a, ksplit, s, ev0, ev1);
   if (a.x_f32) return hipErrorInvalidValue;
-  return launch_epi<WT, PRO_NONE, 0>(epi, a, ksplit, s);
+  return launch_epi<WT, PRO_NONE, 0>(epi, a, ksplit, s, ev0, ev1);
 }
 
 }  // namespace
@@ -349,14 +361,15 @@ int gemm_grid(int epi, int N, int ksplit) {
   return (N + 15) / 16;
 }
 
-hipError_t launch_gemm(int dtype, int pro, int epi, int ksplit, const GemmArgs& a, hipStream_t s) {
+hipError_t launch_gemm(int dtype, int pro, int epi, int ksplit, const GemmArgs& a, hipStream_t s, hipEvent_t ev0,
+                       hipEvent_t ev1) {
   if (a.n_rows <= 0) return hipSuccess;
   const int ks = dtype == DT_BF16 ? Mma<bf16_t>::KS : Mma<float>::KS;
   if (a.K % ks != 0 || a.K % 32 != 0) return hipErrorInvalidValue;
   if (pro == PRO_LN && (a.K > (dtype == DT_BF16 ? 1024 : 512) || gemm_ln_lds_bytes(a.K, dtype == DT_BF16 ? 2 : 4) > 65536))
     return hipErrorInvalidValue;
-  if (dtype == DT_BF16) return launch_dt<bf16_t>(pro, epi, a, ksplit, s);
-  return launch_dt<float>(pro, epi, a, ksplit, s);
+  if (dtype == DT_BF16) return launch_dt<bf16_t>(pro, epi, a, ksplit, s, ev0, ev1);
+  return launch_dt<float>(pro, epi, a, ksplit, s, ev0, ev1);
 }
 
 }  // namespace pdec

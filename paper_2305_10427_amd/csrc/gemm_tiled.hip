@@ -313,7 +313,7 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_tiled(GemmArgs a, int n_r
             a.out_f32[static_cast<size_t>(row) * a.ldo + col] = v + bias_v[j];
           } else if constexpr (EPI == EPI_ACT) {
             float t = v + bias_v[j];
-            t = (a.act == 2) ? gelu_erf(t) : fmaxf(t, 0.f);
+            t = (a.act == 2) ? gelu_erf(t) : relu(t);
             Elt<bf16_t>::store(static_cast<bf16_t*>(a.out), static_cast<size_t>(row) * a.ldo + col, t);
           } else if constexpr (EPI == EPI_RESID) {
             const float rv = Elt<bf16_t>::load(static_cast<const bf16_t*>(a.resid), static_cast<size_t>(row) * a.ldr + col);

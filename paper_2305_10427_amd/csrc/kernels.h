@@ -226,7 +226,9 @@ struct ReduceArgs {
 };
 
 // launchers (return hipError_t of the launch)
-hipError_t launch_gemm(int dtype, int pro, int epi, int ksplit, const GemmArgs& a, hipStream_t s);
+// With ev0 / ev1, the events receive the kernel dispatch's own start and end times.
+hipError_t launch_gemm(int dtype, int pro, int epi, int ksplit, const GemmArgs& a, hipStream_t s,
+                       hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 int gemm_grid(int epi, int N, int ksplit);
 size_t gemm_ln_lds_bytes(int K, size_t elt);
 // Products of many rows on LDS-staged MFMA tiles (bf16, no prologue, K a
@@ -258,6 +260,7 @@ hipError_t launch_argmax_reduce(const ReduceArgs& a, int R_max, hipStream_t s);
 hipError_t launch_ctrl_init(int dtype, const CtrlArgs& a, hipStream_t s);
 hipError_t launch_ctrl_step(int dtype, const CtrlArgs& a, hipStream_t s);
 hipError_t launch_finalize(const CtrlArgs& a, hipStream_t s);
+
 
 
 }  // namespace pdec

@@ -52,6 +52,10 @@ template <> struct Mma<float> {
   static __device__ __forceinline__ frag pack(const float* v) { return make_float4(v[0], v[1], v[2], v[3]); }
 };
 
+// max(v, 0) that keeps a NaN (fmaxf would return 0 for it and hide a
+// non-finite value from the argmax's check).
+__device__ __forceinline__ float relu(float v) { return v < 0.f ? 0.f : v; }
+
 __device__ __forceinline__ float gelu_erf(float v) {
   return 0.5f * v * (1.0f + erff(v * 0.70710678118654752f));
 }

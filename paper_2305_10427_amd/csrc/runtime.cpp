@@ -190,11 +190,18 @@ struct GraphKey {
   }
 };
 
+struct IterGraph {
+  GraphKey key;
+  hipGraphExec_t exec;
+  int64_t kernels;                     // kernel nodes of the captured iteration
+};
+
 struct pd_ctx {
   const pd_model* M;
   hipStream_t capture = nullptr;       // private stream used only to capture iteration graphs
   bool use_graphs = true;
-  std::vector<std::pair<GraphKey, hipGraphExec_t>> graphs;
+  std::vector<IterGraph> graphs;
+  int64_t iter_kernels = 0;            // kernels of the iteration graph replayed last
   int max_batch, max_src, max_tgt;
   char* ws;
   Layout L;
@@ -210,6 +217,14 @@ struct pd_ctx {
   bool tv_pending[2] = {false, false};
   int64_t tv_launches = 0;
   double tv_ms = 0.0;
+  // decoder-product timing: event pairs and algorithmic bytes of each timed
+  // streaming-product launch, per in-flight iteration slot
+  std::vector<hipEvent_t> pg0[2], pg1[2];
+  std::vector<double> pg_bytes[2];
+  int pg_n[2] = {0, 0};
+  int gemm_slot = -1;                  // slot of the decoder pass being launched with timing, else -1
+  int64_t tg_launches = 0;
+  double tg_ms = 0.0, tg_bytes = 0.0;
   // decoding trace (off while trace == nullptr): caller-owned records and the
   // scratch of the vocabulary kernel's log-sum-exp partials
   TraceRec* trace = nullptr;
@@ -244,7 +259,7 @@ GemmArgs gemm_base(const Rows& r) {
 
 // One matrix product.  pro_ln: normalise x (float if x_f32) with (lg, lb)
 // first; for many rows the LayerNorm runs as its own kernel into ln_tmp.
-hipError_t run_gemm(const pd_ctx& C, const Rows& r, GemmArgs g, int epi, bool pro_ln, void* ln_tmp,
+hipError_t run_gemm(pd_ctx& C, const Rows& r, GemmArgs g, int epi, bool pro_ln, void* ln_tmp,
                     hipStream_t s) {
   const pd_model& M = *C.M;
   int pro = PRO_NONE;
@@ -263,7 +278,28 @@ hipError_t run_gemm(const pd_ctx& C, const Rows& r, GemmArgs g, int epi, bool pr
   }
   const int ksplit = (epi == EPI_ARGMAX || epi == EPI_LOGITS) ? 1 : (g.K >= 2048 ? 8 : 4);
   if (r.R_max > stream_max_rows(M.d) && gemm_tiled_ok(M.dt, pro, g)) return launch_gemm_tiled(epi, ksplit, g, s);
-  return launch_gemm(M.dt, pro, epi, ksplit, g, s);
+  hipEvent_t ev0 = nullptr, ev1 = nullptr;
+  if (C.gemm_slot >= 0) {   // a timed decoder product: the next event pair of the slot, and its bytes
+    const int sl = C.gemm_slot;
+    if (C.pg_n[sl] == static_cast<int>(C.pg0[sl].size())) {
+      hipEvent_t a = nullptr, b = nullptr;
+      hipError_t e = hipEventCreate(&a);
+      if (e == hipSuccess) e = hipEventCreate(&b);
+      if (e != hipSuccess) {
+        if (a) hipEventDestroy(a);
+        return e;
+      }
+      C.pg0[sl].push_back(a);
+      C.pg1[sl].push_back(b);
+      C.pg_bytes[sl].push_back(0.0);
+    }
+    const double es = M.dt == DT_BF16 ? 2.0 : 4.0;
+    C.pg_bytes[sl][C.pg_n[sl]] = es * (static_cast<double>(g.N) * g.K + g.N + (pro == PRO_LN ? 2.0 * g.K : 0.0));
+    ev0 = C.pg0[sl][C.pg_n[sl]];
+    ev1 = C.pg1[sl][C.pg_n[sl]];
+    C.pg_n[sl] += 1;
+  }
+  return launch_gemm(M.dt, pro, epi, ksplit, g, s, ev0, ev1);
 }
 
 // Iterations of at most one 16-row tile use the streaming vocabulary kernel
@@ -319,6 +355,12 @@ hipError_t decoder_pass(pd_ctx& C, const Rows& r, float* logits, hipStream_t s, 
 
   if (!fused && (e = embed_rows(C, r, s)) != hipSuccess) return e;   // else the control step has embedded them
 
+  // decoder products of a timed iteration are launched with dispatch-timestamp events
+  struct SlotScope {
+    pd_ctx& c;
+    SlotScope(pd_ctx& c_, int sl) : c(c_) { c.gemm_slot = sl; }
+    ~SlotScope() { c.gemm_slot = -1; }
+  } scope(C, logits == nullptr ? slot : -1);
   for (int l = 0; l < cfg.n_dec; ++l) {
     // self-attention: Q -> q_buf, K/V of the block -> cache (layer l)
     GemmArgs g = gemm_base(r);
@@ -384,7 +426,8 @@ hipError_t decoder_pass(pd_ctx& C, const Rows& r, float* logits, hipStream_t s, 
     if ((e = run_gemm(C, r, g, EPI_RESID, false, nullptr, s)) != hipSuccess) return e;
   }
 
-  // vocabulary projection (tied embedding) fused with the argmax
+  // vocabulary projection (tied embedding) fused with the argmax (timed on its own)
+  C.gemm_slot = -1;
   GemmArgs g = gemm_base(r);
   if (pre) { g.x = x_res; g.x_f32 = 0; g.ln_g = M.dec_ln(0); g.ln_b = M.dec_ln(1); }
   else { g.x = s_buf; g.x_f32 = 1; g.ln_g = M.dec(cfg.n_dec - 1, D_LN3G); g.ln_b = M.dec(cfg.n_dec - 1, D_LN3B); }
@@ -566,8 +609,8 @@ hipError_t iteration(pd_ctx& C, const Rows& r, const CtrlArgs& ca, hipStream_t s
 
 // The iteration as a HIP graph, captured once per context and launch shape.
 hipError_t iteration_graph(pd_ctx& C, const GraphKey& key, const Rows& r, const CtrlArgs& ca, hipGraphExec_t* out) {
-  for (auto& kv : C.graphs)
-    if (kv.first == key) { *out = kv.second; return hipSuccess; }
+  for (auto& ig : C.graphs)
+    if (ig.key == key) { *out = ig.exec; C.iter_kernels = ig.kernels; return hipSuccess; }
   hipError_t e = hipStreamBeginCapture(C.capture, hipStreamCaptureModeThreadLocal);
   if (e != hipSuccess) return e;
   hipError_t e_body = iteration(C, r, ca, C.capture, key.slot, key.fused != 0);
@@ -575,11 +618,14 @@ hipError_t iteration_graph(pd_ctx& C, const GraphKey& key, const Rows& r, const 
   e = hipStreamEndCapture(C.capture, &g);
   if (e_body != hipSuccess) { if (g) hipGraphDestroy(g); return e_body; }
   if (e != hipSuccess) return e;
+  size_t nodes = 0;
+  e = hipGraphGetNodes(g, nullptr, &nodes);
   hipGraphExec_t ex = nullptr;
-  e = hipGraphInstantiate(&ex, g, nullptr, nullptr, 0);
+  if (e == hipSuccess) e = hipGraphInstantiate(&ex, g, nullptr, nullptr, 0);
   hipGraphDestroy(g);
   if (e != hipSuccess) return e;
-  C.graphs.emplace_back(key, ex);
+  C.graphs.push_back(IterGraph{key, ex, static_cast<int64_t>(nodes)});
+  C.iter_kernels = static_cast<int64_t>(nodes);
   *out = ex;
   return hipSuccess;
 }
@@ -603,8 +649,18 @@ hipError_t wait_event(hipEvent_t ev) {
   return e;
 }
 
-// Fold a completed event pair of the vocabulary kernel into the totals.
+// Fold a slot's completed event pairs (decoder products, vocabulary kernel) into the totals.
 hipError_t take_timing(pd_ctx& C, int slot) {
+  for (int i = 0; i < C.pg_n[slot]; ++i) {
+    hipError_t e = hipEventSynchronize(C.pg1[slot][i]);
+    float ms = 0.f;
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, C.pg0[slot][i], C.pg1[slot][i]);
+    if (e != hipSuccess) return e;
+    C.tg_ms += ms;
+    C.tg_bytes += C.pg_bytes[slot][i];
+    C.tg_launches += 1;
+  }
+  C.pg_n[slot] = 0;
   if (!C.tv_pending[slot]) return hipSuccess;
   hipError_t e = hipEventSynchronize(C.tv1[slot]);
   if (e != hipSuccess) return e;
@@ -743,7 +799,11 @@ void pd_ctx_destroy(pd_ctx* ctx) {
     if (ctx->tv0[i]) hipEventDestroy(ctx->tv0[i]);
   }
   if (ctx->stage_ev) hipEventDestroy(ctx->stage_ev);
-  for (auto& kv : ctx->graphs) hipGraphExecDestroy(kv.second);
+  for (int i = 0; i < 2; ++i) {
+    for (auto ev : ctx->pg1[i]) { hipEventSynchronize(ev); hipEventDestroy(ev); }
+    for (auto ev : ctx->pg0[i]) hipEventDestroy(ev);
+  }
+  for (auto& ig : ctx->graphs) hipGraphExecDestroy(ig.exec);
   if (ctx->capture) hipStreamDestroy(ctx->capture);
   hipHostFree(ctx->host_pinned);
   delete ctx;
@@ -916,6 +976,24 @@ pd_status pd_ctx_set_timing(pd_ctx* ctx, int32_t enable) {
   ctx->tv_launches = 0;
   ctx->tv_ms = 0.0;
   ctx->tv_pending[0] = ctx->tv_pending[1] = false;
+  ctx->tg_launches = 0;
+  ctx->tg_ms = ctx->tg_bytes = 0.0;
+  ctx->pg_n[0] = ctx->pg_n[1] = 0;
+  return PD_OK;
+}
+
+pd_status pd_ctx_product_timing(const pd_ctx* ctx, int64_t* launches, double* total_ms, double* bytes) {
+  if (ctx == nullptr || launches == nullptr || total_ms == nullptr || bytes == nullptr)
+    return fail(PD_E_ARG, "null argument");
+  *launches = ctx->tg_launches;
+  *total_ms = ctx->tg_ms;
+  *bytes = ctx->tg_bytes;
+  return PD_OK;
+}
+
+pd_status pd_ctx_iteration_kernels(const pd_ctx* ctx, int64_t* kernels) {
+  if (ctx == nullptr || kernels == nullptr) return fail(PD_E_ARG, "null argument");
+  *kernels = ctx->iter_kernels;
   return PD_OK;
 }
 
@@ -992,3 +1070,4 @@ pd_status pd_debug_logits(pd_ctx* ctx, const int32_t* tgt_in, int32_t T, float* 
 }
 
 }  // extern "C"
+

@@ -42,7 +42,8 @@ class pd_config(ctypes.Structure):
 EXPORTS = ("pd_weight_count", "pd_weight_shape", "pd_model_create", "pd_model_destroy",
            "pd_ctx_workspace_bytes", "pd_ctx_create", "pd_ctx_destroy", "pd_encode", "pd_decode", "pd_decode_init",
            "pd_debug_logits", "pd_ctx_set_timing", "pd_ctx_vocab_timing", "pd_ctx_rows_processed",
-           "pd_trace_scratch_bytes", "pd_ctx_set_trace", "pd_ctx_trace_count", "pd_last_error")
+           "pd_trace_scratch_bytes", "pd_ctx_set_trace", "pd_ctx_trace_count", "pd_ctx_product_timing",
+           "pd_ctx_iteration_kernels", "pd_last_error")
 
 _lib = None
 
@@ -90,6 +91,10 @@ def load_library(path: str = LIB_PATH):
     L.pd_ctx_set_trace.restype = I32
     L.pd_ctx_trace_count.argtypes = [VP, P(I64)]
     L.pd_ctx_trace_count.restype = I32
+    L.pd_ctx_product_timing.argtypes = [VP, P(I64), P(ctypes.c_double), P(ctypes.c_double)]
+    L.pd_ctx_product_timing.restype = I32
+    L.pd_ctx_iteration_kernels.argtypes = [VP, P(I64)]
+    L.pd_ctx_iteration_kernels.restype = I32
     L.pd_last_error.argtypes = []
     L.pd_last_error.restype = ctypes.c_char_p
     _lib = L
@@ -241,6 +246,18 @@ class Context:
         n, ms = ctypes.c_int64(), ctypes.c_double()
         _check(load_library().pd_ctx_vocab_timing(self.handle, ctypes.byref(n), ctypes.byref(ms)))
         return n.value, ms.value
+
+    def product_timing(self):
+        """(launches, total_ms, bytes) of the decoder's timed product launches since set_timing(True)."""
+        n, ms, b = ctypes.c_int64(), ctypes.c_double(), ctypes.c_double()
+        _check(load_library().pd_ctx_product_timing(self.handle, ctypes.byref(n), ctypes.byref(ms), ctypes.byref(b)))
+        return n.value, ms.value, b.value
+
+    def iteration_kernels(self) -> int:
+        """Kernels in the iteration graph replayed last."""
+        n = ctypes.c_int64()
+        _check(load_library().pd_ctx_iteration_kernels(self.handle, ctypes.byref(n)))
+        return n.value
 
     def rows_processed(self) -> int:
         """Rows evaluated by all iterations since set_timing (synchronous)."""

@@ -94,8 +94,8 @@ def test_bench_traffic_figure_is_tied_to_the_kernel_sources(tmp_path, monkeypatc
     good = dict(rec, kernel_source_sha256=hashlib.sha256(src).hexdigest())
     (tmp_path / "profiles" / "vocab_argmax_mt_base_bf16.json").write_text(json.dumps(good))
     monkeypatch.setattr(bench, "ROOT", str(tmp_path))
-    assert bench.measured_traffic() == int(rec["traffic_bytes_per_launch"])
+    assert bench.measured_traffic("vocab_argmax_mt_base_bf16") == int(rec["traffic_bytes_per_launch"])
     # any change to a kernel source voids the figure
     with open(csrc / rec["kernel_sources"][0], "ab") as f:
         f.write(b"\n")
-    assert bench.measured_traffic() is None
+    assert bench.measured_traffic("vocab_argmax_mt_base_bf16") is None
