@@ -310,6 +310,35 @@ pd_status pd_ctx_set_trace(pd_ctx* ctx, void* dev_records, int64_t capacity, voi
                            size_t scratch_bytes);
 pd_status pd_ctx_trace_count(const pd_ctx* ctx, int64_t* records);
 
+/*
+ * For callers that cannot allocate device memory (serving loops and harnesses
+ * that must not call hipMalloc / hipFree or any allocating routine once set
+ * up): pd_decode with the decoding trace on, whose log-sum-exp partials live
+ * in a static device array of the library (PD_TRACE_STATIC_BYTES = 8 MiB per
+ * GPU, held until the process ends) instead of a caller scratch.
+ *   dev_records, capacity  caller-owned device buffer of `capacity` records
+ *                          (pd_trace_record, 16-byte aligned), as for
+ *                          pd_ctx_set_trace; this call writes records from
+ *                          index 0 (pd_ctx_trace_count then returns their
+ *                          count)
+ * Every other argument and every result is as for pd_decode.  The call
+ * allocates nothing: iterations are launched kernel by kernel (no graph is
+ * captured or instantiated) and the record count is zeroed by a kernel on
+ * `stream`.  The context's own pd_ctx_set_trace setting is left as it was.
+ * Limit: an iteration may lay out at most
+ * PD_TRACE_STATIC_BYTES / pd_trace_scratch_bytes(model, 1) rows (B * block
+ * for the block modes, B * m for PD_JACOBI, B for PD_AR); a larger decode
+ * fails with PD_E_WORKSPACE before anything is launched.
+ * Every call on one GPU shares that GPU's array: calls that overlap in time
+ * on one GPU (different streams or threads) race and corrupt each other's
+ * trace.
+ */
+#define PD_TRACE_STATIC_BYTES (8u << 20)
+pd_status pd_decode_traced_static(pd_ctx* ctx, int32_t mode, int32_t block, int32_t horizon, int32_t max_iters,
+                                  const int32_t* tgt_m, int32_t* out_ids, int32_t out_ld, int32_t* out_len,
+                                  int32_t* out_k, int32_t* out_flags, void* dev_records, int64_t capacity,
+                                  void* stream);
+
 /* Message of the last failing call on this thread ("" if none). */
 const char* pd_last_error(void);
 

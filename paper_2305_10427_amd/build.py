@@ -17,7 +17,7 @@ BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libpdec.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-SOURCES = ["gemm.hip", "gemm_tiled.hip", "vocab.hip", "decode_kernels.hip", "runtime.cpp"]
+SOURCES = ["gemm.hip", "gemm_tiled.hip", "vocab.hip", "decode_kernels.hip", "static_scratch.hip", "runtime.cpp"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-ffp-contract=off", "-Wall", "-Wno-unused-result"]
 DEVICE = ["--offload-arch=gfx950", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 

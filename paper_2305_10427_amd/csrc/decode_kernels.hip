@@ -226,6 +226,7 @@ __device__ void emit_rows(const CtrlArgs& a) {
 
 template <typename WT>
 __global__ __launch_bounds__(1024) void k_ctrl_init(CtrlArgs a) {
+  if (a.reset_trace_count && threadIdx.x == 0) *a.trace_count = 0ull;
   for (int s = threadIdx.x; s < a.B; s += blockDim.x) {
     const int m = a.tgt_m[s];
     SentState st;

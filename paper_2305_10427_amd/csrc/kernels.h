@@ -184,6 +184,7 @@ struct CtrlArgs {
   int R_max;
   const int* init;         // initial draft [B][init_ld] (nullptr: all [PAD])
   int init_ld;
+  int reset_trace_count;   // k_ctrl_init zeroes *trace_count first
   // decoding trace (nullptr: off): one record per evaluated row
   TraceRec* trace;
   long long trace_cap;
@@ -261,6 +262,20 @@ hipError_t launch_ctrl_init(int dtype, const CtrlArgs& a, hipStream_t s);
 hipError_t launch_ctrl_step(int dtype, const CtrlArgs& a, hipStream_t s);
 hipError_t launch_finalize(const CtrlArgs& a, hipStream_t s);
 
+}  // namespace pdec
+
+// Traced decode on caller-chosen log-sum-exp scratch (runtime.cpp): pd_decode
+// with the decoding trace on, records appended from index 0 (the count is
+// zeroed on the stream), iterations launched kernel by kernel (no graph is
+// captured or instantiated), the context's own trace setting left as it was.
+struct pd_ctx;
+namespace pdec {
+// Records `msg` as the calling thread's pd_last_error and returns status.
+int32_t fail_with(int32_t status, const char* msg);
+int32_t decode_traced_on(pd_ctx* ctx, int32_t mode, int32_t block, int32_t horizon, int32_t max_iters,
+                         const int32_t* tgt_m, int32_t* out_ids, int32_t out_ld, int32_t* out_len, int32_t* out_k,
+                         int32_t* out_flags, void* records, int64_t capacity, void* scratch, size_t scratch_bytes,
+                         const char* scratch_name, void* stream);
 
 
 }  // namespace pdec

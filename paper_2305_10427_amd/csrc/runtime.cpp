@@ -231,6 +231,7 @@ struct pd_ctx {
   long long trace_cap = 0;
   float2* trace_part = nullptr;
   long long trace_rows = 0;            // rows the scratch holds
+  bool reset_trace = false;            // the next decode zeroes the record count on its stream
   int enc_B = 0, enc_nmax = 0;
   bool encoded = false;
 
@@ -899,6 +900,7 @@ pd_status pd_decode_init(pd_ctx* ctx, int32_t mode, int32_t block, int32_t horiz
     ca.trace_count = C.at<unsigned long long>(C.L.trace_count);
     ca.row_max = C.at<float>(C.L.row_max);
     ca.row_lse = C.at<float>(C.L.row_lse);
+    ca.reset_trace_count = C.reset_trace ? 1 : 0;
   }
   ca.out_ids = out_ids;
   ca.out_ld = out_ld;
@@ -1071,3 +1073,39 @@ pd_status pd_debug_logits(pd_ctx* ctx, const int32_t* tgt_in, int32_t T, float* 
 
 }  // extern "C"
 
+namespace pdec {
+
+int32_t fail_with(int32_t status, const char* msg) { return fail(status, msg); }
+
+int32_t decode_traced_on(pd_ctx* ctx, int32_t mode, int32_t block, int32_t horizon, int32_t max_iters,
+                         const int32_t* tgt_m, int32_t* out_ids, int32_t out_ld, int32_t* out_len, int32_t* out_k,
+                         int32_t* out_flags, void* records, int64_t capacity, void* scratch, size_t scratch_bytes,
+                         const char* scratch_name, void* stream) {
+  if (ctx == nullptr) return fail(PD_E_ARG, "null context");
+  if (records == nullptr || capacity < 1) return fail(PD_E_ARG, "records must be non-null and capacity >= 1");
+  if (scratch == nullptr || !aligned(records, 16) || !aligned(scratch, 16))
+    return fail(PD_E_ARG, "trace buffers must be non-null and 16-byte aligned");
+  pd_ctx& C = *ctx;
+  const TraceRec* trace = C.trace;
+  const long long cap = C.trace_cap, rows = C.trace_rows;
+  float2* part = C.trace_part;
+  const bool graphs = C.use_graphs;
+  C.trace = static_cast<TraceRec*>(records);
+  C.trace_cap = capacity;
+  C.trace_part = static_cast<float2*>(scratch);
+  C.trace_rows = static_cast<long long>(scratch_bytes / trace_row_bytes(*C.M));
+  C.use_graphs = false;
+  C.reset_trace = true;
+  pd_status st = pd_decode_init(ctx, mode, block, horizon, max_iters, tgt_m, nullptr, 0, out_ids, out_ld, out_len,
+                                out_k, out_flags, stream);
+  C.trace = const_cast<TraceRec*>(trace);
+  C.trace_cap = cap;
+  C.trace_part = part;
+  C.trace_rows = rows;
+  C.use_graphs = graphs;
+  C.reset_trace = false;
+  if (st == PD_E_WORKSPACE) g_err = std::string(scratch_name) + ": " + g_err;
+  return st;
+}
+
+}  // namespace pdec

@@ -43,7 +43,8 @@ EXPORTS = ("pd_weight_count", "pd_weight_shape", "pd_model_create", "pd_model_de
            "pd_ctx_workspace_bytes", "pd_ctx_create", "pd_ctx_destroy", "pd_encode", "pd_decode", "pd_decode_init",
            "pd_debug_logits", "pd_ctx_set_timing", "pd_ctx_vocab_timing", "pd_ctx_rows_processed",
            "pd_trace_scratch_bytes", "pd_ctx_set_trace", "pd_ctx_trace_count", "pd_ctx_product_timing",
-           "pd_ctx_iteration_kernels", "pd_last_error")
+           "pd_ctx_iteration_kernels", "pd_decode_traced_static", "pd_last_error")
+TRACE_STATIC_BYTES = 8 << 20      # PD_TRACE_STATIC_BYTES
 
 _lib = None
 
@@ -95,6 +96,8 @@ def load_library(path: str = LIB_PATH):
     L.pd_ctx_product_timing.restype = I32
     L.pd_ctx_iteration_kernels.argtypes = [VP, P(I64)]
     L.pd_ctx_iteration_kernels.restype = I32
+    L.pd_decode_traced_static.argtypes = [VP, I32, I32, I32, I32, P(I32), VP, I32, VP, VP, VP, VP, I64, VP]
+    L.pd_decode_traced_static.restype = I32
     L.pd_last_error.argtypes = []
     L.pd_last_error.restype = ctypes.c_char_p
     _lib = L
@@ -226,6 +229,33 @@ class Context:
                                                  ctypes.c_void_p(fl.data_ptr()),
                                                  ctypes.c_void_p(_stream_handle(stream))))
         return ids, ln, k, fl
+
+    def decode_traced_static(self, mode, tgt_m: Sequence[int], capacity: int, block: int = 1, max_iters: int = 0,
+                             horizon: int = 0, stream=None):
+        """pd_decode_traced_static: decode with the trace on, the trace scratch
+        in the library's static array.  Returns (ids, lengths, k, flags,
+        records, count); records is a numpy structured array (TRACE_DTYPE) of
+        the first min(count, capacity) records."""
+        import torch
+        mode_id = MODE_IDS[mode] if isinstance(mode, str) else int(mode)
+        tgt_m = [int(x) for x in tgt_m]
+        if len(tgt_m) != self.B:
+            raise PdError(1, f"tgt_m has {len(tgt_m)} entries, the encoded batch has {self.B}")
+        B = len(tgt_m)
+        ids = torch.empty((B, max(max(tgt_m), 1)), dtype=torch.int32, device=self.device)
+        ln, k, fl = (torch.empty(B, dtype=torch.int32, device=self.device) for _ in range(3))
+        rec = torch.empty(max(int(capacity), 1) * 6, dtype=torch.int32, device=self.device)
+        _check(load_library().pd_decode_traced_static(
+            self.handle, mode_id, int(block), int(horizon), int(max_iters), _host_i32(tgt_m),
+            ctypes.c_void_p(ids.data_ptr()), ids.shape[1], ctypes.c_void_p(ln.data_ptr()),
+            ctypes.c_void_p(k.data_ptr()), ctypes.c_void_p(fl.data_ptr()), ctypes.c_void_p(rec.data_ptr()),
+            int(capacity), ctypes.c_void_p(_stream_handle(stream))))
+        torch.cuda.current_stream().synchronize() if stream is None else stream.synchronize()
+        n = ctypes.c_int64()
+        _check(load_library().pd_ctx_trace_count(self.handle, ctypes.byref(n)))
+        kept = min(n.value, int(capacity))
+        raw = rec[: kept * 6].cpu().numpy()
+        return ids, ln, k, fl, raw.view(np.dtype(self.TRACE_DTYPE)), n.value
 
     def debug_logits(self, tgt_in, stream=None):
         """Teacher-forced logits [B, T, V] for decoder inputs tgt_in [B, T] (BOS first)."""
