@@ -404,8 +404,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20, help="sentences timed per mode (the first STEPS)")
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--cpu-sentences", type=int, default=1)
-    ap.add_argument("--cpu-m", type=int, default=16, help="target positions of each CPU-baseline sentence")
+    ap.add_argument("--cpu-sentences", type=int, default=2)
+    ap.add_argument("--cpu-m", type=int, default=24, help="target positions of each CPU-baseline sentence")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-mt-base", action="store_true")
     ap.add_argument("--no-tiny", action="store_true")
