@@ -48,8 +48,11 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   const size_t base = (static_cast<size_t>(s) * a.H + hh) * a.T * DH;
   const AT* Kb = static_cast<const AT*>(a.kc) + base;
   const AT* Vb = static_cast<const AT*>(a.vc) + base;
-  KeyChunk<AT, DH> kc;
-  kc.load(Kb, Vb, 0, nk, lane);
+  // two chunk buffers: the loads of the next chunk are issued before the
+  // current one is folded (a chunk past the row's keys loads key 0 and is
+  // never folded)
+  KeyChunk<AT, DH> ka, kb;
+  ka.load(Kb, Vb, 0, nk, lane);
 #pragma unroll
   for (int i = 0; i < (DH + kWave - 1) / kWave; ++i) {
     const int d = lane + kWave * i;
@@ -58,9 +61,28 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   wave_lds_sync();
   RowState<DH> st;
   st.init();
-  for (int key0 = 0; key0 < nk; key0 += kAttnChunk) {
-    if (key0 > 0) kc.load(Kb, Vb, key0, nk, lane);
-    chunk_fold<AT, DH>(s_q[wave], kc, key0, nk, a.scale, lane, s_scr[wave], st);
+  if (nk <= kAttnChunk) {                               // wave-uniform: one chunk
+    chunk_fold<AT, DH>(s_q[wave], ka, 0, nk, a.scale, lane, s_scr[wave], st);
+  } else {
+    // every load below is of a chunk that exists and sits on the straight
+    // path of the loop body (a load under a branch would make the compiler
+    // wait for all outstanding loads before the next use of any of them)
+    for (int key0 = 0;; key0 += 2 * kAttnChunk) {
+      kb.load(Kb, Vb, key0 + kAttnChunk, nk, lane);
+      __builtin_amdgcn_sched_barrier(0);                 // the next chunk's loads go out first
+      chunk_fold<AT, DH>(s_q[wave], ka, key0, nk, a.scale, lane, s_scr[wave], st);
+      if (key0 + 2 * kAttnChunk >= nk) {                // kb holds the last chunk
+        chunk_fold<AT, DH>(s_q[wave], kb, key0 + kAttnChunk, nk, a.scale, lane, s_scr[wave], st);
+        break;
+      }
+      ka.load(Kb, Vb, key0 + 2 * kAttnChunk, nk, lane);
+      __builtin_amdgcn_sched_barrier(0);
+      chunk_fold<AT, DH>(s_q[wave], kb, key0 + kAttnChunk, nk, a.scale, lane, s_scr[wave], st);
+      if (key0 + 3 * kAttnChunk >= nk) {                // ka holds the last chunk
+        chunk_fold<AT, DH>(s_q[wave], ka, key0 + 2 * kAttnChunk, nk, a.scale, lane, s_scr[wave], st);
+        break;
+      }
+    }
   }
   row_output<AT, DH>(st, static_cast<AT*>(a.out) + static_cast<size_t>(row) * a.ldo + hh * DH, lane);
 }
@@ -87,6 +109,57 @@ __device__ __forceinline__ float embed_elem(const WT* emb, const float* pe, int 
                                             int vocab) {
   tok = min(max(tok, 0), vocab - 1);
   return Elt<WT>::load(emb, static_cast<size_t>(tok) * d + c) * scale + pe[static_cast<size_t>(p) * d + c];
+}
+
+// Store 8 consecutive values as the storage type (the rounding of Elt::store).
+template <typename WT> __device__ __forceinline__ void store8(WT* p, size_t i, const float* v);
+template <> __device__ __forceinline__ void store8<float>(float* p, size_t i, const float* v) {
+  *reinterpret_cast<float4*>(p + i) = make_float4(v[0], v[1], v[2], v[3]);
+  *reinterpret_cast<float4*>(p + i + 4) = make_float4(v[4], v[5], v[6], v[7]);
+}
+template <> __device__ __forceinline__ void store8<bf16_t>(bf16_t* p, size_t i, const float* v) {
+  uint32_t w[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    w[j] = static_cast<uint32_t>(f32_to_bf16(v[2 * j])) | (static_cast<uint32_t>(f32_to_bf16(v[2 * j + 1])) << 16);
+  *reinterpret_cast<uint4*>(p + i) = make_uint4(w[0], w[1], w[2], w[3]);
+}
+
+// Embedding of `total` rows into x_out [total][d] by the threads of one
+// workgroup (d a multiple of 8): each item is 8 consecutive columns of a row,
+// and a thread issues the loads of up to kEmbItems items before computing any
+// (the per-element value is embed_elem's: E[tok] * scale + pe, in that order).
+// tok(row) / pos(row) give a row's token and position.
+constexpr int kEmbItems = 4;
+template <typename WT, typename Tok, typename Pos>
+__device__ __forceinline__ void embed_rows_block(const WT* emb, const float* pe, float scale, int d, int vocab,
+                                                 int total, Tok tok, Pos pos, WT* x_out) {
+  const int per_row = d / 8;
+  const int n_items = total * per_row;
+  const int nt = blockDim.x;
+  for (int base = 0; base < n_items; base += kEmbItems * nt) {
+    float ev[kEmbItems][8], pv[kEmbItems][8];
+#pragma unroll
+    for (int u = 0; u < kEmbItems; ++u) {
+      const int it = base + threadIdx.x + u * nt;
+      const int itc = it < n_items ? it : 0;
+      const int row = itc / per_row;
+      const int c = (itc - row * per_row) * 8;
+      const int t = min(max(tok(row), 0), vocab - 1);
+      load_n<WT, 8>(emb, static_cast<size_t>(t) * d + c, ev[u]);
+      load_n<float, 8>(pe, static_cast<size_t>(pos(row)) * d + c, pv[u]);
+    }
+#pragma unroll
+    for (int u = 0; u < kEmbItems; ++u) {
+      const int it = base + threadIdx.x + u * nt;
+      if (it < n_items) {
+        float y[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) y[e] = ev[u][e] * scale + pv[u][e];
+        store8<WT>(x_out, static_cast<size_t>(it) * 8, y);
+      }
+    }
+  }
 }
 
 template <typename WT>
@@ -213,14 +286,9 @@ __device__ void emit_rows(const CtrlArgs& a) {
   }
   if (a.x_out != nullptr) {
     __syncthreads();
-    const size_t n = static_cast<size_t>(total) * a.d;
-    for (size_t t = threadIdx.x; t < n; t += blockDim.x) {
-      const int row = static_cast<int>(t / a.d);
-      const int c = static_cast<int>(t - static_cast<size_t>(row) * a.d);
-      Elt<WT>::store(static_cast<WT*>(a.x_out), t,
-                     embed_elem<WT>(static_cast<const WT*>(a.emb), a.pe, a.row_tok[row], a.row_pos[row], c, a.d,
-                                    a.emb_scale, a.vocab));
-    }
+    embed_rows_block<WT>(static_cast<const WT*>(a.emb), a.pe, a.emb_scale, a.d, a.vocab, total,
+                         [&](int r) { return a.row_tok[r]; }, [&](int r) { return a.row_pos[r]; },
+                         static_cast<WT*>(a.x_out));
   }
 }
 
@@ -470,14 +538,9 @@ __global__ __launch_bounds__(1024) void k_ctrl_rows(CtrlArgs a) {
   }
   if (a.x_out != nullptr) {
     __syncthreads();
-    const size_t n = static_cast<size_t>(total) * a.d;
-    for (size_t t = tid; t < n; t += blockDim.x) {
-      const int row = static_cast<int>(t / a.d);
-      const int c = static_cast<int>(t - static_cast<size_t>(row) * a.d);
-      Elt<WT>::store(static_cast<WT*>(a.x_out), t,
-                     embed_elem<WT>(static_cast<const WT*>(a.emb), a.pe, a.row_tok[row], a.row_pos[row], c, a.d,
-                                    a.emb_scale, a.vocab));
-    }
+    embed_rows_block<WT>(static_cast<const WT*>(a.emb), a.pe, a.emb_scale, a.d, a.vocab, total,
+                         [&](int r) { return a.row_tok[r]; }, [&](int r) { return a.row_pos[r]; },
+                         static_cast<WT*>(a.x_out));
   }
 }
 
@@ -596,16 +659,10 @@ __global__ __launch_bounds__(1024) void k_ctrl_small(CtrlArgs a) {
     }
   }
   __syncthreads();
-  // (3) the embedding of the next rows
-  const int total = s_total;
-  const size_t n = static_cast<size_t>(total) * a.d;
-  for (size_t t = tid; t < n; t += blockDim.x) {
-    const int row = static_cast<int>(t / a.d);
-    const int c = static_cast<int>(t - static_cast<size_t>(row) * a.d);
-    Elt<WT>::store(static_cast<WT*>(a.x_out), t,
-                   embed_elem<WT>(static_cast<const WT*>(a.emb), a.pe, s_rtok[row], s_rpos[row], c, a.d, a.emb_scale,
-                                  a.vocab));
-  }
+  // (3) the embedding of the next rows (tokens and positions from LDS)
+  embed_rows_block<WT>(static_cast<const WT*>(a.emb), a.pe, a.emb_scale, a.d, a.vocab, s_total,
+                       [&](int r) { return s_rtok[r]; }, [&](int r) { return s_rpos[r]; },
+                       static_cast<WT*>(a.x_out));
 }
 
 // Outputs: ids cut after the first [EOS] (inclusive) and [PAD]-filled, the
