@@ -15,13 +15,16 @@ __device__ __forceinline__ float bf16_to_f32(bf16_t h) {
   return __uint_as_float(static_cast<uint32_t>(h) << 16);
 }
 
-// Round-to-nearest-even float -> bfloat16 (NaN kept quiet).
-__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
-  const uint32_t u = __float_as_uint(f);
-  const uint32_t rne = (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;   // round to nearest even
-  const uint32_t qnan = (u >> 16) | 0x40u;                       // NaN: keep sign, set quiet bit
-  const bool is_nan = (u & 0x7fffffffu) > 0x7f800000u;
-  return static_cast<bf16_t>(is_nan ? qnan : rne);              // a select, not a branch
+// Round-to-nearest-even float -> bfloat16 with gfx950's conversion
+// instruction (v_cvt_pk_bf16_f32).  It equals the integer rounding
+// (u + 0x7fff + ((u >> 16) & 1)) >> 16 on every non-NaN float (all 2^32
+// patterns compared on the GPU) and keeps NaNs NaN.
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float floatx2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) { return __builtin_bit_cast(bf16_t, static_cast<__bf16>(f)); }
+// Two values, low half first, in one conversion.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(floatx2_t{lo, hi}, bf16x2_t));
 }
 
 // Storage-type traits: load/store one element as float.
@@ -59,6 +62,18 @@ template <> struct Vec16<bf16_t> {
     }
   }
 };
+
+// Store 8 consecutive values (aligned to 16 bytes for bf16, 32 for float) in
+// the storage type, rounded as Elt::store rounds them.
+template <typename T> __device__ __forceinline__ void store8(T* p, size_t i, const float* v);
+template <> __device__ __forceinline__ void store8<float>(float* p, size_t i, const float* v) {
+  *reinterpret_cast<float4*>(p + i) = make_float4(v[0], v[1], v[2], v[3]);
+  *reinterpret_cast<float4*>(p + i + 4) = make_float4(v[4], v[5], v[6], v[7]);
+}
+template <> __device__ __forceinline__ void store8<bf16_t>(bf16_t* p, size_t i, const float* v) {
+  *reinterpret_cast<uint4*>(p + i) =
+      make_uint4(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7]));
+}
 
 // Load N consecutive elements of T (N = 4 or 8, aligned) as floats.
 template <typename T, int N>

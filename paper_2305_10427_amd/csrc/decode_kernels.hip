@@ -111,20 +111,6 @@ __device__ __forceinline__ float embed_elem(const WT* emb, const float* pe, int 
   return Elt<WT>::load(emb, static_cast<size_t>(tok) * d + c) * scale + pe[static_cast<size_t>(p) * d + c];
 }
 
-// Store 8 consecutive values as the storage type (the rounding of Elt::store).
-template <typename WT> __device__ __forceinline__ void store8(WT* p, size_t i, const float* v);
-template <> __device__ __forceinline__ void store8<float>(float* p, size_t i, const float* v) {
-  *reinterpret_cast<float4*>(p + i) = make_float4(v[0], v[1], v[2], v[3]);
-  *reinterpret_cast<float4*>(p + i + 4) = make_float4(v[4], v[5], v[6], v[7]);
-}
-template <> __device__ __forceinline__ void store8<bf16_t>(bf16_t* p, size_t i, const float* v) {
-  uint32_t w[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j)
-    w[j] = static_cast<uint32_t>(f32_to_bf16(v[2 * j])) | (static_cast<uint32_t>(f32_to_bf16(v[2 * j + 1])) << 16);
-  *reinterpret_cast<uint4*>(p + i) = make_uint4(w[0], w[1], w[2], w[3]);
-}
-
 // Embedding of `total` rows into x_out [total][d] by the threads of one
 // workgroup (d a multiple of 8): each item is 8 consecutive columns of a row,
 // and a thread issues the loads of up to kEmbItems items before computing any

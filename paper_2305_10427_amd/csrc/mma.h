@@ -28,11 +28,8 @@ template <> struct Mma<bf16_t> {
     }
   }
   static __device__ __forceinline__ frag pack(const float* v) {
-    uint32_t w[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      w[j] = static_cast<uint32_t>(f32_to_bf16(v[2 * j])) | (static_cast<uint32_t>(f32_to_bf16(v[2 * j + 1])) << 16);
-    return make_uint4(w[0], w[1], w[2], w[3]);
+    return make_uint4(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]),
+                      pack_bf16x2(v[6], v[7]));
   }
 };
 template <> struct Mma<float> {
@@ -76,12 +73,8 @@ __device__ __forceinline__ void ln_row_apply(const LnRow<XT, NT>& h, int K, floa
       load_n<WT, 8>(b, k0, bv);
 #pragma unroll
       for (int e = 0; e < 8; ++e) y[e] = ln_apply(h.get(t, e), mean, rstd, gv[e], bv[e]);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) Elt<WT>::store(dst, k0 + e, y[e]);
-      if (out != nullptr) {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) Elt<WT>::store(out, k0 + e, y[e]);
-      }
+      store8<WT>(dst, k0, y);
+      if (out != nullptr) store8<WT>(out, k0, y);
     }
   }
 }
