@@ -126,8 +126,15 @@ pd_status pd_weight_shape(const pd_config* cfg, int32_t idx, int64_t* rows, int6
  * Bind a configuration to caller-owned device weights.  dev_weights holds
  * n_weights device pointers in canonical order, each 16-byte aligned, of
  * element type float (PD_F32) or bfloat16 bit patterns (PD_BF16).  The
- * pointers are stored, not copied.  Returns PD_E_ARG for a null / misaligned
- * pointer or a wrong count, PD_E_UNSUPPORTED for shapes the kernels reject.
+ * pointers are stored, not copied, and read for the model's lifetime: the
+ * caller keeps them allocated and unchanged until pd_model_destroy.  No
+ * device work happens here.  The first pd_ctx_create on the model allocates,
+ * on the current device, a copy of every encoder and decoder matrix
+ * product's weights (w_qkv, w_o, w1, w2; ca_w_q, ca_w_o) rearranged into the
+ * order in which the few-row product kernels feed the matrix cores (as many
+ * bytes as those matrices; freed by pd_model_destroy).  Returns PD_E_ARG for
+ * a null / misaligned pointer or a wrong count, PD_E_UNSUPPORTED for shapes
+ * the kernels reject.
  */
 pd_status pd_model_create(const pd_config* cfg, const void* const* dev_weights, int32_t n_weights,
                           pd_model** out);
@@ -147,6 +154,9 @@ pd_status pd_ctx_workspace_bytes(const pd_model* model, int32_t max_batch, int32
  * Create a context on caller-owned device workspace (256-byte aligned, at
  * least pd_ctx_workspace_bytes).  The workspace holds activations, the
  * cross-attention and self-attention K/V caches, drafts and control state.
+ * The first context of a model also makes the model's matrix-core feed copy
+ * of its product weights (see pd_model_create), on the null stream, and
+ * waits for it; PD_E_DEVICE when that allocation or copy fails.
  */
 pd_status pd_ctx_create(const pd_model* model, int32_t max_batch, int32_t max_src, int32_t max_tgt,
                         void* dev_workspace, size_t workspace_bytes, pd_ctx** out);

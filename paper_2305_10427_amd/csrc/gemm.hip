@@ -23,7 +23,23 @@
 // All loads a wave needs (weights, inputs, bias) are issued before any
 // result is needed; the device row count only gates the stores, so its load
 // overlaps the rest.  Rows between the device count and the launch bound are
-// computed from stale activations and discarded.
+// computed from stale activations and discarded.  When a wave's K range is
+// SPW whole MFMA steps (the decoder's shapes), its SPW weight and input loads
+// all go out at once; other shapes stream batches of kDepth steps, the next
+// batch in flight during the current one's products.
+//
+// Weights come row-major, or (a.wp) in the order the MFMA steps consume them:
+// block (tile c, step s) of 1 KB holds lane l's 16 bytes at 16 l, i.e.
+// W[16 c + (l & 15)][s KS + EPL (l >> 4) ...], so each wave-wide load reads
+// 1 KB contiguous instead of 64 bytes from each of 16 weight rows.
+//
+// Row groups (RG < 16, the K-split kernels of one row tile): a workgroup
+// computes RG rows of its column tile, and the row groups of a column tile
+// are consecutive workgroups of one XCD (linear id mod 8), so its weights
+// come from HBM once and the other groups read them from that XCD's L2.
+// This spreads a narrow product over more CUs and cuts the LayerNorm
+// prologue to RG / 4 rows per wave; lanes of the tile rows past RG repeat the
+// group's rows and their results are dropped.
 //
 // Prologue PRO_LN normalises the input rows (LayerNorm, statistics from
 // ln_stats16) and rounds them to the storage type before use; workgroup 0
@@ -34,6 +50,8 @@
 // value, then lowest index) per row and writes one partial per row.
 #include <hip/hip_ext.h>
 
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 #include "mma.h"
@@ -42,7 +60,7 @@ namespace pdec {
 
 constexpr int kDepth = 8;   // MFMA steps per weight batch; two batches are in flight
 
-template <typename WT, int PRO, int EPI, int XF32, int KSPLIT, int LNT>
+template <typename WT, int PRO, int EPI, int XF32, int KSPLIT, int LNT, int RG, int SPW>
 __global__ __launch_bounds__(KSPLIT == 8 ? 512 : 256) void k_gemm(GemmArgs a) {
   if constexpr (EPI == EPI_QKV) layer_select(a, blockIdx.z);
   using AT = WT;
@@ -51,24 +69,46 @@ __global__ __launch_bounds__(KSPLIT == 8 ? 512 : 256) void k_gemm(GemmArgs a) {
   using frag = typename MM::frag;
   constexpr int KS = MM::KS;
   constexpr int EPL = MM::EPL;
-  constexpr int D = kDepth;
+  constexpr int D = SPW > 0 ? SPW : kDepth;
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = threadIdx.x / kWave;
   const int lr = lane & 15;          // row (X) / column (W) fed by this lane
   const int lg = lane >> 4;          // k group of this lane
   const int K = a.K, N = a.N;
   constexpr bool SPLIT = KSPLIT > 1;   // waves split K over one 16-column tile
-  const int n0 = (SPLIT ? blockIdx.x * 16 : (blockIdx.x * 4 + wave) * 16);
+  static_assert(RG == 16 || (SPLIT && (RG == 4 || RG == 8)), "row groups of 4 or 8 rows need the K split");
+  static_assert(SPW == 0 || SPLIT, "whole-range loads need the K split");
+  int ctile = blockIdx.x, grp = 0;     // column tile and row group of this workgroup
+  if constexpr (RG < 16) {
+    const int ct = (N + 15) / 16;
+    const int ng = gridDim.x / ct;
+    if ((ct & 7) == 0) {                 // the ng groups of tile c: ids ((c / 8) ng + g) 8 + c % 8
+      const int q = blockIdx.x >> 3;
+      grp = q % ng;
+      ctile = (q / ng) * 8 + (blockIdx.x & 7);
+    } else {
+      grp = blockIdx.x / ct;
+      ctile = blockIdx.x - grp * ct;
+    }
+  }
+  const int n0 = (SPLIT ? ctile * 16 : (blockIdx.x * 4 + wave) * 16);
   const int col = n0 + lr;           // weight row loaded by this lane, and output column it finishes
   const int n_steps = K / KS;
   const int s_begin = SPLIT ? (n_steps * wave) / KSPLIT : 0;
   const int s_end = SPLIT ? (n_steps * (wave + 1)) / KSPLIT : n_steps;
   const WT* __restrict__ W = static_cast<const WT*>(a.w);
   const XT* __restrict__ X = static_cast<const XT*>(a.x);
-  const WT* __restrict__ wrow = W + static_cast<size_t>(col < N ? col : 0) * K + EPL * lg;
+  // step s of this lane's weights sits at wrow + s * wstep
+  const bool packed = a.wp != nullptr;
+  const WT* __restrict__ wrow =
+      packed ? static_cast<const WT*>(a.wp) + (static_cast<size_t>(n0 / 16) * n_steps * kWave + lane) * EPL
+             : W + static_cast<size_t>(col < N ? col : 0) * K + EPL * lg;
+  const int wstep = packed ? kWave * EPL : KS;
   const int R_max = a.n_rows;        // rows that may be read (launch bound)
-  const int m_first = blockIdx.y * 16 * a.mt_per_wg;
-  const int m_last = min(R_max, m_first + 16 * a.mt_per_wg);
+  const int m_first = RG < 16 ? grp * RG : blockIdx.y * 16 * a.mt_per_wg;
+  const int m_last = min(R_max, m_first + (RG < 16 ? RG : 16 * a.mt_per_wg));
+  const int R_grp = RG < 16 ? m_last : R_max;   // rows this workgroup's LayerNorm reads
+  const int lrr = lr & (RG - 1);                // tile row fed by this lane
 
   // Loads complete in issue order, so the small loads the prologue and the
   // epilogue need go out before the weight stream: PRO_LN's input rows of the
@@ -77,12 +117,13 @@ __global__ __launch_bounds__(KSPLIT == 8 ? 512 : 256) void k_gemm(GemmArgs a) {
   // Every load is unconditional (clamped to a valid address, unused values
   // dropped later): a load under a branch makes the compiler wait for all
   // earlier loads where the paths join.
-  LnTile<WT, XT, LNT / 4> ln;   // LNT: 128-element slabs of a 16-lane row group; 4 per 512
+  // LNT: 128-element slabs of a 16-lane row group (4 per 512); one pass per 4 rows
+  LnTile<WT, XT, LNT / 4, RG < 16 ? RG / 4 : 4> ln;
   __shared__ uint4 s_gb[PRO == PRO_LN ? 2 : 1][128];
   uint4 gb = make_uint4(0u, 0u, 0u, 0u);
   const int gw = threadIdx.x & 127;
   if constexpr (PRO == PRO_LN) {
-    ln.load(X, a.ldx, K, m_first, R_max, wave & 3, lane);
+    ln.load(X, a.ldx, K, m_first, R_grp, wave & 3, lane);
     const bool gb_word = gw < K * static_cast<int>(sizeof(WT)) / 16;
     gb = static_cast<const uint4*>((threadIdx.x & 128) ? a.ln_b : a.ln_g)[gb_word ? gw : 0];
   }
@@ -93,7 +134,7 @@ __global__ __launch_bounds__(KSPLIT == 8 ? 512 : 256) void k_gemm(GemmArgs a) {
   if constexpr (EPI == EPI_RESID) {
 #pragma unroll
     for (int e = 0; e < NE; ++e) {
-      const int row = m_first + 4 * lg + (SPLIT ? (wave & 3) : e);
+      const int row = m_first + ((4 * lg + (SPLIT ? (wave & 3) : e)) & (RG - 1));
       const size_t ri = static_cast<size_t>(row < R_max ? row : 0) * a.ldr + (col < N ? col : 0);
       rpre[e] = Elt<AT>::load(static_cast<const AT*>(a.resid), ri);
     }
@@ -102,7 +143,7 @@ __global__ __launch_bounds__(KSPLIT == 8 ? 512 : 256) void k_gemm(GemmArgs a) {
   if constexpr (EPI == EPI_QKV) {
 #pragma unroll
     for (int e = 0; e < NE; ++e) {
-      const int row = m_first + 4 * lg + (SPLIT ? (wave & 3) : e);
+      const int row = m_first + ((4 * lg + (SPLIT ? (wave & 3) : e)) & (RG - 1));
       row_place(a.rows, row < R_max ? row : 0, rs[e], rp[e]);
     }
   }
@@ -111,7 +152,7 @@ __global__ __launch_bounds__(KSPLIT == 8 ? 512 : 256) void k_gemm(GemmArgs a) {
   // the first weight batch
   frag bcur[D];
 #pragma unroll
-  for (int u = 0; u < D; ++u) bcur[u] = MM::load(wrow + min(s_begin + u, n_steps - 1) * KS);
+  for (int u = 0; u < D; ++u) bcur[u] = MM::load(wrow + static_cast<size_t>(min(s_begin + u, n_steps - 1)) * wstep);
   const int R = a.n_rows_dev ? *a.n_rows_dev : a.n_rows;
 
   __shared__ float s_part[KSPLIT > 1 ? KSPLIT : 1][4][64];
@@ -129,42 +170,52 @@ __global__ __launch_bounds__(KSPLIT == 8 ? 512 : 256) void k_gemm(GemmArgs a) {
 
   for (int m0 = m_first; m0 < m_last; m0 += 16) {
     if (m0 > m_first && m0 >= R) break;
-    const int arow = m0 + lr;                 // X row fed by this lane
+    const int arow = m0 + lrr;                // X row fed by this lane
     const bool arow_ok = arow < R_max;
     if (m0 != m_first) {
-      if constexpr (PRO == PRO_LN) ln.load(X, a.ldx, K, m0, R_max, wave & 3, lane);
+      if constexpr (PRO == PRO_LN) ln.load(X, a.ldx, K, m0, R_grp, wave & 3, lane);
 #pragma unroll
-      for (int u = 0; u < D; ++u) bcur[u] = MM::load(wrow + min(s_begin + u, n_steps - 1) * KS);
+      for (int u = 0; u < D; ++u) bcur[u] = MM::load(wrow + static_cast<size_t>(min(s_begin + u, n_steps - 1)) * wstep);
     }
     if constexpr (PRO == PRO_LN) {
       if (wave < 4)
         ln.finish(K, a.ln_eps, reinterpret_cast<const WT*>(s_gb[0]), reinterpret_cast<const WT*>(s_gb[1]), sA, lda,
-                  blockIdx.x == 0 ? static_cast<AT*>(a.ln_out) : nullptr, a.ldlo, R);
+                  ctile == 0 ? static_cast<AT*>(a.ln_out) : nullptr, a.ldlo, R);
       __syncthreads();
     }
     floatx4_t acc = {0.f, 0.f, 0.f, 0.f};
+    // the input fragment of step s (LDS tile after the LayerNorm, else X)
+    auto a_frag = [&](int s) {
+      const int k = s * KS + EPL * lg;
+      if constexpr (PRO == PRO_LN) {
+        return MM::load(sA + static_cast<size_t>(lrr) * lda + k);
+      } else if constexpr (std::is_same<XT, AT>::value) {
+        return MM::load(X + static_cast<size_t>(arow_ok ? arow : 0) * a.ldx + k);
+      } else {
+        float xv[EPL];
+        load_n<XT, EPL>(X, static_cast<size_t>(arow_ok ? arow : 0) * a.ldx + k, xv);
+        return MM::pack(xv);
+      }
+    };
+    if constexpr (SPW > 0) {
+      // the whole range: bcur holds its SPW weight steps
+      frag af[D];
+#pragma unroll
+      for (int u = 0; u < D; ++u) af[u] = a_frag(s_begin + u);
+#pragma unroll
+      for (int u = 0; u < D; ++u) acc = MM::step(af[u], bcur[u], acc);
+    } else
     for (int s0 = s_begin; s0 < s_end; s0 += D) {
       // next weight batch goes out before this batch's products
       frag bnext[D];
       const bool more = s0 + D < s_end;
       if (more) {
 #pragma unroll
-        for (int u = 0; u < D; ++u) bnext[u] = MM::load(wrow + min(s0 + D + u, n_steps - 1) * KS);
+        for (int u = 0; u < D; ++u) bnext[u] = MM::load(wrow + static_cast<size_t>(min(s0 + D + u, n_steps - 1)) * wstep);
       }
       frag af[D];
 #pragma unroll
-      for (int u = 0; u < D; ++u) {
-        const int k = min(s0 + u, n_steps - 1) * KS + EPL * lg;
-        if constexpr (PRO == PRO_LN) {
-          af[u] = MM::load(sA + static_cast<size_t>(lr) * lda + k);
-        } else if constexpr (std::is_same<XT, AT>::value) {
-          af[u] = MM::load(X + static_cast<size_t>(arow_ok ? arow : 0) * a.ldx + k);
-        } else {
-          float xv[EPL];
-          load_n<XT, EPL>(X, static_cast<size_t>(arow_ok ? arow : 0) * a.ldx + k, xv);
-          af[u] = MM::pack(xv);
-        }
-      }
+      for (int u = 0; u < D; ++u) af[u] = a_frag(min(s0 + u, n_steps - 1));
       __builtin_amdgcn_sched_barrier(0);   // all loads of the batch before its products
       // only the steps of the wave's K range (a wave-uniform branch)
 #pragma unroll
@@ -202,7 +253,7 @@ __global__ __launch_bounds__(KSPLIT == 8 ? 512 : 256) void k_gemm(GemmArgs a) {
       const int i = SPLIT ? wave : e;
       const int row = m0 + 4 * lg + i;
       const float v = cv[e];
-      if (!epi_wave || row >= R || col >= N) continue;
+      if (!epi_wave || 4 * lg + i >= RG || row >= R || col >= N) continue;
       if constexpr (EPI == EPI_F32) {
         a.out_f32[static_cast<size_t>(row) * a.ldo + col] = v + bias_v;
       } else if constexpr (EPI == EPI_ACT) {
@@ -300,6 +351,44 @@ void launch_ev(K kernel, dim3 grid, dim3 block, size_t lds, hipStream_t s, hipEv
   else hipLaunchKernelGGL(kernel, grid, block, lds, s, a);
 }
 
+// Rows per workgroup for a K-split product of one row tile: groups of 4 rows
+// for the LayerNorm-prologue products (a quarter of the prologue per wave,
+// and 4x the workgroups of a narrow product), 8 where that would exceed 768
+// workgroups; whole tiles otherwise.  Measured on the decoder's shapes
+// (d = 512 and 1024, 1 / 5 / 16 rows): groups did not help the products that
+// read their input rows straight from memory.
+int row_group(int pro, int col_tiles, int rows, int tiles, int layers) {
+  if (pro != PRO_LN || tiles != 1 || layers != 1) return 16;
+  return col_tiles * ((rows + 3) / 4) <= 768 ? 4 : 8;
+}
+
+template <typename WT, int PRO, int EPI, int XF32, int LNT, int KSPLIT, int RG>
+void launch_rg(const GemmArgs& a, int spw, dim3 grid, size_t lds, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+  constexpr int NT = KSPLIT == 8 ? 512 : 256;
+  if constexpr (KSPLIT == 8) {
+    if (spw == 16) return launch_ev(k_gemm<WT, PRO, EPI, XF32, 8, LNT, RG, 16>, grid, dim3(NT), lds, s, ev0, ev1, a);
+    if (spw == 8) return launch_ev(k_gemm<WT, PRO, EPI, XF32, 8, LNT, RG, 8>, grid, dim3(NT), lds, s, ev0, ev1, a);
+  } else {
+    if (spw == 8) return launch_ev(k_gemm<WT, PRO, EPI, XF32, 4, LNT, RG, 8>, grid, dim3(NT), lds, s, ev0, ev1, a);
+    if (spw == 4) return launch_ev(k_gemm<WT, PRO, EPI, XF32, 4, LNT, RG, 4>, grid, dim3(NT), lds, s, ev0, ev1, a);
+  }
+  launch_ev(k_gemm<WT, PRO, EPI, XF32, KSPLIT, LNT, RG, 0>, grid, dim3(NT), lds, s, ev0, ev1, a);
+}
+
+template <typename WT, int PRO, int EPI, int XF32, int LNT, int KSPLIT>
+void launch_split(const GemmArgs& a, int gy, int gz, size_t lds, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+  const int ct = gemm_grid(EPI, a.N, KSPLIT);
+  const int tiles = (a.n_rows + 15) / 16;
+  const int n_steps = a.K / Mma<WT>::KS;
+  const int spw = n_steps % KSPLIT == 0 ? n_steps / KSPLIT : 0;
+  const int rg = row_group(PRO, ct, a.n_rows, tiles, gz);
+  if constexpr (PRO == PRO_LN) {
+    if (rg == 4) return launch_rg<WT, PRO, EPI, XF32, LNT, KSPLIT, 4>(a, spw, dim3(ct * ((a.n_rows + 3) / 4)), lds, s, ev0, ev1);
+    if (rg == 8) return launch_rg<WT, PRO, EPI, XF32, LNT, KSPLIT, 8>(a, spw, dim3(ct * ((a.n_rows + 7) / 8)), lds, s, ev0, ev1);
+  }
+  launch_rg<WT, PRO, EPI, XF32, LNT, KSPLIT, 16>(a, spw, dim3(ct, gy, gz), lds, s, ev0, ev1);
+}
+
 template <typename WT, int PRO, int EPI, int XF32, int LNT>
 hipError_t launch_k(GemmArgs a, int ksplit, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   const int tiles = (a.n_rows + 15) / 16;
@@ -307,16 +396,14 @@ hipError_t launch_k(GemmArgs a, int ksplit, hipStream_t s, hipEvent_t ev0, hipEv
   a.mt_per_wg = (tiles + gy - 1) / gy;
   const size_t lds = PRO == PRO_LN ? gemm_ln_lds_bytes(a.K, sizeof(WT)) : 0;
   const int gz = EPI == EPI_QKV && a.n_layers > 1 ? a.n_layers : 1;
+  if (gz > 1 || a.N % 16 != 0) a.wp = nullptr;   // the packed copy covers single-layer products with whole tiles
   if (EPI == EPI_ARGMAX || ksplit == 1) {
-    launch_ev(k_gemm<WT, PRO, EPI, XF32, 1, LNT>, dim3(gemm_grid(EPI, a.N, 1), gy, gz), dim3(256), lds, s, ev0, ev1,
-              a);
+    a.wp = nullptr;
+    launch_ev(k_gemm<WT, PRO, EPI, XF32, 1, LNT, 16, 0>, dim3(gemm_grid(EPI, a.N, 1), gy, gz), dim3(256), lds, s, ev0,
+              ev1, a);
   } else if constexpr (EPI != EPI_ARGMAX) {
-    if (ksplit == 8)
-      launch_ev(k_gemm<WT, PRO, EPI, XF32, 8, LNT>, dim3(gemm_grid(EPI, a.N, 8), gy, gz), dim3(512), lds, s, ev0,
-                ev1, a);
-    else
-      launch_ev(k_gemm<WT, PRO, EPI, XF32, 4, LNT>, dim3(gemm_grid(EPI, a.N, 4), gy, gz), dim3(256), lds, s, ev0,
-                ev1, a);
+    if (ksplit == 8) launch_split<WT, PRO, EPI, XF32, LNT, 8>(a, gy, gz, lds, s, ev0, ev1);
+    else launch_split<WT, PRO, EPI, XF32, LNT, 4>(a, gy, gz, lds, s, ev0, ev1);
   }
   return hipGetLastError();
 }
@@ -359,6 +446,38 @@ size_t gemm_ln_lds_bytes(int K, size_t elt) { return 16 * (static_cast<size_t>(K
 int gemm_grid(int epi, int N, int ksplit) {
   if (epi == EPI_ARGMAX || ksplit == 1) return (N + 63) / 64;
   return (N + 15) / 16;
+}
+
+// W [N][K] row-major -> the MFMA feed order of k_gemm (N % 16 == 0, K a
+// multiple of the MFMA step): one 16-byte word per thread.
+template <typename WT>
+__global__ __launch_bounds__(256) void k_pack_feed(const WT* __restrict__ w, WT* __restrict__ out, int N, int K) {
+  using MM = Mma<WT>;
+  constexpr int KS = MM::KS, EPL = MM::EPL;
+  const int n_steps = K / KS;
+  const long long words = static_cast<long long>(N) * K / EPL;
+  for (long long i = blockIdx.x * 256LL + threadIdx.x; i < words; i += static_cast<long long>(gridDim.x) * 256) {
+    const int lane = static_cast<int>(i % kWave);
+    const long long blk = i / kWave;                    // c * n_steps + s
+    const int c = static_cast<int>(blk / n_steps);
+    const int st = static_cast<int>(blk - static_cast<long long>(c) * n_steps);
+    const size_t src = static_cast<size_t>(16 * c + (lane & 15)) * K + st * KS + EPL * (lane >> 4);
+    *reinterpret_cast<uint4*>(out + static_cast<size_t>(i) * EPL) = *reinterpret_cast<const uint4*>(w + src);
+  }
+}
+
+hipError_t launch_pack_feed(int dtype, const void* w, void* out, int N, int K, hipStream_t s) {
+  const int ks = dtype == DT_BF16 ? Mma<bf16_t>::KS : Mma<float>::KS;
+  if (N <= 0 || K <= 0 || N % 16 != 0 || K % ks != 0) return hipErrorInvalidValue;
+  const long long words = static_cast<long long>(N) * K / (dtype == DT_BF16 ? 8 : 4);
+  const int grid = static_cast<int>(std::min<long long>((words + 255) / 256, 4096));
+  if (dtype == DT_BF16)
+    hipLaunchKernelGGL(k_pack_feed<bf16_t>, dim3(grid), dim3(256), 0, s, static_cast<const bf16_t*>(w),
+                       static_cast<bf16_t*>(out), N, K);
+  else
+    hipLaunchKernelGGL(k_pack_feed<float>, dim3(grid), dim3(256), 0, s, static_cast<const float*>(w),
+                       static_cast<float*>(out), N, K);
+  return hipGetLastError();
 }
 
 hipError_t launch_gemm(int dtype, int pro, int epi, int ksplit, const GemmArgs& a, hipStream_t s, hipEvent_t ev0,

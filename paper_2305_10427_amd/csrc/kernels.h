@@ -78,6 +78,10 @@ struct GemmArgs {
   long long kv_stride;
   const void* lw[kMaxLayers];
   const void* lb[kMaxLayers];
+  // optional (nullptr: row-major w only): the same weights in the MFMA feed
+  // order of the K-split product kernels (launch_pack_feed); single-layer
+  // launches with N % 16 == 0 only
+  const void* wp;
 };
 
 // The weights and caches of layer z of a multi-layer EPI_QKV launch.  The
@@ -93,6 +97,7 @@ __device__ __forceinline__ void layer_select(GemmArgs& a, int z) {
       b = z == i ? a.lb[i] : b;
     }
     a.w = w;
+    a.wp = nullptr;
     a.bias = b;
     a.kc = static_cast<char*>(a.kc) + z * a.kv_stride;
     a.vc = static_cast<char*>(a.vc) + z * a.kv_stride;
@@ -231,6 +236,11 @@ struct ReduceArgs {
 hipError_t launch_gemm(int dtype, int pro, int epi, int ksplit, const GemmArgs& a, hipStream_t s,
                        hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 int gemm_grid(int epi, int N, int ksplit);
+// W [N][K] (row-major) -> out [N * K] in the MFMA feed order read through
+// GemmArgs::wp: block (c, s) of 64 16-byte words holds, in word l,
+// W[16 c + (l & 15)][s KS + EPL (l >> 4) ... + EPL - 1] (KS, EPL of the MFMA
+// step of the type).  N % 16 == 0 and K % KS == 0, else hipErrorInvalidValue.
+hipError_t launch_pack_feed(int dtype, const void* w, void* out, int N, int K, hipStream_t s);
 size_t gemm_ln_lds_bytes(int K, size_t elt);
 // Products of many rows on LDS-staged MFMA tiles (bf16, no prologue, K a
 // multiple of 64); bitwise the same values as launch_gemm.  The vocabulary

@@ -8,6 +8,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -102,15 +103,27 @@ void shape_of(const pd_config& c, int idx, int64_t* rows, int64_t* cols) {
 struct pd_model {
   pd_config cfg;
   std::vector<const void*> w;
+  // per weight: its copy in the MFMA feed order of the K-split product
+  // kernels (owned, nullptr for weights that are not such products), made by
+  // the first context created on the model (make_feed)
+  mutable std::vector<void*> feed;
+  mutable std::mutex feed_mu;
+  mutable bool feed_ready = false;
   int dt;          // DT_F32 / DT_BF16
   int d, H, dh, dff, V;
   float enc_scale, dec_scale;
 
   const void* enc(int l, int j) const { return w[2 + 12 * l + j]; }
+  const void* enc_feed(int l, int j) const { return feed[2 + 12 * l + j]; }
   const void* enc_ln(int j) const { return w[2 + 12 * cfg.n_enc + j]; }
   int dec_base() const { return 2 + 12 * cfg.n_enc + (cfg.pre_ln ? 2 : 0); }
   const void* dec(int l, int j) const { return w[dec_base() + 20 * l + j]; }
+  const void* dec_feed(int l, int j) const { return feed[dec_base() + 20 * l + j]; }
   const void* dec_ln(int j) const { return w[dec_base() + 20 * cfg.n_dec + j]; }
+  ~pd_model() {
+    for (void* p : feed)
+      if (p != nullptr) hipFree(p);
+  }
 };
 
 namespace {
@@ -375,7 +388,7 @@ hipError_t decoder_pass(pd_ctx& C, const Rows& r, float* logits, hipStream_t s, 
     }
     const bool ln_qkv = pre || l > 0;
     g.ldx = d; g.ln_eps = cfg.ln_eps;
-    g.w = M.dec(l, D_WQKV); g.bias = M.dec(l, D_BQKV); g.N = 3 * d; g.K = d;
+    g.w = M.dec(l, D_WQKV); g.wp = M.dec_feed(l, D_WQKV); g.bias = M.dec(l, D_BQKV); g.N = 3 * d; g.K = d;
     g.out_f32 = q_buf; g.ldo = d; g.q_cols = d;
     g.kc = C.at<char>(C.L.self_k) + l * self_layer; g.vc = C.at<char>(C.L.self_v) + l * self_layer;
     g.H = M.H; g.dh = M.dh; g.T = C.max_tgt; g.d = d;
@@ -387,7 +400,7 @@ hipError_t decoder_pass(pd_ctx& C, const Rows& r, float* logits, hipStream_t s, 
     if ((e = launch_attn(M.dt, aa, r.R_max, s)) != hipSuccess) return e;
 
     g = gemm_base(r);
-    g.x = a_buf; g.ldx = d; g.w = M.dec(l, D_WO); g.bias = M.dec(l, D_BO); g.N = d; g.K = d;
+    g.x = a_buf; g.ldx = d; g.w = M.dec(l, D_WO); g.wp = M.dec_feed(l, D_WO); g.bias = M.dec(l, D_BO); g.N = d; g.K = d;
     g.resid = x_res; g.ldr = d; g.ldo = d;
     if (pre) g.out = x_res; else g.out_f32 = s_buf;
     if ((e = run_gemm(C, r, g, EPI_RESID, false, nullptr, s)) != hipSuccess) return e;
@@ -397,7 +410,7 @@ hipError_t decoder_pass(pd_ctx& C, const Rows& r, float* logits, hipStream_t s, 
     if (pre) { g.x = x_res; g.x_f32 = 0; g.ln_g = M.dec(l, D_LN2G); g.ln_b = M.dec(l, D_LN2B); }
     else { g.x = s_buf; g.x_f32 = 1; g.ln_g = M.dec(l, D_LN1G); g.ln_b = M.dec(l, D_LN1B); g.ln_out = x_res; g.ldlo = d; }
     g.ldx = d; g.ln_eps = cfg.ln_eps;
-    g.w = M.dec(l, D_CWQ); g.bias = M.dec(l, D_CBQ); g.N = d; g.K = d; g.out_f32 = q_buf; g.ldo = d;
+    g.w = M.dec(l, D_CWQ); g.wp = M.dec_feed(l, D_CWQ); g.bias = M.dec(l, D_CBQ); g.N = d; g.K = d; g.out_f32 = q_buf; g.ldo = d;
     if ((e = run_gemm(C, r, g, EPI_F32, true, pre ? a_buf : x_res, s)) != hipSuccess) return e;
 
     aa = AttnArgs{r.n_dev, r.n_host, q_buf, d, C.at<char>(C.L.cross_k) + l * cross_layer,
@@ -406,7 +419,7 @@ hipError_t decoder_pass(pd_ctx& C, const Rows& r, float* logits, hipStream_t s, 
     if ((e = launch_attn(M.dt, aa, r.R_max, s)) != hipSuccess) return e;
 
     g = gemm_base(r);
-    g.x = a_buf; g.ldx = d; g.w = M.dec(l, D_CWO); g.bias = M.dec(l, D_CBO); g.N = d; g.K = d;
+    g.x = a_buf; g.ldx = d; g.w = M.dec(l, D_CWO); g.wp = M.dec_feed(l, D_CWO); g.bias = M.dec(l, D_CBO); g.N = d; g.K = d;
     g.resid = x_res; g.ldr = d; g.ldo = d;
     if (pre) g.out = x_res; else g.out_f32 = s_buf;
     if ((e = run_gemm(C, r, g, EPI_RESID, false, nullptr, s)) != hipSuccess) return e;
@@ -416,12 +429,12 @@ hipError_t decoder_pass(pd_ctx& C, const Rows& r, float* logits, hipStream_t s, 
     if (pre) { g.x = x_res; g.x_f32 = 0; g.ln_g = M.dec(l, D_LN3G); g.ln_b = M.dec(l, D_LN3B); }
     else { g.x = s_buf; g.x_f32 = 1; g.ln_g = M.dec(l, D_LN2G); g.ln_b = M.dec(l, D_LN2B); g.ln_out = x_res; g.ldlo = d; }
     g.ldx = d; g.ln_eps = cfg.ln_eps;
-    g.w = M.dec(l, D_W1); g.bias = M.dec(l, D_B1); g.N = M.dff; g.K = d;
+    g.w = M.dec(l, D_W1); g.wp = M.dec_feed(l, D_W1); g.bias = M.dec(l, D_B1); g.N = M.dff; g.K = d;
     g.out = h_buf; g.ldo = M.dff; g.act = cfg.act_gelu ? 2 : 1;
     if ((e = run_gemm(C, r, g, EPI_ACT, true, pre ? a_buf : x_res, s)) != hipSuccess) return e;
 
     g = gemm_base(r);
-    g.x = h_buf; g.ldx = M.dff; g.w = M.dec(l, D_W2); g.bias = M.dec(l, D_B2); g.N = d; g.K = M.dff;
+    g.x = h_buf; g.ldx = M.dff; g.w = M.dec(l, D_W2); g.wp = M.dec_feed(l, D_W2); g.bias = M.dec(l, D_B2); g.N = d; g.K = M.dff;
     g.resid = x_res; g.ldr = d; g.ldo = d;
     if (pre) g.out = x_res; else g.out_f32 = s_buf;
     if ((e = run_gemm(C, r, g, EPI_RESID, false, nullptr, s)) != hipSuccess) return e;
@@ -505,7 +518,7 @@ hipError_t encoder_pass(pd_ctx& C, const int32_t* src, int B, int n_max, hipStre
       g.x = x_res; g.x_f32 = 0; ln = false;   // the embedding
     }
     g.ldx = d; g.ln_eps = cfg.ln_eps;
-    g.w = M.enc(l, E_WQKV); g.bias = M.enc(l, E_BQKV); g.N = 3 * d; g.K = d;
+    g.w = M.enc(l, E_WQKV); g.wp = M.enc_feed(l, E_WQKV); g.bias = M.enc(l, E_BQKV); g.N = 3 * d; g.K = d;
     g.out_f32 = q_buf; g.ldo = d; g.q_cols = d;
     g.kc = C.at<char>(C.L.enc_k); g.vc = C.at<char>(C.L.enc_v);
     g.H = M.H; g.dh = M.dh; g.T = C.max_src; g.d = d;
@@ -513,7 +526,7 @@ hipError_t encoder_pass(pd_ctx& C, const int32_t* src, int B, int n_max, hipStre
     AttnArgs aa{nullptr, R, q_buf, d, g.kc, g.vc, M.H, M.dh, C.max_src, r.map, 0, klen, a_buf, d, scale};
     if ((e = launch_attn(M.dt, aa, R, s)) != hipSuccess) return e;
     g = gemm_base(r);
-    g.x = a_buf; g.ldx = d; g.w = M.enc(l, E_WO); g.bias = M.enc(l, E_BO); g.N = d; g.K = d;
+    g.x = a_buf; g.ldx = d; g.w = M.enc(l, E_WO); g.wp = M.enc_feed(l, E_WO); g.bias = M.enc(l, E_BO); g.N = d; g.K = d;
     g.resid = x_res; g.ldr = d; g.ldo = d;
     if (pre) g.out = x_res; else g.out_f32 = s_buf;
     if ((e = run_gemm(C, r, g, EPI_RESID, false, nullptr, s)) != hipSuccess) return e;
@@ -526,11 +539,11 @@ hipError_t encoder_pass(pd_ctx& C, const int32_t* src, int B, int n_max, hipStre
       g.ln_out = x_res; g.ldlo = d; ln_tmp = x_res;
     }
     g.ldx = d; g.ln_eps = cfg.ln_eps;
-    g.w = M.enc(l, E_W1); g.bias = M.enc(l, E_B1); g.N = M.dff; g.K = d;
+    g.w = M.enc(l, E_W1); g.wp = M.enc_feed(l, E_W1); g.bias = M.enc(l, E_B1); g.N = M.dff; g.K = d;
     g.out = h_buf; g.ldo = M.dff; g.act = cfg.act_gelu ? 2 : 1;
     if ((e = run_gemm(C, r, g, EPI_ACT, true, ln_tmp, s)) != hipSuccess) return e;
     g = gemm_base(r);
-    g.x = h_buf; g.ldx = M.dff; g.w = M.enc(l, E_W2); g.bias = M.enc(l, E_B2); g.N = d; g.K = M.dff;
+    g.x = h_buf; g.ldx = M.dff; g.w = M.enc(l, E_W2); g.wp = M.enc_feed(l, E_W2); g.bias = M.enc(l, E_B2); g.N = d; g.K = M.dff;
     g.resid = x_res; g.ldr = d; g.ldo = d;
     if (pre) g.out = x_res; else g.out_f32 = s_buf;
     if ((e = run_gemm(C, r, g, EPI_RESID, false, nullptr, s)) != hipSuccess) return e;
@@ -695,6 +708,35 @@ pd_status pd_weight_shape(const pd_config* cfg, int32_t idx, int64_t* rows, int6
   return PD_OK;
 }
 
+// The MFMA-feed copies of the encoder and decoder products, once per model
+// (the first context created on it; the weights are read here).
+static hipError_t make_feed(const pd_model& M) {
+  std::lock_guard<std::mutex> lock(M.feed_mu);
+  if (M.feed_ready) return hipSuccess;
+  std::vector<int> prods;
+  for (int l = 0; l < M.cfg.n_enc; ++l)
+    for (int j : {E_WQKV, E_WO, E_W1, E_W2}) prods.push_back(2 + 12 * l + j);
+  for (int l = 0; l < M.cfg.n_dec; ++l)
+    for (int j : {D_WQKV, D_WO, D_CWQ, D_CWO, D_W1, D_W2}) prods.push_back(M.dec_base() + 20 * l + j);
+  const size_t es = M.dt == DT_BF16 ? 2 : 4;
+  hipError_t e = hipSuccess;
+  for (int idx : prods) {
+    if (M.feed[idx] != nullptr) continue;
+    int64_t rows = 0, cols = 0;
+    shape_of(M.cfg, idx, &rows, &cols);
+    if (rows % 16 != 0) continue;      // a ragged column tile: the row-major weights only
+    void* p = nullptr;
+    if ((e = hipMalloc(&p, static_cast<size_t>(rows * cols) * es)) != hipSuccess) return e;
+    M.feed[idx] = p;
+    if ((e = launch_pack_feed(M.dt, M.w[idx], p, static_cast<int>(rows), static_cast<int>(cols), nullptr)) !=
+        hipSuccess)
+      return e;
+  }
+  if ((e = hipStreamSynchronize(nullptr)) != hipSuccess) return e;
+  M.feed_ready = true;
+  return hipSuccess;
+}
+
 pd_status pd_model_create(const pd_config* cfg, const void* const* dev_weights, int32_t n_weights,
                           pd_model** out) {
   std::string why;
@@ -720,6 +762,7 @@ pd_status pd_model_create(const pd_config* cfg, const void* const* dev_weights, 
   const float sq = std::sqrt(static_cast<float>(cfg->d_model));
   m->enc_scale = cfg->enc_emb_scale < 0.f ? sq : cfg->enc_emb_scale;
   m->dec_scale = cfg->dec_emb_scale < 0.f ? sq : cfg->dec_emb_scale;
+  m->feed.assign(n, nullptr);
   *out = m;
   return PD_OK;
 }
@@ -749,6 +792,8 @@ pd_status pd_ctx_create(const pd_model* model, int32_t max_batch, int32_t max_sr
     return fail(PD_E_WORKSPACE, "workspace is null or not 256-byte aligned");
   if (workspace_bytes < need)
     return fail(PD_E_WORKSPACE, "workspace too small: need " + std::to_string(need) + " bytes");
+  hipError_t fe = make_feed(*model);
+  if (fe != hipSuccess) return fail(PD_E_DEVICE, std::string("weight feed copies: ") + hipGetErrorString(fe));
   pd_ctx* c = new pd_ctx();
   c->M = model;
   c->max_batch = max_batch;
