@@ -3,7 +3,9 @@
     python3 -m paper_2305_10427_amd.profsum kt  RUN_kernel_trace.csv
         per-kernel launches and durations per decoding iteration, counted from
         the first vocabulary launch on (the decode; the weight upload and the
-        encoder come before it)
+        encoder come before it); then the same per-launch averages for each
+        half of the decode's vocabulary launches (bench.py --decode-only
+        decodes its sentences twice: graph replay, then the event-timed pass)
     python3 -m paper_2305_10427_amd.profsum pmc RUN_counter_collection.csv COUNTER
         per-kernel mean of COUNTER over the decode, and the three largest
         values of the runtime's copy kernel (the 256 MiB calibration copies
@@ -41,8 +43,20 @@ def kernel_table(path):
         if per >= 0.05:
             print(f"| `{k}` | {len(v) / iters:.2f} | {sum(v) / len(v):.2f} | {per:.1f} |")
     print(f"| sum of kernel durations | | | {total:.1f} |")
+    vocab_at = [i for i, r in enumerate(dec) if "k_vocab" in r["Kernel_Name"]]
+    cut = vocab_at[len(vocab_at) // 2] if len(vocab_at) >= 2 else len(dec)
+    halves = {}
+    for name, part in (("first half", dec[:cut]), ("second half", dec[cut:])):
+        h = collections.defaultdict(list)
+        for r in part:
+            h[_short(r["Kernel_Name"])].append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+        prod = [x for k, v in h.items() if k.startswith("pdec::k_gemm") for x in v]
+        halves[name] = {k: {"launches": len(v), "avg_us": round(sum(v) / len(v), 3)} for k, v in h.items()}
+        halves[name]["all k_gemm"] = {"launches": len(prod), "avg_us": round(sum(prod) / max(len(prod), 1), 3)}
+        print(f"{name}: k_gemm {len(prod)} launches, avg {sum(prod) / max(len(prod), 1):.2f} us; " +
+              "; ".join(f"{k} avg {sum(v) / len(v):.2f} us" for k, v in h.items() if "k_vocab" in k or "k_attn" in k))
     print("JSON " + json.dumps({"iterations": iters, "kernels": {
-        k: {"launches": len(v), "avg_us": round(sum(v) / len(v), 3)} for k, v in agg.items()}}))
+        k: {"launches": len(v), "avg_us": round(sum(v) / len(v), 3)} for k, v in agg.items()}, "halves": halves}))
 
 
 def counter_table(path, counter):
