@@ -18,11 +18,14 @@
  * test (Eq. (3): the block is unchanged) that commits converged blocks and
  * lays out the next iteration, so the loop needs no host round trip.
  *
- * Memory ownership.  Every device buffer (weights, workspace, inputs, outputs)
- * is allocated and freed by the caller; the library never allocates device
- * memory.  pd_model / pd_ctx own host-side state only (plus one pinned host
- * word per context for completion polling).  Weight and workspace buffers
- * must stay valid and unchanged while a model / context uses them.
+ * Memory ownership.  Every device buffer the caller hands over (weights,
+ * workspace, inputs, outputs) is allocated and freed by the caller.  The
+ * library allocates device memory in one place only: the first pd_ctx_create
+ * on a model makes the model's copy of its product weights in matrix-core
+ * feed order (see pd_model_create), freed by pd_model_destroy.  Besides that,
+ * pd_model / pd_ctx own host-side state (plus one pinned host word per
+ * context for completion polling).  Weight and workspace buffers must stay
+ * valid and unchanged while a model / context uses them.
  *
  * Threads and streams.  A pd_ctx is used by one host thread at a time; calls
  * on it are enqueued on the stream given to each call and are asynchronous
