@@ -46,6 +46,20 @@ notes of the repository as well):
 * PJ and PGJ solve all m equations; their output is cut after the first [EOS].
 * Greedy AR stops after producing [EOS] (Eq. (1) with the usual end-of-sentence rule).
 * The argmax takes the lowest index on exact ties; non-finite logits raise.
+
+A stopping-condition variant (the paper leaves other stopping conditions to
+future work, Section 3.3 and the conclusion): stop="prefix" commits, after
+every iteration, the longest prefix of the block that the iteration has
+proven exact, instead of waiting for the whole block to repeat (Eq. (3)).
+Position i (the block start) is exact after any iteration, since its input is
+the committed prefix; if the first t positions of the block came out as they
+went in, those inputs were exact, so positions i .. i+t are exact.  With t the
+number of leading unchanged positions, the iteration commits all L positions
+when t = L (Eq. (3) holds) and t + 1 otherwise; the next block starts right
+after the committed positions and keeps the newer values as its draft.  Every
+iteration commits at least one position, so k <= m without a per-block cap,
+and the output is greedy decoding's (the argument of Proposition 1).  HGJ
+stops at an [EOS] among the committed positions only.
 """
 from __future__ import annotations
 
@@ -151,13 +165,18 @@ def block_length(mode: str, i: int, m: int, b: int, h: int) -> int:
 
 def solve_by_blocks(model: Model, enc: Encoded, m: int, mode: str, b: int = 1, h: Optional[int] = None,
                     init=None, max_iters: Optional[int] = None, recompute: bool = False,
-                    evaluator=None) -> Result:
+                    evaluator=None, stop: str = "block") -> Result:
     """The block fixed-point procedure shared by PJ, PGJ and HGJ (Section 3.2).
 
     evaluator: optional stand-in for the model's Solver (an object with the
     same ``block(y, i, L)`` and ``records``), so that a recorded sequence of
     evaluations of F can be replayed through exactly this control flow.
+    stop: "block" (Eq. (3)) or "prefix" (the variant described above).
     """
+    if stop == "prefix":
+        return _solve_prefix(model, enc, m, mode, b, h, init, max_iters, recompute, evaluator)
+    if stop != "block":
+        raise ValueError(stop)
     F = Solver(model, enc, m, recompute) if evaluator is None else evaluator
     cap = _cap(m, max_iters)
     h = m if h is None else min(h, m)
@@ -190,22 +209,57 @@ def solve_by_blocks(model: Model, enc: Encoded, m: int, mode: str, b: int = 1, h
     return res
 
 
+def _solve_prefix(model: Model, enc: Encoded, m: int, mode: str, b: int, h: Optional[int], init,
+                  max_iters: Optional[int], recompute: bool, evaluator) -> Result:
+    """The blocks of solve_by_blocks under stop="prefix": every iteration
+    commits the block's proven prefix and the block moves on by that much."""
+    F = Solver(model, enc, m, recompute) if evaluator is None else evaluator
+    cap = _cap(m, max_iters)
+    h = m if h is None else min(h, m)
+    y = _init(m, init)
+    res = Result(y, y, 0)
+    i = 0
+    while i < m:
+        if res.k >= cap:
+            res.hit_max_iters = True
+            break
+        L = block_length(mode, i, m, b, h)
+        before = y[i:i + L].copy()
+        y[i:i + L] = F.block(y, i, L)
+        res.k += 1
+        res.iterates.append((res.k, i, y[i:i + L].copy()))
+        t = 0                                     # leading positions that came out as they went in
+        while t < L and y[i + t] == before[t]:
+            t += 1
+        c = L if t == L else t + 1                # positions proven exact
+        if mode == "hybrid":
+            hit = np.nonzero(y[i:i + c] == EOS)[0]
+            if len(hit):                          # an [EOS] among the committed positions
+                y = y[: i + int(hit[0]) + 1].copy()
+                break
+        i += c
+    res.y, res.out, res.records = y, cut_at_eos(y), F.records
+    return res
+
+
 def jacobi(model: Model, enc: Encoded, m: int, init=None, max_iters: Optional[int] = None,
-           recompute: bool = False, evaluator=None) -> Result:
+           recompute: bool = False, evaluator=None, stop: str = "block") -> Result:
     """Parallel Jacobi decoding (Algorithm 1): one block of all m positions."""
     return solve_by_blocks(model, enc, m, "jacobi", init=init, max_iters=max_iters, recompute=recompute,
-                           evaluator=evaluator)
+                           evaluator=evaluator, stop=stop)
 
 
 def gs_jacobi(model: Model, enc: Encoded, m: int, b: int, init=None,
-              max_iters: Optional[int] = None, recompute: bool = False, evaluator=None) -> Result:
+              max_iters: Optional[int] = None, recompute: bool = False, evaluator=None,
+              stop: str = "block") -> Result:
     """Parallel GS-Jacobi decoding (Algorithm 2): Jacobi inside b-blocks, Gauss-Seidel across them."""
     return solve_by_blocks(model, enc, m, "gs_jacobi", b, init=init, max_iters=max_iters, recompute=recompute,
-                           evaluator=evaluator)
+                           evaluator=evaluator, stop=stop)
 
 
 def hybrid(model: Model, enc: Encoded, m: int, b: int, h: Optional[int] = None, init=None,
-           max_iters: Optional[int] = None, recompute: bool = False, evaluator=None) -> Result:
+           max_iters: Optional[int] = None, recompute: bool = False, evaluator=None,
+           stop: str = "block") -> Result:
     """Hybrid GS-Jacobi decoding (Algorithm 3).
 
     GS-Jacobi blocks up to the horizon h; a converged block that holds [EOS]
@@ -213,7 +267,7 @@ def hybrid(model: Model, enc: Encoded, m: int, b: int, h: Optional[int] = None, 
     autoregressively from position h until [EOS] or m.
     """
     return solve_by_blocks(model, enc, m, "hybrid", b, h, init=init, max_iters=max_iters, recompute=recompute,
-                           evaluator=evaluator)
+                           evaluator=evaluator, stop=stop)
 
 
 def decode(model: Model, enc: Encoded, m: int, mode: str, block: int = 1, **kw) -> Result:

@@ -292,3 +292,93 @@ def test_greedy_solution_as_draft_is_a_fixed_point(cfg, seed, kw):
                 r = oracle.gs_jacobi(M, enc, m, b, init=y_star)
                 assert r.k == -(-m // b)
                 np.testing.assert_array_equal(r.y, y_star)
+
+
+# ---------------------------------------------------------------------------
+# The prefix stopping condition (a variant of Eq. (3); see oracle/decode.py)
+
+
+@pytest.mark.parametrize("cfg,seed,kw", CASES, ids=["tiny", "tiny_bias", "chain"])
+def test_prefix_stop_equals_greedy_and_commits_every_iteration(cfg, seed, kw):
+    """Proposition 1 carries over: every mode under stop="prefix" returns the
+    greedy output, from [PAD] drafts and from random ones; every iteration
+    moves the block start forward (at least one position is committed), so
+    k <= m without a cap; and the block start never moves back."""
+    M = _model(cfg, seed, **kw)
+    for si, src in enumerate(_sources(cfg, 5, seed=seed + 30)):
+        enc = M.encode(src)
+        for m in (1, 2, 7, 16):
+            ar_full = oracle.greedy(M, enc, m, stop_at_eos=False)
+            ar = oracle.greedy(M, enc, m)
+            for init in (None, synth.random_draft(m, cfg.vocab, 200 + si)):
+                for mode, b in [("jacobi", 0), ("gs_jacobi", 1), ("gs_jacobi", 3), ("gs_jacobi", 5),
+                                ("hybrid", 2), ("hybrid", 4)]:
+                    r = oracle.decode(M, enc, m, mode, b, init=init, stop="prefix")
+                    np.testing.assert_array_equal(r.out, ar.out, err_msg=f"prefix {mode} b={b} m={m}")
+                    assert 1 <= r.k <= m and not r.hit_max_iters
+                    starts = [i for _, i, _ in r.iterates]
+                    assert all(b2 > a2 for a2, b2 in zip(starts, starts[1:])), starts
+                    if mode != "hybrid":
+                        np.testing.assert_array_equal(r.y, ar_full.y)
+
+
+class _Scripted:
+    """A stand-in for the decoder: F(y)[p] = T[p] when p = 0 or y[p-1] = T[p-1],
+    else the wrong token 3 (a chain whose links are right only after a right
+    predecessor)."""
+
+    def __init__(self, T):
+        self.T, self.records, self.calls = list(T), [], []
+
+    def block(self, y, i, L):
+        self.calls.append((i, L))
+        return np.array([self.T[p] if p == 0 or y[p - 1] == self.T[p - 1] else 3 for p in range(i, i + L)],
+                        np.int32)
+
+
+def test_prefix_stop_worked_example():
+    """A hand-worked case, m = 6, b = 3, T = (5 6 7 8 9 10), draft
+    (5 6 PAD PAD 9 10):
+      prefix: [0,3) -> 5 6 7 (5 6 came out as they went in: commit 3);
+              [3,6) -> 8 3 10 (first position changed: commit 1);
+              [4,6) -> 9 3 (commit 1); [5,6) -> 10 (commit 1): k = 4.
+      Eq. (3): [0,3) 5 6 7, then unchanged (2 iterations); [3,6) 8 3 10,
+              8 9 3, 8 9 10 (cap of 3 iterations): k = 5."""
+    T = [5, 6, 7, 8, 9, 10]
+    draft = np.array([5, 6, PAD, PAD, 9, 10], np.int32)
+    ev = _Scripted(T)
+    r = oracle.gs_jacobi(None, None, 6, 3, init=draft, evaluator=ev, stop="prefix")
+    assert r.k == 4 and ev.calls == [(0, 3), (3, 3), (4, 2), (5, 1)]
+    np.testing.assert_array_equal(r.y, T)
+    ev = _Scripted(T)
+    r = oracle.gs_jacobi(None, None, 6, 3, init=draft, evaluator=ev)
+    assert r.k == 5 and ev.calls == [(0, 3), (0, 3), (3, 3), (3, 3), (3, 3)]
+    np.testing.assert_array_equal(r.y, T)
+    # a perfect draft: every iteration finds its block unchanged and commits it whole
+    ev = _Scripted(T)
+    r = oracle.gs_jacobi(None, None, 6, 4, init=np.array(T, np.int32), evaluator=ev, stop="prefix")
+    assert r.k == 2 and ev.calls == [(0, 4), (4, 2)]
+    # [PAD] drafts: only the block start is ever proven, one position per iteration
+    ev = _Scripted(T)
+    r = oracle.jacobi(None, None, 6, evaluator=ev, stop="prefix")
+    assert r.k == 6 and ev.calls == [(i, 6 - i) for i in range(6)]
+
+
+@pytest.mark.parametrize("cfg,seed", [(TINY, 8), (CHAIN, 9)], ids=["tiny", "chain"])
+@pytest.mark.parametrize("b", [3, 4])
+def test_prefix_stop_hybrid_eos(cfg, seed, b):
+    """[EOS] at a block start, inside a block, at a block's end or absent, crossed
+    with horizons: the prefix variant of HGJ stops exactly where greedy
+    decoding does (an [EOS] is acted on only once it is committed)."""
+    m = 16
+    wkw = dict(bias_std=0.5, ln_std=0.3)
+    found = eos_cases(cfg, seed, wkw, b, m)
+    assert set(found) == {"start", "mid", "last", "absent"}, sorted(found)
+    for kind, (B, src, q) in found.items():
+        M = _model(cfg, seed, eos_bias=B, **wkw)
+        enc = M.encode(src)
+        ar = oracle.greedy(M, enc, m)
+        for h in (1, b, m // 2, m - 1, m):
+            r = oracle.hybrid(M, enc, m, b, h=h, stop="prefix")
+            np.testing.assert_array_equal(r.out, ar.out, err_msg=f"{kind} h={h}")
+            assert r.k <= len(ar.out)

@@ -50,6 +50,14 @@ def decode_pins():
     TD.test_special_cases_between_modes()
 
 
+def prefix_pins():
+    for case in TD.CASES:
+        TD.test_prefix_stop_equals_greedy_and_commits_every_iteration(*case)
+    TD.test_prefix_stop_worked_example()
+    for cfg, seed in [(TD.TINY, 8), (TD.CHAIN, 9)]:
+        TD.test_prefix_stop_hybrid_eos(cfg, seed, 4)
+
+
 MODEL_MUTANTS = {
     "dropped linear bias": (om.Model, "_lin", "x @ self.w[name_w].T + self.w[name_b]", "x @ self.w[name_w].T"),
     "dropped LayerNorm offset": (om, "layer_norm", "np.sqrt(var + eps) * g + b", "np.sqrt(var + eps) * g"),
@@ -89,6 +97,18 @@ DECODE_MUTANTS = {
 }
 
 
+PREFIX_MUTANTS = {
+    "one position committed past the proven prefix": (OD, "_solve_prefix", "c = L if t == L else t + 1",
+                                                      "c = L if t == L else t + 2"),
+    "only the proven positions, never the whole unchanged block": (OD, "_solve_prefix",
+                                                                   "c = L if t == L else t + 1", "c = min(t + 1, L - 1) if L > 1 else 1"),
+    "[EOS] looked for in the whole block": (OD, "_solve_prefix", "hit = np.nonzero(y[i:i + c] == EOS)[0]",
+                                            "hit = np.nonzero(y[i:i + L] == EOS)[0]"),
+    "unchanged positions counted from the block's end": (OD, "_solve_prefix", "y[i + t] == before[t]",
+                                                         "y[i + L - 1 - t] == before[L - 1 - t]"),
+}
+
+
 @pytest.mark.parametrize("name", list(MODEL_MUTANTS))
 def test_model_pins_catch(monkeypatch, name):
     mutate(monkeypatch, *MODEL_MUTANTS[name])
@@ -108,6 +128,13 @@ def test_decode_pins_catch(monkeypatch, name):
     mutate(monkeypatch, *DECODE_MUTANTS[name])
     with pytest.raises((AssertionError, IndexError, ValueError)):
         decode_pins()
+
+
+@pytest.mark.parametrize("name", list(PREFIX_MUTANTS))
+def test_prefix_pins_catch(monkeypatch, name):
+    mutate(monkeypatch, *PREFIX_MUTANTS[name])
+    with pytest.raises((AssertionError, IndexError, ValueError)):
+        prefix_pins()
 
 
 def test_eos_stop_at_block_index_instead_of_position_is_caught(monkeypatch):
@@ -130,4 +157,5 @@ def test_unmutated_pins_pass():
     model_pins()
     bf16_pins()
     decode_pins()
+    prefix_pins()
     np.testing.assert_equal(oracle.cut_at_eos(np.array([5, 2, 7, 2])), [5, 2])
