@@ -82,9 +82,12 @@ def test_bench_refuses_more_than_one_gpu():
     assert res.stdout.strip() == ""
 
 
-def test_bench_traffic_figure_is_tied_to_the_kernel_sources(tmp_path, monkeypatch):
+@pytest.mark.parametrize("name", ["vocab_argmax_large", "gemm_products_large", "vocab_argmax_mt_base",
+                                  "gemm_products_mt_base"])
+def test_bench_traffic_figure_is_tied_to_the_kernel_sources(tmp_path, monkeypatch, name):
     import bench
-    rec = json.load(open(os.path.join(ROOT, "profiles", "vocab_argmax_mt_base_bf16.json")))
+    rec = json.load(open(os.path.join(ROOT, "profiles", name + ".json")))
+    assert abs(rec["traffic_bytes_per_launch"] - rec["fetch_bytes_per_launch"] - rec["write_bytes_per_launch"]) <= 1
     csrc = tmp_path / "paper_2305_10427_amd" / "csrc"
     csrc.mkdir(parents=True)
     (tmp_path / "profiles").mkdir()
@@ -92,10 +95,10 @@ def test_bench_traffic_figure_is_tied_to_the_kernel_sources(tmp_path, monkeypatc
         shutil.copy(os.path.join(ROOT, "paper_2305_10427_amd", "csrc", f), csrc / f)
     src = b"".join((csrc / f).read_bytes() for f in rec["kernel_sources"])
     good = dict(rec, kernel_source_sha256=hashlib.sha256(src).hexdigest())
-    (tmp_path / "profiles" / "vocab_argmax_mt_base_bf16.json").write_text(json.dumps(good))
+    (tmp_path / "profiles" / (name + ".json")).write_text(json.dumps(good))
     monkeypatch.setattr(bench, "ROOT", str(tmp_path))
-    assert bench.measured_traffic("vocab_argmax_mt_base_bf16") == int(rec["traffic_bytes_per_launch"])
+    assert bench.measured_traffic(name) == int(rec["traffic_bytes_per_launch"])
     # any change to a kernel source voids the figure
     with open(csrc / rec["kernel_sources"][0], "ab") as f:
         f.write(b"\n")
-    assert bench.measured_traffic("vocab_argmax_mt_base_bf16") is None
+    assert bench.measured_traffic(name) is None
