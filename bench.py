@@ -35,8 +35,17 @@ if ROOT not in sys.path:
 HBM_PEAK_GBS = 8000.0
 MFMA_BF16_PEAK_TFLOPS = 2500.0   # dense bf16 matrix peak of MI355X
 HEADLINE = ("gs_jacobi", 16)
-LARGE_MODES = [("ar", 1), ("jacobi", 0), ("gs_jacobi", 16), ("hybrid", 16)]
-MT_MODES = [("ar", 1), ("gs_jacobi", 5), ("hybrid", 5)]
+# (mode, block[, stopping condition]); "prefix" is PD_STOP_PREFIX, the
+# stopping-condition variant (the default is Eq. (3))
+LARGE_MODES = [("ar", 1), ("jacobi", 0), ("gs_jacobi", 16), ("hybrid", 16), ("gs_jacobi", 16, "prefix")]
+MT_MODES = [("ar", 1), ("jacobi", 0), ("gs_jacobi", 5), ("hybrid", 5), ("gs_jacobi", 5, "prefix"),
+            ("hybrid", 5, "prefix"), ("jacobi", 0, "prefix")]
+
+
+def mode_key(spec):
+    mode, b = spec[0], spec[1]
+    stop = spec[2] if len(spec) > 2 else "block"
+    return f"{mode}_b{b}" + ("" if stop == "block" else f"_{stop}")
 
 
 def log(*a):
@@ -55,7 +64,7 @@ def load_model(cfg):
     return _MODELS[cfg]
 
 
-def run_mode(ctxs, sents, outs, mode, block, steps, warmup, timing=False):
+def run_mode(ctxs, sents, outs, mode, block, steps, warmup, timing=False, stop="block"):
     """Decodes sentences 0..steps-1 (each its own context, already encoded)
     after warm-up decodes of sentences 0..warmup-1; returns the timed totals."""
     import torch
@@ -64,17 +73,17 @@ def run_mode(ctxs, sents, outs, mode, block, steps, warmup, timing=False):
     # one-time setup: every context captures and instantiates its iteration
     # graph for this mode on its first decode
     for i in range(steps):
-        ctxs[i].decode(mode, [sents[i][1]], block=block, out=outs[i])
+        ctxs[i].decode(mode, [sents[i][1]], block=block, out=outs[i], stop=stop)
     torch.cuda.synchronize()
     for i in range(warmup):
-        ctxs[i % steps].decode(mode, [sents[i % steps][1]], block=block, out=outs[i % steps])
+        ctxs[i % steps].decode(mode, [sents[i % steps][1]], block=block, out=outs[i % steps], stop=stop)
     torch.cuda.synchronize()
     if timing:
         for c in ctxs[:steps]:
             c.set_timing(True)
     t0 = time.perf_counter()
     for i in range(steps):
-        ctxs[i].decode(mode, [sents[i][1]], block=block, out=outs[i])
+        ctxs[i].decode(mode, [sents[i][1]], block=block, out=outs[i], stop=stop)
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
     toks = ks = ms = 0
@@ -296,10 +305,11 @@ def batch1_workload(wl_name, steps, warmup, modes, headline, trace=False, encode
     wl, w, model, sents, ctxs, outs = setup_batch1(wl_name, max(steps, warmup))
     cfg = wl.model
     res = {}
-    for mode, b in modes:
-        r = run_mode(ctxs, sents, outs, mode, b, steps, warmup)
-        res[f"{mode}_b{b}"] = r
-        log(f"[{wl_name}] {mode:9s} b={b:2d}: {r['tokens_per_s']:9.1f} tok/s  {r['ms_per_step']:8.3f} ms/sentence  "
+    for spec in modes:
+        mode, b = spec[0], spec[1]
+        r = run_mode(ctxs, sents, outs, mode, b, steps, warmup, stop=spec[2] if len(spec) > 2 else "block")
+        res[mode_key(spec)] = r
+        log(f"[{wl_name}] {mode_key(spec):18s}: {r['tokens_per_s']:9.1f} tok/s  {r['ms_per_step']:8.3f} ms/sentence  "
             f"k/m={r['k_over_m']:.3f}  {r['us_per_iteration']:7.1f} us/iteration")
     # the event-timed pass of the headline mode: dispatch timestamps of every
     # decoder product and vocabulary launch (iterations launched kernel by

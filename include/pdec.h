@@ -63,6 +63,21 @@ enum {
 /* Decoding modes (Section 3.2). */
 enum { PD_AR = 0, PD_JACOBI = 1, PD_GS_JACOBI = 2, PD_HYBRID = 3 };
 
+/*
+ * Stopping-condition variant, or-ed into the mode of pd_decode /
+ * pd_decode_init / pd_decode_traced_static (the paper leaves stopping
+ * conditions other than Eq. (3) to future work: Section 3.3, conclusion).
+ * Eq. (3) commits a block once an iteration leaves it unchanged (or after L
+ * iterations).  PD_STOP_PREFIX commits after every iteration the positions
+ * that iteration proved exact: the whole block when it is unchanged, else the
+ * leading positions that came out as they went in plus the next one (its
+ * inputs were exact); the block then moves on by that many positions, the
+ * newer values of the rest serving as its draft.  The output is still greedy
+ * decoding's (Proposition 1's argument), k <= m, and PD_HYBRID stops at an
+ * [EOS] once it is committed.  No effect with PD_AR.
+ */
+enum { PD_STOP_PREFIX = 0x100 };
+
 /* Storage types of weights and activations. */
 enum { PD_F32 = 0, PD_BF16 = 1 };
 

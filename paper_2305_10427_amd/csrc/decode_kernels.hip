@@ -245,7 +245,7 @@ __device__ void emit_rows(const CtrlArgs& a) {
     for (int s = 0; s < a.B; ++s) {
       a.st[s].row0 = acc;
       acc += a.st[s].done ? 0 : a.st[s].L;
-      near = near && near_end(a.st[s]);
+      near = near && near_end(a.st[s], a.stop_prefix);
     }
     s_total = acc;
     s_near = near ? 1 : 0;
@@ -370,21 +370,29 @@ __device__ void reduce_rows(const uint2* partials, int part_ld, int n_parts, int
   }
 }
 
-// State transition of a sentence after an iteration of its block:
-// changed = the block differs from its previous value (StopC, Eq. (3)),
-// eos = the new block holds [EOS], nf = a non-finite logit was seen.
-__device__ __forceinline__ void advance_state(const CtrlArgs& a, SentState& st, bool changed, bool eos, int nf) {
+// State transition of a sentence after an iteration of its block: lead =
+// the number of leading block positions the iteration left unchanged (L: the
+// whole block, so Eq. (3) holds), first_eos = the block position of the first
+// [EOS] among the new values (L: none), nf = a non-finite logit was seen.
+// Eq. (3) commits the block when it is unchanged or after its L-th iteration
+// (then exact); the prefix stopping condition commits, every iteration, the
+// positions the iteration proved exact: all L when unchanged, else the lead
+// unchanged ones and the next (their inputs were already exact).  An [EOS]
+// ends PD_AR / PD_HYBRID decoding once it is among the committed positions.
+__device__ __forceinline__ void advance_state(const CtrlArgs& a, SentState& st, int lead, int first_eos, int nf) {
   if (nf) st.flags |= FLAG_NONFINITE;
   st.k += 1;
   st.j += 1;
-  const bool converged = !changed || st.j >= st.L;
-  if (converged) {
-    if ((a.mode == MODE_AR || a.mode == MODE_HYBRID) && eos) {
+  int commit = 0;
+  if (a.stop_prefix) commit = lead >= st.L ? st.L : lead + 1;
+  else if (lead >= st.L || st.j >= st.L) commit = st.L;
+  if (commit > 0) {
+    if ((a.mode == MODE_AR || a.mode == MODE_HYBRID) && first_eos < commit) {
       st.done = 1;
       st.flags |= FLAG_CONVERGED | FLAG_EOS;
     }
     if (!st.done) {
-      st.i += st.L;
+      st.i += commit;
       st.j = 0;
       if (st.i >= st.m) { st.done = 1; st.flags |= FLAG_CONVERGED; }
       else st.L = block_len(a, st.i, st.m);
@@ -414,17 +422,16 @@ __global__ __launch_bounds__(1024) void k_ctrl_step(CtrlArgs a) {
     SentState st = a.st[s];
     if (st.done) continue;
     int* y = a.y + static_cast<size_t>(s) * a.ldy;
-    bool changed = false, eos = false;
-    int nf = 0;
+    int lead = 0, first_eos = st.L, nf = 0;
     for (int r = 0; r < st.L; ++r) {
       const int t = a.new_tok[st.row0 + r];
       nf |= a.row_flags[st.row0 + r];
-      if (y[st.i + r] != t) changed = true;
-      eos |= t == a.eos_id;
+      if (lead == r && y[st.i + r] == t) lead = r + 1;
+      if (first_eos == st.L && t == a.eos_id) first_eos = r;
       y[st.i + r] = t;
       if (a.trace != nullptr) trace_row(a, *a.trace_count, st.row0 + r, st.k + 1, s, st.i + r, t);
     }
-    advance_state(a, st, changed, eos, nf);
+    advance_state(a, st, lead, first_eos, nf);
     a.st[s] = st;
   }
   __syncthreads();
@@ -435,17 +442,20 @@ __global__ __launch_bounds__(1024) void k_ctrl_step(CtrlArgs a) {
 // The control step with one thread per row instead of one per sentence (up
 // to 1024 sentences; k_ctrl_step above is the fallback for more): the rows'
 // loads go out together rather than one block position after another.  The
-// per-sentence results of Eq. (3) (changed, [EOS], non-finite) are gathered
-// with LDS atomic ORs, the states advance exactly as in k_ctrl_step
+// per-sentence results (the first changed block position, the first [EOS],
+// a non-finite logit) are gathered with LDS atomic minima / ORs, the states
+// advance exactly as in k_ctrl_step
 // (advance_state), the next layout's first rows come from a prefix sum over
 // the sentences, and the next rows are written one thread per row.
 constexpr int kCtrlRowsMaxB = 1024;
 
 template <typename WT>
 __global__ __launch_bounds__(1024) void k_ctrl_rows(CtrlArgs a) {
-  __shared__ int s_acc[kCtrlRowsMaxB];         // bit 0 changed, bit 1 [EOS], bit 2 non-finite
+  __shared__ int s_nf[kCtrlRowsMaxB];          // a non-finite logit in the sentence's rows
+  __shared__ int s_chg[kCtrlRowsMaxB];         // first changed block position (or a large value)
+  __shared__ int s_eos[kCtrlRowsMaxB];         // first [EOS] block position (or a large value)
   __shared__ int s_k[kCtrlRowsMaxB];           // iterations so far (trace)
-  __shared__ int s_i[kCtrlRowsMaxB];           // next block start
+  __shared__ int s_i[kCtrlRowsMaxB];           // current, then next block start
   __shared__ int s_scan[2][kCtrlRowsMaxB + 1]; // next block lengths -> first rows (exclusive prefix)
   __shared__ int s_far;                        // some live sentence is not near its end (near_end)
   const int tid = threadIdx.x;
@@ -458,8 +468,10 @@ __global__ __launch_bounds__(1024) void k_ctrl_rows(CtrlArgs a) {
   const bool sent = tid < a.B;
   if (sent) {
     st = a.st[tid];
-    s_acc[tid] = 0;
+    s_nf[tid] = 0;
+    s_chg[tid] = s_eos[tid] = 0x7fffffff;
     s_k[tid] = st.k;
+    s_i[tid] = st.i;
   }
   __syncthreads();
   const unsigned long long tbase = a.trace != nullptr ? *a.trace_count : 0ull;
@@ -467,19 +479,18 @@ __global__ __launch_bounds__(1024) void k_ctrl_rows(CtrlArgs a) {
     const int s = a.row_sent[row], p = a.row_pos[row];
     const int t = a.new_tok[row];
     int* yp = a.y + static_cast<size_t>(s) * a.ldy + p;
-    const int bits = (*yp != t ? 1 : 0) | (t == a.eos_id ? 2 : 0) | (a.row_flags[row] != 0 ? 4 : 0);
+    const int r = p - s_i[s];                   // block position of the row
+    if (*yp != t) atomicMin(&s_chg[s], r);
+    if (t == a.eos_id) atomicMin(&s_eos[s], r);
+    if (a.row_flags[row] != 0) atomicOr(&s_nf[s], 1);
     *yp = t;
-    if (bits != 0) atomicOr(&s_acc[s], bits);
     if (a.trace != nullptr) trace_row(a, tbase, row, s_k[s] + 1, s, p, t);
   }
   __syncthreads();
   int len = 0;
   if (sent) {
-    if (!st.done) {
-      const int acc = s_acc[tid];
-      advance_state(a, st, (acc & 1) != 0, (acc & 2) != 0, (acc & 4) ? 1 : 0);
-    }
-    if (!near_end(st)) s_far = 1;
+    if (!st.done) advance_state(a, st, min(s_chg[tid], st.L), min(s_eos[tid], st.L), s_nf[tid]);
+    if (!near_end(st, a.stop_prefix)) s_far = 1;
     len = st.done ? 0 : st.L;
     s_i[tid] = st.i;
     s_scan[0][tid + 1] = len;
@@ -590,21 +601,20 @@ __global__ __launch_bounds__(1024) void k_ctrl_small(CtrlArgs a) {
   int i_old = 0, row0_old = 0, L_old = 0;
   if (sent && !st.done) {
     int* y = a.y + static_cast<size_t>(tid) * a.ldy;
-    bool changed = false, eos = false;
-    int nf = 0;
+    int lead = 0, first_eos = st.L, nf = 0;
     const unsigned long long tbase = a.trace != nullptr ? *a.trace_count : 0ull;
     for (int r = 0; r < st.L; ++r) {
       const int t = s_tok[st.row0 + r];
       nf |= s_flag[st.row0 + r];
-      changed |= s_win[tid][1 + r] != t;      // previous value y[i + r]
-      eos |= t == a.eos_id;
+      if (lead == r && s_win[tid][1 + r] == t) lead = r + 1;   // previous value y[i + r]
+      if (first_eos == st.L && t == a.eos_id) first_eos = r;
       y[st.i + r] = t;
       if (a.trace != nullptr) trace_row(a, tbase, st.row0 + r, st.k + 1, tid, st.i + r, t);
     }
     i_old = st.i;
     row0_old = st.row0;
     L_old = st.L;
-    advance_state(a, st, changed, eos, nf);
+    advance_state(a, st, lead, first_eos, nf);
   }
   if (sent) s_st[tid] = st;
   __syncthreads();
@@ -615,7 +625,7 @@ __global__ __launch_bounds__(1024) void k_ctrl_small(CtrlArgs a) {
     for (int s = 0; s < a.B; ++s) {
       s_st[s].row0 = acc;
       acc += s_st[s].done ? 0 : s_st[s].L;
-      near = near && near_end(s_st[s]);
+      near = near && near_end(s_st[s], a.stop_prefix);
     }
     s_total = acc;
     *a.n_rows = acc;

@@ -174,6 +174,7 @@ struct CtrlArgs {
   SentState* st;
   int B;
   int mode, block, horizon, max_iters;
+  int stop_prefix;         // 1: commit each iteration's proven prefix (PD_STOP_PREFIX), 0: Eq. (3)
   const int* tgt_m;        // [B]
   int* y;                  // [B][ldy] draft
   int ldy;
@@ -214,10 +215,13 @@ struct CtrlArgs {
 // whether that iteration may be the last one: every live sentence is in its
 // last block, the iteration is not the first of a block of several positions
 // (which compares with an unrefined draft), and the block's cap of L
-// iterations leaves at most kNearEndIters more.  The bit only paces the host.
+// iterations leaves at most kNearEndIters more (under the prefix stopping
+// condition, which commits at least one position per iteration: the last
+// block holds at most kNearEndIters positions).  The bit only paces the host.
 constexpr int kNearEndBit = 1 << 30;
 constexpr int kNearEndIters = 8;
-__device__ __forceinline__ bool near_end(const SentState& st) {
+__device__ __forceinline__ bool near_end(const SentState& st, int stop_prefix) {
+  if (stop_prefix) return st.done || (st.i + st.L >= st.m && st.L <= kNearEndIters);   // >= 1 position per iteration
   return st.done || (st.i + st.L >= st.m && (st.j >= 1 || st.L == 1) && st.L - st.j <= kNearEndIters);
 }
 __host__ __device__ __forceinline__ int host_word(int rows, bool near) { return rows | (near && rows > 0 ? kNearEndBit : 0); }

@@ -888,6 +888,9 @@ pd_status pd_decode_init(pd_ctx* ctx, int32_t mode, int32_t block, int32_t horiz
       out_flags == nullptr)
     return fail(PD_E_ARG, "null argument");
   if (!ctx->encoded) return fail(PD_E_STATE, "pd_decode called before pd_encode");
+  const int key_mode = mode;                   // with the stopping-condition flag (graph key)
+  const int stop_prefix = (mode & PD_STOP_PREFIX) != 0 ? 1 : 0;
+  mode &= ~PD_STOP_PREFIX;
   if (mode < PD_AR || mode > PD_HYBRID) return fail(PD_E_ARG, "unknown mode");
   if ((mode == PD_GS_JACOBI || mode == PD_HYBRID) && block < 1) return fail(PD_E_ARG, "block must be >= 1");
   const int B = ctx->enc_B;
@@ -919,6 +922,7 @@ pd_status pd_decode_init(pd_ctx* ctx, int32_t mode, int32_t block, int32_t horiz
   ca.st = C.at<SentState>(C.L.st);
   ca.B = B;
   ca.mode = mode;
+  ca.stop_prefix = stop_prefix;
   ca.block = std::max(block, 1);
   ca.horizon = horizon;
   ca.max_iters = max_iters;
@@ -976,7 +980,7 @@ pd_status pd_decode_init(pd_ctx* ctx, int32_t mode, int32_t block, int32_t horiz
     if (e == hipSuccess) {
       if (C.use_graphs && slot < 0) {   // iterations timed with events are launched directly
         hipGraphExec_t ex = nullptr;
-        const GraphKey key{mode, block, horizon, max_iters, B, Rb, slot, fused ? 1 : 0, C.trace, C.trace_cap,
+        const GraphKey key{key_mode, block, horizon, max_iters, B, Rb, slot, fused ? 1 : 0, C.trace, C.trace_cap,
                            C.trace_part};
         e = iteration_graph(C, key, r, cb, &ex);
         if (e == hipSuccess) e = hipGraphLaunch(ex, s);

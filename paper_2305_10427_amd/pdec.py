@@ -19,6 +19,13 @@ LIB_PATH = os.path.join(_HERE, "libpdec.so")
 
 PD_AR, PD_JACOBI, PD_GS_JACOBI, PD_HYBRID = 0, 1, 2, 3
 MODE_IDS = {"ar": PD_AR, "jacobi": PD_JACOBI, "gs_jacobi": PD_GS_JACOBI, "hybrid": PD_HYBRID}
+PD_STOP_PREFIX = 0x100                  # or-ed into the mode: the prefix stopping condition
+STOP_FLAGS = {"block": 0, "prefix": PD_STOP_PREFIX}
+
+
+def mode_word(mode, stop="block") -> int:
+    """The mode argument of pd_decode: the mode id, or-ed with the stopping-condition flag."""
+    return (MODE_IDS[mode] if isinstance(mode, str) else int(mode)) | STOP_FLAGS[stop]
 FLAG_CONVERGED, FLAG_EOS, FLAG_MAX_ITERS, FLAG_NONFINITE = 1, 2, 4, 8
 STATUS = {0: "PD_OK", 1: "PD_E_ARG", 2: "PD_E_SHAPE", 3: "PD_E_WORKSPACE", 4: "PD_E_DEVICE",
           5: "PD_E_UNSUPPORTED", 6: "PD_E_STATE"}
@@ -196,11 +203,12 @@ class Context:
         self.B = B
 
     def decode(self, mode, tgt_m: Sequence[int], block: int = 1, max_iters: int = 0, horizon: int = 0,
-               stream=None, out=None, init=None):
+               stream=None, out=None, init=None, stop: str = "block"):
         """Returns (ids [B, m_max], lengths [B], k [B], flags [B]) as device int32 tensors.
-        init: optional int32 tensor [B, >= max(tgt_m)], the initial draft (default all [PAD])."""
+        init: optional int32 tensor [B, >= max(tgt_m)], the initial draft (default all [PAD]).
+        stop: "block" (Eq. (3)) or "prefix" (PD_STOP_PREFIX)."""
         import torch
-        mode_id = MODE_IDS[mode] if isinstance(mode, str) else int(mode)
+        mode_id = mode_word(mode, stop)
         tgt_m = [int(x) for x in tgt_m]
         if len(tgt_m) != self.B:
             raise PdError(1, f"tgt_m has {len(tgt_m)} entries, the encoded batch has {self.B}")
@@ -231,13 +239,13 @@ class Context:
         return ids, ln, k, fl
 
     def decode_traced_static(self, mode, tgt_m: Sequence[int], capacity: int, block: int = 1, max_iters: int = 0,
-                             horizon: int = 0, stream=None):
+                             horizon: int = 0, stream=None, stop: str = "block"):
         """pd_decode_traced_static: decode with the trace on, the trace scratch
         in the library's static array.  Returns (ids, lengths, k, flags,
         records, count); records is a numpy structured array (TRACE_DTYPE) of
         the first min(count, capacity) records."""
         import torch
-        mode_id = MODE_IDS[mode] if isinstance(mode, str) else int(mode)
+        mode_id = mode_word(mode, stop)
         tgt_m = [int(x) for x in tgt_m]
         if len(tgt_m) != self.B:
             raise PdError(1, f"tgt_m has {len(tgt_m)} entries, the encoded batch has {self.B}")

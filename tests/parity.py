@@ -57,8 +57,10 @@ class GpuResult:
     flags: int
 
 
-def gpu_decode_batch(ctx, srcs, ms, mode, block=1, max_iters=0, horizon=0, init=None) -> List[GpuResult]:
-    """init: optional list of initial drafts (one int array of length >= m per sentence)."""
+def gpu_decode_batch(ctx, srcs, ms, mode, block=1, max_iters=0, horizon=0, init=None,
+                     stop="block") -> List[GpuResult]:
+    """init: optional list of initial drafts (one int array of length >= m per sentence);
+    stop: "block" (Eq. (3)) or "prefix" (PD_STOP_PREFIX)."""
     import torch
     B = len(srcs)
     n_max = max(len(s) for s in srcs)
@@ -73,7 +75,7 @@ def gpu_decode_batch(ctx, srcs, ms, mode, block=1, max_iters=0, horizon=0, init=
         for r, d in enumerate(init):
             arr[r, :len(d)] = d
         init_t = torch.from_numpy(arr).cuda()
-    ids, ln, k, fl = ctx.decode(mode, ms, block=block, max_iters=max_iters, horizon=horizon, init=init_t)
+    ids, ln, k, fl = ctx.decode(mode, ms, block=block, max_iters=max_iters, horizon=horizon, init=init_t, stop=stop)
     torch.cuda.synchronize()
     ids, ln, k, fl = (t.cpu().numpy() for t in (ids, ln, k, fl))
     out = []
@@ -242,12 +244,14 @@ class Replay:
         return toks
 
 
-def replay_check(g: GpuResult, rows, mode, b, m, h=None, init=None):
+def replay_check(g: GpuResult, rows, mode, b, m, h=None, init=None, stop="block"):
     """Runs the oracle's control flow on the GPU's recorded evaluations and
     asserts that it reproduces the GPU's ids and k; returns the Replay."""
     rep = Replay(rows)
-    res = oracle.decode(None, None, m, mode, b, evaluator=rep, init=init,
-                        **({"h": h} if h is not None else {}))
+    kw = {"h": h} if h is not None else {}
+    if mode != "ar":
+        kw["stop"] = stop
+    res = oracle.decode(None, None, m, mode, b, evaluator=rep, init=init, **kw)
     assert rep.q == len(rows), f"{len(rows) - rep.q} trace rows left after the oracle finished"
     assert res.k == g.k, f"replayed k {res.k} != GPU k {g.k}"
     np.testing.assert_array_equal(res.out, g.ids)
@@ -274,8 +278,10 @@ def spot_check(rep: Replay, M, enc, dtype, picks) -> List[str]:
     return out
 
 
-def oracle_kwargs(mode, max_iters=0, horizon=0, init=None):
+def oracle_kwargs(mode, max_iters=0, horizon=0, init=None, stop="block"):
     kw = {}
+    if mode != "ar" and stop != "block":
+        kw["stop"] = stop
     if max_iters:
         kw["max_iters"] = max_iters
     if mode == "hybrid" and horizon > 0:
@@ -285,19 +291,21 @@ def oracle_kwargs(mode, max_iters=0, horizon=0, init=None):
     return kw
 
 
-def judge_batch(ctx, M, srcs, ms, mode, b, dtype, max_iters=0, horizon=0, init=None, idx=None, got=None):
+def judge_batch(ctx, M, srcs, ms, mode, b, dtype, max_iters=0, horizon=0, init=None, idx=None, got=None,
+                stop="block"):
     """Decodes the batch on the GPU (unless `got` holds its results) and judges
     the sentences `idx` (default all) against the oracle.  A differing k is
     attributed through one traced re-run of the same batch (which must return
     the same results).  Returns (GPU results, labels)."""
     if got is None:
-        got = gpu_decode_batch(ctx, srcs, ms, mode, b, max_iters=max_iters, horizon=horizon, init=init)
+        got = gpu_decode_batch(ctx, srcs, ms, mode, b, max_iters=max_iters, horizon=horizon, init=init, stop=stop)
     traced = {}
 
     def retrace_for(r):
         def run():
             if "rows" not in traced:
-                res, per = gpu_decode_traced(ctx, srcs, ms, mode, b, max_iters=max_iters, horizon=horizon, init=init)
+                res, per = gpu_decode_traced(ctx, srcs, ms, mode, b, max_iters=max_iters, horizon=horizon, init=init,
+                                             stop=stop)
                 for a, c in zip(got, res):
                     np.testing.assert_array_equal(a.ids, c.ids)
                     assert (a.k, a.flags) == (c.k, c.flags), "the traced decode changed a result"
@@ -309,7 +317,7 @@ def judge_batch(ctx, M, srcs, ms, mode, b, dtype, max_iters=0, horizon=0, init=N
     for r in (range(len(srcs)) if idx is None else idx):
         enc = M.encode(srcs[r])
         d0 = None if init is None else init[r]
-        want = oracle.decode(M, enc, ms[r], mode, b, **oracle_kwargs(mode, max_iters, horizon, d0))
+        want = oracle.decode(M, enc, ms[r], mode, b, **oracle_kwargs(mode, max_iters, horizon, d0, stop))
         greedy = oracle.greedy(M, enc, ms[r])
         labels.append(classify(got[r], want, greedy, dtype, M, enc, mode, ms[r], d0, retrace_for(r)))
     return got, labels
