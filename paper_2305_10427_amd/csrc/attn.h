@@ -164,15 +164,17 @@ __device__ __forceinline__ void chunk_fold(const float* q, const KeyChunk<AT, DH
   st.m = mn;
 }
 
-// Final output o / l of a row's head slice.
-template <typename AT, int DH>
-__device__ __forceinline__ void row_output(const RowState<DH>& st, AT* out, int lane) {
+// Final output o / l of a row's head slice: element d goes to out[at(d)]
+// (d even: at(d + 1) = at(d) + 1 in every layout used).
+template <typename AT, int DH, typename At>
+__device__ __forceinline__ void row_output(const RowState<DH>& st, AT* out, At at, int lane) {
 #pragma unroll
   for (int i = 0; i < RowState<DH>::NP; ++i) {
     const int d = 2 * lane + kWave * i;
     if (lane < 32 && d < DH) {
-      Elt<AT>::store(out, d, st.o[i][0] / st.l);
-      Elt<AT>::store(out, d + 1, st.o[i][1] / st.l);
+      const size_t o = at(d);
+      Elt<AT>::store(out, o, st.o[i][0] / st.l);
+      Elt<AT>::store(out, o + 1, st.o[i][1] / st.l);
     }
   }
 }

@@ -84,7 +84,15 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
       }
     }
   }
-  row_output<AT, DH>(st, static_cast<AT*>(a.out) + static_cast<size_t>(row) * a.ldo + hh * DH, lane);
+  AT* out = static_cast<AT*>(a.out);
+  if (a.out_feed) {
+    const int K = a.H * DH;
+    row_output<AT, DH>(st, out, [&](int d) { return feed_index<Mma<AT>::KS, Mma<AT>::EPL>(row, hh * DH + d, K); },
+                       lane);
+  } else {
+    const size_t base = static_cast<size_t>(row) * a.ldo + hh * DH;
+    row_output<AT, DH>(st, out, [&](int d) { return base + d; }, lane);
+  }
 }
 
 // ---------------------------------------------------------------------------

@@ -190,7 +190,10 @@ __global__ __launch_bounds__(KSPLIT == 8 ? 512 : 256) void k_gemm(GemmArgs a) {
       if constexpr (PRO == PRO_LN) {
         return MM::load(sA + static_cast<size_t>(lrr) * lda + k);
       } else if constexpr (std::is_same<XT, AT>::value) {
-        return MM::load(X + static_cast<size_t>(arow_ok ? arow : 0) * a.ldx + k);
+        // row-major rows, or the tile's feed-order words (one 1 KB block per step)
+        const size_t off = a.x_feed ? (static_cast<size_t>(m0 >> 4) * n_steps + s) * (kWave * EPL) + lane * EPL
+                                    : static_cast<size_t>(arow_ok ? arow : 0) * a.ldx + k;
+        return MM::load(X + off);
       } else {
         float xv[EPL];
         load_n<XT, EPL>(X, static_cast<size_t>(arow_ok ? arow : 0) * a.ldx + k, xv);
@@ -259,7 +262,8 @@ __global__ __launch_bounds__(KSPLIT == 8 ? 512 : 256) void k_gemm(GemmArgs a) {
       } else if constexpr (EPI == EPI_ACT) {
         float t = v + bias_v;
         t = (a.act == 2) ? gelu_erf(t) : relu(t);
-        Elt<AT>::store(static_cast<AT*>(a.out), static_cast<size_t>(row) * a.ldo + col, t);
+        Elt<AT>::store(static_cast<AT*>(a.out),
+                       a.out_feed ? feed_index<KS, EPL>(row, col, N) : static_cast<size_t>(row) * a.ldo + col, t);
       } else if constexpr (EPI == EPI_RESID) {
         const size_t ri = static_cast<size_t>(row) * a.ldr + col;
         const float rv = m0 == m_first ? rpre[e] : Elt<AT>::load(static_cast<const AT*>(a.resid), ri);
@@ -483,6 +487,8 @@ hipError_t launch_pack_feed(int dtype, const void* w, void* out, int N, int K, h
 hipError_t launch_gemm(int dtype, int pro, int epi, int ksplit, const GemmArgs& a, hipStream_t s, hipEvent_t ev0,
                        hipEvent_t ev1) {
   if (a.n_rows <= 0) return hipSuccess;
+  if (a.x_feed && (pro == PRO_LN || a.x_f32 || ksplit == 1)) return hipErrorInvalidValue;
+  if (a.out_feed && (epi != EPI_ACT || ksplit == 1 || a.N % 32 != 0)) return hipErrorInvalidValue;
   const int ks = dtype == DT_BF16 ? Mma<bf16_t>::KS : Mma<float>::KS;
   if (a.K % ks != 0 || a.K % 32 != 0) return hipErrorInvalidValue;
   if (pro == PRO_LN && (a.K > (dtype == DT_BF16 ? 1024 : 512) || gemm_ln_lds_bytes(a.K, dtype == DT_BF16 ? 2 : 4) > 65536))

@@ -468,6 +468,7 @@ hipError_t launch_gemm_tiled_cfg(int epi, int ksplit, int cfg, const GemmArgs& a
 }
 
 hipError_t launch_gemm_tiled(int epi, int ksplit, const GemmArgs& a, hipStream_t s) {
+  if (a.x_feed || a.out_feed) return hipErrorInvalidValue;   // row-major operands only
   return launch_gemm_tiled_cfg(epi, ksplit, gemm_tiled_cfg(epi, a.N, a.n_rows), a, s);
 }
 

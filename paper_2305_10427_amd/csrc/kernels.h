@@ -17,6 +17,15 @@ struct RowMap {
   int per_sent;
 };
 
+// Element offset of x[r][k] in the MFMA feed order of a [rows][K] matrix
+// (KS, EPL: the MFMA step and elements per lane of the storage type):
+// 16-row tile r / 16, step k / KS, lane (r mod 16) + 16 ((k mod KS) / EPL).
+template <int KS, int EPL>
+__host__ __device__ __forceinline__ size_t feed_index(int r, int k, int K) {
+  const int s = k / KS, kk = k - s * KS;
+  return ((static_cast<size_t>(r >> 4) * (K / KS) + s) * 64 + (r & 15) + 16 * (kk / EPL)) * EPL + (kk % EPL);
+}
+
 // (sentence, position) of row `row`.
 __device__ __forceinline__ void row_place(const RowMap& m, int row, int& s, int& p) {
   if (m.sent != nullptr) { s = m.sent[row]; p = m.pos[row]; }
@@ -43,6 +52,11 @@ struct GemmArgs {
   const void* x;
   int ldx;
   int x_f32;
+  // 1: x (storage type, no LayerNorm prologue) is in the MFMA feed order of
+  // the K-split kernels instead: 16-row tile t, step s: 64 16-byte words,
+  // word l = x[16 t + (l & 15)][s KS + EPL (l >> 4) ...] (see feed_index)
+  int x_feed;
+  int out_feed;            // EPI_ACT: out (storage type, [rows][N]) written in that feed order
   // LayerNorm prologue (PRO_LN): x <- LN(x) * g + b, rounded to the storage type
   const void* ln_g;
   const void* ln_b;
@@ -119,6 +133,7 @@ struct AttnArgs {
   int ldo;
   float scale;             // 1/sqrt(dh)
   int rows_max;            // launch bound on the rows (set by launch_attn)
+  int out_feed;            // 1: out ([R][H dh]) written in the MFMA feed order (feed_index), ldo unused
 };
 
 struct EmbedArgs {
