@@ -355,15 +355,17 @@ void launch_ev(K kernel, dim3 grid, dim3 block, size_t lds, hipStream_t s, hipEv
   else hipLaunchKernelGGL(kernel, grid, block, lds, s, a);
 }
 
-// Rows per workgroup for a K-split product of one row tile: groups of 4 rows
-// for the LayerNorm-prologue products (a quarter of the prologue per wave,
-// and 4x the workgroups of a narrow product), 8 where that would exceed 768
-// workgroups; whole tiles otherwise.  Measured on the decoder's shapes
-// (d = 512 and 1024, 1 / 5 / 16 rows): groups did not help the products that
-// read their input rows straight from memory.
-int row_group(int pro, int col_tiles, int rows, int tiles, int layers) {
-  if (pro != PRO_LN || tiles != 1 || layers != 1) return 16;
-  return col_tiles * ((rows + 3) / 4) <= 768 ? 4 : 8;
+// Rows per workgroup for a K-split product: groups of 4 rows for the
+// LayerNorm-prologue products (a quarter of the prologue per wave, and more
+// workgroups for a narrow product) up to 768 workgroups, groups of 8 up to
+// 1024, whole 16-row tiles beyond.  Measured on the decoder's shapes (d = 512
+// and 1024, 1 / 5 / 16 rows): groups did not help the products that read
+// their input rows straight from memory.
+int row_group(int pro, int col_tiles, int rows, int layers) {
+  if (pro != PRO_LN || layers != 1) return 16;
+  if (col_tiles * ((rows + 3) / 4) <= 768) return 4;
+  if (col_tiles * ((rows + 7) / 8) <= 1024) return 8;
+  return 16;
 }
 
 template <typename WT, int PRO, int EPI, int XF32, int LNT, int KSPLIT, int RG>
@@ -382,10 +384,9 @@ void launch_rg(const GemmArgs& a, int spw, dim3 grid, size_t lds, hipStream_t s,
 template <typename WT, int PRO, int EPI, int XF32, int LNT, int KSPLIT>
 void launch_split(const GemmArgs& a, int gy, int gz, size_t lds, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   const int ct = gemm_grid(EPI, a.N, KSPLIT);
-  const int tiles = (a.n_rows + 15) / 16;
   const int n_steps = a.K / Mma<WT>::KS;
   const int spw = n_steps % KSPLIT == 0 ? n_steps / KSPLIT : 0;
-  const int rg = row_group(PRO, ct, a.n_rows, tiles, gz);
+  const int rg = row_group(PRO, ct, a.n_rows, gz);
   if constexpr (PRO == PRO_LN) {
     if (rg == 4) return launch_rg<WT, PRO, EPI, XF32, LNT, KSPLIT, 4>(a, spw, dim3(ct * ((a.n_rows + 3) / 4)), lds, s, ev0, ev1);
     if (rg == 8) return launch_rg<WT, PRO, EPI, XF32, LNT, KSPLIT, 8>(a, spw, dim3(ct * ((a.n_rows + 7) / 8)), lds, s, ev0, ev1);
