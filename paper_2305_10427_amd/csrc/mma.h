@@ -7,6 +7,7 @@ namespace pdec {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float floatx4_t __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 
 template <typename T> struct Mma;
 template <> struct Mma<bf16_t> {
@@ -18,6 +19,16 @@ template <> struct Mma<bf16_t> {
                                                    c, 0, 0, 0);
   }
   static __device__ __forceinline__ frag load(const bf16_t* p) { return *reinterpret_cast<const uint4*>(p); }
+  // NT: a non-temporal load (global_load ... nt), for data a launch streams
+  // once, such as the weights of a batch-1 product
+  template <int NT> static __device__ __forceinline__ frag wload(const bf16_t* p) {
+    if constexpr (NT != 0) {
+      const u32x4_t t = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
+      return make_uint4(t.x, t.y, t.z, t.w);
+    } else {
+      return load(p);
+    }
+  }
   static __device__ __forceinline__ frag zero() { return make_uint4(0, 0, 0, 0); }
   static __device__ __forceinline__ void unpack(frag f, float* v) {
     const uint32_t w[4] = {f.x, f.y, f.z, f.w};
@@ -44,6 +55,14 @@ template <> struct Mma<float> {
     return c;
   }
   static __device__ __forceinline__ frag load(const float* p) { return *reinterpret_cast<const float4*>(p); }
+  template <int NT> static __device__ __forceinline__ frag wload(const float* p) {
+    if constexpr (NT != 0) {
+      const floatx4_t t = __builtin_nontemporal_load(reinterpret_cast<const floatx4_t*>(p));
+      return make_float4(t.x, t.y, t.z, t.w);
+    } else {
+      return load(p);
+    }
+  }
   static __device__ __forceinline__ frag zero() { return make_float4(0.f, 0.f, 0.f, 0.f); }
   static __device__ __forceinline__ void unpack(frag f, float* v) { v[0] = f.x; v[1] = f.y; v[2] = f.z; v[3] = f.w; }
   static __device__ __forceinline__ frag pack(const float* v) { return make_float4(v[0], v[1], v[2], v[3]); }
