@@ -21,10 +21,10 @@
  * Memory ownership.  Every device buffer the caller hands over (weights,
  * workspace, inputs, outputs) is allocated and freed by the caller.  The
  * library allocates device memory in one place only: the first pd_ctx_create
- * on a model makes the model's copy of its product weights in matrix-core
- * feed order (see pd_model_create), freed by pd_model_destroy.  Besides that,
- * pd_model / pd_ctx own host-side state (plus one pinned host word per
- * context for completion polling).  Weight and workspace buffers must stay
+ * on a model makes the model's copy of its product weights and embedding in
+ * matrix-core feed order (see pd_model_create), freed by pd_model_destroy.
+ * Besides that, pd_model / pd_ctx own host-side state (plus one pinned host
+ * word per context for completion polling).  Weight and workspace buffers must stay
  * valid and unchanged while a model / context uses them.
  *
  * Threads and streams.  A pd_ctx is used by one host thread at a time; calls
@@ -148,9 +148,11 @@ pd_status pd_weight_shape(const pd_config* cfg, int32_t idx, int64_t* rows, int6
  * caller keeps them allocated and unchanged until pd_model_destroy.  No
  * device work happens here.  The first pd_ctx_create on the model allocates,
  * on the current device, a copy of every encoder and decoder matrix
- * product's weights (w_qkv, w_o, w1, w2; ca_w_q, ca_w_o) rearranged into the
- * order in which the few-row product kernels feed the matrix cores (as many
- * bytes as those matrices; freed by pd_model_destroy).  Returns PD_E_ARG for
+ * product's weights (w_qkv, w_o, w1, w2; ca_w_q, ca_w_o) and of the token
+ * embedding E (the vocabulary projection's weights) rearranged into the
+ * order in which the few-row kernels feed the matrix cores (as many bytes as
+ * those matrices, E's rows rounded up to a multiple of 16; freed by
+ * pd_model_destroy).  Returns PD_E_ARG for
  * a null / misaligned pointer or a wrong count, PD_E_UNSUPPORTED for shapes
  * the kernels reject.
  */
@@ -173,8 +175,8 @@ pd_status pd_ctx_workspace_bytes(const pd_model* model, int32_t max_batch, int32
  * least pd_ctx_workspace_bytes).  The workspace holds activations, the
  * cross-attention and self-attention K/V caches, drafts and control state.
  * The first context of a model also makes the model's matrix-core feed copy
- * of its product weights (see pd_model_create), on the null stream, and
- * waits for it; PD_E_DEVICE when that allocation or copy fails.
+ * of its product weights and embedding (see pd_model_create), on the null
+ * stream, and waits for it; PD_E_DEVICE when that allocation or copy fails.
  */
 pd_status pd_ctx_create(const pd_model* model, int32_t max_batch, int32_t max_src, int32_t max_tgt,
                         void* dev_workspace, size_t workspace_bytes, pd_ctx** out);

@@ -460,28 +460,30 @@ int gemm_grid(int epi, int N, int ksplit) {
   return (N + 15) / 16;
 }
 
-// W [N][K] row-major -> the MFMA feed order of k_gemm (N % 16 == 0, K a
-// multiple of the MFMA step): one 16-byte word per thread.
+// W [N][K] row-major -> the MFMA feed order of k_gemm (K a multiple of the
+// MFMA step): ceil(N / 16) column tiles, the rows of a ragged last tile past
+// N repeating row N - 1; one 16-byte word per thread.
 template <typename WT>
 __global__ __launch_bounds__(256) void k_pack_feed(const WT* __restrict__ w, WT* __restrict__ out, int N, int K) {
   using MM = Mma<WT>;
   constexpr int KS = MM::KS, EPL = MM::EPL;
   const int n_steps = K / KS;
-  const long long words = static_cast<long long>(N) * K / EPL;
+  const long long words = static_cast<long long>((N + 15) / 16) * 16 * K / EPL;
   for (long long i = blockIdx.x * 256LL + threadIdx.x; i < words; i += static_cast<long long>(gridDim.x) * 256) {
     const int lane = static_cast<int>(i % kWave);
     const long long blk = i / kWave;                    // c * n_steps + s
     const int c = static_cast<int>(blk / n_steps);
     const int st = static_cast<int>(blk - static_cast<long long>(c) * n_steps);
-    const size_t src = static_cast<size_t>(16 * c + (lane & 15)) * K + st * KS + EPL * (lane >> 4);
+    const int row = min(16 * c + (lane & 15), N - 1);
+    const size_t src = static_cast<size_t>(row) * K + st * KS + EPL * (lane >> 4);
     *reinterpret_cast<uint4*>(out + static_cast<size_t>(i) * EPL) = *reinterpret_cast<const uint4*>(w + src);
   }
 }
 
 hipError_t launch_pack_feed(int dtype, const void* w, void* out, int N, int K, hipStream_t s) {
   const int ks = dtype == DT_BF16 ? Mma<bf16_t>::KS : Mma<float>::KS;
-  if (N <= 0 || K <= 0 || N % 16 != 0 || K % ks != 0) return hipErrorInvalidValue;
-  const long long words = static_cast<long long>(N) * K / (dtype == DT_BF16 ? 8 : 4);
+  if (N <= 0 || K <= 0 || K % ks != 0) return hipErrorInvalidValue;
+  const long long words = static_cast<long long>((N + 15) / 16) * 16 * K / (dtype == DT_BF16 ? 8 : 4);
   const int grid = static_cast<int>(std::min<long long>((words + 255) / 256, 4096));
   if (dtype == DT_BF16)
     hipLaunchKernelGGL(k_pack_feed<bf16_t>, dim3(grid), dim3(256), 0, s, static_cast<const bf16_t*>(w),

@@ -94,7 +94,7 @@ struct GemmArgs {
   const void* lb[kMaxLayers];
   // optional (nullptr: row-major w only): the same weights in the MFMA feed
   // order of the K-split product kernels (launch_pack_feed); single-layer
-  // launches with N % 16 == 0 only
+  // launches with N % 16 == 0 only, and the vocabulary kernel (any N)
   const void* wp;
 };
 
@@ -255,10 +255,11 @@ struct ReduceArgs {
 hipError_t launch_gemm(int dtype, int pro, int epi, int ksplit, const GemmArgs& a, hipStream_t s,
                        hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 int gemm_grid(int epi, int N, int ksplit);
-// W [N][K] (row-major) -> out [N * K] in the MFMA feed order read through
-// GemmArgs::wp: block (c, s) of 64 16-byte words holds, in word l,
-// W[16 c + (l & 15)][s KS + EPL (l >> 4) ... + EPL - 1] (KS, EPL of the MFMA
-// step of the type).  N % 16 == 0 and K % KS == 0, else hipErrorInvalidValue.
+// W [N][K] (row-major) -> out [ceil(N / 16) 16 K] in the MFMA feed order read
+// through GemmArgs::wp: block (c, s) of 64 16-byte words holds, in word l,
+// W[min(16 c + (l & 15), N - 1)][s KS + EPL (l >> 4) ... + EPL - 1] (KS, EPL of
+// the MFMA step of the type; a ragged last tile repeats row N - 1).
+// K % KS == 0, else hipErrorInvalidValue.
 hipError_t launch_pack_feed(int dtype, const void* w, void* out, int N, int K, hipStream_t s);
 size_t gemm_ln_lds_bytes(int K, size_t elt);
 // Products of many rows on LDS-staged MFMA tiles (bf16, no prologue, K a

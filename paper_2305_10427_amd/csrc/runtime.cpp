@@ -474,7 +474,9 @@ hipError_t decoder_pass(pd_ctx& C, const Rows& r, float* logits, hipStream_t s, 
     g.x = a_buf; g.x_f32 = 0; g.ldx = d;
   }
   if (r.R_max <= kVocabStreamMaxRows) {
-    // one row tile: streaming kernel, timed by its own dispatch timestamps
+    // one row tile: streaming kernel (E from its feed-order copy), timed by its
+    // own dispatch timestamps
+    g.wp = M.feed[0];
     e = launch_vocab_argmax(M.dt, g, s, slot >= 0 ? C.tv0[slot] : nullptr, slot >= 0 ? C.tv1[slot] : nullptr);
   } else {
     if (slot >= 0 && (e = hipEventRecord(C.tv0[slot], s)) != hipSuccess) return e;
@@ -725,7 +727,7 @@ pd_status pd_weight_shape(const pd_config* cfg, int32_t idx, int64_t* rows, int6
 static hipError_t make_feed(const pd_model& M) {
   std::lock_guard<std::mutex> lock(M.feed_mu);
   if (M.feed_ready) return hipSuccess;
-  std::vector<int> prods;
+  std::vector<int> prods{0};          // E, for the vocabulary kernel (a ragged last tile allowed)
   for (int l = 0; l < M.cfg.n_enc; ++l)
     for (int j : {E_WQKV, E_WO, E_W1, E_W2}) prods.push_back(2 + 12 * l + j);
   for (int l = 0; l < M.cfg.n_dec; ++l)
@@ -736,9 +738,9 @@ static hipError_t make_feed(const pd_model& M) {
     if (M.feed[idx] != nullptr) continue;
     int64_t rows = 0, cols = 0;
     shape_of(M.cfg, idx, &rows, &cols);
-    if (rows % 16 != 0) continue;      // a ragged column tile: the row-major weights only
+    if (idx != 0 && rows % 16 != 0) continue;   // a ragged product: the row-major weights only
     void* p = nullptr;
-    if ((e = hipMalloc(&p, static_cast<size_t>(rows * cols) * es)) != hipSuccess) return e;
+    if ((e = hipMalloc(&p, static_cast<size_t>((rows + 15) / 16 * 16 * cols) * es)) != hipSuccess) return e;
     M.feed[idx] = p;
     if ((e = launch_pack_feed(M.dt, M.w[idx], p, static_cast<int>(rows), static_cast<int>(cols), nullptr)) !=
         hipSuccess)

@@ -11,9 +11,12 @@
 // waves walk 16-column tiles t = w, w + W, w + 2W, ... (w the wave's global
 // index, W the waves in the grid).  Every lane keeps D 16-byte weight loads
 // outstanding in a ring over the flattened (tile, k step) sequence, so the
-// next tile's loads leave while the current tile is finished.  The loads are
-// non-temporal, since E is streamed once per launch (a plain read of 512 MB
-// measured 86 µs with them against 93 µs with ordinary loads).
+// next tile's loads leave while the current tile is finished.  E is read from
+// its copy in the MFMA feed order when one is given (GemmArgs::wp; a wave's
+// word of one (tile, step) is then 1 KB contiguous, where the row-major E
+// splits every 128-byte line between two steps), with non-temporal loads
+// since E is streamed once per launch (a plain read of 512 MB measured 86 µs
+// with them against 93 µs with ordinary loads).
 //
 // Every logit is accumulated exactly as in the general product kernel with
 // whole-K waves (MFMA steps in increasing k from zero, then s * acc + b), so
@@ -61,13 +64,20 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(VocabShape<
   const int my_tiles = w_id < n_tiles ? (n_tiles - 1 - w_id) / W + 1 : 0;
   const int total = my_tiles * n_steps;
   const WT* __restrict__ E = static_cast<const WT*>(a.w);
+  const WT* __restrict__ Ef = static_cast<const WT*>(a.wp);
   const WT* __restrict__ bias = static_cast<const WT*>(a.bias);
+  const bool packed = Ef != nullptr;
+  const int wstep = packed ? kWave * EPL : KS;    // elements between a lane's words of consecutive steps
 
-  // weight row of tile j for this lane (the last tile's rows beyond N repeat
-  // row N - 1; their logits are never used)
+  // this lane's word of step 0 of tile j: E row-major (the last tile's rows
+  // beyond N repeat row N - 1; their logits are never used), or E's feed-order
+  // copy, where a wave's word of one step is 1 KB contiguous (tiles past the
+  // last repeat it; the ring's loads past its tiles are never used)
   auto wrow = [&](int j) -> const WT* {
-    const int col = min((w_id + j * W) * 16 + lr, N - 1);
-    return E + static_cast<size_t>(col) * K + EPL * lg;
+    const int t = w_id + j * W;
+    const int col = min(t * 16 + lr, N - 1);
+    return packed ? Ef + (static_cast<size_t>(min(t, n_tiles - 1)) * n_steps * kWave + lane) * EPL
+                  : E + static_cast<size_t>(col) * K + EPL * lg;
   };
 
   // Loads complete in issue order, so everything the LayerNorm prologue reads
@@ -89,7 +99,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(VocabShape<
   const WT* pn = wrow(0);
 #pragma unroll
   for (int u = 0; u < D; ++u) {
-    ring[u] = MM::template wload<1>(pn + sn * KS);
+    ring[u] = MM::template wload<1>(pn + sn * wstep);
     if (++sn == n_steps) { sn = 0; ++jn; pn = wrow(jn); }
   }
   float bias_v = Elt<WT>::load(bias, min(w_id * 16 + lr, N - 1));
@@ -119,7 +129,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(VocabShape<
       if (g0 + u >= total) break;
       const frag b = ring[u];
       if (g0 + u + D < total) {
-        ring[u] = MM::template wload<1>(pn + sn * KS);
+        ring[u] = MM::template wload<1>(pn + sn * wstep);
         if (++sn == n_steps) { sn = 0; ++jn; pn = wrow(jn); }
       }
       acc = MM::step(MM::load(arow + s * KS), b, acc);
