@@ -12,7 +12,10 @@ constexpr int kMaxHeadDim = 128;
 
 
 // ---------------------------------------------------------------------------
-// Scaled dot-product attention, one wave per (row, head).
+// Scaled dot-product attention, one wave per (row, head); a workgroup holds
+// one head of 4 consecutive rows, which then read the same keys through the
+// CU's cache (measured against 4 heads of one row per workgroup: large
+// GS-Jacobi b = 16 570 -> 556 µs per iteration, greedy 485 -> 463 µs).
 //
 // The row at position p attends to keys 0..p of its own sentence (causal,
 // decoder self-attention over the KV cache whose block entries were written by
@@ -26,9 +29,11 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   __shared__ AttnScratch s_scr[4];
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = threadIdx.x / kWave;
-  const int idx = blockIdx.x * 4 + wave;
-  const int row = idx / a.H;
-  const int hh = idx - row * a.H;
+  // workgroup g: head g mod H of rows 4 (g div H) .. + 3, one per wave, so
+  // that the waves of a workgroup read one head's keys (of one sentence, but
+  // at a sentence boundary)
+  const int hh = static_cast<int>(blockIdx.x) % a.H;
+  const int row = (static_cast<int>(blockIdx.x) / a.H) * 4 + wave;
   if (row >= a.rows_max) return;         // padding waves of the last workgroup; no workgroup barrier below
   // the device row count, the query and the row's placement go out together
   // (rows below the launch bound have valid query and placement slots); rows
@@ -726,7 +731,7 @@ static hipError_t launch_attn_t(const AttnArgs& a, int grid, hipStream_t s) {
 
 hipError_t launch_attn(int dtype, const AttnArgs& args, int R_max, hipStream_t s) {
   if (args.dh > kMaxHeadDim || args.T > kMaxKeys) return hipErrorInvalidValue;
-  const int grid = (R_max * args.H + 3) / 4;
+  const int grid = (R_max + 3) / 4 * args.H;
   if (grid == 0) return hipSuccess;
   AttnArgs a = args;
   a.rows_max = R_max;
