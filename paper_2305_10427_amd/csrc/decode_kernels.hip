@@ -13,27 +13,30 @@ constexpr int kMaxHeadDim = 128;
 
 // ---------------------------------------------------------------------------
 // Scaled dot-product attention, one wave per (row, head); a workgroup holds
-// one head of 4 consecutive rows, which then read the same keys through the
-// CU's cache (measured against 4 heads of one row per workgroup: large
-// GS-Jacobi b = 16 570 -> 556 µs per iteration, greedy 485 -> 463 µs).
+// one head of kAttnRows consecutive rows.  One row per workgroup spreads a
+// launch over the most CUs; measured per large GS-Jacobi b = 16 iteration:
+// 4 heads of one row per workgroup 570 µs, one head of 8 / 4 / 2 / 1 rows
+// 597 / 559 / 549 / 544 µs (greedy 485 µs, then 462 µs for every size).
 //
 // The row at position p attends to keys 0..p of its own sentence (causal,
 // decoder self-attention over the KV cache whose block entries were written by
 // the QKV product of this iteration) or to keys 0..n_s-1 (encoder memory /
 // encoder self-attention, padded keys excluded).  The wave walks the row's
-// 64-key chunks in order (chunk_partial, merge_chunk); chunk boundaries depend
-// only on the row's own key count.
+// 64-key chunks in order (chunk_fold); chunk boundaries depend only on the
+// row's own key count.
+constexpr int kAttnRows = 1;   // rows (waves) per workgroup
+
 template <typename AT, int DH>
-__global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
-  __shared__ float s_q[4][DH];
-  __shared__ AttnScratch s_scr[4];
+__global__ __launch_bounds__(kAttnRows * kWave) void k_attn(AttnArgs a) {
+  __shared__ float s_q[kAttnRows][DH];
+  __shared__ AttnScratch s_scr[kAttnRows];
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = threadIdx.x / kWave;
-  // workgroup g: head g mod H of rows 4 (g div H) .. + 3, one per wave, so
-  // that the waves of a workgroup read one head's keys (of one sentence, but
-  // at a sentence boundary)
+  // workgroup g: head g mod H of rows kAttnRows (g div H) + wave, so that the
+  // waves of a workgroup read one head's keys (of one sentence, but at a
+  // sentence boundary)
   const int hh = static_cast<int>(blockIdx.x) % a.H;
-  const int row = (static_cast<int>(blockIdx.x) / a.H) * 4 + wave;
+  const int row = (static_cast<int>(blockIdx.x) / a.H) * kAttnRows + wave;
   if (row >= a.rows_max) return;         // padding waves of the last workgroup; no workgroup barrier below
   // the device row count, the query and the row's placement go out together
   // (rows below the launch bound have valid query and placement slots); rows
@@ -720,10 +723,10 @@ __global__ __launch_bounds__(256) void k_argmax_reduce(ReduceArgs a) {
 template <typename AT>
 static hipError_t launch_attn_t(const AttnArgs& a, int grid, hipStream_t s) {
   switch (a.dh) {
-    case 16: hipLaunchKernelGGL((k_attn<AT, 16>), dim3(grid), dim3(256), 0, s, a); break;
-    case 32: hipLaunchKernelGGL((k_attn<AT, 32>), dim3(grid), dim3(256), 0, s, a); break;
-    case 64: hipLaunchKernelGGL((k_attn<AT, 64>), dim3(grid), dim3(256), 0, s, a); break;
-    case 128: hipLaunchKernelGGL((k_attn<AT, 128>), dim3(grid), dim3(256), 0, s, a); break;
+    case 16: hipLaunchKernelGGL((k_attn<AT, 16>), dim3(grid), dim3(kAttnRows * kWave), 0, s, a); break;
+    case 32: hipLaunchKernelGGL((k_attn<AT, 32>), dim3(grid), dim3(kAttnRows * kWave), 0, s, a); break;
+    case 64: hipLaunchKernelGGL((k_attn<AT, 64>), dim3(grid), dim3(kAttnRows * kWave), 0, s, a); break;
+    case 128: hipLaunchKernelGGL((k_attn<AT, 128>), dim3(grid), dim3(kAttnRows * kWave), 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -731,7 +734,7 @@ static hipError_t launch_attn_t(const AttnArgs& a, int grid, hipStream_t s) {
 
 hipError_t launch_attn(int dtype, const AttnArgs& args, int R_max, hipStream_t s) {
   if (args.dh > kMaxHeadDim || args.T > kMaxKeys) return hipErrorInvalidValue;
-  const int grid = (R_max + 3) / 4 * args.H;
+  const int grid = (R_max + kAttnRows - 1) / kAttnRows * args.H;
   if (grid == 0) return hipSuccess;
   AttnArgs a = args;
   a.rows_max = R_max;
