@@ -493,11 +493,13 @@ def main():
             "mt_base_b64": {"workload": "mt_base bf16, batch 64, first 4 batches of 64 sources, n ~ clipped "
                                         "log-normal (median 25, max 128), m = n + 10",
                             **batched_workload("mt_base_b64", 4, [("ar", 1), ("hybrid", 2), ("hybrid", 3),
-                                                                  ("hybrid", 5), ("hybrid", 8)], 2)},
+                                                                  ("hybrid", 5), ("hybrid", 8), ("gs_jacobi", 5),
+                                                                  ("jacobi", 0)], 2)},
             "large_b32": {"workload": "large bf16, batch 32, first 2 batches of 32 sources, n ~ U[20,120], "
                                       "m = min(n + 10, 256)",
                           **batched_workload("large_b32", 2, [("ar", 1)] + [(m, b) for m in ("gs_jacobi", "hybrid")
-                                                                          for b in (1, 2, 4, 8, 16, 32)], 1)},
+                                                                          for b in (1, 2, 4, 8, 16, 32)]
+                                             + [("jacobi", 0)], 1)},
         }
 
     line = {
