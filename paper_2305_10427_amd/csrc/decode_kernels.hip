@@ -252,8 +252,24 @@ __device__ __forceinline__ int block_len(const CtrlArgs& a, int i, int m) {
 // Lay out the rows of the next iteration (sentence order, block order),
 // publish the row count and, when the control step owns the embedding,
 // write the embedded rows.  Single workgroup.
+// The control step's sequence number (thread 0 only): the context's counter
+// of control steps, advanced (k_ctrl_init sets it to the host's count, seq0).
+__device__ __forceinline__ int next_seq(const CtrlArgs& a, bool init) {
+  if (a.seq == nullptr) return 0;
+  const int q = (init ? a.seq0 : *a.seq + 1) & kSeqMask;
+  *a.seq = q;
+  return q;
+}
+
+// Publishes "no rows" for a control step that finds the decode finished.
+__device__ __forceinline__ void publish_done(const CtrlArgs& a) {
+  if (threadIdx.x == 0 && a.host_rows != nullptr)
+    __hip_atomic_store(a.host_rows, host_word(0, false, next_seq(a, false)), __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
 template <typename WT>
-__device__ void emit_rows(const CtrlArgs& a) {
+__device__ void emit_rows(const CtrlArgs& a, bool init) {
   __shared__ int s_total, s_near;
   if (threadIdx.x == 0) {
     int acc = 0;
@@ -284,7 +300,8 @@ __device__ void emit_rows(const CtrlArgs& a) {
     *a.n_rows = total;
     if (a.rows_total != nullptr) *a.rows_total += static_cast<unsigned long long>(total);
     if (a.host_rows != nullptr)
-      __hip_atomic_store(a.host_rows, host_word(total, s_near != 0), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+      __hip_atomic_store(a.host_rows, host_word(total, s_near != 0, next_seq(a, init)), __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_SYSTEM);
   }
   if (a.x_out != nullptr) {
     __syncthreads();
@@ -315,7 +332,7 @@ __global__ __launch_bounds__(1024) void k_ctrl_init(CtrlArgs a) {
     for (int t = 0; t < a.ldy; ++t) y[t] = (init != nullptr && t < m) ? init[t] : a.pad_id;
   }
   __syncthreads();
-  emit_rows<WT>(a);
+  emit_rows<WT>(a, true);
 }
 
 // Best entry of a set of argmax partials.
@@ -431,7 +448,10 @@ __device__ __forceinline__ void trace_row(const CtrlArgs& a, unsigned long long 
 template <typename WT>
 __global__ __launch_bounds__(1024) void k_ctrl_step(CtrlArgs a) {
   const int R = *a.n_rows;
-  if (R == 0) return;
+  if (R == 0) {                          // workgroup-uniform: the decode had already finished
+    publish_done(a);
+    return;
+  }
   if (a.partials != nullptr)
     reduce_rows(a.partials, a.part_ld, a.n_parts, R, const_cast<int*>(a.new_tok), const_cast<int*>(a.row_flags));
   for (int s = threadIdx.x; s < a.B; s += blockDim.x) {
@@ -452,7 +472,7 @@ __global__ __launch_bounds__(1024) void k_ctrl_step(CtrlArgs a) {
   }
   __syncthreads();
   if (a.trace != nullptr && threadIdx.x == 0) *a.trace_count += static_cast<unsigned long long>(R);
-  emit_rows<WT>(a);
+  emit_rows<WT>(a, false);
 }
 
 // The control step with one thread per row instead of one per sentence (up
@@ -476,7 +496,10 @@ __global__ __launch_bounds__(1024) void k_ctrl_rows(CtrlArgs a) {
   __shared__ int s_far;                        // some live sentence is not near its end (near_end)
   const int tid = threadIdx.x;
   const int R = *a.n_rows;
-  if (R == 0) return;                          // workgroup-uniform: the decode had already finished
+  if (R == 0) {                                // workgroup-uniform: the decode had already finished
+    publish_done(a);
+    return;
+  }
   if (tid == 0) s_far = 0;
   if (a.partials != nullptr)
     reduce_rows(a.partials, a.part_ld, a.n_parts, R, const_cast<int*>(a.new_tok), const_cast<int*>(a.row_flags));
@@ -547,7 +570,8 @@ __global__ __launch_bounds__(1024) void k_ctrl_rows(CtrlArgs a) {
     *a.n_rows = total;
     if (a.rows_total != nullptr) *a.rows_total += static_cast<unsigned long long>(total);
     if (a.host_rows != nullptr)
-      __hip_atomic_store(a.host_rows, host_word(total, s_far == 0), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+      __hip_atomic_store(a.host_rows, host_word(total, s_far == 0, next_seq(a, false)), __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_SYSTEM);
   }
   if (a.x_out != nullptr) {
     __syncthreads();
@@ -613,7 +637,10 @@ __global__ __launch_bounds__(1024) void k_ctrl_small(CtrlArgs a) {
     if (it / kCtrlWindow < a.B) s_win[it / kCtrlWindow][it % kCtrlWindow] = wv[u];
   }
   __syncthreads();
-  if (R == 0) return;                          // workgroup-uniform: the decode had already finished
+  if (R == 0) {                                // workgroup-uniform: the decode had already finished
+    publish_done(a);
+    return;
+  }
   int i_old = 0, row0_old = 0, L_old = 0;
   if (sent && !st.done) {
     int* y = a.y + static_cast<size_t>(tid) * a.ldy;
@@ -647,7 +674,8 @@ __global__ __launch_bounds__(1024) void k_ctrl_small(CtrlArgs a) {
     *a.n_rows = acc;
     if (a.rows_total != nullptr) *a.rows_total += static_cast<unsigned long long>(acc);
     if (a.host_rows != nullptr)
-      __hip_atomic_store(a.host_rows, host_word(acc, near), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+      __hip_atomic_store(a.host_rows, host_word(acc, near, next_seq(a, false)), __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_SYSTEM);
   }
   __syncthreads();
   // the next rows: sentence order, block order; the shifted-left input of

@@ -200,7 +200,9 @@ struct CtrlArgs {
   int* row_tok;
   int* n_rows;             // device scalar
   unsigned long long* rows_total;   // device counter: rows of every iteration laid out (may be null)
-  int* host_rows;          // mapped pinned host word (may be null): host_word(rows of the next iteration, near_end)
+  int* host_rows;          // mapped pinned host word (may be null): host_word(rows of the next iteration, near_end, seq)
+  int* seq;                // device counter of the context's control steps (mod 64)
+  int seq0;                // k_ctrl_init: the value it sets the counter to and publishes
   int pad_id, bos_id, eos_id;
   int R_max;
   const int* init;         // initial draft [B][init_ld] (nullptr: all [PAD])
@@ -233,13 +235,22 @@ struct CtrlArgs {
 // iterations leaves at most kNearEndIters more (under the prefix stopping
 // condition, which commits at least one position per iteration: the last
 // block holds at most kNearEndIters positions).  The bit only paces the host.
+// Bits 24..29 carry the number of control steps run so far (mod 64), so that
+// the host recognises the word of the step it waits for without an event
+// record after every iteration (each costs a few µs of GPU time); the rows
+// take the low 24 bits (every launch has fewer than 2^24 rows).
 constexpr int kNearEndBit = 1 << 30;
+constexpr int kSeqShift = 24;
+constexpr int kSeqMask = 63;
+constexpr int kRowsMask = (1 << kSeqShift) - 1;
 constexpr int kNearEndIters = 8;
 __device__ __forceinline__ bool near_end(const SentState& st, int stop_prefix) {
   if (stop_prefix) return st.done || (st.i + st.L >= st.m && st.L <= kNearEndIters);   // >= 1 position per iteration
   return st.done || (st.i + st.L >= st.m && (st.j >= 1 || st.L == 1) && st.L - st.j <= kNearEndIters);
 }
-__host__ __device__ __forceinline__ int host_word(int rows, bool near) { return rows | (near && rows > 0 ? kNearEndBit : 0); }
+__host__ __device__ __forceinline__ int host_word(int rows, bool near, int seq) {
+  return rows | (near && rows > 0 ? kNearEndBit : 0) | ((seq & kSeqMask) << kSeqShift);
+}
 
 struct ReduceArgs {
   const int* n_rows_dev;

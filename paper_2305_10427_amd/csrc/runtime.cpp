@@ -138,7 +138,7 @@ struct Layout {
   size_t x_res, s_buf, q_buf, a_buf, h_buf;
   size_t enc_k, enc_v, cross_k, cross_v, self_k, self_v;
   size_t partials, new_tok, row_flags, row_sent, row_pos, row_tok;
-  size_t st, y, tgt_m, src_len, n_rows, rows_total, pe, trace_count, row_max, row_lse;
+  size_t st, y, tgt_m, src_len, n_rows, seq, rows_total, pe, trace_count, row_max, row_lse;
   size_t total;
 };
 
@@ -180,6 +180,7 @@ Layout plan(const pd_model& M, int max_batch, int max_src, int max_tgt) {
   L.tgt_m = take(static_cast<size_t>(max_batch) * 4);
   L.src_len = take(static_cast<size_t>(max_batch) * 4);
   L.n_rows = take(4);
+  L.seq = take(4);
   L.rows_total = take(8);
   L.trace_count = take(8);
   L.row_max = take(rows_dec * 4);
@@ -224,7 +225,8 @@ struct pd_ctx {
   int* stage_src;         // pinned staging copies of host length arrays
   int* stage_tgt;
   hipEvent_t stage_ev = nullptr;
-  std::vector<hipEvent_t> it_ev;
+  std::vector<hipEvent_t> it_ev;   // [0]: recorded after a decode's last launch
+  int seq_next = 0;                // sequence number of the next control step launched (mod 64)
   // vocabulary-kernel timing: event pairs per in-flight iteration slot
   bool timing = false;
   hipEvent_t tv0[2] = {nullptr, nullptr}, tv1[2] = {nullptr, nullptr};
@@ -670,11 +672,28 @@ bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) %
 
 // Spin until the event has completed (the iteration loop polls rather than
 // blocking: a blocking wait adds a wake-up latency to every iteration).
-hipError_t wait_event(hipEvent_t ev) {
-  hipError_t e;
-  while ((e = hipEventQuery(ev)) == hipErrorNotReady) {
+// Waits until the host word carries the sequence number `target` of a
+// control step, or that of the step after it (mod 64; the host is never more
+// than one step behind), and returns the word.  Every few thousand polls it
+// asks the stream for a failure; an idle stream without the word is one too.
+hipError_t wait_word(volatile int* word_p, int target, hipStream_t s, int* word) {
+  auto ok = [&](int w) { return (((w >> kSeqShift) - target) & kSeqMask) <= 1; };
+  for (unsigned n = 1;; ++n) {
+    const int w = *word_p;
+    if (ok(w)) {
+      *word = w;
+      return hipSuccess;
+    }
+    if ((n & 4095u) == 0) {
+      const hipError_t e = hipStreamQuery(s);
+      if (e == hipErrorNotReady) continue;
+      if (e != hipSuccess) return e;
+      const int w2 = *word_p;      // the stream has drained: the step has run
+      if (!ok(w2)) return hipErrorUnknown;
+      *word = w2;
+      return hipSuccess;
+    }
   }
-  return e;
 }
 
 // Fold a slot's completed event pairs (decoder products, vocabulary kernel) into the totals.
@@ -827,7 +846,7 @@ pd_status pd_ctx_create(const pd_model* model, int32_t max_batch, int32_t max_sr
   }
   c->stage_src = c->host_pinned + 1;
   c->stage_tgt = c->host_pinned + 1 + max_batch;
-  c->it_ev.resize(2, nullptr);
+  c->it_ev.resize(1, nullptr);
   e = hipEventCreateWithFlags(&c->stage_ev, hipEventDisableTiming);
   for (auto& ev : c->it_ev)
     if (e == hipSuccess) e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
@@ -951,6 +970,7 @@ pd_status pd_decode_init(pd_ctx* ctx, int32_t mode, int32_t block, int32_t horiz
   ca.n_rows = C.at<int>(C.L.n_rows);
   ca.rows_total = C.at<unsigned long long>(C.L.rows_total);
   ca.host_rows = C.host_rows_dev;
+  ca.seq = C.at<int>(C.L.seq);
   ca.pad_id = M.cfg.pad_id;
   ca.bos_id = M.cfg.bos_id;
   ca.eos_id = M.cfg.eos_id;
@@ -974,9 +994,11 @@ pd_status pd_decode_init(pd_ctx* ctx, int32_t mode, int32_t block, int32_t horiz
   // the first rows (at most R_max) are laid out, and embedded when the first
   // iteration's control step is the fused one, by the initial step
   bool prev_fused = R_max <= kFuseCtrlMaxRows;
-  const CtrlArgs c0 = ctrl_for_bound(C, ca, R_max);
+  CtrlArgs c0 = ctrl_for_bound(C, ca, R_max);
+  c0.seq0 = C.seq_next;            // every control step launched advances the count, even after the end
   hipError_t e = launch_ctrl_init(M.dt, c0, s);
   if (e != hipSuccess) return fail(PD_E_DEVICE, std::string("init launch: ") + hipGetErrorString(e));
+  C.seq_next = (C.seq_next + 1) & kSeqMask;
   volatile int* host_rows = C.host_pinned;
   int bound = R_max;   // rows of the next iteration launched are at most this
   for (int it = 0; it < iters; ++it) {
@@ -1002,30 +1024,28 @@ pd_status pd_decode_init(pd_ctx* ctx, int32_t mode, int32_t block, int32_t horiz
         e = iteration(C, r, cb, s, slot, fused);
       }
     }
-    if (e == hipSuccess) e = hipEventRecord(C.it_ev[it & 1], s);
     if (e != hipSuccess) return fail(PD_E_DEVICE, std::string("iteration launch: ") + hipGetErrorString(e));
+    const int q = C.seq_next;        // this iteration's control step
+    C.seq_next = (C.seq_next + 1) & kSeqMask;
     if (it >= 1) {
-      // the previous iteration has finished when its event completes; its
-      // control step (or a later one) has published the row count of the
-      // iteration after it (0 when every sentence is done, else a bound on
-      // the rows of every iteration not launched yet) and whether that
-      // iteration, the one in flight, may be the last: then it is waited for
-      // too, rather than launching one more iteration that may find nothing
-      // to do
-      if ((e = wait_event(C.it_ev[(it - 1) & 1])) != hipSuccess)
+      // the previous iteration's control step (or the next one) has published
+      // the row count of the iteration after it (0 when every sentence is
+      // done, else a bound on the rows of every iteration not launched yet)
+      // and whether that iteration, the one in flight, may be the last: then
+      // it is waited for too, rather than launching one more iteration that
+      // may find nothing to do
+      int word = 0;
+      if ((e = wait_word(host_rows, q - 1, s, &word)) != hipSuccess)
         return fail(PD_E_DEVICE, std::string("iteration: ") + hipGetErrorString(e));
-      int word = *host_rows;
-      if ((word & kNearEndBit) != 0) {
-        if ((e = wait_event(C.it_ev[it & 1])) != hipSuccess)
-          return fail(PD_E_DEVICE, std::string("iteration: ") + hipGetErrorString(e));
-        word = *host_rows;
-      }
-      const int rows = word & ~kNearEndBit;
+      if ((word & kNearEndBit) != 0 && (e = wait_word(host_rows, q, s, &word)) != hipSuccess)
+        return fail(PD_E_DEVICE, std::string("iteration: ") + hipGetErrorString(e));
+      const int rows = word & kRowsMask;
       if (rows <= 0) break;
       bound = std::min(bound, rows);
     }
   }
   e = launch_finalize(ca, s);
+  if (e == hipSuccess) e = hipEventRecord(C.it_ev[0], s);   // the decode's last work (pd_ctx_destroy waits for it)
   if (e != hipSuccess) return fail(PD_E_DEVICE, std::string("finalize launch: ") + hipGetErrorString(e));
   if (C.timing) {
     for (int slot = 0; slot < 2; ++slot)
