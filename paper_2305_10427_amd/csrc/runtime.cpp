@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <chrono>
 #include <cmath>
 #include <cstdio>
 #include <cstdlib>
@@ -688,10 +689,17 @@ hipError_t wait_word(volatile int* word_p, int target, hipStream_t s, int* word)
       const hipError_t e = hipStreamQuery(s);
       if (e == hipErrorNotReady) continue;
       if (e != hipSuccess) return e;
-      const int w2 = *word_p;      // the stream has drained: the step has run
-      if (!ok(w2)) return hipErrorUnknown;
-      *word = w2;
-      return hipSuccess;
+      // the stream has drained, so the step has run: its write to host memory
+      // is given a moment to land before the word counts as missing
+      const auto t0 = std::chrono::steady_clock::now();
+      while (std::chrono::steady_clock::now() - t0 < std::chrono::milliseconds(50)) {
+        const int w2 = *word_p;
+        if (ok(w2)) {
+          *word = w2;
+          return hipSuccess;
+        }
+      }
+      return hipErrorUnknown;
     }
   }
 }
