@@ -31,7 +31,9 @@
  * on it are enqueued on the stream given to each call and are asynchronous
  * unless stated otherwise.  A context's workspace holds the encoder state
  * between pd_encode and pd_decode, so those two calls must be ordered (same
- * stream, or synchronised).
+ * stream, or synchronised); so must any two calls that use one context's
+ * workspace (a decode returns with its outputs, and possibly an iteration
+ * that finds nothing left to do, still queued on its stream).
  *
  * Errors.  Every call returns pd_status.  Argument / shape / state errors are
  * detected on the host before anything is enqueued.  PD_E_DEVICE reports a
