@@ -326,10 +326,14 @@ __global__ __launch_bounds__(1024) void k_ctrl_init(CtrlArgs a) {
     st.L = st.done ? 0 : block_len(a, 0, m);
     st.row0 = 0;
     a.st[s] = st;
-    int* y = a.y + static_cast<size_t>(s) * a.ldy;
-    // InitT: the caller's draft over the m positions, else all [PAD]
-    const int* init = a.init != nullptr ? a.init + static_cast<size_t>(s) * a.init_ld : nullptr;
-    for (int t = 0; t < a.ldy; ++t) y[t] = (init != nullptr && t < m) ? init[t] : a.pad_id;
+  }
+  // InitT: the caller's draft over the m positions, else all [PAD]; one
+  // (sentence, position) item per thread and step
+  const long long n_y = static_cast<long long>(a.B) * a.ldy;
+  for (long long i = threadIdx.x; i < n_y; i += blockDim.x) {
+    const int s = static_cast<int>(i / a.ldy);
+    const int t = static_cast<int>(i - static_cast<long long>(s) * a.ldy);
+    a.y[i] = (a.init != nullptr && t < a.tgt_m[s]) ? a.init[static_cast<size_t>(s) * a.init_ld + t] : a.pad_id;
   }
   __syncthreads();
   emit_rows<WT>(a, true);
