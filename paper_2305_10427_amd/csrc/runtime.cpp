@@ -671,12 +671,12 @@ pd_status stage_lengths(pd_ctx* C, int* stage, const int32_t* host, int B, int* 
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
-// Spin until the event has completed (the iteration loop polls rather than
-// blocking: a blocking wait adds a wake-up latency to every iteration).
 // Waits until the host word carries the sequence number `target` of a
 // control step, or that of the step after it (mod 64; the host is never more
-// than one step behind), and returns the word.  Every few thousand polls it
-// asks the stream for a failure; an idle stream without the word is one too.
+// than one step behind), and returns the word.  It polls rather than blocking
+// (a blocking wait adds a wake-up latency to every iteration); every few
+// thousand polls it asks the stream for a failure, and an idle stream without
+// the word is one too.
 hipError_t wait_word(volatile int* word_p, int target, hipStream_t s, int* word) {
   auto ok = [&](int w) { return (((w >> kSeqShift) - target) & kSeqMask) <= 1; };
   for (unsigned n = 1;; ++n) {
