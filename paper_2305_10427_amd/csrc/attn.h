@@ -44,10 +44,16 @@ template <typename AT, int DH> struct KeyChunk {
   uint4 k[NW];
   Pair v[NP][32];
   __device__ __forceinline__ void load(const AT* Kb, const AT* Vb, int key0, int nk, int lane) {
+    load_k(Kb, key0, nk, lane);
+    load_v(Vb, key0, nk, lane);
+  }
+  __device__ __forceinline__ void load_k(const AT* Kb, int key0, int nk, int lane) {
     const int key = key0 + lane < nk ? key0 + lane : 0;
     const uint4* kr = reinterpret_cast<const uint4*>(Kb + static_cast<size_t>(key) * DH);
 #pragma unroll
     for (int i = 0; i < NW; ++i) k[i] = kr[i];
+  }
+  __device__ __forceinline__ void load_v(const AT* Vb, int key0, int nk, int lane) {
     const int d0 = 2 * (lane & 31);
     const int kh = key0 + 32 * (lane >> 5);
 #pragma unroll
@@ -98,11 +104,18 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// One chunk folded into the row state.  q: the row's query (DH floats, LDS).
-// All 64 lanes must be active.
+// One chunk's own softmax statistics and unnormalised output: m_c, l_c and
+// o_c (lane l < 32: dimensions 2l, 2l + 1 (+ 64 i)).
+template <int DH> struct ChunkOut {
+  float m, l;
+  float o[RowState<DH>::NP][2];
+};
+
+// Evaluates one chunk (keys key0 .. key0+63 below nk) for the query q (DH
+// floats, LDS).  All 64 lanes must be active.
 template <typename AT, int DH>
-__device__ __forceinline__ void chunk_fold(const float* q, const KeyChunk<AT, DH>& kc, int key0, int nk, float scale,
-                                           int lane, AttnScratch& sm, RowState<DH>& st) {
+__device__ __forceinline__ void chunk_eval(const float* q, const KeyChunk<AT, DH>& kc, int key0, int nk, float scale,
+                                           int lane, AttnScratch& sm, ChunkOut<DH>& c) {
   using KC = KeyChunk<AT, DH>;
   constexpr int V16 = KC::V16;
   const bool valid = key0 + lane < nk;
@@ -119,10 +132,8 @@ __device__ __forceinline__ void chunk_fold(const float* q, const KeyChunk<AT, DH
   const float sc = valid ? acc * scale : -INFINITY;
   const float mc = wave_max(sc);
   const float p = valid ? expf(sc - mc) : 0.f;   // zero past the row's keys
-  const float lc = wave_sum(p);
-  const float mn = fmaxf(st.m, mc);
-  const float a1 = expf(st.m - mn);
-  const float a2 = expf(mc - mn);
+  c.m = mc;
+  c.l = wave_sum(p);
   sm.p[lane] = p;
   wave_lds_sync();
   // P.V: each lane sums its two dimensions over its half of the keys.  Keys
@@ -153,15 +164,38 @@ __device__ __forceinline__ void chunk_fold(const float* q, const KeyChunk<AT, DH
     }
     wave_lds_sync();
     if (lane < 32) {
-      const float oc0 = o[i][0] + sm.half[lane][0];
-      const float oc1 = o[i][1] + sm.half[lane][1];
-      st.o[i][0] = st.o[i][0] * a1 + oc0 * a2;
-      st.o[i][1] = st.o[i][1] * a1 + oc1 * a2;
+      c.o[i][0] = o[i][0] + sm.half[lane][0];
+      c.o[i][1] = o[i][1] + sm.half[lane][1];
     }
     wave_lds_sync();
   }
-  st.l = st.l * a1 + lc * a2;
+}
+
+// Folds an evaluated chunk into the row state (chunks in key order):
+//   m' = max(m, m_c),  o <- o exp(m - m') + o_c exp(m_c - m'),  l likewise.
+template <int DH>
+__device__ __forceinline__ void fold_chunk(const ChunkOut<DH>& c, int lane, RowState<DH>& st) {
+  const float mn = fmaxf(st.m, c.m);
+  const float a1 = expf(st.m - mn);
+  const float a2 = expf(c.m - mn);
+#pragma unroll
+  for (int i = 0; i < RowState<DH>::NP; ++i) {
+    if (lane < 32) {
+      st.o[i][0] = st.o[i][0] * a1 + c.o[i][0] * a2;
+      st.o[i][1] = st.o[i][1] * a1 + c.o[i][1] * a2;
+    }
+  }
+  st.l = st.l * a1 + c.l * a2;
   st.m = mn;
+}
+
+// One chunk folded into the row state.
+template <typename AT, int DH>
+__device__ __forceinline__ void chunk_fold(const float* q, const KeyChunk<AT, DH>& kc, int key0, int nk, float scale,
+                                           int lane, AttnScratch& sm, RowState<DH>& st) {
+  ChunkOut<DH> c;
+  chunk_eval<AT, DH>(q, kc, key0, nk, scale, lane, sm, c);
+  fold_chunk<DH>(c, lane, st);
 }
 
 // Final output o / l of a row's head slice: element d goes to out[at(d)]

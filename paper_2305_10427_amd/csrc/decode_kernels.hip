@@ -8,6 +8,7 @@
 namespace pdec {
 
 constexpr int kMaxKeys = 1024;
+static_assert(kAttnChunk == kAttnChunkKeys, "attention chunk of the host-side launch choice");
 constexpr int kMaxHeadDim = 128;
 
 
@@ -100,6 +101,113 @@ __global__ __launch_bounds__(kAttnRows * kWave) void k_attn(AttnArgs a) {
   } else {
     const size_t base = static_cast<size_t>(row) * a.ldo + hh * DH;
     row_output<AT, DH>(st, out, [&](int d) { return base + d; }, lane);
+  }
+}
+
+// Attention of few rows: one workgroup of W waves per (row, head).  Wave w
+// evaluates chunks w, w + W, ... of the row (chunk_eval) and leaves each
+// chunk's (m_c, l_c, o_c) in LDS; wave 0 then folds them in key order
+// (fold_chunk).  That is k_attn's arithmetic in k_attn's order, so a row's
+// output is bitwise the same, while the chunks of a long row are evaluated
+// side by side instead of one after another.
+template <typename AT, int DH, int W>
+__global__ __launch_bounds__(W * kWave) void k_attn_split(AttnArgs a) {
+  constexpr int NQ = (DH + kWave - 1) / kWave;
+  constexpr int NP = RowState<DH>::NP;
+  constexpr int NC = kMaxKeys / kAttnChunk;
+  struct Slot {
+    float m, l;
+    float o[NP][32][2];
+  };
+  __shared__ float s_q[W][DH];
+  __shared__ AttnScratch s_scr[W];
+  __shared__ Slot s_c[NC];
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = threadIdx.x / kWave;
+  const int hh = static_cast<int>(blockIdx.x) % a.H;
+  const int row = static_cast<int>(blockIdx.x) / a.H;   // below rows_max (grid)
+  // the device row count, the query and the row's placement go out together;
+  // a row at or past the count leaves with its whole workgroup
+  const int R = a.n_rows_dev ? *a.n_rows_dev : a.n_rows;
+  const float* q = a.q + static_cast<size_t>(row) * a.ldq + hh * DH;
+  float qv[NQ];
+#pragma unroll
+  for (int i = 0; i < NQ; ++i) {
+    const int d = lane + kWave * i;
+    qv[i] = q[d < DH ? d : 0];           // unconditional load
+  }
+  int s, p;
+  row_place(a.rows, row, s, p);
+  if (row >= R) return;
+  const int nk = a.causal ? p + 1 : a.klen[s];
+  const int nc = (nk + kAttnChunk - 1) / kAttnChunk;    // 1 .. NC
+  const size_t base = (static_cast<size_t>(s) * a.H + hh) * a.T * DH;
+  const AT* Kb = static_cast<const AT*>(a.kc) + base;
+  const AT* Vb = static_cast<const AT*>(a.vc) + base;
+  if (nc == 1 && wave != 0) return;     // workgroup-uniform: one chunk, no barrier below
+  // every wave loads its first chunk on the straight path (a wave past the
+  // row's chunks loads key 0 and evaluates nothing)
+  KeyChunk<AT, DH> kc;
+  kc.load_k(Kb, wave * kAttnChunk, nk, lane);
+  __builtin_amdgcn_sched_barrier(0);     // the K rows first: the scores start while V arrives
+  kc.load_v(Vb, wave * kAttnChunk, nk, lane);
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int i = 0; i < NQ; ++i) {
+    const int d = lane + kWave * i;
+    if (d < DH) s_q[wave][d] = qv[i];
+  }
+  wave_lds_sync();
+  auto keep = [&](const ChunkOut<DH>& c, int j) {
+    if (lane < 32) {
+#pragma unroll
+      for (int i = 0; i < NP; ++i) {
+        s_c[j].o[i][lane][0] = c.o[i][0];
+        s_c[j].o[i][lane][1] = c.o[i][1];
+      }
+    }
+    if (lane == 0) {
+      s_c[j].m = c.m;
+      s_c[j].l = c.l;
+    }
+  };
+  ChunkOut<DH> c0;                        // wave 0's chunk 0 stays in registers
+  if (wave < nc) {                        // wave-uniform
+    chunk_eval<AT, DH>(s_q[wave], kc, wave * kAttnChunk, nk, a.scale, lane, s_scr[wave], c0);
+    if (wave != 0) keep(c0, wave);
+    for (int j = wave + W; j < nc; j += W) {   // rows of more than W chunks
+      kc.load(Kb, Vb, j * kAttnChunk, nk, lane);
+      ChunkOut<DH> c;
+      chunk_eval<AT, DH>(s_q[wave], kc, j * kAttnChunk, nk, a.scale, lane, s_scr[wave], c);
+      keep(c, j);
+    }
+  }
+  if (nc > 1) __syncthreads();
+  if (wave != 0) return;
+  RowState<DH> st;
+  st.init();
+  fold_chunk<DH>(c0, lane, st);
+  for (int j = 1; j < nc; ++j) {
+    ChunkOut<DH> c;
+    c.m = s_c[j].m;
+    c.l = s_c[j].l;
+    if (lane < 32) {
+#pragma unroll
+      for (int i = 0; i < NP; ++i) {
+        c.o[i][0] = s_c[j].o[i][lane][0];
+        c.o[i][1] = s_c[j].o[i][lane][1];
+      }
+    }
+    fold_chunk<DH>(c, lane, st);
+  }
+  AT* out = static_cast<AT*>(a.out);
+  if (a.out_feed) {
+    const int K = a.H * DH;
+    row_output<AT, DH>(st, out, [&](int d) { return feed_index<Mma<AT>::KS, Mma<AT>::EPL>(row, hh * DH + d, K); },
+                       lane);
+  } else {
+    const size_t ob = static_cast<size_t>(row) * a.ldo + hh * DH;
+    row_output<AT, DH>(st, out, [&](int d) { return ob + d; }, lane);
   }
 }
 
@@ -752,8 +860,30 @@ __global__ __launch_bounds__(256) void k_argmax_reduce(ReduceArgs a) {
   }
 }
 
+template <typename AT, int W>
+static hipError_t launch_attn_split(const AttnArgs& a, int grid, hipStream_t s) {
+  switch (a.dh) {
+    case 16: hipLaunchKernelGGL((k_attn_split<AT, 16, W>), dim3(grid), dim3(W * kWave), 0, s, a); break;
+    case 32: hipLaunchKernelGGL((k_attn_split<AT, 32, W>), dim3(grid), dim3(W * kWave), 0, s, a); break;
+    case 64: hipLaunchKernelGGL((k_attn_split<AT, 64, W>), dim3(grid), dim3(W * kWave), 0, s, a); break;
+    case 128: hipLaunchKernelGGL((k_attn_split<AT, 128, W>), dim3(grid), dim3(W * kWave), 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+// Launches of at most kAttnSplitRows rows whose rows may have more than one
+// chunk of keys evaluate a row's chunks on kAttnSplitWaves waves side by
+// side (k_attn_split); larger launches keep one wave per (row, head), which
+// measured faster there (and the one-wave kernel is faster for rows of one
+// chunk).  Both give bitwise the same rows.
+constexpr int kAttnSplitRows = 64;
+constexpr int kAttnSplitWaves = 4;
+
 template <typename AT>
 static hipError_t launch_attn_t(const AttnArgs& a, int grid, hipStream_t s) {
+  if (a.rows_max <= kAttnSplitRows && a.max_keys > kAttnChunk)
+    return launch_attn_split<AT, kAttnSplitWaves>(a, a.rows_max * a.H, s);
   switch (a.dh) {
     case 16: hipLaunchKernelGGL((k_attn<AT, 16>), dim3(grid), dim3(kAttnRows * kWave), 0, s, a); break;
     case 32: hipLaunchKernelGGL((k_attn<AT, 32>), dim3(grid), dim3(kAttnRows * kWave), 0, s, a); break;

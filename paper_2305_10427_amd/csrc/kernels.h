@@ -118,6 +118,8 @@ __device__ __forceinline__ void layer_select(GemmArgs& a, int z) {
   }
 }
 
+constexpr int kAttnChunkKeys = 64;   // keys per attention chunk (one per lane of a wave)
+
 struct AttnArgs {
   const int* n_rows_dev;
   int n_rows;
@@ -134,6 +136,7 @@ struct AttnArgs {
   float scale;             // 1/sqrt(dh)
   int rows_max;            // launch bound on the rows (set by launch_attn)
   int out_feed;            // 1: out ([R][H dh]) written in the MFMA feed order (feed_index), ldo unused
+  int max_keys;            // host bound on any row's key count (0: unknown); chooses the launch shape only
 };
 
 struct EmbedArgs {

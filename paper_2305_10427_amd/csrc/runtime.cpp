@@ -195,13 +195,15 @@ Layout plan(const pd_model& M, int max_batch, int max_src, int max_tgt) {
 
 struct GraphKey {
   int mode, block, horizon, max_iters, B, R_max, slot, fused;
+  int long_keys;   // rows of more than one key chunk possible: 1 self-attention, 2 cross-attention
   // the trace buffers are kernel arguments of a traced iteration
   const void* trace;
   long long trace_cap;
   const void* trace_part;
   bool operator==(const GraphKey& o) const {
     return mode == o.mode && block == o.block && horizon == o.horizon && max_iters == o.max_iters && B == o.B &&
-           R_max == o.R_max && slot == o.slot && fused == o.fused && trace == o.trace && trace_cap == o.trace_cap &&
+           R_max == o.R_max && slot == o.slot && fused == o.fused && long_keys == o.long_keys && trace == o.trace &&
+           trace_cap == o.trace_cap &&
            trace_part == o.trace_part;
   }
 };
@@ -250,6 +252,9 @@ struct pd_ctx {
   long long trace_rows = 0;            // rows the scratch holds
   bool reset_trace = false;            // the next decode zeroes the record count on its stream
   int enc_B = 0, enc_nmax = 0;
+  // host bounds on the key count of any row: the longest encoded source, and
+  // the longest target of the running decode (or debug_logits' T)
+  int src_keys = 0, self_keys = 0;
   bool encoded = false;
 
   template <typename T> T* at(size_t off) const { return reinterpret_cast<T*>(ws + off); }
@@ -409,6 +414,7 @@ hipError_t decoder_pass(pd_ctx& C, const Rows& r, float* logits, hipStream_t s, 
     AttnArgs aa{r.n_dev, r.n_host, q_buf, d, g.kc, g.vc, M.H, M.dh, C.max_tgt, r.map, 1, nullptr,
                 a_buf, d, 1.0f / std::sqrt(static_cast<float>(M.dh))};
     aa.out_feed = feed;
+    aa.max_keys = C.self_keys;
     if ((e = launch_attn(M.dt, aa, r.R_max, s)) != hipSuccess) return e;
 
     g = gemm_base(r);
@@ -430,6 +436,7 @@ hipError_t decoder_pass(pd_ctx& C, const Rows& r, float* logits, hipStream_t s, 
                   C.at<char>(C.L.cross_v) + l * cross_layer, M.H, M.dh, C.max_src, r.map, 0,
                   C.at<int>(C.L.src_len), a_buf, d, 1.0f / std::sqrt(static_cast<float>(M.dh))};
     aa.out_feed = feed;
+    aa.max_keys = C.src_keys;
     if ((e = launch_attn(M.dt, aa, r.R_max, s)) != hipSuccess) return e;
 
     g = gemm_base(r);
@@ -541,6 +548,7 @@ hipError_t encoder_pass(pd_ctx& C, const int32_t* src, int B, int n_max, hipStre
     g.H = M.H; g.dh = M.dh; g.T = C.max_src; g.d = d;
     if ((e = run_gemm(C, r, g, EPI_QKV, ln, ln_tmp, s)) != hipSuccess) return e;
     AttnArgs aa{nullptr, R, q_buf, d, g.kc, g.vc, M.H, M.dh, C.max_src, r.map, 0, klen, a_buf, d, scale};
+    aa.max_keys = C.src_keys;
     if ((e = launch_attn(M.dt, aa, R, s)) != hipSuccess) return e;
     g = gemm_base(r);
     g.x = a_buf; g.ldx = d; g.w = M.enc(l, E_WO); g.wp = M.enc_feed(l, E_WO); g.bias = M.enc(l, E_BO); g.N = d; g.K = d;
@@ -905,6 +913,8 @@ pd_status pd_encode(pd_ctx* ctx, const int32_t* src_ids, const int32_t* src_len,
     if (src_len[b] < 1 || src_len[b] > n_max) return fail(PD_E_ARG, "src_len[" + std::to_string(b) + "] out of [1, n_max]");
   hipStream_t s = static_cast<hipStream_t>(stream);
   ctx->encoded = false;
+  ctx->src_keys = 0;
+  for (int b = 0; b < B; ++b) ctx->src_keys = std::max(ctx->src_keys, static_cast<int>(src_len[b]));
   pd_status st = stage_lengths(ctx, ctx->stage_src, src_len, B, ctx->at<int>(ctx->L.src_len), s);
   if (st != PD_OK) return st;
   hipError_t e = encoder_pass(*ctx, src_ids, B, n_max, s);
@@ -957,6 +967,7 @@ pd_status pd_decode_init(pd_ctx* ctx, int32_t mode, int32_t block, int32_t horiz
                                     " rows, the decode needs " + std::to_string(R_max));
   pd_status st = stage_lengths(ctx, C.stage_tgt, tgt_m, B, C.at<int>(C.L.tgt_m), s);
   if (st != PD_OK) return st;
+  C.self_keys = m_max;
 
   CtrlArgs ca;
   std::memset(&ca, 0, sizeof(ca));
@@ -1024,8 +1035,9 @@ pd_status pd_decode_init(pd_ctx* ctx, int32_t mode, int32_t block, int32_t horiz
     if (e == hipSuccess) {
       if (C.use_graphs && slot < 0) {   // iterations timed with events are launched directly
         hipGraphExec_t ex = nullptr;
-        const GraphKey key{key_mode, block, horizon, max_iters, B, Rb, slot, fused ? 1 : 0, C.trace, C.trace_cap,
-                           C.trace_part};
+        const int long_keys = (C.self_keys > kAttnChunkKeys ? 1 : 0) | (C.src_keys > kAttnChunkKeys ? 2 : 0);
+        const GraphKey key{key_mode, block, horizon, max_iters, B, Rb, slot, fused ? 1 : 0, long_keys, C.trace,
+                           C.trace_cap, C.trace_part};
         e = iteration_graph(C, key, r, cb, &ex);
         if (e == hipSuccess) e = hipGraphLaunch(ex, s);
       } else {
@@ -1157,6 +1169,7 @@ pd_status pd_debug_logits(pd_ctx* ctx, const int32_t* tgt_in, int32_t T, float* 
   const int B = ctx->enc_B;
   const int R = B * T;
   Rows r{nullptr, R, RowMap{nullptr, nullptr, T}, tgt_in, R};
+  ctx->self_keys = T;
   hipError_t e = decoder_pass(*ctx, r, logits, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(PD_E_DEVICE, std::string("decoder launch: ") + hipGetErrorString(e));
   return PD_OK;

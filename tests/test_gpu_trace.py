@@ -174,3 +174,57 @@ def test_trace_capacity_and_scratch_limits():
     want = oracle.decode(M, M.encode(src), 16, "jacobi")
     g = gpu_decode_batch(ctx, [src], [16], "jacobi")[0]
     np.testing.assert_array_equal(g.ids, want.out)
+
+
+MID_F32 = dataclasses.replace(C.TINY, name="mid_f32", d_model=128, n_heads=2, d_ff=256, vocab=700)
+WIDE_PRE_BF16 = dataclasses.replace(C.TINY, name="wide_pre", n_dec=1, n_enc=1, d_model=640, n_heads=10, d_ff=640,
+                                    vocab=500, pre_ln=True, act_gelu=True, dtype=C.BF16)
+
+
+@pytest.mark.parametrize("cfg,wkw", [(CHAIN, dict(bias_std=0.5, ln_std=0.3)), (MID_F32, {}),
+                                     (WIDE_PRE_BF16, dict(bias_std=0.3, ln_std=0.2))],
+                         ids=["chain_f32_dh16", "mid_f32_dh64", "wide_pre_bf16_dh64"])
+def test_rows_of_several_key_chunks_agree_across_launch_shapes(cfg, wkw):
+    """Rows whose keys span several 64-key chunks: a launch of up to 64 rows
+    evaluates a row's chunks on several waves side by side and folds them in
+    key order, a larger launch folds them on one wave as it goes; the rows
+    are bitwise the same.  Self- and cross-attention: greedy steps (one row,
+    m = 100, sources of 100 tokens) against the last evaluation of each
+    position in a Jacobi decode (100 rows per iteration), whose prefix is the
+    same greedy output: same tokens, top-1 logits bitwise.  Cross-attention
+    alone: teacher-forced logits of 8 positions of 3 sentences (24 rows)
+    against 30 positions (90 rows), sources of 100, 90 and 70 tokens."""
+    import torch
+    gm, ctx, M = build(cfg, seed=9, max_batch=3, max_src=128, max_tgt=128, **wkw)
+    srcs = [np.random.default_rng(31 + i).integers(4, cfg.vocab, n).astype(np.int32) for i, n in
+            enumerate((100, 90, 70))]
+    src = np.zeros((3, 100), np.int32)
+    for r, s in enumerate(srcs):
+        src[r, :len(s)] = s
+    ctx.encode(torch.from_numpy(src).cuda(), [len(s) for s in srcs])
+    tgt = np.concatenate([np.ones((3, 1), np.int32),
+                          np.random.default_rng(32).integers(0, cfg.vocab, (3, 29)).astype(np.int32)], 1)
+    say(f"case several chunks cfg={cfg.name}: teacher-forced 24 vs 90 rows")
+    full = ctx.debug_logits(torch.from_numpy(tgt)).cpu().numpy()
+    part = ctx.debug_logits(torch.from_numpy(np.ascontiguousarray(tgt[:, :8]))).cpu().numpy()
+    np.testing.assert_array_equal(part, full[:, :8])
+
+    m = 100
+    say(f"case several chunks cfg={cfg.name}: greedy vs Jacobi, m={m}")
+    ctx.set_trace(16384, m)
+    ar = gpu_decode_batch(ctx, srcs[:1], [m], "ar")[0]
+    rec_ar, n_ar = ctx.trace()
+    assert n_ar == len(rec_ar)
+    jac = gpu_decode_batch(ctx, srcs[:1], [m], "jacobi")[0]
+    rec_j, n_j = ctx.trace()
+    assert n_j == len(rec_j)
+    ctx.set_trace(0, 0)
+    np.testing.assert_array_equal(jac.ids, ar.ids)
+    last = {}
+    for r in rec_j:                                   # evaluation order: the last record of a position wins
+        last[int(r["position"])] = r
+    assert len(rec_ar) == len(ar.ids) >= 65, (len(rec_ar), len(ar.ids))
+    for r in rec_ar:
+        j = last[int(r["position"])]
+        assert int(j["token"]) == int(r["token"])
+        assert np.float32(j["top1"]).view(np.uint32) == np.float32(r["top1"]).view(np.uint32), (r, j)
