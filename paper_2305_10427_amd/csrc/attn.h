@@ -90,12 +90,17 @@ __device__ __forceinline__ void unpack_pair(uint2 w, float& a, float& b) {
   b = __uint_as_float(w.y);
 }
 
-// Per-wave LDS of the chunk computation: the weights p_k and the upper
-// key-half partial outputs.
+// Per-wave LDS of the chunk computation: the weights p_k.
 struct AttnScratch {
   float p[kAttnChunk];
-  float half[32][2];
 };
+
+// Lane l < 32 receives v of lane l + 32 (v_permlane32_swap exchanges the
+// upper half of its first operand with the lower half of its second).
+__device__ __forceinline__ float upper_half(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[1]);
+}
 
 // Orders the wave's LDS writes before its following reads.
 __device__ __forceinline__ void wave_lds_sync() {
@@ -155,19 +160,13 @@ __device__ __forceinline__ void chunk_eval(const float* q, const KeyChunk<AT, DH
     o[i][0] = (oa[0] + oa[1]) + (oa[2] + oa[3]);
     o[i][1] = (ob[0] + ob[1]) + (ob[2] + ob[3]);
   }
-  // lower key half + upper key half, per dimension group
+  // lower key half + upper key half, per dimension group: lane l < 32 takes
+  // lane l + 32's partial sums by a swap of the wave's halves (lanes >= 32
+  // hold values that are never used)
 #pragma unroll
   for (int i = 0; i < KC::NP; ++i) {
-    if (lane >= 32) {
-      sm.half[lane - 32][0] = o[i][0];
-      sm.half[lane - 32][1] = o[i][1];
-    }
-    wave_lds_sync();
-    if (lane < 32) {
-      c.o[i][0] = o[i][0] + sm.half[lane][0];
-      c.o[i][1] = o[i][1] + sm.half[lane][1];
-    }
-    wave_lds_sync();
+    c.o[i][0] = o[i][0] + upper_half(o[i][0]);
+    c.o[i][1] = o[i][1] + upper_half(o[i][1]);
   }
 }
 
