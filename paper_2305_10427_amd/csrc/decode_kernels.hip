@@ -722,13 +722,15 @@ __global__ __launch_bounds__(1024) void k_ctrl_small(CtrlArgs a) {
   constexpr int kItems = kCtrlSmallMax * kCtrlWindow / kCtrlSmallThreads;
   const int tid = threadIdx.x;
   const bool sent = tid < a.B;
-  // (1) states and the row count
+  // (1) states and the row count (and the running row total, read here so
+  // that its update below waits for no load)
   SentState st;
   if (sent) {
     st = a.st[tid];
     s_st[tid] = st;
   }
   const int R = *a.n_rows;
+  const unsigned long long rows_done = tid == 0 && a.rows_total != nullptr ? *a.rows_total : 0ull;
   __syncthreads();
   // (2) the draft windows (positions clamped into the row; values outside
   // [0, m) are never used), then the argmax partials of every row the launch
@@ -784,7 +786,7 @@ __global__ __launch_bounds__(1024) void k_ctrl_small(CtrlArgs a) {
     }
     s_total = acc;
     *a.n_rows = acc;
-    if (a.rows_total != nullptr) *a.rows_total += static_cast<unsigned long long>(acc);
+    if (a.rows_total != nullptr) *a.rows_total = rows_done + static_cast<unsigned long long>(acc);
     if (a.host_rows != nullptr)
       __hip_atomic_store(a.host_rows, host_word(acc, near, next_seq(a, false)), __ATOMIC_RELAXED,
                          __HIP_MEMORY_SCOPE_SYSTEM);
