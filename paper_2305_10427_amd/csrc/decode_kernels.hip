@@ -104,7 +104,8 @@ __global__ __launch_bounds__(kAttnRows * kWave) void k_attn(AttnArgs a) {
   }
 }
 
-// Attention of few rows: one workgroup of W waves per (row, head).  Wave w
+// Attention of rows with several key chunks: one workgroup of W waves per
+// (row, head).  Wave w
 // evaluates chunks w, w + W, ... of the row (chunk_eval) and leaves each
 // chunk's (m_c, l_c, o_c) in LDS; wave 0 then folds them in key order
 // (fold_chunk).  That is k_attn's arithmetic in k_attn's order, so a row's
@@ -874,18 +875,17 @@ static hipError_t launch_attn_split(const AttnArgs& a, int grid, hipStream_t s) 
   return hipGetLastError();
 }
 
-// Launches of at most kAttnSplitRows rows whose rows may have more than one
-// chunk of keys evaluate a row's chunks on kAttnSplitWaves waves side by
-// side (k_attn_split); larger launches keep one wave per (row, head), which
-// measured faster there (and the one-wave kernel is faster for rows of one
-// chunk).  Both give bitwise the same rows.
-constexpr int kAttnSplitRows = 64;
-constexpr int kAttnSplitWaves = 4;
+// Launches whose rows may have more than one chunk of keys (by the host's
+// bound) evaluate a row's chunks on kAttnSplitWaves waves side by side
+// (k_attn_split); the others keep one wave per (row, head), which is faster
+// for rows of one chunk.  Both give bitwise the same rows.  Two waves
+// measured best at every row count (four: the same at batch 1, slower above
+// 64 rows).
+constexpr int kAttnSplitWaves = 2;
 
 template <typename AT>
 static hipError_t launch_attn_t(const AttnArgs& a, int grid, hipStream_t s) {
-  if (a.rows_max <= kAttnSplitRows && a.max_keys > kAttnChunk)
-    return launch_attn_split<AT, kAttnSplitWaves>(a, a.rows_max * a.H, s);
+  if (a.max_keys > kAttnChunk) return launch_attn_split<AT, kAttnSplitWaves>(a, a.rows_max * a.H, s);
   switch (a.dh) {
     case 16: hipLaunchKernelGGL((k_attn<AT, 16>), dim3(grid), dim3(kAttnRows * kWave), 0, s, a); break;
     case 32: hipLaunchKernelGGL((k_attn<AT, 32>), dim3(grid), dim3(kAttnRows * kWave), 0, s, a); break;

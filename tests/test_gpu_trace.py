@@ -185,29 +185,34 @@ WIDE_PRE_BF16 = dataclasses.replace(C.TINY, name="wide_pre", n_dec=1, n_enc=1, d
                                      (WIDE_PRE_BF16, dict(bias_std=0.3, ln_std=0.2))],
                          ids=["chain_f32_dh16", "mid_f32_dh64", "wide_pre_bf16_dh64"])
 def test_rows_of_several_key_chunks_agree_across_launch_shapes(cfg, wkw):
-    """Rows whose keys span several 64-key chunks: a launch of up to 64 rows
-    evaluates a row's chunks on several waves side by side and folds them in
-    key order, a larger launch folds them on one wave as it goes; the rows
-    are bitwise the same.  Self- and cross-attention: greedy steps (one row,
-    m = 100, sources of 100 tokens) against the last evaluation of each
-    position in a Jacobi decode (100 rows per iteration), whose prefix is the
-    same greedy output: same tokens, top-1 logits bitwise.  Cross-attention
-    alone: teacher-forced logits of 8 positions of 3 sentences (24 rows)
-    against 30 positions (90 rows), sources of 100, 90 and 70 tokens."""
+    """Launches whose rows may see more than 64 keys (by the host's bound on
+    the key counts) evaluate a row's 64-key chunks on several waves side by
+    side and fold them in key order; the others fold one chunk after another
+    on one wave.  A row is bitwise the same either way, and whatever the
+    launch's row count.  Cross-attention: a 40-token source's teacher-forced
+    logits in a batch with a 100-token one (several-wave launch) against the
+    same source encoded alone (one-wave launch), and 8 against 30 positions.
+    Self- and cross-attention with up to 100 keys: greedy steps (one row,
+    m = 100) against the last evaluation of each position in a Jacobi decode
+    (100 rows per iteration), whose prefix is the same greedy output: same
+    tokens, top-1 logits bitwise."""
     import torch
     gm, ctx, M = build(cfg, seed=9, max_batch=3, max_src=128, max_tgt=128, **wkw)
-    srcs = [np.random.default_rng(31 + i).integers(4, cfg.vocab, n).astype(np.int32) for i, n in
-            enumerate((100, 90, 70))]
+    lens = (100, 40, 70)
+    srcs = [np.random.default_rng(31 + i).integers(4, cfg.vocab, n).astype(np.int32) for i, n in enumerate(lens)]
     src = np.zeros((3, 100), np.int32)
     for r, s in enumerate(srcs):
         src[r, :len(s)] = s
-    ctx.encode(torch.from_numpy(src).cuda(), [len(s) for s in srcs])
     tgt = np.concatenate([np.ones((3, 1), np.int32),
                           np.random.default_rng(32).integers(0, cfg.vocab, (3, 29)).astype(np.int32)], 1)
-    say(f"case several chunks cfg={cfg.name}: teacher-forced 24 vs 90 rows")
+    say(f"case several chunks cfg={cfg.name}: teacher-forced, batch of sources {lens} and the 40-token one alone")
+    ctx.encode(torch.from_numpy(src).cuda(), list(lens))
     full = ctx.debug_logits(torch.from_numpy(tgt)).cpu().numpy()
     part = ctx.debug_logits(torch.from_numpy(np.ascontiguousarray(tgt[:, :8]))).cpu().numpy()
     np.testing.assert_array_equal(part, full[:, :8])
+    ctx.encode(torch.from_numpy(np.ascontiguousarray(src[1:2, :40])).cuda(), [40])
+    alone = ctx.debug_logits(torch.from_numpy(np.ascontiguousarray(tgt[1:2]))).cpu().numpy()
+    np.testing.assert_array_equal(alone[0], full[1])
 
     m = 100
     say(f"case several chunks cfg={cfg.name}: greedy vs Jacobi, m={m}")
