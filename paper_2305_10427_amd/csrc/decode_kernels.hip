@@ -275,6 +275,8 @@ __device__ __forceinline__ void embed_rows_block(const WT* emb, const float* pe,
 
 template <typename WT>
 __global__ __launch_bounds__(256) void k_embed(EmbedArgs a) {
+  if (blockIdx.x == 0 && a.len_out != nullptr)
+    for (int i = threadIdx.x; i < a.n_len; i += blockDim.x) a.len_out[i] = a.len_in[i];
   const int R = a.n_rows_dev ? *a.n_rows_dev : a.n_rows;
   const size_t total = static_cast<size_t>(R) * a.d;
   for (size_t t = blockIdx.x * blockDim.x + threadIdx.x; t < total; t += static_cast<size_t>(gridDim.x) * blockDim.x) {

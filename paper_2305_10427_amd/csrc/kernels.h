@@ -150,7 +150,13 @@ struct EmbedArgs {
   int d;
   int vocab;               // ids outside [0, vocab) are clamped into it
   void* out;               // [R][d] storage type
+  // optional: n_len (<= kInlineLens) integers copied from the arguments to
+  // len_out by the launch (per-sentence lengths without a staging copy)
+  int* len_out;
+  int n_len;
+  int len_in[64];
 };
+constexpr int kInlineLens = 64;
 
 struct LnArgs {
   const int* n_rows_dev;

@@ -506,7 +506,8 @@ hipError_t decoder_pass(pd_ctx& C, const Rows& r, float* logits, hipStream_t s, 
   return launch_argmax_reduce(ra, r.R_max, s);
 }
 
-hipError_t encoder_pass(pd_ctx& C, const int32_t* src, int B, int n_max, hipStream_t s) {
+hipError_t encoder_pass(pd_ctx& C, const int32_t* src, int B, int n_max, const int32_t* inline_len,
+                        hipStream_t s) {
   const pd_model& M = *C.M;
   const pd_config& cfg = M.cfg;
   const int d = M.d;
@@ -525,6 +526,11 @@ hipError_t encoder_pass(pd_ctx& C, const int32_t* src, int B, int n_max, hipStre
   hipError_t e;
 
   EmbedArgs ea{nullptr, R, src, r.map, M.w[0], C.at<float>(C.L.pe), M.enc_scale, d, M.V, x_res};
+  if (inline_len != nullptr) {           // the source lengths travel with the embedding launch
+    ea.len_out = C.at<int>(C.L.src_len);
+    ea.n_len = B;
+    std::memcpy(ea.len_in, inline_len, sizeof(int32_t) * B);
+  }
   if ((e = launch_embed(M.dt, ea, R, s)) != hipSuccess) return e;
   // Every LayerNorm feeding a product runs in that product's prologue (a
   // separate kernel above 64 rows, run_gemm); post-LN stores the normalised
@@ -573,20 +579,17 @@ hipError_t encoder_pass(pd_ctx& C, const int32_t* src, int B, int n_max, hipStre
     if (pre) g.out = x_res; else g.out_f32 = s_buf;
     if ((e = run_gemm(C, r, g, EPI_RESID, false, nullptr, s)) != hipSuccess) return e;
   }
-  // the memory: the last LayerNorm (post-LN: the last layer's second; pre-LN:
-  // the encoder's final one), stored once for every cross-attention product
-  const void* mem = pre ? a_buf : x_res;
-  {
-    LnArgs la = pre ? LnArgs{nullptr, R, x_res, 0, M.enc_ln(0), M.enc_ln(1), cfg.ln_eps, d, a_buf}
-                    : LnArgs{nullptr, R, s_buf, 1, M.enc(cfg.n_enc - 1, E_LN2G), M.enc(cfg.n_enc - 1, E_LN2B),
-                             cfg.ln_eps, d, x_res};
-    if ((e = launch_ln(M.dt, la, R, s)) != hipSuccess) return e;
-  }
-  // cross-attention K / V of every decoder layer, up to kMaxLayers layers per launch
+  // cross-attention K / V of every decoder layer, up to kMaxLayers layers per
+  // launch, from the memory: the last LayerNorm (post-LN: the last layer's
+  // second; pre-LN: the encoder's final one) runs in the product's prologue
+  // (above the streaming row bound: a LayerNorm kernel into a_buf first)
   for (int l0 = 0; l0 < cfg.n_dec; l0 += kMaxLayers) {
     const int nl = std::min(kMaxLayers, cfg.n_dec - l0);
     GemmArgs g = gemm_base(r);
-    g.x = mem; g.ldx = d; g.w = M.dec(l0, D_CWKV); g.bias = M.dec(l0, D_CBKV); g.N = 2 * d; g.K = d;
+    if (pre) { g.x = x_res; g.x_f32 = 0; g.ln_g = M.enc_ln(0); g.ln_b = M.enc_ln(1); }
+    else { g.x = s_buf; g.x_f32 = 1; g.ln_g = M.enc(cfg.n_enc - 1, E_LN2G); g.ln_b = M.enc(cfg.n_enc - 1, E_LN2B); }
+    g.ln_eps = cfg.ln_eps;
+    g.ldx = d; g.w = M.dec(l0, D_CWKV); g.bias = M.dec(l0, D_CBKV); g.N = 2 * d; g.K = d;
     g.q_cols = 0;
     g.kc = C.at<char>(C.L.cross_k) + l0 * cross_layer; g.vc = C.at<char>(C.L.cross_v) + l0 * cross_layer;
     g.H = M.H; g.dh = M.dh; g.T = C.max_src; g.d = d;
@@ -596,7 +599,7 @@ hipError_t encoder_pass(pd_ctx& C, const int32_t* src, int B, int n_max, hipStre
       g.lw[z] = M.dec(l0 + z, D_CWKV);
       g.lb[z] = M.dec(l0 + z, D_CBKV);
     }
-    if ((e = run_gemm(C, r, g, EPI_QKV, false, nullptr, s)) != hipSuccess) return e;
+    if ((e = run_gemm(C, r, g, EPI_QKV, true, a_buf, s)) != hipSuccess) return e;
   }
   return hipSuccess;
 }
@@ -915,9 +918,14 @@ pd_status pd_encode(pd_ctx* ctx, const int32_t* src_ids, const int32_t* src_len,
   ctx->encoded = false;
   ctx->src_keys = 0;
   for (int b = 0; b < B; ++b) ctx->src_keys = std::max(ctx->src_keys, static_cast<int>(src_len[b]));
-  pd_status st = stage_lengths(ctx, ctx->stage_src, src_len, B, ctx->at<int>(ctx->L.src_len), s);
-  if (st != PD_OK) return st;
-  hipError_t e = encoder_pass(*ctx, src_ids, B, n_max, s);
+  // up to kInlineLens lengths go to the device with the first encoder kernel,
+  // more through the staging copy
+  const bool inline_len = B <= kInlineLens;
+  if (!inline_len) {
+    pd_status st = stage_lengths(ctx, ctx->stage_src, src_len, B, ctx->at<int>(ctx->L.src_len), s);
+    if (st != PD_OK) return st;
+  }
+  hipError_t e = encoder_pass(*ctx, src_ids, B, n_max, inline_len ? src_len : nullptr, s);
   if (e != hipSuccess) return fail(PD_E_DEVICE, std::string("encoder launch: ") + hipGetErrorString(e));
   ctx->enc_B = B;
   ctx->enc_nmax = n_max;
