@@ -423,10 +423,11 @@ __device__ void emit_rows(const CtrlArgs& a, bool init) {
 }
 
 template <typename WT>
-__global__ __launch_bounds__(1024) void k_ctrl_init(CtrlArgs a) {
+__global__ __launch_bounds__(1024) void k_ctrl_init(CtrlArgs a, InlineLens lens) {
   if (a.reset_trace_count && threadIdx.x == 0) *a.trace_count = 0ull;
+  const int* tgt_m = lens.n > 0 ? lens.v : a.tgt_m;
   for (int s = threadIdx.x; s < a.B; s += blockDim.x) {
-    const int m = a.tgt_m[s];
+    const int m = tgt_m[s];
     SentState st;
     st.m = m;
     st.i = 0;
@@ -444,7 +445,7 @@ __global__ __launch_bounds__(1024) void k_ctrl_init(CtrlArgs a) {
   for (long long i = threadIdx.x; i < n_y; i += blockDim.x) {
     const int s = static_cast<int>(i / a.ldy);
     const int t = static_cast<int>(i - static_cast<long long>(s) * a.ldy);
-    a.y[i] = (a.init != nullptr && t < a.tgt_m[s]) ? a.init[static_cast<size_t>(s) * a.init_ld + t] : a.pad_id;
+    a.y[i] = (a.init != nullptr && t < tgt_m[s]) ? a.init[static_cast<size_t>(s) * a.init_ld + t] : a.pad_id;
   }
   __syncthreads();
   emit_rows<WT>(a, true);
@@ -958,9 +959,9 @@ hipError_t launch_argmax_reduce(const ReduceArgs& a, int R_max, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_ctrl_init(int dtype, const CtrlArgs& a, hipStream_t s) {
-  if (dtype == DT_BF16) hipLaunchKernelGGL(k_ctrl_init<bf16_t>, dim3(1), dim3(1024), 0, s, a);
-  else hipLaunchKernelGGL(k_ctrl_init<float>, dim3(1), dim3(1024), 0, s, a);
+hipError_t launch_ctrl_init(int dtype, const CtrlArgs& a, const InlineLens& lens, hipStream_t s) {
+  if (dtype == DT_BF16) hipLaunchKernelGGL(k_ctrl_init<bf16_t>, dim3(1), dim3(1024), 0, s, a, lens);
+  else hipLaunchKernelGGL(k_ctrl_init<float>, dim3(1), dim3(1024), 0, s, a, lens);
   return hipGetLastError();
 }
 

@@ -158,6 +158,13 @@ struct EmbedArgs {
 };
 constexpr int kInlineLens = 64;
 
+// Per-sentence target lengths carried by k_ctrl_init's arguments (n > 0), in
+// place of CtrlArgs::tgt_m, for up to kInlineLens sentences.
+struct InlineLens {
+  int n;
+  int v[kInlineLens];
+};
+
 struct LnArgs {
   const int* n_rows_dev;
   int n_rows;
@@ -308,7 +315,7 @@ hipError_t launch_lse_reduce(const float2* part, int part_ld, int n_parts, const
 hipError_t launch_pe_table(float* pe, int n_pos, int d, hipStream_t s);
 hipError_t launch_ln(int dtype, const LnArgs& a, int R_max, hipStream_t s);
 hipError_t launch_argmax_reduce(const ReduceArgs& a, int R_max, hipStream_t s);
-hipError_t launch_ctrl_init(int dtype, const CtrlArgs& a, hipStream_t s);
+hipError_t launch_ctrl_init(int dtype, const CtrlArgs& a, const InlineLens& lens, hipStream_t s);
 hipError_t launch_ctrl_step(int dtype, const CtrlArgs& a, hipStream_t s);
 hipError_t launch_finalize(const CtrlArgs& a, hipStream_t s);
 

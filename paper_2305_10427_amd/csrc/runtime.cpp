@@ -973,8 +973,17 @@ pd_status pd_decode_init(pd_ctx* ctx, int32_t mode, int32_t block, int32_t horiz
   if (C.trace != nullptr && R_max > C.trace_rows)
     return fail(PD_E_WORKSPACE, "trace scratch holds " + std::to_string(C.trace_rows) +
                                     " rows, the decode needs " + std::to_string(R_max));
-  pd_status st = stage_lengths(ctx, C.stage_tgt, tgt_m, B, C.at<int>(C.L.tgt_m), s);
-  if (st != PD_OK) return st;
+  // up to kInlineLens target lengths go with the initial control step's
+  // arguments, more through the staging copy
+  InlineLens lens;
+  lens.n = 0;
+  if (B <= kInlineLens) {
+    lens.n = B;
+    std::memcpy(lens.v, tgt_m, sizeof(int32_t) * B);
+  } else {
+    pd_status st = stage_lengths(ctx, C.stage_tgt, tgt_m, B, C.at<int>(C.L.tgt_m), s);
+    if (st != PD_OK) return st;
+  }
   C.self_keys = m_max;
 
   CtrlArgs ca;
@@ -1023,7 +1032,7 @@ pd_status pd_decode_init(pd_ctx* ctx, int32_t mode, int32_t block, int32_t horiz
   bool prev_fused = R_max <= kFuseCtrlMaxRows;
   CtrlArgs c0 = ctrl_for_bound(C, ca, R_max);
   c0.seq0 = C.seq_next;            // every control step launched advances the count, even after the end
-  hipError_t e = launch_ctrl_init(M.dt, c0, s);
+  hipError_t e = launch_ctrl_init(M.dt, c0, lens, s);
   if (e != hipSuccess) return fail(PD_E_DEVICE, std::string("init launch: ") + hipGetErrorString(e));
   C.seq_next = (C.seq_next + 1) & kSeqMask;
   volatile int* host_rows = C.host_pinned;
