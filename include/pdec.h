@@ -188,7 +188,9 @@ void pd_ctx_destroy(pd_ctx* ctx);
  * Encode a batch of B sources (the conditioning x of p_theta(y | x)).
  *   src_ids  device int32 [B][n_max], token ids, rows padded after src_len[b]
  *            (ids outside [0, vocab) are clamped into it)
- *   src_len  HOST int32 [B], 1 <= src_len[b] <= n_max
+ *   src_len  HOST int32 [B], 1 <= src_len[b] <= n_max (read before the call
+ *            returns; up to 64 lengths go with the first kernel's arguments,
+ *            more through a pinned staging copy)
  * Runs the encoder and writes the cross-attention K/V of every decoder layer
  * into the context.  Padded positions are masked out of every attention.
  * PD_E_SHAPE if B > max_batch or n_max > max_src.
@@ -205,7 +207,8 @@ pd_status pd_encode(pd_ctx* ctx, const int32_t* src_ids, const int32_t* src_len,
  *   max_iters per-sentence cap on decoder forwards (<= 0: m, which every mode
  *             needs at most, Proposition 1)
  *   tgt_m     HOST int32 [B] (B of the last pd_encode), number of target
- *             positions m of each sentence, 1 <= tgt_m[b] <= max_tgt
+ *             positions m of each sentence, 1 <= tgt_m[b] <= max_tgt (read
+ *             before the call returns, as src_len of pd_encode)
  *   out_ids   device int32 [B][out_ld], out_ld >= max(tgt_m): the solution
  *             cut after its first [EOS] (inclusive) and [PAD]-filled
  *   out_len   device int32 [B]: output length (first [EOS] + 1, else m)
