@@ -200,6 +200,26 @@ def test_batched_sentences_equal_single_decodes():
         assert not any(lab.startswith("FAIL") for lab in labs), labs
 
 
+def test_batch_above_the_inline_length_limit():
+    """More than 64 sentences: the source and target lengths reach the device
+    through the pinned staging copy instead of the first kernel's arguments;
+    every sentence still equals its single decode (lengths passed inline)
+    and the oracle."""
+    _, _, ctx, M = build(TINY, seed=12, max_batch=70, bias_std=0.5, ln_std=0.3)
+    g = np.random.default_rng(41)
+    srcs = [g.integers(4, TINY.vocab, int(n)).astype(np.int32) for n in g.integers(1, 17, 70)]
+    ms = [int(m) for m in g.integers(1, 17, 70)]
+    for mode, b in [("gs_jacobi", 4), ("hybrid", 3)]:
+        say(f"case batch of 70 mode={mode} b={b}")
+        batch = gpu_decode_batch(ctx, srcs, ms, mode, b)
+        for r in range(0, 70, 7):
+            one = gpu_decode_batch(ctx, [srcs[r]], [ms[r]], mode, b)[0]
+            np.testing.assert_array_equal(batch[r].ids, one.ids)
+            assert batch[r].k == one.k
+        _, labs = judge_batch(ctx, M, srcs, ms, mode, b, C.F32, idx=list(range(0, 70, 7)), got=batch)
+        assert not any(lab.startswith("FAIL") for lab in labs), labs
+
+
 @pytest.mark.parametrize("cfg,wkw", [(TINY, {}), (SMALL_PRE_BF16, dict(bias_std=0.5, ln_std=0.3))],
                          ids=["tiny_f32", "small_pre_bf16"])
 def test_launch_bound_shrinks_with_the_rows(cfg, wkw):
