@@ -190,17 +190,18 @@ def test_rows_of_several_key_chunks_agree_across_launch_shapes(cfg, wkw):
     side and fold them in key order; the others fold one chunk after another
     on one wave.  A row is bitwise the same either way, and whatever the
     launch's row count.  Cross-attention: a 40-token source's teacher-forced
-    logits in a batch with a 100-token one (several-wave launch) against the
+    logits in a batch with a 200-token one (several-wave launch) against the
     same source encoded alone (one-wave launch), and 8 against 30 positions.
-    Self- and cross-attention with up to 100 keys: greedy steps (one row,
-    m = 100) against the last evaluation of each position in a Jacobi decode
-    (100 rows per iteration), whose prefix is the same greedy output: same
-    tokens, top-1 logits bitwise."""
+    Self- and cross-attention with up to 200 keys (four chunks, more than the
+    waves of a row, so a wave also folds a later chunk): greedy steps (one
+    row, m = 200) against the last evaluation of each position in a Jacobi
+    decode (200 rows per iteration), whose prefix is the same greedy output:
+    same tokens, top-1 logits bitwise."""
     import torch
-    gm, ctx, M = build(cfg, seed=9, max_batch=3, max_src=128, max_tgt=128, **wkw)
-    lens = (100, 40, 70)
+    gm, ctx, M = build(cfg, seed=9, max_batch=3, max_src=256, max_tgt=256, **wkw)
+    lens = (200, 40, 70)
     srcs = [np.random.default_rng(31 + i).integers(4, cfg.vocab, n).astype(np.int32) for i, n in enumerate(lens)]
-    src = np.zeros((3, 100), np.int32)
+    src = np.zeros((3, 200), np.int32)
     for r, s in enumerate(srcs):
         src[r, :len(s)] = s
     tgt = np.concatenate([np.ones((3, 1), np.int32),
@@ -214,9 +215,9 @@ def test_rows_of_several_key_chunks_agree_across_launch_shapes(cfg, wkw):
     alone = ctx.debug_logits(torch.from_numpy(np.ascontiguousarray(tgt[1:2]))).cpu().numpy()
     np.testing.assert_array_equal(alone[0], full[1])
 
-    m = 100
+    m = 200
     say(f"case several chunks cfg={cfg.name}: greedy vs Jacobi, m={m}")
-    ctx.set_trace(16384, m)
+    ctx.set_trace(65536, m)
     ar = gpu_decode_batch(ctx, srcs[:1], [m], "ar")[0]
     rec_ar, n_ar = ctx.trace()
     assert n_ar == len(rec_ar)
@@ -228,7 +229,7 @@ def test_rows_of_several_key_chunks_agree_across_launch_shapes(cfg, wkw):
     last = {}
     for r in rec_j:                                   # evaluation order: the last record of a position wins
         last[int(r["position"])] = r
-    assert len(rec_ar) == len(ar.ids) >= 65, (len(rec_ar), len(ar.ids))
+    assert len(rec_ar) == len(ar.ids) >= 129, (len(rec_ar), len(ar.ids))
     for r in rec_ar:
         j = last[int(r["position"])]
         assert int(j["token"]) == int(r["token"])
