@@ -27,7 +27,13 @@ constexpr int kMaxHeadDim = 128;
 // row's own key count.
 constexpr int kAttnRows = 1;   // rows (waves) per workgroup
 
-template <typename AT, int DH>
+// ONE: every row is of sentence 0 and attends to its whole source (a batch
+// of one, non-causal): the first chunk's key slots are loaded with the query,
+// before the key count klen[0] and the row count arrive.  Slots past the key
+// count hold finite values (the caches are zeroed at set-up and only ever
+// written with finite ones), whose p = 0 adds exact zeros, as key 0 does
+// in the other loads; a row past the count leaves after its loads.
+template <typename AT, int DH, int ONE>
 __global__ __launch_bounds__(kAttnRows * kWave) void k_attn(AttnArgs a) {
   __shared__ float s_q[kAttnRows][DH];
   __shared__ AttnScratch s_scr[kAttnRows];
@@ -50,18 +56,30 @@ __global__ __launch_bounds__(kAttnRows * kWave) void k_attn(AttnArgs a) {
     const int d = lane + kWave * i;
     qv[i] = q[d < DH ? d : 0];           // unconditional load
   }
-  int s, p;
-  row_place(a.rows, row, s, p);
-  if (row >= R) return;
-  const int nk = a.causal ? p + 1 : a.klen[s];
-  const size_t base = (static_cast<size_t>(s) * a.H + hh) * a.T * DH;
-  const AT* Kb = static_cast<const AT*>(a.kc) + base;
-  const AT* Vb = static_cast<const AT*>(a.vc) + base;
   // two chunk buffers: the loads of the next chunk are issued before the
   // current one is folded (a chunk past the row's keys loads key 0 and is
   // never folded)
   KeyChunk<AT, DH> ka, kb;
-  ka.load(Kb, Vb, 0, nk, lane);
+  int nk;
+  const AT* Kb;
+  const AT* Vb;
+  if constexpr (ONE != 0) {
+    nk = *a.klen;
+    const size_t base = static_cast<size_t>(hh) * a.T * DH;
+    Kb = static_cast<const AT*>(a.kc) + base;
+    Vb = static_cast<const AT*>(a.vc) + base;
+    ka.load(Kb, Vb, 0, a.T, lane);       // every slot of the first chunk
+    if (row >= R) return;
+  } else {
+    int s, p;
+    row_place(a.rows, row, s, p);
+    if (row >= R) return;
+    nk = a.causal ? p + 1 : a.klen[s];
+    const size_t base = (static_cast<size_t>(s) * a.H + hh) * a.T * DH;
+    Kb = static_cast<const AT*>(a.kc) + base;
+    Vb = static_cast<const AT*>(a.vc) + base;
+    ka.load(Kb, Vb, 0, nk, lane);
+  }
 #pragma unroll
   for (int i = 0; i < (DH + kWave - 1) / kWave; ++i) {
     const int d = lane + kWave * i;
@@ -111,7 +129,7 @@ __global__ __launch_bounds__(kAttnRows * kWave) void k_attn(AttnArgs a) {
 // (fold_chunk).  That is k_attn's arithmetic in k_attn's order, so a row's
 // output is bitwise the same, while the chunks of a long row are evaluated
 // side by side instead of one after another.
-template <typename AT, int DH, int W>
+template <typename AT, int DH, int W, int ONE>
 __global__ __launch_bounds__(W * kWave) void k_attn_split(AttnArgs a) {
   constexpr int NQ = (DH + kWave - 1) / kWave;
   constexpr int NP = RowState<DH>::NP;
@@ -137,22 +155,34 @@ __global__ __launch_bounds__(W * kWave) void k_attn_split(AttnArgs a) {
     const int d = lane + kWave * i;
     qv[i] = q[d < DH ? d : 0];           // unconditional load
   }
-  int s, p;
-  row_place(a.rows, row, s, p);
-  if (row >= R) return;
-  const int nk = a.causal ? p + 1 : a.klen[s];
+  int s = 0, p = 0, nk;
+  KeyChunk<AT, DH> kc;
+  if constexpr (ONE != 0) {
+    // every wave loads its first chunk's slots before the key count arrives
+    nk = *a.klen;
+    kc.load_k(static_cast<const AT*>(a.kc) + static_cast<size_t>(hh) * a.T * DH, wave * kAttnChunk, a.T, lane);
+    __builtin_amdgcn_sched_barrier(0);
+    kc.load_v(static_cast<const AT*>(a.vc) + static_cast<size_t>(hh) * a.T * DH, wave * kAttnChunk, a.T, lane);
+    __builtin_amdgcn_sched_barrier(0);
+    if (row >= R) return;                // the whole workgroup (row is uniform)
+  } else {
+    row_place(a.rows, row, s, p);
+    if (row >= R) return;
+    nk = a.causal ? p + 1 : a.klen[s];
+  }
   const int nc = (nk + kAttnChunk - 1) / kAttnChunk;    // 1 .. NC
   const size_t base = (static_cast<size_t>(s) * a.H + hh) * a.T * DH;
   const AT* Kb = static_cast<const AT*>(a.kc) + base;
   const AT* Vb = static_cast<const AT*>(a.vc) + base;
   if (nc == 1 && wave != 0) return;     // workgroup-uniform: one chunk, no barrier below
-  // every wave loads its first chunk on the straight path (a wave past the
-  // row's chunks loads key 0 and evaluates nothing)
-  KeyChunk<AT, DH> kc;
-  kc.load_k(Kb, wave * kAttnChunk, nk, lane);
-  __builtin_amdgcn_sched_barrier(0);     // the K rows first: the scores start while V arrives
-  kc.load_v(Vb, wave * kAttnChunk, nk, lane);
-  __builtin_amdgcn_sched_barrier(0);
+  if constexpr (ONE == 0) {
+    // every wave loads its first chunk on the straight path (a wave past the
+    // row's chunks loads key 0 and evaluates nothing)
+    kc.load_k(Kb, wave * kAttnChunk, nk, lane);
+    __builtin_amdgcn_sched_barrier(0);   // the K rows first: the scores start while V arrives
+    kc.load_v(Vb, wave * kAttnChunk, nk, lane);
+    __builtin_amdgcn_sched_barrier(0);
+  }
 #pragma unroll
   for (int i = 0; i < NQ; ++i) {
     const int d = lane + kWave * i;
@@ -866,13 +896,13 @@ __global__ __launch_bounds__(256) void k_argmax_reduce(ReduceArgs a) {
   }
 }
 
-template <typename AT, int W>
+template <typename AT, int W, int ONE>
 static hipError_t launch_attn_split(const AttnArgs& a, int grid, hipStream_t s) {
   switch (a.dh) {
-    case 16: hipLaunchKernelGGL((k_attn_split<AT, 16, W>), dim3(grid), dim3(W * kWave), 0, s, a); break;
-    case 32: hipLaunchKernelGGL((k_attn_split<AT, 32, W>), dim3(grid), dim3(W * kWave), 0, s, a); break;
-    case 64: hipLaunchKernelGGL((k_attn_split<AT, 64, W>), dim3(grid), dim3(W * kWave), 0, s, a); break;
-    case 128: hipLaunchKernelGGL((k_attn_split<AT, 128, W>), dim3(grid), dim3(W * kWave), 0, s, a); break;
+    case 16: hipLaunchKernelGGL((k_attn_split<AT, 16, W, ONE>), dim3(grid), dim3(W * kWave), 0, s, a); break;
+    case 32: hipLaunchKernelGGL((k_attn_split<AT, 32, W, ONE>), dim3(grid), dim3(W * kWave), 0, s, a); break;
+    case 64: hipLaunchKernelGGL((k_attn_split<AT, 64, W, ONE>), dim3(grid), dim3(W * kWave), 0, s, a); break;
+    case 128: hipLaunchKernelGGL((k_attn_split<AT, 128, W, ONE>), dim3(grid), dim3(W * kWave), 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -886,21 +916,27 @@ static hipError_t launch_attn_split(const AttnArgs& a, int grid, hipStream_t s) 
 // 64 rows).
 constexpr int kAttnSplitWaves = 2;
 
-template <typename AT>
-static hipError_t launch_attn_t(const AttnArgs& a, int grid, hipStream_t s) {
-  if (a.max_keys > kAttnChunk) return launch_attn_split<AT, kAttnSplitWaves>(a, a.rows_max * a.H, s);
+template <typename AT, int ONE>
+static hipError_t launch_attn_f(const AttnArgs& a, int grid, hipStream_t s) {
+  if (a.max_keys > kAttnChunk) return launch_attn_split<AT, kAttnSplitWaves, ONE>(a, a.rows_max * a.H, s);
   switch (a.dh) {
-    case 16: hipLaunchKernelGGL((k_attn<AT, 16>), dim3(grid), dim3(kAttnRows * kWave), 0, s, a); break;
-    case 32: hipLaunchKernelGGL((k_attn<AT, 32>), dim3(grid), dim3(kAttnRows * kWave), 0, s, a); break;
-    case 64: hipLaunchKernelGGL((k_attn<AT, 64>), dim3(grid), dim3(kAttnRows * kWave), 0, s, a); break;
-    case 128: hipLaunchKernelGGL((k_attn<AT, 128>), dim3(grid), dim3(kAttnRows * kWave), 0, s, a); break;
+    case 16: hipLaunchKernelGGL((k_attn<AT, 16, ONE>), dim3(grid), dim3(kAttnRows * kWave), 0, s, a); break;
+    case 32: hipLaunchKernelGGL((k_attn<AT, 32, ONE>), dim3(grid), dim3(kAttnRows * kWave), 0, s, a); break;
+    case 64: hipLaunchKernelGGL((k_attn<AT, 64, ONE>), dim3(grid), dim3(kAttnRows * kWave), 0, s, a); break;
+    case 128: hipLaunchKernelGGL((k_attn<AT, 128, ONE>), dim3(grid), dim3(kAttnRows * kWave), 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
+template <typename AT>
+static hipError_t launch_attn_t(const AttnArgs& a, int grid, hipStream_t s) {
+  return a.one_source ? launch_attn_f<AT, 1>(a, grid, s) : launch_attn_f<AT, 0>(a, grid, s);
+}
+
 hipError_t launch_attn(int dtype, const AttnArgs& args, int R_max, hipStream_t s) {
   if (args.dh > kMaxHeadDim || args.T > kMaxKeys) return hipErrorInvalidValue;
+  if (args.one_source && (args.causal || args.klen == nullptr)) return hipErrorInvalidValue;
   const int grid = (R_max + kAttnRows - 1) / kAttnRows * args.H;
   if (grid == 0) return hipSuccess;
   AttnArgs a = args;

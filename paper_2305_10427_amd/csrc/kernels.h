@@ -137,6 +137,8 @@ struct AttnArgs {
   int rows_max;            // launch bound on the rows (set by launch_attn)
   int out_feed;            // 1: out ([R][H dh]) written in the MFMA feed order (feed_index), ldo unused
   int max_keys;            // host bound on any row's key count (0: unknown); chooses the launch shape only
+  int one_source;          // 1: every row is of sentence 0 and non-causal (a batch of one): key slots are
+                           // loaded before klen[0] arrives (the caches must hold finite values throughout)
 };
 
 struct EmbedArgs {

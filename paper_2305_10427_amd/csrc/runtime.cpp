@@ -555,6 +555,10 @@ hipError_t encoder_pass(pd_ctx& C, const int32_t* src, int B, int n_max, const i
     if ((e = run_gemm(C, r, g, EPI_QKV, ln, ln_tmp, s)) != hipSuccess) return e;
     AttnArgs aa{nullptr, R, q_buf, d, g.kc, g.vc, M.H, M.dh, C.max_src, r.map, 0, klen, a_buf, d, scale};
     aa.max_keys = C.src_keys;
+    // one source: its key slots load with the queries (in the decoder's
+    // cross-attention this measured slower for the large model: slots past
+    // the source come from HBM there, not from the cache the encoder filled)
+    aa.one_source = B == 1 ? 1 : 0;
     if ((e = launch_attn(M.dt, aa, R, s)) != hipSuccess) return e;
     g = gemm_base(r);
     g.x = a_buf; g.ldx = d; g.w = M.enc(l, E_WO); g.wp = M.enc_feed(l, E_WO); g.bias = M.enc(l, E_BO); g.N = d; g.K = d;
@@ -875,6 +879,11 @@ pd_status pd_ctx_create(const pd_model* model, int32_t max_batch, int32_t max_sr
   }
   if (e == hipSuccess) e = hipStreamCreateWithFlags(&c->capture, hipStreamNonBlocking);
   if (e == hipSuccess) e = hipMemset(c->at<unsigned long long>(c->L.rows_total), 0, sizeof(unsigned long long));
+  // the encoder and cross-attention caches start at zero, so that every key
+  // slot holds a finite value before the first encode writes it (batch-of-one
+  // attention loads slots past a source's length and weighs them by zero)
+  // (enc_k, enc_v, cross_k and cross_v lie back to back, up to self_k)
+  if (e == hipSuccess) e = hipMemset(c->at<char>(c->L.enc_k), 0, c->L.self_k - c->L.enc_k);
   if (e == hipSuccess) e = launch_pe_table(c->at<float>(c->L.pe), std::max(max_src, max_tgt), model->d, nullptr);
   if (e == hipSuccess) e = hipDeviceSynchronize();
   if (e != hipSuccess) {
