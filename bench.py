@@ -280,9 +280,17 @@ def cpu_baseline(wl, w, sents, ctxs, mode, block, m_cap, n_sent):
             exact += 1
         else:
             near += 1
+    # argmaxes of the float64 oracle on the sample whose top-2 margin lies
+    # within the logit tolerance (5e-2 of max|logit| in bf16, 1e-3 in fp32):
+    # the decisions a correct GPU path may take either way
+    tol = 5e-2 if cfg.dtype == "bf16" else 1e-3
+    n_arg = sum(len(r.records) for r in results)
+    n_tie = sum(1 for r in results for rec in r.records if rec.top1 - rec.top2 < tol * max(rec.linf, 1e-30))
     out["parity_sample"] = {"sentences": len(sample), "exact": exact, "not_exact": near,
+                            "argmaxes": n_arg, "near_ties": n_tie, "near_tie_margin": tol,
                             "note": "ids and k of the GPU against the float64 oracle on the baseline sample; "
-                                    "the GPU tests judge every difference"}
+                                    "near_ties: oracle argmaxes whose top-2 margin is below near_tie_margin x "
+                                    "max|logit|; the GPU tests judge every difference"}
     return out
 
 
