@@ -234,3 +234,33 @@ def test_rows_of_several_key_chunks_agree_across_launch_shapes(cfg, wkw):
         j = last[int(r["position"])]
         assert int(j["token"]) == int(r["token"])
         assert np.float32(j["top1"]).view(np.uint32) == np.float32(r["top1"]).view(np.uint32), (r, j)
+
+
+@pytest.mark.parametrize("cfg,wkw", [(CHAIN, dict(bias_std=0.5, ln_std=0.3)), (MID_F32, {}),
+                                     (WIDE_PRE_BF16, dict(bias_std=0.3, ln_std=0.2))],
+                         ids=["chain_f32_dh16", "mid_f32_dh64", "wide_pre_bf16_dh64"])
+def test_one_source_padding_changes_no_row(cfg, wkw):
+    """A batch of one source (its key slots loaded before its length arrives)
+    encoded with padding past its length, and as the first of a batch of two:
+    the teacher-forced logits equal those of the unpadded encode bitwise, for
+    sources of one and of several key chunks."""
+    import torch
+    gm, ctx, M = build(cfg, seed=10, max_batch=2, max_src=256, max_tgt=32, **wkw)
+    tgt = np.concatenate([np.ones((1, 1), np.int32),
+                          np.random.default_rng(33).integers(0, cfg.vocab, (1, 15)).astype(np.int32)], 1)
+    for n in (10, 100):
+        say(f"case one source cfg={cfg.name} n={n}")
+        src = np.random.default_rng(34 + n).integers(4, cfg.vocab, n).astype(np.int32)
+        ctx.encode(torch.from_numpy(src[None, :]).cuda(), [n])
+        plain = ctx.debug_logits(torch.from_numpy(tgt)).cpu().numpy()
+        padded = np.zeros((1, n + 37), np.int32)
+        padded[0, :n] = src
+        ctx.encode(torch.from_numpy(padded).cuda(), [n])
+        np.testing.assert_array_equal(ctx.debug_logits(torch.from_numpy(tgt)).cpu().numpy(), plain)
+        pair = np.zeros((2, n + 5), np.int32)
+        pair[0, :n] = src
+        pair[1, :] = np.random.default_rng(35).integers(4, cfg.vocab, n + 5)
+        ctx.encode(torch.from_numpy(pair).cuda(), [n, n + 5])
+        two = ctx.debug_logits(torch.from_numpy(np.repeat(tgt, 2, axis=0))).cpu().numpy()
+        np.testing.assert_array_equal(two[0], plain[0])
+
