@@ -24,6 +24,9 @@ MID_F32 = dataclasses.replace(C.TINY, name="mid_f32", d_model=128, n_heads=2, d_
 MID_BF16 = dataclasses.replace(C.TINY, name="mid_bf16", d_model=256, n_heads=8, d_ff=512, vocab=700, dtype=C.BF16)
 WIDE_PRE_BF16 = dataclasses.replace(C.TINY, name="wide_pre", n_dec=1, n_enc=1, d_model=640, n_heads=10, d_ff=640,
                                     vocab=500, pre_ln=True, act_gelu=True, dtype=C.BF16)
+# an FFN down-projection with K = 2048: eight K ranges (split over workgroups
+# in the tiled products of many rows)
+FFN2K_BF16 = dataclasses.replace(C.TINY, name="ffn2k", d_model=256, n_heads=4, d_ff=2048, vocab=700, dtype=C.BF16)
 
 
 def say(*a):
@@ -161,8 +164,8 @@ def test_teacher_forced_logits_within_tolerance(cfg):
         assert rel.max() < EPS[cfg.dtype] <= TOL[cfg.dtype]
 
 
-@pytest.mark.parametrize("cfg", [TINY, SMALL_PRE_BF16, MID_F32, MID_BF16, WIDE_PRE_BF16],
-                         ids=["tiny_f32", "small_pre_bf16", "mid_f32", "mid_bf16", "wide_pre_bf16"])
+@pytest.mark.parametrize("cfg", [TINY, SMALL_PRE_BF16, MID_F32, MID_BF16, WIDE_PRE_BF16, FFN2K_BF16],
+                         ids=["tiny_f32", "small_pre_bf16", "mid_f32", "mid_bf16", "wide_pre_bf16", "ffn2k_bf16"])
 def test_rows_are_invariant_to_block_and_batch(cfg):
     """A row's logits are bitwise the same whatever else is in the call: fewer
     or more positions (row tiles, fused or separate LayerNorm) and batch mates."""
